@@ -1,0 +1,202 @@
+"""Benchmark: AllReduce plan execution for n emulated processors on one
+MI355X, through the C ABI.
+
+A step is one execution of the whole plan (every ReduceScatter and
+AllGather phase) over the n input buffers, which are resident in HBM before
+the timed region starts.  The plan runs in place; the inputs are restored
+from a pristine device copy after warm-up, then K steps run back to back
+(values grow by a factor of about n per step, which does not change the
+work: fp32 adds take the same time whatever the operands).
+
+Prints one JSON line:
+  value       AllReduce algorithm bandwidth n * N * e / time, GB/s
+  roofline    the reduce-phase kernel: algorithmic bytes per launch
+              ((k + 1) * len * e per k-way reduce step) over its mean
+              launch duration (HIP events on the launch stream), against
+              MI355X's 8 TB/s HBM peak
+  cpu_baseline  the CPU oracle executing the same plan on the host
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+DEFAULT = "rhd_n8_f32"
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kernels.hpp", "exec.hip"):
+        with open(os.path.join(ROOT, "paper_2409_04202_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload):
+    """HBM traffic per reduce launch from a committed rocprofv3 --pmc
+    summary, if it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_sources") != kernel_source_hash():
+        return None
+    return d.get("reduce_bytes_per_launch")
+
+
+def cpu_baseline(name, budget_s=25.0):
+    """The oracle, as written, on the same workload (single thread)."""
+    import numpy as np  # noqa: F401
+    import oracle
+    from paper_2409_04202_amd import workloads
+    c = workloads.CONFIGS[name]
+    plan = oracle.make_plan(c["kind"], c["n"], c["N"], c["fanin"])
+    xs = workloads.inputs(name)
+    total = c["n"] * c["N"] * workloads.ESIZE[c["dtype"]]
+    runs, spent = 0, 0.0
+    while spent < budget_s * 0.4 and runs < 20:
+        bufs = [x.copy() for x in xs]
+        t0 = time.perf_counter()
+        oracle.execute(plan, bufs, c["dtype"])
+        spent += time.perf_counter() - t0
+        runs += 1
+    return {"value": round(total * runs / spent / 1e9, 4), "unit": "GB/s",
+            "cores": 1, "kind": "oracle",
+            "sample": "%d full executions of the %s plan (n=%d, N=%d %s), "
+                      "numpy, one thread" % (runs, c["kind"], c["n"], c["N"],
+                                             c["dtype"]),
+            "seconds": round(spent, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default=DEFAULT)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build executes every emulated processor on one "
+              "GPU; runs on more than one GPU are not supported (--gpus 1).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2409_04202_amd import arplan, workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    name = args.config
+    c = workloads.CONFIGS[name]
+    n, N, dt = c["n"], c["N"], c["dtype"]
+    esize = workloads.ESIZE[dt]
+    tdt = {"f32": torch.float32, "i32": torch.int32, "bf16": torch.int16}[dt]
+    print("bench: %s n=%d N=%d %s: drawing inputs" % (name, n, N, dt),
+          file=sys.stderr, flush=True)
+    xs = workloads.inputs(name)
+    import numpy as np
+    view = np.int16 if dt == "bf16" else xs[0].dtype
+    pristine = [torch.from_numpy(x.view(view)).to("cuda") for x in xs]
+    bufs = [torch.empty_like(p) for p in pristine]
+    del xs
+
+    plan = arplan.Plan(n, N, dt, c["kind"], c["fanin"])
+    stream = torch.cuda.current_stream()
+    phase_ops, phase_bytes = [], []
+    for ph in range(plan.num_phases):
+        op, _, _, b = plan.phase_info(ph)
+        phase_ops.append(op)
+        phase_bytes.append(b)
+    red_b, cpy_b = plan.bytes()
+
+    def restore():
+        for b, p in zip(bufs, pristine):
+            b.copy_(p)
+
+    restore()
+    for _ in range(args.warmup):
+        plan.execute(bufs, stream)
+    restore()
+    K = args.steps
+    timer = arplan.ar_timer_create(max(1, K * plan.num_phases * 2))
+    torch.cuda.synchronize()
+    print("bench: timing %d steps" % K, file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for _ in range(K):
+        plan.execute_timed(bufs, stream, timer)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = arplan.ar_timer_read(timer, K * plan.num_phases * 2)
+    arplan.ar_timer_destroy(timer)
+
+    ms_step = (t1 - t0) * 1e3 / K
+    total = n * N * esize
+    value = total / (ms_step * 1e-3) / 1e9
+
+    ph_ms = [0.0] * plan.num_phases
+    for ph, ms in recs:
+        ph_ms[ph] += ms / K
+    red_ms = sum(m for m, op in zip(ph_ms, phase_ops) if op == arplan.AR_OP_REDUCE)
+    n_red = sum(1 for op in phase_ops if op == arplan.AR_OP_REDUCE)
+    kern_ms = sum(ph_ms)
+    achieved = red_b / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
+    traffic = load_traffic(name)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic,
+                "kernel": "phase_kernel (reduce phases, k=%s)" % (
+                    sorted({len(s[3]) for s in plan.steps()
+                            if s[1] == arplan.AR_OP_REDUCE}) or "-"),
+                "launches_per_step": n_red,
+                "bytes_per_launch": round(red_b / max(1, n_red)),
+                "ms_per_launch": round(red_ms / max(1, n_red), 5)}
+    out = {
+        "metric": "AllReduce algbw GB/s and % HBM roofline per plan at 1 MI355X",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic (seeded %s inputs)" % c["dist"],
+        "config": {"workload": name, "plan": c["kind"], "n": n, "N": N,
+                   "fanin": list(c["fanin"]) if c["fanin"] else None,
+                   "parallelism": "emulated %d processors on 1 GPU" % n},
+        "plan_bytes_per_step": red_b + cpy_b,
+        "plan_gbs": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9, 1),
+        "plan_frac": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "kernel_ms_per_step": round(kern_ms, 5),
+        "phases": [{"phase": i, "op": "reduce" if op == 0 else "copy",
+                    "bytes": b, "ms": round(m, 5),
+                    "gbs": round(b / (m * 1e-3) / 1e9, 1) if m > 0 else None}
+                   for i, (op, b, m) in enumerate(zip(phase_ops, phase_bytes, ph_ms))],
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    plan.close()
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        del bufs, pristine
+        out["cpu_baseline"] = cpu_baseline(name)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,233 @@
+/*
+ * ar_plan.h -- C ABI of the MI355X AllReduce-plan executor.
+ *
+ * The library executes AllReduce plans in the sense of "Revisiting the Time
+ * Cost Model of AllReduce" (GenModel / GenTree, arXiv 2409.04202) for n
+ * emulated processors whose buffers of N elements all live in the memory of
+ * one GPU.
+ *
+ *   AllReduce: every processor ends with the element-wise sum of all
+ *   processors' data (Section 1; Section 2.1).  A *plan* is an ordering of
+ *   data-movement and reduce steps (Section 2.1).  The ReduceScatter /
+ *   AllGather plans split the data into n blocks, each processor reduces one
+ *   share, then the shares are sent back to everyone (Section 2.1).
+ *
+ * A plan is expanded on the host into an explicit list of steps grouped in
+ * phases.  A step is
+ *
+ *   reduce:  x_dst[b, e) <- x_srcs[0][b, e) + ... + x_srcs[k-1][b, e),
+ *            folded left to right (the k-way sum of Section 3.1, which costs
+ *            k reads and one write per element, the memory term of GenModel)
+ *   copy:    x_dst[b, e) <- x_src[b, e)
+ *
+ * Every step of a phase reads the buffers as they were when the phase
+ * started; the library checks at creation that no step of a phase reads or
+ * writes a range another step of the same phase writes, so the steps of a
+ * phase may run in any order or all at once.  Phases run in order.
+ *
+ * Arithmetic (fixed, so a plan has one exact result):
+ *   AR_F32   IEEE binary32 adds, round to nearest even, no contraction,
+ *            denormals kept, in the step's source order;
+ *   AR_I32   two's-complement wrap-around adds;
+ *   AR_BF16  buffers hold bfloat16; each reduce step widens its inputs to
+ *            fp32, folds them in fp32 in source order and rounds the result
+ *            once to bf16 (round to nearest even).
+ *
+ * Conventions for every call:
+ *   - Every function returns an ar_status; AR_OK is 0.  No C++ exception
+ *     crosses this interface.  On failure a description is available from
+ *     ar_last_error() (per thread, valid until the next call on the thread).
+ *   - Out-parameters are written only on success; on failure a plan/timer
+ *     out-pointer is set to NULL.
+ *   - Plan creation and introspection make no GPU call and work without a
+ *     GPU.  Execution needs a gfx950 device.
+ */
+#ifndef AR_PLAN_H
+#define AR_PLAN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum ar_status {
+    AR_OK = 0,
+    AR_ERR_INVALID_ARG = 1,  /* bad pointer, size, index or plan shape      */
+    AR_ERR_UNSUPPORTED = 2,  /* valid request the library does not handle    */
+    AR_ERR_OOM = 3,          /* host or device allocation failed             */
+    AR_ERR_HIP = 4,          /* a HIP runtime call or kernel launch failed   */
+    AR_ERR_INTERNAL = 5
+} ar_status;
+
+typedef enum ar_dtype { AR_F32 = 0, AR_I32 = 1, AR_BF16 = 2 } ar_dtype;
+
+/* Plan kinds (Section 2.1 and Section 3.3, Tables 1 and 2):
+ *  AR_RING  Ring: 2(n-1) steps; in step j processor i receives block
+ *           (i - j) mod n from processor i - 1 and, in the first n - 1 steps,
+ *           adds its own block to it (reduce step with srcs {i, i-1}); in
+ *           the last n - 1 steps it stores it (copy).  After the
+ *           ReduceScatter half processor i owns block (i + 2) mod n.
+ *  AR_RHD   Recursive halving-doubling, n a power of two: in halving step j
+ *           processor r pairs with r XOR 2^j, keeps the lower half of the
+ *           range it holds if bit j of r is 0 and the upper half otherwise,
+ *           and reduces it over the pair (2^-(j+1) of the data in step j);
+ *           the doubling steps run the halving steps backwards as copies.
+ *           Other n: AR_ERR_UNSUPPORTED.
+ *  AR_CPS   Co-located PS: processor p reduces block p over all n inputs in
+ *           one n-way step, then the n - 1 others copy it.
+ *  AR_TREE  Hierarchical co-located PS on a symmetric tree, i.e. the GenTree
+ *           basic sub-plan of Algorithm 1 for a tree whose switches at level
+ *           l all have fanin[l] children (fanin[0] = servers per bottom
+ *           switch).  n must equal the product of the fan-ins.  Rank r has
+ *           digits d_l = (r / (f_0...f_{l-1})) mod f_l.  ReduceScatter level
+ *           l reduces, over the f_l ranks that differ from r only in digit
+ *           l (ascending), the part of r's previous range that r owns;
+ *           AllGather runs the levels in reverse as copies.  Rank r owns
+ *           after level l the n/(f_0...f_l) blocks starting at block
+ *           o_l(r) * n/(f_0...f_l), o_l = o_{l-1} * f_l + d_l, o_{-1} = 0
+ *           (the bottom-up placement of Algorithm 1).  Levels with fan-in 1
+ *           add no phase.
+ *  AR_RB    Reduce-Broadcast (parameter server): rank 0 reduces all n full
+ *           buffers in one n-way step, then the others copy the result.
+ *
+ * Block split: block b of the n-way split covers [b*q + min(b, rem),
+ * (b+1)*q + min(b+1, rem)) with q = N / n, rem = N mod n (the floor share,
+ * one more for the first rem blocks, as in Algorithm 1).
+ */
+typedef enum ar_kind {
+    AR_RING = 0, AR_RHD = 1, AR_CPS = 2, AR_TREE = 3, AR_RB = 4
+} ar_kind;
+
+typedef enum ar_op { AR_OP_REDUCE = 0, AR_OP_COPY = 1 } ar_op;
+
+typedef struct ar_topology {
+    int32_t kind;          /* ar_kind                                       */
+    int32_t num_levels;    /* AR_TREE: number of fan-in levels (>= 1)       */
+    const int32_t* fanin;  /* AR_TREE: fanin[0..num_levels), innermost first;
+                              ignored for other kinds; read during the call */
+} ar_topology;
+
+typedef struct ar_step {
+    int32_t phase;         /* 0-based; phases execute in increasing order   */
+    int32_t op;            /* ar_op                                         */
+    int32_t dst;           /* processor written, 0 <= dst < n               */
+    int32_t nsrc;          /* number of sources (copy: exactly 1)           */
+    const int32_t* srcs;   /* nsrc processor indices, folded in this order  */
+    int64_t begin;         /* element range [begin, end), 0 <= b <= e <= N  */
+    int64_t end;
+} ar_step;
+
+typedef struct ar_plan ar_plan;
+typedef struct ar_timer ar_timer;
+
+/* ---------------------------------------------------------------- plans */
+
+/* Expand a plan of kind topo->kind for n processors of N elements of dtype.
+ * n >= 1, N >= 0 (n = 1 or N = 0 gives a plan with no work; N < n gives
+ * empty blocks, which are kept as empty steps).  n <= 65536.
+ * Errors: AR_ERR_INVALID_ARG (NULL out/topo, n < 1, N < 0, unknown dtype or
+ * kind, tree fan-in < 1, missing fan-ins or product != n, N * element size
+ * overflowing int64), AR_ERR_UNSUPPORTED (RHD with n not a power of two),
+ * AR_ERR_OOM.  The plan owns all its memory; free it with ar_plan_destroy. */
+ar_status ar_plan_create(int32_t n, int64_t N, int32_t dtype,
+                         const ar_topology* topo, ar_plan** out);
+
+/* Build a plan from an explicit step list (any order; steps are grouped by
+ * phase, phases must be numbered 0..P-1 without gaps).  Each step is
+ * validated (indices, ranges, copy has one source, reduce at least one) and
+ * each phase is checked for hazards: AR_ERR_INVALID_ARG if a step writes a
+ * range that another step of the same phase reads or writes.  The arrays
+ * are copied; the caller keeps ownership of `steps`.  Such a plan has no
+ * owner map (ar_plan_owner returns AR_ERR_UNSUPPORTED). */
+ar_status ar_plan_create_custom(int32_t n, int64_t N, int32_t dtype,
+                                const ar_step* steps, int64_t nsteps,
+                                ar_plan** out);
+
+/* Free a plan and the device memory it holds.  NULL is a no-op.  Must not be
+ * called while an execution of the plan may still be running. */
+ar_status ar_plan_destroy(ar_plan* plan);
+
+/* ------------------------------------------------------------ execution */
+
+/* Execute the plan in place on bufs[0..n): n device pointers on the current
+ * device, each to at least N * element-size bytes, pairwise non-overlapping
+ * (checked on the host: AR_ERR_INVALID_ARG for NULL or overlapping
+ * buffers).  `stream` is a hipStream_t (NULL = the default stream).  The
+ * call is asynchronous and stream-ordered: it enqueues one kernel launch per
+ * phase (more only for phases mixing source counts) and returns; when the
+ * stream reaches that point every buffer holds the AllReduce result.  The
+ * pointer array is read during the call only.  Any pointer alignment works;
+ * 16-byte-aligned buffers take the vector path.  The first call on a device
+ * uploads the plan's step tables (device memory owned by the plan).
+ * Executions of one plan must be ordered (one stream, or synchronised): the
+ * plan keeps one device copy of recently used pointer tables.  Distinct plans
+ * are independent.  Errors: AR_ERR_INVALID_ARG, AR_ERR_OOM, AR_ERR_HIP. */
+ar_status ar_plan_execute(ar_plan* plan, void* const* bufs, void* stream);
+
+/* Same, with buffer p at (char*)base + p * stride_bytes; stride_bytes must
+ * be >= N * element size. */
+ar_status ar_plan_execute_strided(ar_plan* plan, void* base,
+                                  int64_t stride_bytes, void* stream);
+
+/* ar_plan_execute that also records a pair of HIP events on `stream`
+ * around every kernel launch into `timer` (appended; AR_ERR_INVALID_ARG
+ * when the timer is full).  Results are read with ar_timer_read. */
+ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
+                                void* stream, ar_timer* timer);
+
+/* -------------------------------------------------------- introspection */
+
+/* Shape of the plan: any out-pointer may be NULL. */
+ar_status ar_plan_info(const ar_plan* plan, int32_t* n, int64_t* N,
+                       int32_t* dtype, int32_t* num_phases,
+                       int64_t* num_steps);
+
+/* Step i (0 <= i < num_steps) in execution order (by phase).  out->srcs
+ * points into the plan and stays valid until ar_plan_destroy. */
+ar_status ar_plan_get_step(const ar_plan* plan, int64_t i, ar_step* out);
+
+/* Phase p: `op` is AR_OP_REDUCE if any step reduces, else AR_OP_COPY;
+ * steps [first_step, first_step + num_steps); `bytes` is the phase's
+ * algorithmic traffic: (k + 1) * len * e per k-way reduce step, 2 * len * e
+ * per copy step (GenModel's memory term for reduces, Section 3.1; a copy
+ * reads and writes each element once).  Any out-pointer may be NULL. */
+ar_status ar_plan_phase_info(const ar_plan* plan, int32_t phase, int32_t* op,
+                             int64_t* first_step, int64_t* num_steps,
+                             int64_t* bytes);
+
+/* Range [begin, end) that processor p holds fully reduced once the
+ * ReduceScatter phases are done (empty for processors that own nothing,
+ * e.g. non-root ranks of AR_RB).  AR_ERR_UNSUPPORTED for custom plans. */
+ar_status ar_plan_owner(const ar_plan* plan, int32_t p, int64_t* begin,
+                        int64_t* end);
+
+/* Total algorithmic bytes of all reduce steps and of all copy steps (same
+ * rule as ar_plan_phase_info).  Either out-pointer may be NULL. */
+ar_status ar_plan_bytes(const ar_plan* plan, int64_t* reduce_bytes,
+                        int64_t* copy_bytes);
+
+/* --------------------------------------------------------------- timing */
+
+/* A timer holds up to `capacity` launch records (capacity >= 1).  Its HIP
+ * events are created on first use, on the device current at that time. */
+ar_status ar_timer_create(int64_t capacity, ar_timer** out);
+ar_status ar_timer_reset(ar_timer* timer);          /* forget all records */
+/* Wait for the recorded events and copy out up to `cap` records: phase[i]
+ * is the plan phase of launch i and ms[i] its duration in milliseconds
+ * (begin-to-end event time on the launch stream).  *count receives the
+ * number of records copied.  phase or ms may be NULL. */
+ar_status ar_timer_read(ar_timer* timer, int64_t cap, int64_t* count,
+                        int32_t* phase, float* ms);
+ar_status ar_timer_destroy(ar_timer* timer);        /* NULL is a no-op */
+
+/* -------------------------------------------------------------- errors */
+
+const char* ar_status_string(ar_status s);  /* static string, never NULL   */
+const char* ar_last_error(void);            /* "" when there is none       */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AR_PLAN_H */

@@ -1,0 +1,72 @@
+"""Build the HIP library ``lib/libarplan.so`` for gfx950 with hipcc.
+
+Run ``python -m paper_2409_04202_amd.build`` (or ``__graft_entry__.build()``).
+Host-only translation units are compiled with the host compiler, the HIP
+translation unit with ``hipcc --offload-arch=gfx950``, and hipcc links the
+shared library.  Always recompiles.
+"""
+
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(PKG, "csrc")
+LIBDIR = os.path.join(PKG, "lib")
+LIB = os.path.join(LIBDIR, "libarplan.so")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+
+HOST_SRCS = ["plan.cpp", "capi.cpp"]
+HIP_SRCS = ["exec.hip"]
+
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
+          "-Wextra", "-Wno-unused-parameter"]
+# fp32 adds must round exactly as written: no contraction, denormals kept,
+# and no packed-fp32 instructions.
+HIP_FLAGS = ["--offload-arch=gfx950", "-ffp-contract=off",
+             "-fno-gpu-flush-denormals-to-zero",
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
+                       text=True)
+    out = "\n".join(l for l in r.stdout.splitlines()
+                    if "packed-fp32-ops" not in l)
+    if r.returncode != 0:
+        raise RuntimeError("build failed: %s\n%s" % (" ".join(cmd), r.stdout))
+    if verbose and out.strip():
+        print(out)
+
+
+def build(verbose=False):
+    hipcc = os.environ.get("HIPCC", os.path.join(ROCM, "bin", "hipcc"))
+    cxx = os.environ.get("CXX", "g++")
+    os.makedirs(LIBDIR, exist_ok=True)
+    tmp = tempfile.mkdtemp(prefix="arplan_build_")
+    try:
+        objs = []
+        for s in HOST_SRCS:
+            o = os.path.join(tmp, s + ".o")
+            _run([cxx, "-c", os.path.join(CSRC, s), "-o", o] + COMMON, verbose)
+            objs.append(o)
+        for s in HIP_SRCS:
+            o = os.path.join(tmp, s + ".o")
+            _run([hipcc, "-c", "-x", "hip", os.path.join(CSRC, s), "-o", o]
+                 + COMMON + HIP_FLAGS, verbose)
+            objs.append(o)
+        tmp_lib = os.path.join(tmp, "libarplan.so")
+        _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o",
+              tmp_lib] + objs, verbose)
+        shutil.move(tmp_lib, LIB)   # atomic replace of the loaded file
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

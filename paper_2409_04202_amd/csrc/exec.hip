@@ -1,0 +1,592 @@
+// Executor: turns a plan's phases into batched kernel launches on a HIP
+// stream, plus the timing API.
+//
+// Per phase, the steps are grouped by source count k (copies are k = 1) and
+// each group becomes one launch of phase_kernel<dtype, k, aligned>; the
+// built-in plans have one group per phase.  The step tables are uploaded to
+// the device on the first execute on a device; the n buffer pointers go
+// through a small per-plan cache of device pointer tables, so repeated
+// executes on the same buffers launch kernels only.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "internal.hpp"
+#include "kernels.hpp"
+
+namespace arp {
+
+namespace {
+
+constexpr int kCache = 4;               // pointer tables kept per device
+constexpr int64_t kTargetUnits = 16384; // wave tiles per launch to aim for
+constexpr int64_t kMaxBlocks = int64_t(1) << 24;
+
+struct LaunchDesc {
+    int32_t phase;
+    int32_t kern_k;          // template K (0 = runtime source count)
+    int64_t first;           // first entry of the device step table
+    int64_t count;           // steps in this launch
+    int64_t tile_elems;
+    int64_t tiles_per_step;  // arithmetic mapping
+    int64_t nunits;          // wave tiles
+    int64_t tile_off;        // -1, or first entry of the device tile table
+};
+
+struct PtrEntry {
+    std::vector<void*> key;
+    void** dev = nullptr;
+    void** pinned = nullptr;
+    hipEvent_t done = nullptr;
+    uint64_t stamp = 0;
+    bool valid = false;
+    bool aligned = false;
+};
+
+struct DevState {
+    int device = -1;
+    DevStep* steps = nullptr;
+    int32_t* srcs = nullptr;
+    int2* tiles = nullptr;
+    PtrEntry cache[kCache];
+    uint64_t clock = 0;
+};
+
+int kernel_k(int32_t k) {
+    switch (k) {
+        case 1: case 2: case 3: case 4: case 8: case 16: return k;
+        default: return 0;
+    }
+}
+
+int host_unroll(int K) {
+    switch (K) {
+        case 0: return Unroll<0>::U;
+        case 1: return Unroll<1>::U;
+        case 2: return Unroll<2>::U;
+        case 3: return Unroll<3>::U;
+        case 4: return Unroll<4>::U;
+        case 8: return Unroll<8>::U;
+        case 16: return Unroll<16>::U;
+        default: return 1;
+    }
+}
+
+std::string hip_msg(const char* what, hipError_t e) {
+    return std::string(what) + ": " + hipGetErrorName(e) + " (" +
+           hipGetErrorString(e) + ")";
+}
+
+}  // namespace
+
+struct ExecState {
+    std::vector<LaunchDesc> launches;
+    std::vector<DevStep> hsteps;
+    std::vector<int32_t> hsrcs;
+    std::vector<int2> htiles;
+    std::vector<DevState*> dev;  // indexed by device ordinal
+};
+
+// Group the steps of every phase by source count and choose the tiling of
+// each launch.  Host only.
+static void build_launches(const Plan& p, ExecState& ex) {
+    const int64_t VEC = 16 / p.esize;
+    for (int32_t ph = 0; ph < p.num_phases(); ++ph) {
+        const int64_t s0 = p.phase_first[size_t(ph)];
+        const int64_t s1 = p.phase_first[size_t(ph) + 1];
+        std::vector<int64_t> idx;
+        for (int64_t i = s0; i < s1; ++i) idx.push_back(i);
+        auto kof = [&](int64_t i) {
+            const Step& s = p.steps[size_t(i)];
+            return s.op == OP_COPY ? 1 : s.nsrc;
+        };
+        std::stable_sort(idx.begin(), idx.end(),
+                         [&](int64_t a, int64_t b) { return kof(a) < kof(b); });
+        size_t g0 = 0;
+        while (g0 < idx.size()) {
+            size_t g1 = g0;
+            const int32_t k = kof(idx[g0]);
+            while (g1 < idx.size() && kof(idx[g1]) == k) ++g1;
+            LaunchDesc L{};
+            L.phase = ph;
+            L.kern_k = kernel_k(k);
+            L.first = int64_t(ex.hsteps.size());
+            L.count = int64_t(g1 - g0);
+            int64_t maxspan = 0;
+            std::vector<int64_t> spans;
+            for (size_t g = g0; g < g1; ++g) {
+                const Step& s = p.steps[size_t(idx[g])];
+                DevStep d{};
+                d.begin = s.begin;
+                d.end = s.end;
+                d.dst = s.dst;
+                d.src_off = int32_t(ex.hsrcs.size());
+                d.k = k;
+                for (int32_t t = 0; t < s.nsrc; ++t)
+                    ex.hsrcs.push_back(p.srcs[size_t(s.src_off + t)]);
+                ex.hsteps.push_back(d);
+                const int64_t span =
+                    s.end > s.begin ? s.end - (s.begin & ~(VEC - 1)) : 0;
+                spans.push_back(span);
+                maxspan = std::max(maxspan, span);
+            }
+            if (maxspan == 0) {  // nothing to move in this group
+                g0 = g1;
+                continue;
+            }
+            const int64_t iter = 64 * VEC * host_unroll(L.kern_k);
+            int64_t te = iter;
+            auto units_for = [&](int64_t t) {
+                return L.count * ((maxspan + t - 1) / t);
+            };
+            while (te < 64 * iter && units_for(te) > kTargetUnits) te *= 2;
+            while ((units_for(te) + kWavesPerBlock - 1) / kWavesPerBlock > kMaxBlocks)
+                te *= 2;
+            L.tile_elems = te;
+            L.tiles_per_step = (maxspan + te - 1) / te;
+            int64_t used = 0;
+            for (int64_t sp : spans) used += (sp + te - 1) / te;
+            if (used * 5 < L.count * L.tiles_per_step * 4) {
+                // uneven steps: explicit tile table
+                L.tile_off = int64_t(ex.htiles.size());
+                for (int64_t j = 0; j < L.count; ++j) {
+                    const int64_t nt = (spans[size_t(j)] + te - 1) / te;
+                    for (int64_t t = 0; t < nt; ++t)
+                        ex.htiles.push_back(make_int2(int(j), int(t)));
+                }
+                L.nunits = used;
+            } else {
+                L.tile_off = -1;
+                L.nunits = L.count * L.tiles_per_step;
+            }
+            ex.launches.push_back(L);
+            g0 = g1;
+        }
+    }
+}
+
+static ExecState* exec_state(Plan& p) {
+    if (!p.exec) {
+        ExecState* ex = new ExecState();
+        try {
+            build_launches(p, *ex);
+        } catch (...) {
+            delete ex;
+            throw;
+        }
+        p.exec = ex;
+    }
+    return p.exec;
+}
+
+static void free_dev(DevState* d) {
+    if (!d) return;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(d->device);
+    if (d->steps) (void)hipFree(d->steps);
+    if (d->srcs) (void)hipFree(d->srcs);
+    if (d->tiles) (void)hipFree(d->tiles);
+    for (PtrEntry& e : d->cache) {
+        if (e.done) {
+            (void)hipEventSynchronize(e.done);
+            (void)hipEventDestroy(e.done);
+        }
+        if (e.dev) (void)hipFree(e.dev);
+        if (e.pinned) (void)hipHostFree(e.pinned);
+    }
+    if (cur >= 0) (void)hipSetDevice(cur);
+    delete d;
+}
+
+void exec_release(Plan& p) {
+    if (!p.exec) return;
+    for (DevState* d : p.exec->dev) free_dev(d);
+    delete p.exec;
+    p.exec = nullptr;
+}
+
+template <class T>
+static ar_status upload(T** dst, const std::vector<T>& src, const char* what) {
+    if (src.empty()) return AR_OK;
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(dst), src.size() * sizeof(T));
+    if (e != hipSuccess) {
+        *dst = nullptr;
+        (void)hipGetLastError();
+        return fail(e == hipErrorOutOfMemory ? AR_ERR_OOM : AR_ERR_HIP,
+                    hip_msg(what, e));
+    }
+    e = hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg(what, e));
+    return AR_OK;
+}
+
+static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipGetDevice", e));
+    if (dev < 0) return fail(AR_ERR_HIP, "no current device");
+    if (size_t(dev) >= ex.dev.size()) ex.dev.resize(size_t(dev) + 1, nullptr);
+    if (!ex.dev[size_t(dev)]) {
+        DevState* d = new DevState();
+        d->device = dev;
+        ar_status s = upload(&d->steps, ex.hsteps, "step table");
+        if (s == AR_OK) s = upload(&d->srcs, ex.hsrcs, "source table");
+        if (s == AR_OK) s = upload(&d->tiles, ex.htiles, "tile table");
+        if (s != AR_OK) {
+            free_dev(d);
+            return s;
+        }
+        ex.dev[size_t(dev)] = d;
+    }
+    *out = ex.dev[size_t(dev)];
+    (void)p;
+    return AR_OK;
+}
+
+// Host-side checks of the buffer set: non-NULL and pairwise disjoint.
+static ar_status check_buffers(const Plan& p, const std::vector<void*>& bufs) {
+    const uint64_t bytes = uint64_t(p.N) * uint64_t(p.esize);
+    std::vector<std::pair<uint64_t, int32_t>> a;
+    a.reserve(bufs.size());
+    for (size_t i = 0; i < bufs.size(); ++i) {
+        if (!bufs[i])
+            return fail(AR_ERR_INVALID_ARG, "buffer " + std::to_string(i) + " is NULL");
+        a.emplace_back(reinterpret_cast<uint64_t>(bufs[i]), int32_t(i));
+    }
+    std::sort(a.begin(), a.end());
+    for (size_t i = 1; i < a.size(); ++i)
+        if (a[i].first < a[i - 1].first + bytes)
+            return fail(AR_ERR_INVALID_ARG,
+                        "buffers " + std::to_string(a[i - 1].second) + " and " +
+                            std::to_string(a[i].second) + " overlap");
+    return AR_OK;
+}
+
+static ar_status pointer_table(const Plan& p, DevState& d,
+                               const std::vector<void*>& bufs,
+                               hipStream_t stream, PtrEntry** out) {
+    ++d.clock;
+    for (PtrEntry& e : d.cache)
+        if (e.valid && e.key == bufs) {
+            e.stamp = d.clock;
+            *out = &e;
+            return AR_OK;
+        }
+    ar_status s = check_buffers(p, bufs);
+    if (s != AR_OK) return s;
+    PtrEntry* v = &d.cache[0];
+    for (PtrEntry& e : d.cache) {
+        if (!e.valid) { v = &e; break; }
+        if (e.stamp < v->stamp) v = &e;
+    }
+    const size_t nb = bufs.size() * sizeof(void*);
+    hipError_t e = hipSuccess;
+    if (!v->dev) {
+        e = hipMalloc(reinterpret_cast<void**>(&v->dev), nb);
+        if (e != hipSuccess) {
+            v->dev = nullptr;
+            return fail(AR_ERR_OOM, hip_msg("pointer table", e));
+        }
+        e = hipHostMalloc(reinterpret_cast<void**>(&v->pinned), nb, hipHostMallocDefault);
+        if (e != hipSuccess) {
+            v->pinned = nullptr;
+            return fail(AR_ERR_OOM, hip_msg("pointer staging", e));
+        }
+        e = hipEventCreateWithFlags(&v->done, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            v->done = nullptr;
+            return fail(AR_ERR_HIP, hip_msg("hipEventCreate", e));
+        }
+    } else {
+        // the previous upload from the staging buffer must have finished
+        e = hipEventSynchronize(v->done);
+        if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventSynchronize", e));
+    }
+    v->valid = false;
+    std::memcpy(v->pinned, bufs.data(), nb);
+    e = hipMemcpyAsync(v->dev, v->pinned, nb, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("pointer upload", e));
+    e = hipEventRecord(v->done, stream);
+    if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", e));
+    v->key = bufs;
+    v->valid = true;
+    v->stamp = d.clock;
+    v->aligned = true;
+    for (void* b : bufs)
+        if (reinterpret_cast<uint64_t>(b) & 15) v->aligned = false;
+    *out = v;
+    return AR_OK;
+}
+
+template <int DT, int K>
+static void launch_dk(bool vecok, int64_t blocks, hipStream_t st, const DevStep* steps,
+                      const int32_t* srcs, void* const* ptrs, const int2* tiles,
+                      int64_t nunits, int64_t tps, int64_t te) {
+    const dim3 grid(static_cast<uint32_t>(blocks)), block(kBlockThreads);
+    if (vecok)
+        hipLaunchKernelGGL((phase_kernel<DT, K, true>), grid, block, 0, st, steps,
+                           srcs, ptrs, tiles, nunits, tps, te);
+    else
+        hipLaunchKernelGGL((phase_kernel<DT, K, false>), grid, block, 0, st, steps,
+                           srcs, ptrs, tiles, nunits, tps, te);
+}
+
+template <int DT>
+static void launch_d(int K, bool vecok, int64_t blocks, hipStream_t st,
+                     const DevStep* steps, const int32_t* srcs, void* const* ptrs,
+                     const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
+    switch (K) {
+        case 1: launch_dk<DT, 1>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 2: launch_dk<DT, 2>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 3: launch_dk<DT, 3>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 4: launch_dk<DT, 4>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 8: launch_dk<DT, 8>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 16: launch_dk<DT, 16>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        default: launch_dk<DT, 0>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+    }
+}
+
+}  // namespace arp
+
+struct ar_timer {
+    int64_t cap = 0;
+    int64_t count = 0;
+    std::vector<hipEvent_t> ev;  // 2 per record, created lazily
+    std::vector<int32_t> phase;
+};
+
+using namespace arp;
+
+static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
+                     hipStream_t stream, ar_timer* timer) {
+    try {
+        if (plan->N == 0 || plan->num_phases() == 0) return AR_OK;
+        ExecState* ex = exec_state(*plan);
+        if (ex->launches.empty()) return AR_OK;
+        if (timer && timer->count + int64_t(ex->launches.size()) > timer->cap)
+            return fail(AR_ERR_INVALID_ARG, "timer is full");
+        DevState* d = nullptr;
+        ar_status s = device_state(*plan, *ex, &d);
+        if (s != AR_OK) return s;
+        PtrEntry* pe = nullptr;
+        s = pointer_table(*plan, *d, bufs, stream, &pe);
+        if (s != AR_OK) return s;
+        for (const LaunchDesc& L : ex->launches) {
+            const int64_t blocks = (L.nunits + kWavesPerBlock - 1) / kWavesPerBlock;
+            hipEvent_t e0 = nullptr, e1 = nullptr;
+            if (timer) {
+                const int64_t r = timer->count;
+                for (int j = 0; j < 2; ++j) {
+                    hipEvent_t& ev = timer->ev[size_t(2 * r + j)];
+                    if (!ev) {
+                        hipError_t he = hipEventCreate(&ev);
+                        if (he != hipSuccess) {
+                            ev = nullptr;
+                            return fail(AR_ERR_HIP, hip_msg("hipEventCreate", he));
+                        }
+                    }
+                }
+                e0 = timer->ev[size_t(2 * r)];
+                e1 = timer->ev[size_t(2 * r + 1)];
+                hipError_t he = hipEventRecord(e0, stream);
+                if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", he));
+            }
+            const DevStep* steps = d->steps + L.first;
+            const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
+            switch (plan->dtype) {
+                case AR_F32:
+                    launch_d<DT_F32>(L.kern_k, pe->aligned, blocks, stream, steps, d->srcs,
+                                     pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                    break;
+                case AR_I32:
+                    launch_d<DT_I32>(L.kern_k, pe->aligned, blocks, stream, steps, d->srcs,
+                                     pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                    break;
+                default:
+                    launch_d<DT_BF16>(L.kern_k, pe->aligned, blocks, stream, steps, d->srcs,
+                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                    break;
+            }
+            hipError_t he = hipGetLastError();
+            if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("kernel launch", he));
+            if (timer) {
+                he = hipEventRecord(e1, stream);
+                if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", he));
+                timer->phase[size_t(timer->count)] = L.phase;
+                ++timer->count;
+            }
+        }
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}
+
+AR_EXPORT ar_status ar_plan_execute(ar_plan* plan, void* const* bufs, void* stream) {
+    clear_error();
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    if (!bufs) return fail(AR_ERR_INVALID_ARG, "bufs is NULL");
+    return run(plan, std::vector<void*>(bufs, bufs + plan->n),
+               static_cast<hipStream_t>(stream), nullptr);
+}
+
+AR_EXPORT ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs, void* stream,
+                                          ar_timer* timer) {
+    clear_error();
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    if (!bufs) return fail(AR_ERR_INVALID_ARG, "bufs is NULL");
+    if (!timer) return fail(AR_ERR_INVALID_ARG, "timer is NULL");
+    return run(plan, std::vector<void*>(bufs, bufs + plan->n),
+               static_cast<hipStream_t>(stream), timer);
+}
+
+AR_EXPORT ar_status ar_plan_execute_strided(ar_plan* plan, void* base, int64_t stride_bytes,
+                                            void* stream) {
+    clear_error();
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    if (!base) return fail(AR_ERR_INVALID_ARG, "base is NULL");
+    if (stride_bytes < plan->N * plan->esize)
+        return fail(AR_ERR_INVALID_ARG, "stride_bytes < N * element size");
+    std::vector<void*> bufs(size_t(plan->n));
+    for (int32_t i = 0; i < plan->n; ++i)
+        bufs[size_t(i)] = static_cast<char*>(base) + int64_t(i) * stride_bytes;
+    return run(plan, bufs, static_cast<hipStream_t>(stream), nullptr);
+}
+
+AR_EXPORT ar_status ar_timer_create(int64_t capacity, ar_timer** out) {
+    clear_error();
+    if (!out) return fail(AR_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (capacity < 1 || capacity > (int64_t(1) << 24))
+        return fail(AR_ERR_INVALID_ARG, "capacity must be in [1, 2^24]");
+    try {
+        ar_timer* t = new ar_timer();
+        t->cap = capacity;
+        t->ev.assign(size_t(2 * capacity), nullptr);
+        t->phase.assign(size_t(capacity), -1);
+        *out = t;
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    }
+}
+
+AR_EXPORT ar_status ar_timer_reset(ar_timer* timer) {
+    clear_error();
+    if (!timer) return fail(AR_ERR_INVALID_ARG, "timer is NULL");
+    timer->count = 0;
+    return AR_OK;
+}
+
+AR_EXPORT ar_status ar_timer_read(ar_timer* timer, int64_t cap, int64_t* count,
+                                  int32_t* phase, float* ms) {
+    clear_error();
+    if (!timer || !count) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    if (cap < 0) return fail(AR_ERR_INVALID_ARG, "cap < 0");
+    const int64_t m = std::min(cap, timer->count);
+    for (int64_t i = 0; i < m; ++i) {
+        if (ms) {
+            hipError_t e = hipEventSynchronize(timer->ev[size_t(2 * i + 1)]);
+            if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventSynchronize", e));
+            float t = 0.f;
+            e = hipEventElapsedTime(&t, timer->ev[size_t(2 * i)], timer->ev[size_t(2 * i + 1)]);
+            if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventElapsedTime", e));
+            ms[i] = t;
+        }
+        if (phase) phase[i] = timer->phase[size_t(i)];
+    }
+    *count = m;
+    return AR_OK;
+}
+
+AR_EXPORT ar_status ar_timer_destroy(ar_timer* timer) {
+    clear_error();
+    if (!timer) return AR_OK;
+    for (hipEvent_t e : timer->ev)
+        if (e) (void)hipEventDestroy(e);
+    delete timer;
+    return AR_OK;
+}
+
+// Host-side check of the launch tiling (no GPU): walks every wave tile of
+// every launch with the kernel's own index helpers and verifies that the
+// steps are covered exactly once, in bounds, with 16-byte aligned vector
+// parts.  Declared in csrc/ar_debug.h (test hook, not part of the ABI).
+AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
+                                          char* msg, int64_t msglen) {
+    clear_error();
+    auto bad = [&](const std::string& m) {
+        if (msg && msglen > 0) {
+            std::strncpy(msg, m.c_str(), size_t(msglen - 1));
+            msg[msglen - 1] = 0;
+        }
+        return fail(AR_ERR_INTERNAL, m);
+    };
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    try {
+        ExecState* ex = exec_state(*plan);
+        const int64_t VEC = 16 / plan->esize;
+        std::vector<std::vector<std::pair<int64_t, int64_t>>> cover(ex->hsteps.size());
+        std::vector<char> launched(ex->hsteps.size(), 0);
+        for (const LaunchDesc& L : ex->launches) {
+            if (L.nunits <= 0) return bad("launch without work units");
+            const int64_t blocks = (L.nunits + kWavesPerBlock - 1) / kWavesPerBlock;
+            if (blocks > kMaxBlocks) return bad("grid too large");
+            if (L.tile_elems % (64 * VEC) != 0) return bad("tile not a multiple of a wave vector");
+            const int2* tiles = L.tile_off >= 0 ? ex->htiles.data() + L.tile_off : nullptr;
+            if (tiles && L.tile_off + L.nunits > int64_t(ex->htiles.size()))
+                return bad("tile table overrun");
+            for (int64_t j = 0; j < L.count; ++j) launched[size_t(L.first + j)] = 1;
+            for (int64_t unit = 0; unit < blocks * kWavesPerBlock; ++unit) {
+                if (unit >= L.nunits) continue;  // the kernel returns here
+                int64_t s, t;
+                unit_tile(unit, tiles, L.tiles_per_step, s, t);
+                if (s < 0 || s >= L.count || t < 0) return bad("unit maps outside the launch");
+                const DevStep& st = ex->hsteps[size_t(L.first + s)];
+                if (st.k < 1 || st.src_off < 0 ||
+                    int64_t(st.src_off) + st.k > int64_t(ex->hsrcs.size()))
+                    return bad("source list out of range");
+                for (int32_t q = 0; q < st.k; ++q) {
+                    const int32_t src = ex->hsrcs[size_t(st.src_off + q)];
+                    if (src < 0 || src >= plan->n) return bad("source index out of range");
+                }
+                if (st.dst < 0 || st.dst >= plan->n) return bad("dst out of range");
+                const TileSpan sp = tile_span(st.begin, st.end, t, L.tile_elems, VEC, vecok != 0);
+                if (sp.lo >= sp.hi) continue;
+                if (sp.lo < st.begin || sp.hi > st.end || st.begin < 0 || st.end > plan->N)
+                    return bad("tile outside its step");
+                if (!(sp.lo <= sp.vlo && sp.vlo <= sp.vhi && sp.vhi <= sp.hi))
+                    return bad("vector part outside its tile");
+                if (sp.vhi > sp.vlo && (!vecok || sp.vlo % VEC || sp.vhi % VEC))
+                    return bad("misaligned vector part");
+                if (sp.vlo - sp.lo >= VEC || (sp.vhi > sp.vlo && sp.hi - sp.vhi >= VEC))
+                    if (sp.vhi > sp.vlo) return bad("head or tail longer than a vector");
+                cover[size_t(L.first + s)].push_back({sp.lo, sp.hi});
+            }
+        }
+        for (size_t i = 0; i < ex->hsteps.size(); ++i) {
+            const DevStep& st = ex->hsteps[i];
+            auto& c = cover[i];
+            if (st.end > st.begin && !launched[i]) return bad("step never launched");
+            std::sort(c.begin(), c.end());
+            int64_t at = st.begin;
+            for (auto& iv : c) {
+                if (iv.first != at) return bad("gap or overlap in step " + std::to_string(i));
+                at = iv.second;
+            }
+            if (st.end > st.begin && at != st.end)
+                return bad("step " + std::to_string(i) + " not covered to its end");
+        }
+        if (msg && msglen > 0) msg[0] = 0;
+        return AR_OK;
+    } catch (const std::exception& e) {
+        return bad(e.what());
+    }
+}

@@ -1,0 +1,315 @@
+// Batched phase kernel for gfx950: one launch executes every step of one
+// phase that has the same source count k (a copy is the k = 1 case).
+//
+// Work decomposition.  Each step's element range is cut into wave tiles of
+// `tile_elems` elements, aligned to 16 bytes in the buffer; a 64-lane
+// wavefront executes one tile.  A launch therefore covers all steps of the
+// phase at once, whatever their number and length.  Tile -> (step, tile in
+// step) is arithmetic when the steps are about equally long and otherwise
+// comes from a per-launch table.
+//
+// Inner loop.  Per iteration every lane moves U 16-byte vectors of each of
+// the K sources (global_load_dwordx4; the wave touches 1 KiB contiguous per
+// vector slot), folds them in source order in fp32 (bf16 widened; int32 with
+// wrap-around) and stores U vectors.  Unaligned head and tail elements of a
+// step are done element-wise.  The step descriptor, its source indices and
+// the buffer pointers are wave-uniform and live in scalar registers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace arp {
+
+enum DType : int32_t { DT_F32 = 0, DT_I32 = 1, DT_BF16 = 2 };
+
+struct DevStep {      // 32 bytes, one per step, grouped by launch
+    int64_t begin;
+    int64_t end;
+    int32_t dst;
+    int32_t src_off;  // first source in the device source pool
+    int32_t k;
+    int32_t pad;
+};
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlockThreads = 64 * kWavesPerBlock;
+
+// Vectors in flight per lane and source: about 16 loads in flight per lane.
+template <int K> struct Unroll { static constexpr int U = K >= 16 ? 1 : (K >= 8 ? 2 : (K >= 4 ? 4 : 8)); };
+template <> struct Unroll<0> { static constexpr int U = 4; };
+template <> struct Unroll<2> { static constexpr int U = 4; };
+template <> struct Unroll<3> { static constexpr int U = 4; };
+
+template <int DT> struct Elem;
+template <> struct Elem<DT_F32> { using T = float;    static constexpr int VEC = 4; };
+template <> struct Elem<DT_I32> { using T = uint32_t; static constexpr int VEC = 4; };
+template <> struct Elem<DT_BF16> { using T = uint16_t; static constexpr int VEC = 8; };
+
+// ---------------------------------------------------------------- bf16
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x0040u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// ---------------------------------------------- 16-byte vector accumulator
+
+template <int DT> struct VAcc;
+
+template <> struct VAcc<DT_F32> {
+    float v[4];
+    __device__ __forceinline__ void init(const uint4 x) {
+        v[0] = __uint_as_float(x.x); v[1] = __uint_as_float(x.y);
+        v[2] = __uint_as_float(x.z); v[3] = __uint_as_float(x.w);
+    }
+    __device__ __forceinline__ void add(const uint4 x) {
+        v[0] += __uint_as_float(x.x); v[1] += __uint_as_float(x.y);
+        v[2] += __uint_as_float(x.z); v[3] += __uint_as_float(x.w);
+    }
+    __device__ __forceinline__ uint4 out() const {
+        return make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
+                          __float_as_uint(v[2]), __float_as_uint(v[3]));
+    }
+};
+
+template <> struct VAcc<DT_I32> {
+    uint32_t v[4];
+    __device__ __forceinline__ void init(const uint4 x) { v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w; }
+    __device__ __forceinline__ void add(const uint4 x) { v[0] += x.x; v[1] += x.y; v[2] += x.z; v[3] += x.w; }
+    __device__ __forceinline__ uint4 out() const { return make_uint4(v[0], v[1], v[2], v[3]); }
+};
+
+template <> struct VAcc<DT_BF16> {
+    float v[8];
+    __device__ __forceinline__ void init(const uint4 x) {
+        v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
+        v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
+    }
+    __device__ __forceinline__ void add(const uint4 x) {
+        v[0] += bf16_lo(x.x); v[1] += bf16_hi(x.x); v[2] += bf16_lo(x.y); v[3] += bf16_hi(x.y);
+        v[4] += bf16_lo(x.z); v[5] += bf16_hi(x.z); v[6] += bf16_lo(x.w); v[7] += bf16_hi(x.w);
+    }
+    __device__ __forceinline__ uint4 out() const {
+        uint4 r;
+        r.x = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
+        r.y = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
+        r.z = f32_to_bf16_bits(v[4]) | (f32_to_bf16_bits(v[5]) << 16);
+        r.w = f32_to_bf16_bits(v[6]) | (f32_to_bf16_bits(v[7]) << 16);
+        return r;
+    }
+};
+
+// ------------------------------------------------ single-element accumulator
+
+template <int DT> struct SAcc;
+template <> struct SAcc<DT_F32> {
+    float v;
+    __device__ __forceinline__ void init(float x) { v = x; }
+    __device__ __forceinline__ void add(float x) { v += x; }
+    __device__ __forceinline__ float out() const { return v; }
+};
+template <> struct SAcc<DT_I32> {
+    uint32_t v;
+    __device__ __forceinline__ void init(uint32_t x) { v = x; }
+    __device__ __forceinline__ void add(uint32_t x) { v += x; }
+    __device__ __forceinline__ uint32_t out() const { return v; }
+};
+template <> struct SAcc<DT_BF16> {
+    float v;
+    __device__ __forceinline__ void init(uint16_t x) { v = __uint_as_float(uint32_t(x) << 16); }
+    __device__ __forceinline__ void add(uint16_t x) { v += __uint_as_float(uint32_t(x) << 16); }
+    __device__ __forceinline__ uint16_t out() const { return uint16_t(f32_to_bf16_bits(v)); }
+};
+
+// Element ranges of wave tile t of a step [begin, end): the tile is
+// [lo, hi); inside it [vlo, vhi) is done with 16-byte vectors and the head
+// [lo, vlo) and tail [vhi, hi) element-wise.  Tiles are aligned to 16 bytes
+// of the buffer (`vecok`: every buffer base is 16-byte aligned), so only the
+// first and last tile of a step have a head or tail.  Shared by the kernel
+// and the host-side tiling check.
+struct TileSpan {
+    int64_t lo, hi, vlo, vhi;
+};
+
+__host__ __device__ __forceinline__ TileSpan tile_span(int64_t begin, int64_t end,
+                                                       int64_t t, int64_t te,
+                                                       int64_t vec, bool vecok) {
+    TileSpan r;
+    const int64_t abase = vecok ? (begin & ~(vec - 1)) : begin;
+    const int64_t a = abase + t * te, b = abase + (t + 1) * te;
+    r.lo = a > begin ? a : begin;
+    r.hi = b < end ? b : end;
+    r.vlo = r.vhi = r.hi;
+    if (vecok && r.lo < r.hi) {
+        const int64_t vlo = (r.lo + vec - 1) & ~(vec - 1);
+        const int64_t vhi = r.hi & ~(vec - 1);
+        if (vhi > vlo) {
+            r.vlo = vlo;
+            r.vhi = vhi;
+        }
+    }
+    return r;
+}
+
+// Wave tile `unit` of a launch -> (step s within the launch, tile t of it):
+// from the launch's tile table when it has one, else arithmetic with a
+// fixed number of tiles per step.
+__host__ __device__ __forceinline__ void unit_tile(int64_t unit, const int2* tiles,
+                                                   int64_t tiles_per_step,
+                                                   int64_t& s, int64_t& t) {
+    if (tiles) {
+        const int2 e = tiles[unit];
+        s = e.x;
+        t = e.y;
+    } else {
+        s = unit / tiles_per_step;
+        t = unit - s * tiles_per_step;
+    }
+}
+
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(x)));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(x) >> 32));
+    return int64_t((uint64_t(hi) << 32) | lo);
+}
+
+// Fold elements [lo, hi) of `nsrc` sources into dst, one element per lane
+// per pass (used for unaligned heads/tails and for unaligned buffers).
+template <int DT, int K>
+__device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
+                                            const int32_t* __restrict__ srcl,
+                                            int k, int32_t dst, int64_t lo,
+                                            int64_t hi, int lane) {
+    using T = typename Elem<DT>::T;
+    constexpr int SU = 4;
+    T* d = static_cast<T*>(ptrs[dst]);
+    if (K == 1 || (K == 0 && k == 1)) {  // copy: move the bits unchanged
+        const T* s = static_cast<const T*>(ptrs[srcl[0]]);
+        for (int64_t e = lo + lane; e < hi; e += 64) d[e] = s[e];
+        return;
+    }
+    for (int64_t e0 = lo; e0 < hi; e0 += 64 * SU) {
+        SAcc<DT> acc[SU];
+        bool ok[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) ok[u] = e0 + u * 64 + lane < hi;
+        {
+            const T* s = static_cast<const T*>(ptrs[srcl[0]]);
+#pragma unroll
+            for (int u = 0; u < SU; ++u)
+                if (ok[u]) acc[u].init(s[e0 + u * 64 + lane]);
+        }
+        const int kk = K ? K : k;
+        for (int t = 1; t < kk; ++t) {
+            const T* s = static_cast<const T*>(ptrs[srcl[t]]);
+#pragma unroll
+            for (int u = 0; u < SU; ++u)
+                if (ok[u]) acc[u].add(s[e0 + u * 64 + lane]);
+        }
+#pragma unroll
+        for (int u = 0; u < SU; ++u)
+            if (ok[u]) d[e0 + u * 64 + lane] = acc[u].out();
+    }
+}
+
+// One launch: `nunits` wave tiles over the steps steps[0..).  K = 0 means
+// the source count is read from each step (any k >= 1).
+template <int DT, int K, bool VECOK>
+__global__ __launch_bounds__(kBlockThreads) void phase_kernel(
+    const DevStep* __restrict__ steps, const int32_t* __restrict__ srcs,
+    void* const* __restrict__ ptrs, const int2* __restrict__ tiles,
+    int64_t nunits, int64_t tiles_per_step, int64_t tile_elems) {
+    constexpr int VEC = Elem<DT>::VEC;
+    constexpr int U = Unroll<K>::U;
+    const int lane = int(threadIdx.x) & 63;
+    const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock +
+                         int64_t(__builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+    if (unit >= nunits) return;
+    int64_t s, t;
+    unit_tile(unit, tiles, tiles_per_step, s, t);
+    s = uniform64(s);
+    t = uniform64(t);
+    const DevStep st = steps[s];
+    const int k = K ? K : st.k;
+    const int32_t* srcl = srcs + st.src_off;
+
+    const TileSpan sp = tile_span(st.begin, st.end, t, tile_elems, VEC, VECOK);
+    if (sp.lo >= sp.hi) return;
+    if (sp.vlo > sp.lo) fold_scalar<DT, K>(ptrs, srcl, k, st.dst, sp.lo, sp.vlo, lane);
+    if (sp.hi > sp.vhi) fold_scalar<DT, K>(ptrs, srcl, k, st.dst, sp.vhi, sp.hi, lane);
+    if (!VECOK || sp.vhi <= sp.vlo) return;
+    const int64_t vlo = sp.vlo, vhi = sp.vhi;
+
+    const int64_t v0 = vlo / VEC;
+    const int64_t nv = (vhi - vlo) / VEC;
+    uint4* __restrict__ d = static_cast<uint4*>(ptrs[st.dst]) + v0;
+
+    if constexpr (K > 0) {
+        const uint4* sp[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) sp[j] = static_cast<const uint4*>(ptrs[srcl[j]]) + v0;
+        for (int64_t base = 0; base < nv; base += 64 * U) {
+            uint4 x[K][U];
+            bool ok[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) ok[u] = base + u * 64 + lane < nv;
+#pragma unroll
+            for (int j = 0; j < K; ++j)
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (ok[u]) x[j][u] = sp[j][base + u * 64 + lane];
+            if constexpr (K == 1) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (ok[u]) d[base + u * 64 + lane] = x[0][u];
+            } else {
+                VAcc<DT> acc[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[u].init(x[0][u]);
+#pragma unroll
+                for (int j = 1; j < K; ++j)
+#pragma unroll
+                    for (int u = 0; u < U; ++u) acc[u].add(x[j][u]);
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (ok[u]) d[base + u * 64 + lane] = acc[u].out();
+            }
+        }
+    } else {
+        for (int64_t base = 0; base < nv; base += 64 * U) {
+            bool ok[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) ok[u] = base + u * 64 + lane < nv;
+            VAcc<DT> acc[U];
+            {
+                const uint4* s0 = static_cast<const uint4*>(ptrs[srcl[0]]) + v0;
+                uint4 x[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (ok[u]) x[u] = s0[base + u * 64 + lane];
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[u].init(x[u]);
+            }
+            for (int j = 1; j < k; ++j) {
+                const uint4* sj = static_cast<const uint4*>(ptrs[srcl[j]]) + v0;
+                uint4 x[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (ok[u]) x[u] = sj[base + u * 64 + lane];
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[u].add(x[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (ok[u]) d[base + u * 64 + lane] = acc[u].out();
+        }
+    }
+}
+
+}  // namespace arp

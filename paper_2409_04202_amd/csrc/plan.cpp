@@ -1,0 +1,283 @@
+// Plan expanders and the phase hazard check (host only, no HIP).
+//
+// Plan definitions follow Section 2.1 (Ring, RHD, co-located PS,
+// Reduce-Broadcast), Section 3.3 (hierarchical co-located PS) and the
+// bottom-up block placement of Algorithm 1; the exact rules are stated
+// with each kind in include/ar_plan.h.
+#include "plan.hpp"
+
+#include <algorithm>
+#include <stdexcept>
+
+namespace arp {
+
+void Plan::add(int32_t phase, int32_t op, int32_t dst,
+               const std::vector<int32_t>& s, int64_t b, int64_t e) {
+    Step st;
+    st.phase = phase;
+    st.op = op;
+    st.dst = dst;
+    st.nsrc = int32_t(s.size());
+    st.src_off = int64_t(srcs.size());
+    st.begin = b;
+    st.end = e;
+    srcs.insert(srcs.end(), s.begin(), s.end());
+    steps.push_back(st);
+}
+
+void Plan::finish_phases() {
+    phase_first.clear();
+    int32_t nph = steps.empty() ? 0 : steps.back().phase + 1;
+    phase_first.assign(size_t(nph) + 1, int64_t(steps.size()));
+    for (int64_t i = int64_t(steps.size()) - 1; i >= 0; --i)
+        phase_first[size_t(steps[size_t(i)].phase)] = i;
+    for (int32_t ph = nph - 1; ph >= 0; --ph)  // phases without steps
+        if (phase_first[size_t(ph)] > phase_first[size_t(ph) + 1])
+            phase_first[size_t(ph)] = phase_first[size_t(ph) + 1];
+}
+
+static inline int32_t pmod(int64_t a, int32_t n) {
+    int64_t r = a % n;
+    return int32_t(r < 0 ? r + n : r);
+}
+
+// Ring: in step j processor i receives block (i - j) mod n from i - 1.
+void expand_ring(Plan& p) {
+    const int32_t n = p.n;
+    const int64_t N = p.N;
+    p.owner_begin.assign(size_t(n), 0);
+    p.owner_end.assign(size_t(n), N);
+    if (n == 1) { p.finish_phases(); return; }
+    for (int32_t j = 0; j < 2 * (n - 1); ++j) {
+        for (int32_t i = 0; i < n; ++i) {
+            const int32_t b = pmod(int64_t(i) - j, n);
+            const int32_t left = pmod(int64_t(i) - 1, n);
+            const int64_t lo = block_off(N, n, b), hi = block_off(N, n, b + 1);
+            if (j < n - 1)
+                p.add(j, OP_REDUCE, i, {i, left}, lo, hi);
+            else
+                p.add(j, OP_COPY, i, {left}, lo, hi);
+        }
+    }
+    for (int32_t i = 0; i < n; ++i) {  // block reduced in step n - 2
+        const int32_t b = pmod(int64_t(i) + 2, n);
+        p.owner_begin[size_t(i)] = block_off(N, n, b);
+        p.owner_end[size_t(i)] = block_off(N, n, b + 1);
+    }
+    p.finish_phases();
+}
+
+// Recursive halving-doubling, nearest partner (r XOR 1) first; r keeps the
+// lower half when bit j of r is 0.
+void expand_rhd(Plan& p) {
+    const int32_t n = p.n;
+    const int64_t N = p.N;
+    if (n & (n - 1))
+        throw Unsupported("RHD needs a power-of-two processor count");
+    int32_t k = 0;
+    while ((1 << k) < n) ++k;
+    std::vector<std::pair<int32_t, int32_t>> held(size_t(n), {0, n});
+    std::vector<std::vector<std::pair<int32_t, int32_t>>> kept;
+    for (int32_t j = 0; j < k; ++j) {
+        std::vector<std::pair<int32_t, int32_t>> nk(static_cast<size_t>(n));
+        for (int32_t r = 0; r < n; ++r) {
+            const auto [lo, hi] = held[size_t(r)];
+            const int32_t mid = (lo + hi) / 2;
+            nk[size_t(r)] = ((r >> j) & 1) ? std::make_pair(mid, hi)
+                                           : std::make_pair(lo, mid);
+            const int32_t q = r ^ (1 << j);
+            p.add(j, OP_REDUCE, r, {std::min(r, q), std::max(r, q)},
+                  block_off(N, n, nk[size_t(r)].first),
+                  block_off(N, n, nk[size_t(r)].second));
+        }
+        held = nk;
+        kept.push_back(nk);
+    }
+    for (int32_t jj = 0; jj < k; ++jj) {
+        const int32_t j = k - 1 - jj;
+        for (int32_t r = 0; r < n; ++r) {
+            const int32_t q = r ^ (1 << j);
+            const auto [lo, hi] = kept[size_t(j)][size_t(q)];
+            p.add(k + jj, OP_COPY, r, {q}, block_off(N, n, lo),
+                  block_off(N, n, hi));
+        }
+    }
+    p.owner_begin.resize(size_t(n));
+    p.owner_end.resize(size_t(n));
+    for (int32_t r = 0; r < n; ++r) {
+        p.owner_begin[size_t(r)] = block_off(N, n, held[size_t(r)].first);
+        p.owner_end[size_t(r)] = block_off(N, n, held[size_t(r)].second);
+    }
+    p.finish_phases();
+}
+
+// Co-located PS: one n-way reduce per block, then n - 1 copies per block.
+void expand_cps(Plan& p) {
+    const int32_t n = p.n;
+    const int64_t N = p.N;
+    p.owner_begin.resize(size_t(n));
+    p.owner_end.resize(size_t(n));
+    for (int32_t r = 0; r < n; ++r) {
+        p.owner_begin[size_t(r)] = block_off(N, n, r);
+        p.owner_end[size_t(r)] = block_off(N, n, r + 1);
+    }
+    if (n == 1) { p.finish_phases(); return; }
+    std::vector<int32_t> all(static_cast<size_t>(n));
+    for (int32_t r = 0; r < n; ++r) all[size_t(r)] = r;
+    for (int32_t r = 0; r < n; ++r)
+        p.add(0, OP_REDUCE, r, all, block_off(N, n, r), block_off(N, n, r + 1));
+    for (int32_t r = 0; r < n; ++r)
+        for (int32_t q = 0; q < n; ++q)
+            if (q != r)
+                p.add(1, OP_COPY, r, {q}, block_off(N, n, q),
+                      block_off(N, n, q + 1));
+    p.finish_phases();
+}
+
+// Hierarchical co-located PS over fan-ins f_0 (innermost) .. f_{m-1}.
+void expand_tree(Plan& p) {
+    const int32_t n = p.n;
+    const int64_t N = p.N;
+    const int32_t m = int32_t(p.fanin.size());
+    std::vector<int64_t> stride(static_cast<size_t>(m)), prod(static_cast<size_t>(m));
+    int64_t s = 1;
+    for (int32_t l = 0; l < m; ++l) {
+        stride[size_t(l)] = s;
+        s *= p.fanin[size_t(l)];
+        prod[size_t(l)] = s;
+    }
+    if (s != n) throw std::invalid_argument("product of fan-ins != n");
+    auto digit = [&](int32_t r, int32_t l) {
+        return int32_t((r / stride[size_t(l)]) % p.fanin[size_t(l)]);
+    };
+    // own_lo[l][r]: first block owned by r after level l (width n / prod[l])
+    std::vector<std::vector<int64_t>> own_lo(static_cast<size_t>(m),
+                                             std::vector<int64_t>(static_cast<size_t>(n)));
+    std::vector<int64_t> o(size_t(n), 0);
+    for (int32_t l = 0; l < m; ++l) {
+        const int64_t width = n / prod[size_t(l)];
+        for (int32_t r = 0; r < n; ++r) {
+            o[size_t(r)] = o[size_t(r)] * p.fanin[size_t(l)] + digit(r, l);
+            own_lo[size_t(l)][size_t(r)] = o[size_t(r)] * width;
+        }
+    }
+    auto group = [&](int32_t r, int32_t l) {
+        std::vector<int32_t> g(static_cast<size_t>(p.fanin[size_t(l)]));
+        const int32_t d = digit(r, l);
+        for (int32_t a = 0; a < p.fanin[size_t(l)]; ++a)
+            g[size_t(a)] = int32_t(r + (int64_t(a) - d) * stride[size_t(l)]);
+        return g;
+    };
+    auto range = [&](int32_t l, int32_t r) {
+        const int64_t width = n / prod[size_t(l)];
+        const int64_t lo = own_lo[size_t(l)][size_t(r)];
+        return std::make_pair(block_off(N, n, lo), block_off(N, n, lo + width));
+    };
+    int32_t ph = 0;
+    for (int32_t l = 0; l < m; ++l) {
+        if (p.fanin[size_t(l)] == 1) continue;
+        for (int32_t r = 0; r < n; ++r) {
+            const auto [b, e] = range(l, r);
+            p.add(ph, OP_REDUCE, r, group(r, l), b, e);
+        }
+        ++ph;
+    }
+    for (int32_t l = m - 1; l >= 0; --l) {
+        if (p.fanin[size_t(l)] == 1) continue;
+        for (int32_t r = 0; r < n; ++r) {
+            for (int32_t q : group(r, l)) {
+                if (q == r) continue;
+                const auto [b, e] = range(l, q);
+                p.add(ph, OP_COPY, r, {q}, b, e);
+            }
+        }
+        ++ph;
+    }
+    p.owner_begin.resize(size_t(n));
+    p.owner_end.resize(size_t(n));
+    for (int32_t r = 0; r < n; ++r) {
+        if (m == 0) {
+            p.owner_begin[size_t(r)] = 0;
+            p.owner_end[size_t(r)] = N;
+        } else {
+            const auto [b, e] = range(m - 1, r);
+            p.owner_begin[size_t(r)] = b;
+            p.owner_end[size_t(r)] = e;
+        }
+    }
+    p.finish_phases();
+}
+
+// Reduce-Broadcast: rank 0 reduces everything, then everyone copies it.
+void expand_rb(Plan& p) {
+    const int32_t n = p.n;
+    const int64_t N = p.N;
+    p.owner_begin.assign(size_t(n), 0);
+    p.owner_end.assign(size_t(n), 0);
+    p.owner_end[0] = N;
+    if (n == 1) { p.finish_phases(); return; }
+    std::vector<int32_t> all(static_cast<size_t>(n));
+    for (int32_t r = 0; r < n; ++r) all[size_t(r)] = r;
+    p.add(0, OP_REDUCE, 0, all, 0, N);
+    for (int32_t r = 1; r < n; ++r) p.add(1, OP_COPY, r, {0}, 0, N);
+    p.finish_phases();
+}
+
+int64_t step_bytes(const Plan& p, const Step& s) {
+    const int64_t len = s.end - s.begin;
+    const int64_t k = s.op == OP_COPY ? 1 : s.nsrc;
+    return (k + 1) * len * p.esize;
+}
+
+namespace {
+struct Iv {
+    int32_t buf;
+    int64_t b, e;
+    int64_t step;
+};
+}  // namespace
+
+void validate_phases(const Plan& p) {
+    for (int32_t ph = 0; ph < p.num_phases(); ++ph) {
+        const int64_t s0 = p.phase_first[size_t(ph)];
+        const int64_t s1 = p.phase_first[size_t(ph) + 1];
+        std::vector<Iv> w;
+        w.reserve(size_t(s1 - s0));
+        for (int64_t i = s0; i < s1; ++i) {
+            const Step& st = p.steps[size_t(i)];
+            if (st.end > st.begin) w.push_back({st.dst, st.begin, st.end, i});
+        }
+        std::sort(w.begin(), w.end(), [](const Iv& a, const Iv& b) {
+            return a.buf != b.buf ? a.buf < b.buf : a.b < b.b;
+        });
+        for (size_t i = 1; i < w.size(); ++i)
+            if (w[i].buf == w[i - 1].buf && w[i].b < w[i - 1].e)
+                throw std::invalid_argument(
+                    "phase " + std::to_string(ph) + ": steps " +
+                    std::to_string(w[i - 1].step) + " and " +
+                    std::to_string(w[i].step) + " write overlapping ranges");
+        // reads must not overlap another step's write
+        for (int64_t i = s0; i < s1; ++i) {
+            const Step& st = p.steps[size_t(i)];
+            if (st.end <= st.begin) continue;
+            for (int32_t t = 0; t < st.nsrc; ++t) {
+                const int32_t buf = p.srcs[size_t(st.src_off + t)];
+                // first write on `buf` whose end is past st.begin
+                auto it = std::lower_bound(
+                    w.begin(), w.end(), std::make_pair(buf, st.begin),
+                    [](const Iv& a, const std::pair<int32_t, int64_t>& key) {
+                        return a.buf != key.first ? a.buf < key.first
+                                                  : a.e <= key.second;
+                    });
+                for (; it != w.end() && it->buf == buf && it->b < st.end; ++it)
+                    if (it->step != i)
+                        throw std::invalid_argument(
+                            "phase " + std::to_string(ph) + ": step " +
+                            std::to_string(i) + " reads a range that step " +
+                            std::to_string(it->step) + " writes");
+            }
+        }
+    }
+}
+
+}  // namespace arp

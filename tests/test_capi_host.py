@@ -1,0 +1,261 @@
+"""Host-side tests of the C-ABI library (no GPU needed).
+
+The library loads, exports every function include/ar_plan.h declares, and
+its plan expansion (steps, owners, byte counts) equals the oracle's
+independent expansion; bad arguments and hazardous custom plans are
+rejected with the documented status codes.  No compute call is made.
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import model
+
+arplan = pytest.importorskip(
+    "paper_2409_04202_amd.arplan",
+    reason="HIP library not built (run python -m paper_2409_04202_amd.build)")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ar_plan.h")
+
+
+def test_library_exports_every_declared_function():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(ar_[a-z_]+)\s*\(", text))
+    assert declared, "no declarations found"
+    lib = ctypes.CDLL(arplan.LIB_PATH)
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert declared == set(arplan.EXPORTED)
+
+
+def _norm(phases):
+    return [sorted((op, dst, tuple(srcs), b, e) for op, dst, srcs, b, e in ph)
+            for ph in phases]
+
+
+def _oracle_phases(p):
+    return [[(s.op, s.dst, tuple(s.srcs), s.begin, s.end) for s in ph]
+            for ph in p.phases]
+
+
+CASES = []
+for _n in (1, 2, 3, 4, 5, 7, 8, 12, 16):
+    for _N in sorted({0, 1, _n - 1, _n, 2 * _n + 3, 1000}):
+        CASES.append(("ring", _n, _N, None))
+        CASES.append(("cps", _n, _N, None))
+        CASES.append(("rb", _n, _N, None))
+        if _n & (_n - 1) == 0:
+            CASES.append(("rhd", _n, _N, None))
+for _fan in ((2, 2), (3, 2), (2, 3), (4, 4), (2, 3, 2), (8, 8), (2, 2, 2, 2),
+             (1, 4), (4, 1, 2)):
+    for _N in (0, 5, 64, 1001):
+        CASES.append(("tree", int(np.prod(_fan)), _N, _fan))
+
+
+@pytest.mark.parametrize("kind,n,N,fan", CASES)
+def test_steps_match_oracle(kind, n, N, fan):
+    ref = oracle.make_plan(kind, n, N, fan)
+    with arplan.Plan(n, N, "f32", kind, fan) as p:
+        assert p.num_phases == len(ref.phases)
+        assert _norm(p.phases()) == _norm(_oracle_phases(ref))
+        red, cpy = p.bytes()
+        assert (red, cpy) == model.algorithmic_bytes(ref, 4)
+        for ph in range(p.num_phases):
+            op, first, cnt, b = p.phase_info(ph)
+            steps = ref.phases[ph]
+            assert cnt == len(steps)
+            assert op == (arplan.AR_OP_REDUCE if any(s.op == "reduce" for s in steps)
+                          else arplan.AR_OP_COPY)
+            assert b == sum((len(s.srcs) + 1 if s.op == "reduce" else 2)
+                            * (s.end - s.begin) * 4 for s in steps)
+
+
+@pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("ring", 8, None),
+                                        ("rhd", 8, None), ("cps", 6, None),
+                                        ("tree", 12, (3, 4)),
+                                        ("tree", 64, (8, 8)),
+                                        ("tree", 512, (8, 8, 8))])
+def test_owner_is_last_reduce_range(kind, n, fan):
+    N = 7 * n + 3
+    ref = oracle.make_plan(kind, n, N, fan)
+    red = [ph for ph in ref.phases if ph[0].op == "reduce"]
+    with arplan.Plan(n, N, "bf16", kind, fan) as p:
+        for st in red[-1]:
+            assert p.owner(st.dst) == (st.begin, st.end)
+
+
+@pytest.mark.parametrize("fan", [(8, 8), (2, 3, 4), (8, 8, 8)])
+def test_tree_owner_matches_algorithm_1(fan):
+    n = int(np.prod(fan))
+    N = 3 * n
+    root = oracle.symmetric_tree(fan)
+    place = oracle.basic_placement(root, n)[id(root)]
+    off = oracle.block_bounds(N, n)
+    with arplan.Plan(n, N, "i32", "tree", fan) as p:
+        for sid, blocks in place.items():
+            assert p.owner(sid) == (off[blocks[0]], off[blocks[-1] + 1])
+
+
+def test_config_shapes():
+    # phase and step counts of the benchmark workloads
+    shapes = [("ring", 4, 1 << 16, None, 6, 24), ("rhd", 8, 1 << 26, None, 6, 48),
+              ("cps", 16, 1 << 24, None, 2, 256), ("tree", 64, 1 << 22, (8, 8), 4, 1024),
+              ("tree", 512, 1 << 18, (8, 8, 8), 6, 12288),
+              ("ring", 64, 1 << 20, None, 126, 8064)]
+    for kind, n, N, fan, nph, nst in shapes:
+        with arplan.Plan(n, N, "f32", kind, fan) as p:
+            assert (p.num_phases, p.num_steps) == (nph, nst)
+
+
+def _status(fn, *args):
+    try:
+        fn(*args)
+    except arplan.ArError as e:
+        return e.status
+    return arplan.AR_OK
+
+
+def test_create_errors():
+    E = arplan
+    assert _status(E.ar_plan_create, 0, 10, "f32", "ring") == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 4, -1, "f32", "ring") == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 4, 10, 7, "ring") == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 4, 10, "f32", 9) == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 6, 10, "f32", "rhd") == E.AR_ERR_UNSUPPORTED
+    assert _status(E.ar_plan_create, 6, 10, "f32", "tree", [2, 2]) == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 4, 10, "f32", "tree", [4, 0]) == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 4, 10, "f32", "tree", []) == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 4, 2**62, "f32", "ring") == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create, 40000, 10, "f32", "ring") == E.AR_ERR_UNSUPPORTED
+    # NULL out / topo
+    lib = arplan._lib
+    topo = arplan.ar_topology(arplan.AR_RING, 0, None)
+    assert lib.ar_plan_create(4, 10, 0, ctypes.byref(topo), None) == E.AR_ERR_INVALID_ARG
+    out = ctypes.c_void_p(123)
+    assert lib.ar_plan_create(4, 10, 0, None, ctypes.byref(out)) == E.AR_ERR_INVALID_ARG
+    assert out.value is None
+    assert "topo" in E.ar_last_error()
+    assert lib.ar_plan_destroy(None) == E.AR_OK
+    assert E.ar_status_string(E.AR_ERR_HIP) == "AR_ERR_HIP"
+
+
+def test_execute_argument_errors_need_no_gpu():
+    E = arplan
+    lib = arplan._lib
+    assert lib.ar_plan_execute(None, None, None) == E.AR_ERR_INVALID_ARG
+    h = E.ar_plan_create(4, 16, "f32", "ring")
+    try:
+        assert lib.ar_plan_execute(h, None, None) == E.AR_ERR_INVALID_ARG
+        assert lib.ar_plan_execute_strided(h, None, 64, None) == E.AR_ERR_INVALID_ARG
+        assert lib.ar_plan_execute_strided(h, 4096, 63, None) == E.AR_ERR_INVALID_ARG
+    finally:
+        E.ar_plan_destroy(h)
+    # empty plans return without touching the GPU
+    h = E.ar_plan_create(1, 16, "f32", "ring")
+    try:
+        E.ar_plan_execute(h, [0x1000])
+    finally:
+        E.ar_plan_destroy(h)
+
+
+def test_custom_plan_roundtrip_and_validation():
+    E = arplan
+    ref = oracle.tree((3, 4), 50)
+    steps = [(ph, s.op, s.dst, s.srcs, s.begin, s.end)
+             for ph, stp in enumerate(ref.phases) for s in stp]
+    h = E.ar_plan_create_custom(12, 50, "f32", reversed(steps))
+    try:
+        n, N, dt, nph, nst = E.ar_plan_info(h)
+        assert (n, N, nph, nst) == (12, 50, 4, len(steps))
+        got = [E.ar_plan_get_step(h, i) for i in range(nst)]
+        norm = lambda L: sorted((a, b if isinstance(b, int) else
+                                 (0 if b == "reduce" else 1), c, tuple(d), e, f)
+                                for a, b, c, d, e, f in L)
+        assert norm(got) == norm(steps)
+        assert _status(E.ar_plan_owner, h, 0) == E.AR_ERR_UNSUPPORTED
+    finally:
+        E.ar_plan_destroy(h)
+    bad = {
+        "write/write": [(0, "copy", 1, [0], 0, 6), (0, "copy", 1, [2], 5, 9)],
+        "read/write": [(0, "reduce", 1, [0, 1], 0, 4), (0, "copy", 0, [2], 3, 5)],
+        "gap": [(0, "copy", 1, [0], 0, 4), (2, "copy", 1, [0], 0, 4)],
+        "copy 2 srcs": [(0, "copy", 1, [0, 2], 0, 4)],
+        "dst range": [(0, "copy", 3, [0], 0, 4)],
+        "src range": [(0, "reduce", 1, [0, 3], 0, 4)],
+        "elem range": [(0, "copy", 1, [0], 0, 11)],
+        "reversed": [(0, "copy", 1, [0], 5, 4)],
+        "no src": [(0, "reduce", 1, [], 0, 4)],
+    }
+    for name, st in bad.items():
+        assert _status(E.ar_plan_create_custom, 3, 10, "f32", st) == \
+            E.AR_ERR_INVALID_ARG, name
+    # a step may read and write its own range; different phases may overlap
+    ok = [(0, "reduce", 1, [0, 1, 2], 0, 10), (1, "copy", 0, [1], 0, 10),
+          (1, "copy", 2, [1], 0, 10)]
+    E.ar_plan_destroy(E.ar_plan_create_custom(3, 10, "bf16", ok))
+
+
+def test_timer_host_side():
+    E = arplan
+    t = E.ar_timer_create(8)
+    try:
+        assert E.ar_timer_read(t, 8) == []
+        E.ar_timer_reset(t)
+    finally:
+        E.ar_timer_destroy(t)
+    assert _status(E.ar_timer_create, 0) == E.AR_ERR_INVALID_ARG
+
+
+def _check_tiling(handle, vecok):
+    lib = ctypes.CDLL(arplan.LIB_PATH)
+    f = lib.ar_debug_check_tiling
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_char_p, ctypes.c_int64]
+    f.restype = ctypes.c_int32
+    buf = ctypes.create_string_buffer(512)
+    st = f(handle, vecok, buf, 512)
+    return st, buf.value.decode()
+
+
+TILING = [("ring", 4, 1 << 16, None), ("rhd", 8, 1 << 26, None),
+          ("cps", 16, 1 << 24, None), ("tree", 64, 1 << 22, (8, 8)),
+          ("tree", 512, 1 << 18, (8, 8, 8)), ("ring", 64, 1 << 20, None),
+          ("ring", 64, 1 << 12, None), ("tree", 64, 1 << 12, (8, 8)),
+          ("rhd", 8, (1 << 20) + 13, None), ("cps", 16, (1 << 18) + 7, None),
+          ("tree", 512, (1 << 13) + 3, (8, 8, 8)), ("rb", 6, 100003, None),
+          ("cps", 5, 50021, None), ("cps", 32, 50021, None),
+          ("tree", 12, 4099, (3, 4)), ("ring", 5, 1, None), ("ring", 5, 4, None),
+          ("rhd", 4, 3, None), ("tree", 8, 10007, (4, 2)), ("ring", 3, 4099, None)]
+
+
+@pytest.mark.parametrize("kind,n,N,fan", TILING)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_kernel_tiling_covers_steps_exactly(kind, n, N, fan, dtype):
+    h = arplan.ar_plan_create(n, N, dtype, kind, fan)
+    try:
+        for vecok in (1, 0):
+            st, msg = _check_tiling(h, vecok)
+            assert st == arplan.AR_OK, msg
+    finally:
+        arplan.ar_plan_destroy(h)
+
+
+def test_kernel_tiling_uneven_custom_phase():
+    steps = [(0, "reduce", 0, [0, 1, 2], 0, 280000),
+             (0, "reduce", 3, [3, 1], 280000, 280007),
+             (0, "reduce", 2, [2, 3], 280007, 300001),
+             (1, "copy", 1, [0], 0, 280000), (1, "copy", 0, [3], 280000, 280007),
+             (1, "copy", 3, [2], 290000, 290001)]
+    for dtype in ("f32", "bf16", "i32"):
+        h = arplan.ar_plan_create_custom(4, 300001, dtype, steps)
+        try:
+            for vecok in (1, 0):
+                st, msg = _check_tiling(h, vecok)
+                assert st == arplan.AR_OK, msg
+        finally:
+            arplan.ar_plan_destroy(h)

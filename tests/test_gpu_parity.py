@@ -1,0 +1,282 @@
+"""GPU parity: the HIP path, called through the C ABI, against the oracle.
+
+fp32 and int32 must match bit for bit (the plan fixes the association
+order); bf16 must match the oracle's per-step rounding bit for bit and lie
+within 1e-2 normwise of the fp64 sum.  Small and scaled-down workloads are
+compared element by element over every buffer; the full-size workloads are
+compared at sampled positions (every block edge, tile edges and random
+positions, for every processor) plus the property that all n outputs are
+identical over the whole buffer.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2409_04202_amd import workloads
+
+from gpu_helpers import run_plan, say, to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2409_04202_amd import arplan
+
+
+def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
+                  pad=0, xs0=None):
+    say("case: %s n=%d N=%d %s fan=%s pad=%d" % (kind, n, N, dtype, fan, pad))
+    if xs0 is None:
+        xs0 = workloads.draw(n, N, dtype, dist, seed)
+    ref = oracle.execute(oracle.make_plan(kind, n, N, fan),
+                         [x.copy() for x in xs0], dtype)
+    ts = to_device(xs0, dtype, pad)
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        run_plan(p, ts)
+    got = to_host(ts, dtype)
+    for q in range(n):
+        if not np.array_equal(got[q], ref[q]):
+            bad = np.nonzero(got[q] != ref[q])[0]
+            raise AssertionError("%s n=%d N=%d %s: processor %d differs at %d "
+                                 "positions, first %s" % (kind, n, N, dtype, q,
+                                                          len(bad), bad[:8]))
+    return got, xs0
+
+
+def _normwise_bf16(y_bits, xs0):
+    r = np.sum([oracle.bf16_to_f32(x).astype(np.float64) for x in xs0], axis=0)
+    y = oracle.bf16_to_f32(y_bits).astype(np.float64)
+    return np.linalg.norm(y - r) / max(np.linalg.norm(r), 1e-300)
+
+
+# ------------------------------------------------ small and scaled configs
+
+@pytest.mark.parametrize("name", ["ring_n4_f32", "ring_n4_i32"])
+def test_small_config_bit_exact(name):
+    c = workloads.CONFIGS[name]
+    _full_compare(c["kind"], c["n"], c["N"], c["dtype"], c["fanin"],
+                  c["dist"], c["seed"])
+
+
+SCALED = [("rhd", 8, (1 << 20) + 13, "f32", None, "uniform"),
+          ("cps", 16, (1 << 18) + 7, "f32", None, "normal"),
+          ("tree", 64, (1 << 16) + 5, "f32", (8, 8), "uniform"),
+          ("tree", 64, (1 << 16) + 5, "i32", (8, 8), "int1000"),
+          ("tree", 512, (1 << 13) + 3, "bf16", (8, 8, 8), "uniform"),
+          ("tree", 512, 1 << 15, "bf16", (8, 8, 8), "uniform"),
+          ("ring", 4, (1 << 16) + 3, "bf16", None, "uniform"),
+          ("rb", 6, 100003, "f32", None, "uniform")]
+
+
+@pytest.mark.parametrize("kind,n,N,dtype,fan,dist", SCALED)
+def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist):
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=5)
+    if dtype == "bf16":
+        assert _normwise_bf16(got[0], xs0) <= 1e-2
+
+
+@pytest.mark.parametrize("name", sorted(k for k in workloads.CONFIGS
+                                        if k.startswith("sweep_")))
+def test_sweep_configs_bit_exact(name):
+    c = workloads.CONFIGS[name]
+    got, xs0 = _full_compare(c["kind"], c["n"], c["N"], c["dtype"],
+                             c["fanin"], c["dist"], c["seed"])
+    if c["dtype"] == "bf16":
+        assert _normwise_bf16(got[0], xs0) <= 1e-2
+
+
+# ------------------------------------------------- full-size, sampled check
+
+def _sample_positions(n, N, rng):
+    off = np.array(oracle.block_bounds(N, n))
+    edges = np.concatenate([off, off - 1, off + 1])
+    if len(edges) > 4096:
+        edges = rng.choice(edges, 4096, replace=False)
+    tiles = np.arange(0, N, 1 << 15)
+    idx = np.concatenate([edges, tiles, tiles - 1, rng.integers(0, N, 4096),
+                          [0, N - 1]])
+    return np.unique(idx[(idx >= 0) & (idx < N)])
+
+
+@pytest.mark.parametrize("name", ["rhd_n8_f32", "cps_n16_f32",
+                                  "tree8x8_n64_f32", "tree8x8_n64_i32",
+                                  "tree8x8x8_n512_bf16"])
+def test_full_size_configs(name):
+    c = workloads.CONFIGS[name]
+    n, N, dt = c["n"], c["N"], c["dtype"]
+    say("case: full-size %s" % name)
+    xs0 = workloads.inputs(name)
+    ts = to_device(xs0, dt)
+    rng = np.random.default_rng(99)
+    idx = _sample_positions(n, N, rng)
+    with arplan.Plan(n, N, dt, c["kind"], c["fanin"]) as p:
+        run_plan(p, ts)
+    plan = oracle.make_plan(c["kind"], n, N, c["fanin"])
+    want = oracle.execute_sampled(plan, [x[idx] for x in xs0], idx, dt)
+    it = torch.from_numpy(idx).to("cuda")
+    for q in range(n):
+        g = ts[q].index_select(0, it).cpu().numpy()
+        g = g.view(np.uint16) if dt == "bf16" else g
+        assert np.array_equal(g, want[q]), (name, q)
+        assert torch.equal(ts[q], ts[0]), (name, q)
+    if dt == "bf16":
+        y = ts[0].cpu().numpy().view(np.uint16)
+        err = _normwise_bf16(y, xs0)
+        say("bf16 normwise error %.3e" % err)
+        assert err <= 1e-2
+
+
+# --------------------------------------------------------------- edge cases
+
+@pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("rhd", 4, None),
+                                        ("cps", 7, None), ("tree", 12, (3, 4)),
+                                        ("rb", 3, None)])
+@pytest.mark.parametrize("dtype", ["f32", "i32", "bf16"])
+def test_ragged_and_tiny_sizes(kind, n, fan, dtype):
+    for N in (1, n - 1, n, n + 1, 2 * n + 3, 4099):
+        dist = "int1000" if dtype == "i32" else "uniform"
+        _full_compare(kind, n, N, dtype, fan, dist, seed=N)
+
+
+def test_empty_buffers_are_a_no_op():
+    for kind, n, fan in (("ring", 4, None), ("tree", 4, (2, 2))):
+        ts = to_device([np.zeros(0, np.float32)] * n, "f32")
+        with arplan.Plan(n, 0, "f32", kind, fan) as p:
+            run_plan(p, ts)
+
+
+@pytest.mark.parametrize("dtype,pad", [("f32", 1), ("f32", 2), ("i32", 3),
+                                       ("bf16", 1), ("bf16", 5)])
+def test_unaligned_buffers(dtype, pad):
+    dist = "int1000" if dtype == "i32" else "uniform"
+    _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, pad=pad)
+    _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, pad=pad)
+
+
+@pytest.mark.parametrize("n", [3, 5, 16, 32])
+def test_source_counts(n):
+    # k = 3 and 16 have unrolled kernels, 5 and 32 use the runtime loop
+    for dtype in ("f32", "bf16"):
+        _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n)
+
+
+def test_fp32_denormals_are_kept():
+    n, N = 4, 8192
+    rng = np.random.default_rng(7)
+    xs0 = [((rng.random(N) * 2 - 1) * 1e-39).astype(np.float32)
+           for _ in range(n)]
+    assert any(np.any((np.abs(x) < 1.17e-38) & (x != 0)) for x in xs0)
+    got, _ = _full_compare("cps", n, N, "f32", xs0=xs0)
+    assert np.any((np.abs(got[0]) < 1.17e-38) & (got[0] != 0))
+
+
+def test_int32_wraps():
+    n, N = 4, 4096
+    xs0 = [np.full(N, 2**31 - 1 - q, np.int32) for q in range(n)]
+    _full_compare("ring", n, N, "i32", xs0=xs0)
+    _full_compare("cps", n, N, "i32", xs0=xs0)
+
+
+def test_bf16_ties_round_to_even():
+    # 1 + 2^-8 and 1 + 3*2^-8 are halfway between bf16 neighbours.
+    n, N = 2, 4096
+    one = np.uint16(0x3F80)                  # 1.0
+    eps = np.uint16(0x3B80)                  # 2^-8
+    three = np.uint16(0x3C40)                # 3 * 2^-8
+    a = np.full(N, one, np.uint16)
+    b = np.where(np.arange(N) % 2 == 0, eps, three).astype(np.uint16)
+    got, _ = _full_compare("cps", n, N, "bf16", xs0=[a, b])
+    assert np.all(got[0][0::2] == 0x3F80)    # tie to even: 1.0
+    assert np.all(got[0][1::2] == 0x3F82)    # 1 + 2^-6 (even mantissa)
+
+
+def test_custom_plan_mixed_sources_and_uneven_steps():
+    # one phase with a 3-way reduce over a long range and 2-way reduces over
+    # tiny ranges (explicit tile table), then copies of uneven lengths
+    n, N = 4, 300001
+    steps = [(0, "reduce", 0, [0, 1, 2], 0, 280000),
+             (0, "reduce", 3, [3, 1], 280000, 280007),
+             (0, "reduce", 2, [2, 3], 280007, 300001),
+             (1, "copy", 1, [0], 0, 280000),
+             (1, "copy", 0, [3], 280000, 280007),
+             (1, "copy", 3, [2], 290000, 290001)]
+    xs0 = workloads.draw(n, N, "f32", "uniform", 8)
+    ref = [x.copy() for x in xs0]
+    ph = [[oracle.Step(o, d, tuple(s), b, e) for (p_, o, d, s, b, e) in steps
+           if p_ == k] for k in (0, 1)]
+    oracle.execute(oracle.Plan("custom", n, N, ph), ref, "f32")
+    ts = to_device(xs0, "f32")
+    h = arplan.ar_plan_create_custom(n, N, "f32", steps)
+    try:
+        arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+    finally:
+        arplan.ar_plan_destroy(h)
+    got = to_host(ts, "f32")
+    for q in range(n):
+        assert np.array_equal(got[q], ref[q]), q
+
+
+def test_pointer_table_cache_and_strided():
+    n, N = 8, 65539
+    plan_o = oracle.rhd(n, N)
+    with arplan.Plan(n, N, "f32", "rhd") as p:
+        for rep in range(6):            # more buffer sets than cached tables
+            xs0 = workloads.draw(n, N, "f32", "uniform", 100 + rep)
+            ref = oracle.execute(plan_o, [x.copy() for x in xs0], "f32")
+            ts = to_device(xs0, "f32")
+            run_plan(p, ts)
+            got = to_host(ts, "f32")
+            assert all(np.array_equal(got[q], ref[q]) for q in range(n)), rep
+        xs0 = workloads.draw(n, N, "f32", "uniform", 200)
+        ref = oracle.execute(plan_o, [x.copy() for x in xs0], "f32")
+        stride = N + 29
+        big = torch.zeros(n * stride, dtype=torch.float32, device="cuda")
+        for q in range(n):
+            big[q * stride:q * stride + N].copy_(torch.from_numpy(xs0[q]))
+        p.execute_strided(big, stride * 4, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        for q in range(n):
+            g = big[q * stride:q * stride + N].cpu().numpy()
+            assert np.array_equal(g, ref[q]), q
+
+
+def test_repeated_execution_and_overlapping_buffers_rejected():
+    n, N = 16, 40000
+    xs0 = workloads.draw(n, N, "f32", "normal", 12)
+    plan_o = oracle.tree((4, 4), N)
+    ref = oracle.execute(plan_o, [x.copy() for x in xs0], "f32")
+    ref = oracle.execute(plan_o, ref, "f32")
+    ts = to_device(xs0, "f32")
+    with arplan.Plan(n, N, "f32", "tree", (4, 4)) as p:
+        run_plan(p, ts)
+        run_plan(p, ts)
+        got = to_host(ts, "f32")
+        assert all(np.array_equal(got[q], ref[q]) for q in range(n))
+        bad = list(ts)
+        bad[3] = ts[2][5:]
+        with pytest.raises(arplan.ArError) as e:
+            p.execute(bad, torch.cuda.current_stream())
+        assert e.value.status == arplan.AR_ERR_INVALID_ARG
+        bad[3] = 0
+        with pytest.raises(arplan.ArError):
+            p.execute(bad, torch.cuda.current_stream())
+
+
+def test_timer_records_each_launch():
+    n, N = 8, 1 << 20
+    xs0 = workloads.draw(n, N, "f32", "uniform", 13)
+    ts = to_device(xs0, "f32")
+    t = arplan.ar_timer_create(64)
+    try:
+        with arplan.Plan(n, N, "f32", "rhd") as p:
+            for _ in range(2):
+                p.execute_timed(ts, torch.cuda.current_stream(), t)
+            recs = arplan.ar_timer_read(t, 64)
+            assert [ph for ph, _ in recs] == list(range(6)) * 2
+            assert all(ms > 0 for _, ms in recs)
+            arplan.ar_timer_reset(t)
+            assert arplan.ar_timer_read(t, 64) == []
+    finally:
+        arplan.ar_timer_destroy(t)
