@@ -15,6 +15,15 @@ import ctypes
 import os
 from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_void_p
 
+# One HIP runtime per process: buffers and streams come from torch, so the
+# library must bind to the HIP runtime torch loads.  Both runtimes carry the
+# SONAME libamdhip64.so.7; loading torch first makes the library's
+# dependency resolve to torch's copy instead of a second runtime instance.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    torch = None
+
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib",
                         "libarplan.so")
 if not os.path.exists(LIB_PATH):

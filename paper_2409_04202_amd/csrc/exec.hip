@@ -23,8 +23,12 @@ namespace arp {
 namespace {
 
 constexpr int kCache = 4;               // pointer tables kept per device
-constexpr int64_t kTargetUnits = 16384; // wave tiles per launch to aim for
+constexpr int64_t kMinUnits = 2048;     // shrink tiles until a launch has this many
 constexpr int64_t kMaxBlocks = int64_t(1) << 24;
+// Launches moving at least this many bytes stream through the caches with
+// nontemporal loads and stores; smaller ones keep their data cached for the
+// next phase.
+constexpr int64_t kNtBytes = int64_t(64) << 20;
 
 struct LaunchDesc {
     int32_t phase;
@@ -35,6 +39,8 @@ struct LaunchDesc {
     int64_t tiles_per_step;  // arithmetic mapping
     int64_t nunits;          // wave tiles
     int64_t tile_off;        // -1, or first entry of the device tile table
+    int32_t wpb;             // wavefronts per block
+    bool nt;                 // nontemporal loads and stores
 };
 
 struct PtrEntry {
@@ -60,19 +66,6 @@ int kernel_k(int32_t k) {
     switch (k) {
         case 1: case 2: case 3: case 4: case 8: case 16: return k;
         default: return 0;
-    }
-}
-
-int host_unroll(int K) {
-    switch (K) {
-        case 0: return Unroll<0>::U;
-        case 1: return Unroll<1>::U;
-        case 2: return Unroll<2>::U;
-        case 3: return Unroll<3>::U;
-        case 4: return Unroll<4>::U;
-        case 8: return Unroll<8>::U;
-        case 16: return Unroll<16>::U;
-        default: return 1;
     }
 }
 
@@ -138,14 +131,20 @@ static void build_launches(const Plan& p, ExecState& ex) {
                 g0 = g1;
                 continue;
             }
-            const int64_t iter = 64 * VEC * host_unroll(L.kern_k);
-            int64_t te = iter;
+            // wave tile: the measured best size for this source count,
+            // halved while the launch has too few tiles to fill the chip
+            const KCfg cfg = kcfg(L.kern_k);
+            const int64_t tmin = int64_t(64) * cfg.U * VEC;
+            int64_t te = int64_t(cfg.TE) * VEC;
             auto units_for = [&](int64_t t) {
                 return L.count * ((maxspan + t - 1) / t);
             };
-            while (te < 64 * iter && units_for(te) > kTargetUnits) te *= 2;
-            while ((units_for(te) + kWavesPerBlock - 1) / kWavesPerBlock > kMaxBlocks)
-                te *= 2;
+            while (te > tmin && units_for(te) < kMinUnits) te /= 2;
+            while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
+            L.wpb = cfg.WPB;
+            int64_t bytes = 0;
+            for (size_t g = g0; g < g1; ++g) bytes += step_bytes(p, p.steps[size_t(idx[g])]);
+            L.nt = bytes >= kNtBytes;
             L.tile_elems = te;
             L.tiles_per_step = (maxspan + te - 1) / te;
             int64_t used = 0;
@@ -324,30 +323,33 @@ static ar_status pointer_table(const Plan& p, DevState& d,
 }
 
 template <int DT, int K>
-static void launch_dk(bool vecok, int64_t blocks, hipStream_t st, const DevStep* steps,
-                      const int32_t* srcs, void* const* ptrs, const int2* tiles,
-                      int64_t nunits, int64_t tps, int64_t te) {
-    const dim3 grid(static_cast<uint32_t>(blocks)), block(kBlockThreads);
-    if (vecok)
-        hipLaunchKernelGGL((phase_kernel<DT, K, true>), grid, block, 0, st, steps,
+static void launch_dk(bool vecok, bool nt, int64_t blocks, hipStream_t st,
+                      const DevStep* steps, const int32_t* srcs, void* const* ptrs,
+                      const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
+    const dim3 grid(static_cast<uint32_t>(blocks)), block(64 * kcfg(K).WPB);
+    if (vecok && nt)
+        hipLaunchKernelGGL((phase_kernel<DT, K, true, true>), grid, block, 0, st, steps,
+                           srcs, ptrs, tiles, nunits, tps, te);
+    else if (vecok)
+        hipLaunchKernelGGL((phase_kernel<DT, K, true, false>), grid, block, 0, st, steps,
                            srcs, ptrs, tiles, nunits, tps, te);
     else
-        hipLaunchKernelGGL((phase_kernel<DT, K, false>), grid, block, 0, st, steps,
+        hipLaunchKernelGGL((phase_kernel<DT, K, false, false>), grid, block, 0, st, steps,
                            srcs, ptrs, tiles, nunits, tps, te);
 }
 
 template <int DT>
-static void launch_d(int K, bool vecok, int64_t blocks, hipStream_t st,
+static void launch_d(int K, bool vecok, bool nt, int64_t blocks, hipStream_t st,
                      const DevStep* steps, const int32_t* srcs, void* const* ptrs,
                      const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
     switch (K) {
-        case 1: launch_dk<DT, 1>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 2: launch_dk<DT, 2>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 3: launch_dk<DT, 3>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 4: launch_dk<DT, 4>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 8: launch_dk<DT, 8>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 16: launch_dk<DT, 16>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        default: launch_dk<DT, 0>(vecok, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 1: launch_dk<DT, 1>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 2: launch_dk<DT, 2>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 3: launch_dk<DT, 3>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 4: launch_dk<DT, 4>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 8: launch_dk<DT, 8>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 16: launch_dk<DT, 16>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        default: launch_dk<DT, 0>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
     }
 }
 
@@ -377,7 +379,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
         s = pointer_table(*plan, *d, bufs, stream, &pe);
         if (s != AR_OK) return s;
         for (const LaunchDesc& L : ex->launches) {
-            const int64_t blocks = (L.nunits + kWavesPerBlock - 1) / kWavesPerBlock;
+            const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
             hipEvent_t e0 = nullptr, e1 = nullptr;
             if (timer) {
                 const int64_t r = timer->count;
@@ -400,15 +402,15 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
             switch (plan->dtype) {
                 case AR_F32:
-                    launch_d<DT_F32>(L.kern_k, pe->aligned, blocks, stream, steps, d->srcs,
+                    launch_d<DT_F32>(L.kern_k, pe->aligned, L.nt, blocks, stream, steps, d->srcs,
                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
                 case AR_I32:
-                    launch_d<DT_I32>(L.kern_k, pe->aligned, blocks, stream, steps, d->srcs,
+                    launch_d<DT_I32>(L.kern_k, pe->aligned, L.nt, blocks, stream, steps, d->srcs,
                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
                 default:
-                    launch_d<DT_BF16>(L.kern_k, pe->aligned, blocks, stream, steps, d->srcs,
+                    launch_d<DT_BF16>(L.kern_k, pe->aligned, L.nt, blocks, stream, steps, d->srcs,
                                       pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
             }
@@ -537,14 +539,15 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
         std::vector<char> launched(ex->hsteps.size(), 0);
         for (const LaunchDesc& L : ex->launches) {
             if (L.nunits <= 0) return bad("launch without work units");
-            const int64_t blocks = (L.nunits + kWavesPerBlock - 1) / kWavesPerBlock;
+            const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
             if (blocks > kMaxBlocks) return bad("grid too large");
+            if (L.wpb != kcfg(L.kern_k).WPB) return bad("block size differs from the kernel's");
             if (L.tile_elems % (64 * VEC) != 0) return bad("tile not a multiple of a wave vector");
             const int2* tiles = L.tile_off >= 0 ? ex->htiles.data() + L.tile_off : nullptr;
             if (tiles && L.tile_off + L.nunits > int64_t(ex->htiles.size()))
                 return bad("tile table overrun");
             for (int64_t j = 0; j < L.count; ++j) launched[size_t(L.first + j)] = 1;
-            for (int64_t unit = 0; unit < blocks * kWavesPerBlock; ++unit) {
+            for (int64_t unit = 0; unit < blocks * L.wpb; ++unit) {
                 if (unit >= L.nunits) continue;  // the kernel returns here
                 int64_t s, t;
                 unit_tile(unit, tiles, L.tiles_per_step, s, t);

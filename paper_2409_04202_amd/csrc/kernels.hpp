@@ -11,7 +11,8 @@
 // Inner loop.  Per iteration every lane moves U 16-byte vectors of each of
 // the K sources (global_load_dwordx4; the wave touches 1 KiB contiguous per
 // vector slot), folds them in source order in fp32 (bf16 widened; int32 with
-// wrap-around) and stores U vectors.  Unaligned head and tail elements of a
+// wrap-around) and stores U vectors; large launches use nontemporal loads
+// and stores.  Unaligned head and tail elements of a
 // step are done element-wise.  The step descriptor, its source indices and
 // the buffer pointers are wave-uniform and live in scalar registers.
 #pragma once
@@ -32,14 +33,50 @@ struct DevStep {      // 32 bytes, one per step, grouped by launch
     int32_t pad;
 };
 
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlockThreads = 64 * kWavesPerBlock;
+// Per source count K (K = 0: source count read at run time):
+//   U   16-byte vectors in flight per lane and source,
+//   WPB wavefronts per block,
+//   TE  largest wave tile, in 16-byte vectors per source.
+// Chosen by measurement on MI355X: a 2-input fold and a copy stream best
+// with 16 KiB per source per wave and 8-wave blocks; wide folds want fewer
+// vectors per source in flight and smaller tiles.
+struct KCfg {
+    int U, WPB, TE;
+};
+__host__ __device__ constexpr KCfg kcfg(int K) {
+    return K == 1 ? KCfg{8, 8, 1024}
+         : K == 2 ? KCfg{4, 8, 1024}
+         : K <= 4 && K > 0 ? KCfg{4, 4, 512}
+         : K == 8 ? KCfg{2, 4, 256}
+         : K == 16 ? KCfg{1, 4, 512}
+         : KCfg{4, 4, 256};
+}
 
-// Vectors in flight per lane and source: about 16 loads in flight per lane.
-template <int K> struct Unroll { static constexpr int U = K >= 16 ? 1 : (K >= 8 ? 2 : (K >= 4 ? 4 : 8)); };
-template <> struct Unroll<0> { static constexpr int U = 4; };
-template <> struct Unroll<2> { static constexpr int U = 4; };
-template <> struct Unroll<3> { static constexpr int U = 4; };
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer pointers come from a table of generic pointers; marking them as
+// global-memory pointers lets the compiler use global_load/global_store
+// (vector memory counter only) instead of flat instructions.
+#define AR_GLOBAL __attribute__((address_space(1)))
+typedef AR_GLOBAL u32x4 gvec;
+
+template <class T>
+__device__ __forceinline__ AR_GLOBAL T* as_global(void* p) {
+    return (AR_GLOBAL T*)(p);
+}
+
+// Streaming loads and stores of whole vectors; NT marks them nontemporal
+// (large phases do not reuse what they read or write).
+template <bool NT>
+__device__ __forceinline__ u32x4 vload(const gvec* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+template <bool NT>
+__device__ __forceinline__ void vstore(gvec* p, u32x4 v) {
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
 
 template <int DT> struct Elem;
 template <> struct Elem<DT_F32> { using T = float;    static constexpr int VEC = 4; };
@@ -64,44 +101,42 @@ template <int DT> struct VAcc;
 
 template <> struct VAcc<DT_F32> {
     float v[4];
-    __device__ __forceinline__ void init(const uint4 x) {
-        v[0] = __uint_as_float(x.x); v[1] = __uint_as_float(x.y);
-        v[2] = __uint_as_float(x.z); v[3] = __uint_as_float(x.w);
+    __device__ __forceinline__ void init(const u32x4 x) {
+        v[0] = __uint_as_float(x[0]); v[1] = __uint_as_float(x[1]);
+        v[2] = __uint_as_float(x[2]); v[3] = __uint_as_float(x[3]);
     }
-    __device__ __forceinline__ void add(const uint4 x) {
-        v[0] += __uint_as_float(x.x); v[1] += __uint_as_float(x.y);
-        v[2] += __uint_as_float(x.z); v[3] += __uint_as_float(x.w);
+    __device__ __forceinline__ void add(const u32x4 x) {
+        v[0] += __uint_as_float(x[0]); v[1] += __uint_as_float(x[1]);
+        v[2] += __uint_as_float(x[2]); v[3] += __uint_as_float(x[3]);
     }
-    __device__ __forceinline__ uint4 out() const {
-        return make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
-                          __float_as_uint(v[2]), __float_as_uint(v[3]));
+    __device__ __forceinline__ u32x4 out() const {
+        return u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]),
+                     __float_as_uint(v[2]), __float_as_uint(v[3])};
     }
 };
 
 template <> struct VAcc<DT_I32> {
     uint32_t v[4];
-    __device__ __forceinline__ void init(const uint4 x) { v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w; }
-    __device__ __forceinline__ void add(const uint4 x) { v[0] += x.x; v[1] += x.y; v[2] += x.z; v[3] += x.w; }
-    __device__ __forceinline__ uint4 out() const { return make_uint4(v[0], v[1], v[2], v[3]); }
+    __device__ __forceinline__ void init(const u32x4 x) { v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3]; }
+    __device__ __forceinline__ void add(const u32x4 x) { v[0] += x[0]; v[1] += x[1]; v[2] += x[2]; v[3] += x[3]; }
+    __device__ __forceinline__ u32x4 out() const { return u32x4{v[0], v[1], v[2], v[3]}; }
 };
 
 template <> struct VAcc<DT_BF16> {
     float v[8];
-    __device__ __forceinline__ void init(const uint4 x) {
-        v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
-        v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
+    __device__ __forceinline__ void init(const u32x4 x) {
+        v[0] = bf16_lo(x[0]); v[1] = bf16_hi(x[0]); v[2] = bf16_lo(x[1]); v[3] = bf16_hi(x[1]);
+        v[4] = bf16_lo(x[2]); v[5] = bf16_hi(x[2]); v[6] = bf16_lo(x[3]); v[7] = bf16_hi(x[3]);
     }
-    __device__ __forceinline__ void add(const uint4 x) {
-        v[0] += bf16_lo(x.x); v[1] += bf16_hi(x.x); v[2] += bf16_lo(x.y); v[3] += bf16_hi(x.y);
-        v[4] += bf16_lo(x.z); v[5] += bf16_hi(x.z); v[6] += bf16_lo(x.w); v[7] += bf16_hi(x.w);
+    __device__ __forceinline__ void add(const u32x4 x) {
+        v[0] += bf16_lo(x[0]); v[1] += bf16_hi(x[0]); v[2] += bf16_lo(x[1]); v[3] += bf16_hi(x[1]);
+        v[4] += bf16_lo(x[2]); v[5] += bf16_hi(x[2]); v[6] += bf16_lo(x[3]); v[7] += bf16_hi(x[3]);
     }
-    __device__ __forceinline__ uint4 out() const {
-        uint4 r;
-        r.x = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
-        r.y = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
-        r.z = f32_to_bf16_bits(v[4]) | (f32_to_bf16_bits(v[5]) << 16);
-        r.w = f32_to_bf16_bits(v[6]) | (f32_to_bf16_bits(v[7]) << 16);
-        return r;
+    __device__ __forceinline__ u32x4 out() const {
+        return u32x4{f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16),
+                     f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16),
+                     f32_to_bf16_bits(v[4]) | (f32_to_bf16_bits(v[5]) << 16),
+                     f32_to_bf16_bits(v[6]) | (f32_to_bf16_bits(v[7]) << 16)};
     }
 };
 
@@ -188,9 +223,9 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
                                             int64_t hi, int lane) {
     using T = typename Elem<DT>::T;
     constexpr int SU = 4;
-    T* d = static_cast<T*>(ptrs[dst]);
+    AR_GLOBAL T* d = as_global<T>(ptrs[dst]);
     if (K == 1 || (K == 0 && k == 1)) {  // copy: move the bits unchanged
-        const T* s = static_cast<const T*>(ptrs[srcl[0]]);
+        const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[0]]);
         for (int64_t e = lo + lane; e < hi; e += 64) d[e] = s[e];
         return;
     }
@@ -200,14 +235,14 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
 #pragma unroll
         for (int u = 0; u < SU; ++u) ok[u] = e0 + u * 64 + lane < hi;
         {
-            const T* s = static_cast<const T*>(ptrs[srcl[0]]);
+            const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[0]]);
 #pragma unroll
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) acc[u].init(s[e0 + u * 64 + lane]);
         }
         const int kk = K ? K : k;
         for (int t = 1; t < kk; ++t) {
-            const T* s = static_cast<const T*>(ptrs[srcl[t]]);
+            const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[t]]);
 #pragma unroll
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) acc[u].add(s[e0 + u * 64 + lane]);
@@ -218,17 +253,83 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
     }
 }
 
+// U vectors per lane of K sources at vector offset `at` (+ u * 64 + lane),
+// folded in source order and stored.  FULL: all U vectors are in range, so
+// the loads are issued back to back with no per-vector branch.
+template <int DT, int K, int U, bool NT, bool FULL>
+__device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
+                                             int64_t at, int64_t nv, int lane) {
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
+    u32x4 x[K][U];
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) x[j][u] = vload<NT>(sp[j] + at + u * 64 + lane);
+    if constexpr (K == 1) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) vstore<NT>(d + at + u * 64 + lane, x[0][u]);
+    } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            VAcc<DT> acc;
+            acc.init(x[0][u]);
+#pragma unroll
+            for (int j = 1; j < K; ++j) acc.add(x[j][u]);
+            if (ok[u]) vstore<NT>(d + at + u * 64 + lane, acc.out());
+        }
+    }
+}
+
+// Runtime source count: one source at a time, U vectors in flight.
+template <int DT, int U, bool NT, bool FULL>
+__device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
+                                                const int32_t* __restrict__ srcl,
+                                                int k, int64_t v0, gvec* d,
+                                                int64_t at, int64_t nv, int lane) {
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
+    VAcc<DT> acc[U];
+    {
+        const gvec* s0 = as_global<u32x4>(ptrs[srcl[0]]) + v0;
+        u32x4 x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) x[u] = vload<NT>(s0 + at + u * 64 + lane);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[u].init(x[u]);
+    }
+    for (int j = 1; j < k; ++j) {
+        const gvec* sj = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+        u32x4 x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) x[u] = vload<NT>(sj + at + u * 64 + lane);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[u].add(x[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        if (ok[u]) vstore<NT>(d + at + u * 64 + lane, acc[u].out());
+}
+
 // One launch: `nunits` wave tiles over the steps steps[0..).  K = 0 means
-// the source count is read from each step (any k >= 1).
-template <int DT, int K, bool VECOK>
-__global__ __launch_bounds__(kBlockThreads) void phase_kernel(
+// the source count is read from each step (any k >= 1).  VECOK: every
+// buffer is 16-byte aligned.  NT: nontemporal vector loads and stores.
+template <int DT, int K, bool VECOK, bool NT>
+__global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const DevStep* __restrict__ steps, const int32_t* __restrict__ srcs,
     void* const* __restrict__ ptrs, const int2* __restrict__ tiles,
     int64_t nunits, int64_t tiles_per_step, int64_t tile_elems) {
     constexpr int VEC = Elem<DT>::VEC;
-    constexpr int U = Unroll<K>::U;
+    constexpr int U = kcfg(K).U;
+    constexpr int WPB = kcfg(K).WPB;
     const int lane = int(threadIdx.x) & 63;
-    const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock +
+    const int64_t unit = int64_t(blockIdx.x) * WPB +
                          int64_t(__builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
     if (unit >= nunits) return;
     int64_t s, t;
@@ -244,71 +345,22 @@ __global__ __launch_bounds__(kBlockThreads) void phase_kernel(
     if (sp.vlo > sp.lo) fold_scalar<DT, K>(ptrs, srcl, k, st.dst, sp.lo, sp.vlo, lane);
     if (sp.hi > sp.vhi) fold_scalar<DT, K>(ptrs, srcl, k, st.dst, sp.vhi, sp.hi, lane);
     if (!VECOK || sp.vhi <= sp.vlo) return;
-    const int64_t vlo = sp.vlo, vhi = sp.vhi;
 
-    const int64_t v0 = vlo / VEC;
-    const int64_t nv = (vhi - vlo) / VEC;
-    uint4* __restrict__ d = static_cast<uint4*>(ptrs[st.dst]) + v0;
-
+    const int64_t v0 = sp.vlo / VEC;
+    const int64_t nv = (sp.vhi - sp.vlo) / VEC;
+    gvec* d = as_global<u32x4>(ptrs[st.dst]) + v0;
+    int64_t at = 0;
     if constexpr (K > 0) {
-        const uint4* sp[K];
+        const gvec* sv[K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) sp[j] = static_cast<const uint4*>(ptrs[srcl[j]]) + v0;
-        for (int64_t base = 0; base < nv; base += 64 * U) {
-            uint4 x[K][U];
-            bool ok[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) ok[u] = base + u * 64 + lane < nv;
-#pragma unroll
-            for (int j = 0; j < K; ++j)
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (ok[u]) x[j][u] = sp[j][base + u * 64 + lane];
-            if constexpr (K == 1) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (ok[u]) d[base + u * 64 + lane] = x[0][u];
-            } else {
-                VAcc<DT> acc[U];
-#pragma unroll
-                for (int u = 0; u < U; ++u) acc[u].init(x[0][u]);
-#pragma unroll
-                for (int j = 1; j < K; ++j)
-#pragma unroll
-                    for (int u = 0; u < U; ++u) acc[u].add(x[j][u]);
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (ok[u]) d[base + u * 64 + lane] = acc[u].out();
-            }
-        }
+        for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+        for (; at + 64 * U <= nv; at += 64 * U)
+            fold_vectors<DT, K, U, NT, true>(sv, d, at, nv, lane);
+        if (at < nv) fold_vectors<DT, K, U, NT, false>(sv, d, at, nv, lane);
     } else {
-        for (int64_t base = 0; base < nv; base += 64 * U) {
-            bool ok[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) ok[u] = base + u * 64 + lane < nv;
-            VAcc<DT> acc[U];
-            {
-                const uint4* s0 = static_cast<const uint4*>(ptrs[srcl[0]]) + v0;
-                uint4 x[U];
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (ok[u]) x[u] = s0[base + u * 64 + lane];
-#pragma unroll
-                for (int u = 0; u < U; ++u) acc[u].init(x[u]);
-            }
-            for (int j = 1; j < k; ++j) {
-                const uint4* sj = static_cast<const uint4*>(ptrs[srcl[j]]) + v0;
-                uint4 x[U];
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (ok[u]) x[u] = sj[base + u * 64 + lane];
-#pragma unroll
-                for (int u = 0; u < U; ++u) acc[u].add(x[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (ok[u]) d[base + u * 64 + lane] = acc[u].out();
-        }
+        for (; at + 64 * U <= nv; at += 64 * U)
+            fold_vectors_rt<DT, U, NT, true>(ptrs, srcl, k, v0, d, at, nv, lane);
+        if (at < nv) fold_vectors_rt<DT, U, NT, false>(ptrs, srcl, k, v0, d, at, nv, lane);
     }
 }
 

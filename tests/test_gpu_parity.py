@@ -280,3 +280,23 @@ def test_timer_records_each_launch():
             assert arplan.ar_timer_read(t, 64) == []
     finally:
         arplan.ar_timer_destroy(t)
+
+
+def test_runs_on_a_side_stream_in_order():
+    # inputs are written, the plan runs and the result is read back, all on
+    # a non-default torch stream: the library must honour its ordering
+    n, N = 16, (1 << 18) + 3
+    xs0 = workloads.draw(n, N, "f32", "uniform", 14)
+    ref = oracle.execute(oracle.cps(n, N), [x.copy() for x in xs0], "f32")
+    hs = [torch.from_numpy(x).pin_memory() for x in xs0]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        ts = [torch.empty(N, dtype=torch.float32, device="cuda") for _ in range(n)]
+        for t, h in zip(ts, hs):
+            t.copy_(h, non_blocking=True)
+        with arplan.Plan(n, N, "f32", "cps") as p:
+            p.execute(ts, s)
+            outs = [t.to("cpu", non_blocking=False) for t in ts]
+    s.synchronize()
+    for q in range(n):
+        assert np.array_equal(outs[q].numpy(), ref[q]), q
