@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <tuple>
 #include <new>
 #include <string>
 #include <vector>
@@ -25,10 +26,14 @@ namespace {
 constexpr int kCache = 4;               // pointer tables kept per device
 constexpr int64_t kMinUnits = 2048;     // shrink tiles until a launch has this many
 constexpr int64_t kMaxBlocks = int64_t(1) << 24;
-// Launches moving at least this many bytes stream through the caches with
-// nontemporal loads and stores; smaller ones keep their data cached for the
-// next phase.
+// Cache policy per launch (measured on MI355X).  Launches moving less than
+// kNtBytes keep everything cached.  Larger ones load nontemporally unless a
+// source range is read by more than one step of the launch (then the repeated
+// reads hit the cache), and store nontemporally unless the next phase reads
+// what they write and it is at most kKeepBytes, small enough to stay in the
+// 256 MiB last-level cache until then.
 constexpr int64_t kNtBytes = int64_t(64) << 20;
+constexpr int64_t kKeepBytes = int64_t(256) << 20;
 
 struct LaunchDesc {
     int32_t phase;
@@ -40,7 +45,7 @@ struct LaunchDesc {
     int64_t nunits;          // wave tiles
     int64_t tile_off;        // -1, or first entry of the device tile table
     int32_t wpb;             // wavefronts per block
-    bool nt;                 // nontemporal loads and stores
+    int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
 };
 
 struct PtrEntry {
@@ -84,6 +89,42 @@ struct ExecState {
     std::vector<DevState*> dev;  // indexed by device ordinal
 };
 
+// The element ranges a phase reads, per buffer, merged into disjoint sorted
+// intervals; answers "does the phase read anything of buf in [b, e)?".
+struct ReadSet {
+    std::vector<std::tuple<int32_t, int64_t, int64_t>> iv;  // (buf, begin, end)
+    ReadSet(const Plan& p, int32_t ph) {
+        if (ph >= p.num_phases()) return;
+        std::vector<std::tuple<int32_t, int64_t, int64_t>> raw;
+        for (int64_t i = p.phase_first[size_t(ph)]; i < p.phase_first[size_t(ph) + 1]; ++i) {
+            const Step& st = p.steps[size_t(i)];
+            if (st.end <= st.begin) continue;
+            for (int32_t t = 0; t < st.nsrc; ++t)
+                raw.emplace_back(p.srcs[size_t(st.src_off + t)], st.begin, st.end);
+        }
+        std::sort(raw.begin(), raw.end());
+        for (const auto& r : raw) {
+            if (!iv.empty() && std::get<0>(iv.back()) == std::get<0>(r) &&
+                std::get<1>(r) <= std::get<2>(iv.back()))
+                std::get<2>(iv.back()) = std::max(std::get<2>(iv.back()), std::get<2>(r));
+            else
+                iv.push_back(r);
+        }
+    }
+    bool reads(int32_t buf, int64_t b, int64_t e) const {
+        if (e <= b) return false;
+        // first interval of `buf` whose end is past b
+        auto it = std::lower_bound(iv.begin(), iv.end(), std::make_tuple(buf, b, b),
+                                   [](const std::tuple<int32_t, int64_t, int64_t>& a,
+                                      const std::tuple<int32_t, int64_t, int64_t>& k) {
+                                       return std::get<0>(a) != std::get<0>(k)
+                                                  ? std::get<0>(a) < std::get<0>(k)
+                                                  : std::get<2>(a) <= std::get<1>(k);
+                                   });
+        return it != iv.end() && std::get<0>(*it) == buf && std::get<1>(*it) < e;
+    }
+};
+
 // Group the steps of every phase by source count and choose the tiling of
 // each launch.  Host only.
 static void build_launches(const Plan& p, ExecState& ex) {
@@ -91,14 +132,21 @@ static void build_launches(const Plan& p, ExecState& ex) {
     for (int32_t ph = 0; ph < p.num_phases(); ++ph) {
         const int64_t s0 = p.phase_first[size_t(ph)];
         const int64_t s1 = p.phase_first[size_t(ph) + 1];
+        const ReadSet next(p, ph + 1);
         std::vector<int64_t> idx;
         for (int64_t i = s0; i < s1; ++i) idx.push_back(i);
         auto kof = [&](int64_t i) {
             const Step& s = p.steps[size_t(i)];
             return s.op == OP_COPY ? 1 : s.nsrc;
         };
-        std::stable_sort(idx.begin(), idx.end(),
-                         [&](int64_t a, int64_t b) { return kof(a) < kof(b); });
+        // group by source count; inside a group, steps reading the same
+        // source range become neighbours (their repeated reads share cache)
+        auto src0 = [&](int64_t i) { return p.srcs[size_t(p.steps[size_t(i)].src_off)]; };
+        std::stable_sort(idx.begin(), idx.end(), [&](int64_t a, int64_t b) {
+            if (kof(a) != kof(b)) return kof(a) < kof(b);
+            if (src0(a) != src0(b)) return src0(a) < src0(b);
+            return p.steps[size_t(a)].begin < p.steps[size_t(b)].begin;
+        });
         size_t g0 = 0;
         while (g0 < idx.size()) {
             size_t g1 = g0;
@@ -142,9 +190,28 @@ static void build_launches(const Plan& p, ExecState& ex) {
             while (te > tmin && units_for(te) < kMinUnits) te /= 2;
             while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
             L.wpb = cfg.WPB;
-            int64_t bytes = 0;
-            for (size_t g = g0; g < g1; ++g) bytes += step_bytes(p, p.steps[size_t(idx[g])]);
-            L.nt = bytes >= kNtBytes;
+            int64_t bytes = 0, written = 0;
+            std::vector<std::tuple<int32_t, int64_t, int64_t>> ranges;
+            for (size_t g = g0; g < g1; ++g) {
+                const Step& st = p.steps[size_t(idx[g])];
+                bytes += step_bytes(p, st);
+                written += (st.end - st.begin) * p.esize;
+                if (st.end > st.begin)
+                    for (int32_t t = 0; t < st.nsrc; ++t)
+                        ranges.emplace_back(p.srcs[size_t(st.src_off + t)], st.begin, st.end);
+            }
+            std::sort(ranges.begin(), ranges.end());
+            const bool reuse = std::adjacent_find(ranges.begin(), ranges.end()) != ranges.end();
+            L.cm = 0;
+            if (bytes >= kNtBytes) {
+                if (!reuse) L.cm |= 1;
+                bool next_reads = false;
+                for (size_t g = g0; g < g1 && !next_reads; ++g) {
+                    const Step& st = p.steps[size_t(idx[g])];
+                    next_reads = next.reads(st.dst, st.begin, st.end);
+                }
+                if (written > kKeepBytes || !next_reads) L.cm |= 2;
+            }
             L.tile_elems = te;
             L.tiles_per_step = (maxspan + te - 1) / te;
             int64_t used = 0;
@@ -323,33 +390,33 @@ static ar_status pointer_table(const Plan& p, DevState& d,
 }
 
 template <int DT, int K>
-static void launch_dk(bool vecok, bool nt, int64_t blocks, hipStream_t st,
+static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
                       const DevStep* steps, const int32_t* srcs, void* const* ptrs,
                       const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
     const dim3 grid(static_cast<uint32_t>(blocks)), block(64 * kcfg(K).WPB);
-    if (vecok && nt)
-        hipLaunchKernelGGL((phase_kernel<DT, K, true, true>), grid, block, 0, st, steps,
-                           srcs, ptrs, tiles, nunits, tps, te);
-    else if (vecok)
-        hipLaunchKernelGGL((phase_kernel<DT, K, true, false>), grid, block, 0, st, steps,
-                           srcs, ptrs, tiles, nunits, tps, te);
-    else
-        hipLaunchKernelGGL((phase_kernel<DT, K, false, false>), grid, block, 0, st, steps,
-                           srcs, ptrs, tiles, nunits, tps, te);
+#define AR_LAUNCH(V, C)                                                              \
+    hipLaunchKernelGGL((phase_kernel<DT, K, V, C>), grid, block, 0, st, steps, srcs, \
+                       ptrs, tiles, nunits, tps, te)
+    if (!vecok) AR_LAUNCH(false, 0);
+    else if (cm == 0) AR_LAUNCH(true, 0);
+    else if (cm == 1) AR_LAUNCH(true, 1);
+    else if (cm == 2) AR_LAUNCH(true, 2);
+    else AR_LAUNCH(true, 3);
+#undef AR_LAUNCH
 }
 
 template <int DT>
-static void launch_d(int K, bool vecok, bool nt, int64_t blocks, hipStream_t st,
+static void launch_d(int K, bool vecok, int cm, int64_t blocks, hipStream_t st,
                      const DevStep* steps, const int32_t* srcs, void* const* ptrs,
                      const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
     switch (K) {
-        case 1: launch_dk<DT, 1>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 2: launch_dk<DT, 2>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 3: launch_dk<DT, 3>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 4: launch_dk<DT, 4>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 8: launch_dk<DT, 8>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 16: launch_dk<DT, 16>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        default: launch_dk<DT, 0>(vecok, nt, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        default: launch_dk<DT, 0>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
     }
 }
 
@@ -402,15 +469,15 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
             switch (plan->dtype) {
                 case AR_F32:
-                    launch_d<DT_F32>(L.kern_k, pe->aligned, L.nt, blocks, stream, steps, d->srcs,
+                    launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->srcs,
                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
                 case AR_I32:
-                    launch_d<DT_I32>(L.kern_k, pe->aligned, L.nt, blocks, stream, steps, d->srcs,
+                    launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->srcs,
                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
                 default:
-                    launch_d<DT_BF16>(L.kern_k, pe->aligned, L.nt, blocks, stream, steps, d->srcs,
+                    launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->srcs,
                                       pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
             }

@@ -11,8 +11,9 @@
 // Inner loop.  Per iteration every lane moves U 16-byte vectors of each of
 // the K sources (global_load_dwordx4; the wave touches 1 KiB contiguous per
 // vector slot), folds them in source order in fp32 (bf16 widened; int32 with
-// wrap-around) and stores U vectors; large launches use nontemporal loads
-// and stores.  Unaligned head and tail elements of a
+// wrap-around) and stores U vectors.  Loads are nontemporal unless the launch
+// reads some range more than once, stores unless the launch's output is small
+// enough to stay cached for the next phase.  Unaligned head and tail elements of a
 // step are done element-wise.  The step descriptor, its source indices and
 // the buffer pointers are wave-uniform and live in scalar registers.
 #pragma once
@@ -44,11 +45,11 @@ struct KCfg {
     int U, WPB, TE;
 };
 __host__ __device__ constexpr KCfg kcfg(int K) {
-    return K == 1 ? KCfg{8, 8, 1024}
-         : K == 2 ? KCfg{4, 8, 1024}
+    return K == 1 ? KCfg{16, 8, 1024}
+         : K == 2 ? KCfg{8, 8, 1024}
          : K <= 4 && K > 0 ? KCfg{4, 4, 512}
          : K == 8 ? KCfg{2, 4, 256}
-         : K == 16 ? KCfg{1, 4, 512}
+         : K == 16 ? KCfg{1, 4, 256}
          : KCfg{4, 4, 256};
 }
 
@@ -65,8 +66,8 @@ __device__ __forceinline__ AR_GLOBAL T* as_global(void* p) {
     return (AR_GLOBAL T*)(p);
 }
 
-// Streaming loads and stores of whole vectors; NT marks them nontemporal
-// (large phases do not reuse what they read or write).
+// Vector loads and stores; NT marks them nontemporal (data that will not be
+// touched again soon streams past the caches).
 template <bool NT>
 __device__ __forceinline__ u32x4 vload(const gvec* p) {
     if constexpr (NT) return __builtin_nontemporal_load(p);
@@ -256,7 +257,9 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
 // U vectors per lane of K sources at vector offset `at` (+ u * 64 + lane),
 // folded in source order and stored.  FULL: all U vectors are in range, so
 // the loads are issued back to back with no per-vector branch.
-template <int DT, int K, int U, bool NT, bool FULL>
+// Cache mode CM of a launch: bit 0 = nontemporal loads, bit 1 = nontemporal
+// stores.
+template <int DT, int K, int U, int CM, bool FULL>
 __device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
                                              int64_t at, int64_t nv, int lane) {
     bool ok[U];
@@ -267,11 +270,11 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
     for (int j = 0; j < K; ++j)
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) x[j][u] = vload<NT>(sp[j] + at + u * 64 + lane);
+            if (ok[u]) x[j][u] = vload<(CM & 1) != 0>(sp[j] + at + u * 64 + lane);
     if constexpr (K == 1) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) vstore<NT>(d + at + u * 64 + lane, x[0][u]);
+            if (ok[u]) vstore<(CM & 2) != 0>(d + at + u * 64 + lane, x[0][u]);
     } else {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -279,13 +282,13 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
             acc.init(x[0][u]);
 #pragma unroll
             for (int j = 1; j < K; ++j) acc.add(x[j][u]);
-            if (ok[u]) vstore<NT>(d + at + u * 64 + lane, acc.out());
+            if (ok[u]) vstore<(CM & 2) != 0>(d + at + u * 64 + lane, acc.out());
         }
     }
 }
 
 // Runtime source count: one source at a time, U vectors in flight.
-template <int DT, int U, bool NT, bool FULL>
+template <int DT, int U, int CM, bool FULL>
 __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
                                                 const int32_t* __restrict__ srcl,
                                                 int k, int64_t v0, gvec* d,
@@ -299,7 +302,7 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
         u32x4 x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) x[u] = vload<NT>(s0 + at + u * 64 + lane);
+            if (ok[u]) x[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
 #pragma unroll
         for (int u = 0; u < U; ++u) acc[u].init(x[u]);
     }
@@ -308,19 +311,19 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
         u32x4 x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) x[u] = vload<NT>(sj + at + u * 64 + lane);
+            if (ok[u]) x[u] = vload<(CM & 1) != 0>(sj + at + u * 64 + lane);
 #pragma unroll
         for (int u = 0; u < U; ++u) acc[u].add(x[u]);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
-        if (ok[u]) vstore<NT>(d + at + u * 64 + lane, acc[u].out());
+        if (ok[u]) vstore<(CM & 2) != 0>(d + at + u * 64 + lane, acc[u].out());
 }
 
 // One launch: `nunits` wave tiles over the steps steps[0..).  K = 0 means
 // the source count is read from each step (any k >= 1).  VECOK: every
-// buffer is 16-byte aligned.  NT: nontemporal vector loads and stores.
-template <int DT, int K, bool VECOK, bool NT>
+// buffer is 16-byte aligned.  CM: cache mode of the vector loads and stores.
+template <int DT, int K, bool VECOK, int CM>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const DevStep* __restrict__ steps, const int32_t* __restrict__ srcs,
     void* const* __restrict__ ptrs, const int2* __restrict__ tiles,
@@ -355,12 +358,12 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
 #pragma unroll
         for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(ptrs[srcl[j]]) + v0;
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors<DT, K, U, NT, true>(sv, d, at, nv, lane);
-        if (at < nv) fold_vectors<DT, K, U, NT, false>(sv, d, at, nv, lane);
+            fold_vectors<DT, K, U, CM, true>(sv, d, at, nv, lane);
+        if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, d, at, nv, lane);
     } else {
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors_rt<DT, U, NT, true>(ptrs, srcl, k, v0, d, at, nv, lane);
-        if (at < nv) fold_vectors_rt<DT, U, NT, false>(ptrs, srcl, k, v0, d, at, nv, lane);
+            fold_vectors_rt<DT, U, CM, true>(ptrs, srcl, k, v0, d, at, nv, lane);
+        if (at < nv) fold_vectors_rt<DT, U, CM, false>(ptrs, srcl, k, v0, d, at, nv, lane);
     }
 }
 
