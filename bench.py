@@ -10,10 +10,10 @@ work: fp32 adds take the same time whatever the operands).
 
 Prints one JSON line:
   value       AllReduce algorithm bandwidth n * N * e / time, GB/s
-  roofline    the reduce-phase kernel: algorithmic bytes per launch
-              ((k + 1) * len * e per k-way reduce step) over its mean
-              launch duration (HIP events on the launch stream), against
-              MI355X's 8 TB/s HBM peak
+  roofline    the reduce launches of the phase kernel: algorithmic bytes per
+              launch ((k + d) * len * e per step folding k sources into d
+              destinations) over their mean duration (HIP events on the
+              launch stream), against MI355X's 8 TB/s HBM peak
   cpu_baseline  the CPU oracle executing the same plan on the host
 """
 
@@ -84,6 +84,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default=DEFAULT)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="run every plan step as listed (AR_OPT_FUSE = 0)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build executes every emulated processor on one "
@@ -113,12 +115,10 @@ def main():
     del xs
 
     plan = arplan.Plan(n, N, dt, c["kind"], c["fanin"])
+    if args.no_fuse:
+        plan.set_option(arplan.AR_OPT_FUSE, 0)
     stream = torch.cuda.current_stream()
-    phase_ops, phase_bytes = [], []
-    for ph in range(plan.num_phases):
-        op, _, _, b = plan.phase_info(ph)
-        phase_ops.append(op)
-        phase_bytes.append(b)
+    launches = plan.launches()          # (phase, nsrc, max_dst, steps, bytes)
     red_b, cpy_b = plan.bytes()
 
     def restore():
@@ -130,7 +130,8 @@ def main():
         plan.execute(bufs, stream)
     restore()
     K = args.steps
-    timer = arplan.ar_timer_create(max(1, K * plan.num_phases * 2))
+    cap = max(1, K * len(launches))
+    timer = arplan.ar_timer_create(cap)
     torch.cuda.synchronize()
     print("bench: timing %d steps" % K, file=sys.stderr, flush=True)
     t0 = time.perf_counter()
@@ -138,31 +139,31 @@ def main():
         plan.execute_timed(bufs, stream, timer)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    recs = arplan.ar_timer_read(timer, K * plan.num_phases * 2)
+    recs = arplan.ar_timer_read(timer, cap)
     arplan.ar_timer_destroy(timer)
 
     ms_step = (t1 - t0) * 1e3 / K
     total = n * N * esize
     value = total / (ms_step * 1e-3) / 1e9
 
-    ph_ms = [0.0] * plan.num_phases
-    for ph, ms in recs:
-        ph_ms[ph] += ms / K
-    red_ms = sum(m for m, op in zip(ph_ms, phase_ops) if op == arplan.AR_OP_REDUCE)
-    n_red = sum(1 for op in phase_ops if op == arplan.AR_OP_REDUCE)
-    kern_ms = sum(ph_ms)
-    achieved = red_b / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
-    traffic = load_traffic(name)
+    l_ms = [0.0] * len(launches)
+    for li, ms in recs:
+        l_ms[li] += ms / K
+    # dominant kernel: the launches that reduce (k >= 2 sources)
+    red = [i for i, L in enumerate(launches) if L[1] >= 2]
+    red_ms = sum(l_ms[i] for i in red)
+    red_bytes = sum(launches[i][4] for i in red)
+    achieved = red_bytes / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
+    traffic = load_traffic(name) if not args.no_fuse else None
     roofline = {"bound": "hbm", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
-                "kernel": "phase_kernel (reduce phases, k=%s)" % (
-                    sorted({len(s[3]) for s in plan.steps()
-                            if s[1] == arplan.AR_OP_REDUCE}) or "-"),
-                "launches_per_step": n_red,
-                "bytes_per_launch": round(red_b / max(1, n_red)),
-                "ms_per_launch": round(red_ms / max(1, n_red), 5)}
+                "kernel": "phase_kernel, reduce launches (k = %s)" % (
+                    sorted({launches[i][1] for i in red}) or "-"),
+                "launches_per_step": len(red),
+                "bytes_per_launch": round(red_bytes / max(1, len(red))),
+                "ms_per_launch": round(red_ms / max(1, len(red)), 5)}
     out = {
         "metric": "AllReduce algbw GB/s and % HBM roofline per plan at 1 MI355X",
         "value": round(value, 2),
@@ -178,15 +179,17 @@ def main():
         "data": "synthetic (seeded %s inputs)" % c["dist"],
         "config": {"workload": name, "plan": c["kind"], "n": n, "N": N,
                    "fanin": list(c["fanin"]) if c["fanin"] else None,
+                   "fuse": not args.no_fuse,
                    "parallelism": "emulated %d processors on 1 GPU" % n},
         "plan_bytes_per_step": red_b + cpy_b,
         "plan_gbs": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9, 1),
-        "plan_frac": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-        "kernel_ms_per_step": round(kern_ms, 5),
-        "phases": [{"phase": i, "op": "reduce" if op == 0 else "copy",
-                    "bytes": b, "ms": round(m, 5),
-                    "gbs": round(b / (m * 1e-3) / 1e9, 1) if m > 0 else None}
-                   for i, (op, b, m) in enumerate(zip(phase_ops, phase_bytes, ph_ms))],
+        "kernel_bytes_per_step": sum(L[4] for L in launches),
+        "kernel_gbs": round(sum(L[4] for L in launches) / (ms_step * 1e-3) / 1e9, 1),
+        "kernel_ms_per_step": round(sum(l_ms), 5),
+        "launches": [{"phase": L[0], "k": L[1], "max_dst": L[2], "steps": L[3],
+                      "bytes": L[4], "ms": round(m, 5),
+                      "gbs": round(L[4] / (m * 1e-3) / 1e9, 1) if m > 0 else None}
+                     for L, m in zip(launches, l_ms)],
         "roofline": roofline,
         "cpu_baseline": None,
     }

@@ -154,9 +154,10 @@ ar_status ar_plan_destroy(ar_plan* plan);
  * device, each to at least N * element-size bytes, pairwise non-overlapping
  * (checked on the host: AR_ERR_INVALID_ARG for NULL or overlapping
  * buffers).  `stream` is a hipStream_t (NULL = the default stream).  The
- * call is asynchronous and stream-ordered: it enqueues one kernel launch per
- * phase (more only for phases mixing source counts) and returns; when the
- * stream reaches that point every buffer holds the AllReduce result.  The
+ * call is asynchronous and stream-ordered: it enqueues about one kernel
+ * launch per phase (see ar_plan_num_launches) and returns; when the stream
+ * reaches that point every buffer holds the AllReduce result, bit for bit
+ * the result of running the steps phase by phase as listed.  The
  * pointer array is read during the call only.  Any pointer alignment works;
  * 16-byte-aligned buffers take the vector path.  The first call on a device
  * uploads the plan's step tables (device memory owned by the plan).
@@ -175,6 +176,33 @@ ar_status ar_plan_execute_strided(ar_plan* plan, void* base,
  * when the timer is full).  Results are read with ar_timer_read. */
 ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
                                 void* stream, ar_timer* timer);
+
+/* Executor options (ar_plan_set_option).
+ *  AR_OPT_FUSE (default 1): let the executor merge steps where that removes
+ *  memory traffic without changing any result bit:
+ *   - copies of one phase that read the same range of the same buffer run
+ *     as one step that reads it once and stores it to every destination;
+ *   - a copy of a range that a reduce step of the previous phase has just
+ *     produced is absorbed into that reduce step, which stores its result to
+ *     the copy's destination too (where the last ReduceScatter phase meets
+ *     the first AllGather phase), provided no other step of that phase
+ *     touches the absorbed destination range.
+ *  With 0, every plan step runs as listed, one launch per phase and source
+ *  count.  Changing an option drops the plan's device state; it must not
+ *  be done while an execution of the plan may still be running. */
+typedef enum ar_option { AR_OPT_FUSE = 0 } ar_option;
+ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value);
+
+/* The kernel launches one execution issues (host only, no GPU call): their
+ * number, and for launch i the plan phase its steps come from, their
+ * source count, the most destinations any of its steps stores to, its
+ * number of steps and its algorithmic bytes: (k + destinations) * len * e
+ * summed over its steps (each source read once, each destination written
+ * once).  Any out-pointer may be NULL. */
+ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count);
+ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t* phase,
+                              int32_t* nsrc, int32_t* max_dst,
+                              int64_t* num_steps, int64_t* bytes);
 
 /* -------------------------------------------------------- introspection */
 
@@ -213,12 +241,13 @@ ar_status ar_plan_bytes(const ar_plan* plan, int64_t* reduce_bytes,
  * events are created on first use, on the device current at that time. */
 ar_status ar_timer_create(int64_t capacity, ar_timer** out);
 ar_status ar_timer_reset(ar_timer* timer);          /* forget all records */
-/* Wait for the recorded events and copy out up to `cap` records: phase[i]
- * is the plan phase of launch i and ms[i] its duration in milliseconds
- * (begin-to-end event time on the launch stream).  *count receives the
- * number of records copied.  phase or ms may be NULL. */
+/* Wait for the recorded events and copy out up to `cap` records: launch[i]
+ * is the index (as in ar_plan_launch_info) of the launch record i timed and
+ * ms[i] its duration in milliseconds (begin-to-end event time on the launch
+ * stream).  *count receives the number of records copied.  launch or ms may
+ * be NULL. */
 ar_status ar_timer_read(ar_timer* timer, int64_t cap, int64_t* count,
-                        int32_t* phase, float* ms);
+                        int32_t* launch, float* ms);
 ar_status ar_timer_destroy(ar_timer* timer);        /* NULL is a no-op */
 
 /* -------------------------------------------------------------- errors */

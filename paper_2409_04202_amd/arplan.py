@@ -37,6 +37,7 @@ AR_OK, AR_ERR_INVALID_ARG, AR_ERR_UNSUPPORTED, AR_ERR_OOM, AR_ERR_HIP, \
 AR_F32, AR_I32, AR_BF16 = range(3)
 AR_RING, AR_RHD, AR_CPS, AR_TREE, AR_RB = range(5)
 AR_OP_REDUCE, AR_OP_COPY = range(2)
+AR_OPT_FUSE = 0
 
 DTYPES = {"f32": AR_F32, "i32": AR_I32, "bf16": AR_BF16}
 KINDS = {"ring": AR_RING, "rhd": AR_RHD, "cps": AR_CPS, "tree": AR_TREE,
@@ -72,6 +73,10 @@ _sig = {
                            POINTER(c_int64), POINTER(c_int64)],
     "ar_plan_owner": [_P, c_int32, POINTER(c_int64), POINTER(c_int64)],
     "ar_plan_bytes": [_P, POINTER(c_int64), POINTER(c_int64)],
+    "ar_plan_set_option": [_P, c_int32, c_int64],
+    "ar_plan_num_launches": [_P, POINTER(c_int32)],
+    "ar_plan_launch_info": [_P, c_int32, POINTER(c_int32), POINTER(c_int32),
+                            POINTER(c_int32), POINTER(c_int64), POINTER(c_int64)],
     "ar_timer_create": [c_int64, POINTER(_P)],
     "ar_timer_reset": [_P],
     "ar_timer_read": [_P, c_int64, POINTER(c_int64), POINTER(c_int32),
@@ -224,6 +229,25 @@ def ar_plan_bytes(plan):
     return r.value, c.value
 
 
+def ar_plan_set_option(plan, option, value):
+    _check(_lib.ar_plan_set_option(plan, int(option), int(value)))
+
+
+def ar_plan_num_launches(plan):
+    c = c_int32()
+    _check(_lib.ar_plan_num_launches(plan, ctypes.byref(c)))
+    return c.value
+
+
+def ar_plan_launch_info(plan, i):
+    """(phase, nsrc, max_dst, num_steps, bytes)"""
+    ph, k, d, n, b = c_int32(), c_int32(), c_int32(), c_int64(), c_int64()
+    _check(_lib.ar_plan_launch_info(plan, int(i), ctypes.byref(ph),
+                                    ctypes.byref(k), ctypes.byref(d),
+                                    ctypes.byref(n), ctypes.byref(b)))
+    return ph.value, k.value, d.value, n.value, b.value
+
+
 # ---------------------------------------------------------------- timing
 
 def ar_timer_create(capacity):
@@ -237,7 +261,7 @@ def ar_timer_reset(timer):
 
 
 def ar_timer_read(timer, cap):
-    """Returns a list of (phase, ms) for up to ``cap`` records."""
+    """Returns a list of (launch index, ms) for up to ``cap`` records."""
     cnt = c_int64()
     ph = (c_int32 * max(1, cap))()
     ms = (c_float * max(1, cap))()
@@ -288,6 +312,14 @@ class Plan:
 
     def bytes(self):
         return ar_plan_bytes(self.handle)
+
+    def set_option(self, option, value):
+        ar_plan_set_option(self.handle, option, value)
+
+    def launches(self):
+        """[(phase, nsrc, max_dst, num_steps, bytes)] per kernel launch."""
+        return [ar_plan_launch_info(self.handle, i)
+                for i in range(ar_plan_num_launches(self.handle))]
 
     def close(self):
         if self.handle:

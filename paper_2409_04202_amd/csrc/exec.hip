@@ -11,6 +11,8 @@
 
 #include <algorithm>
 #include <cstring>
+#include <map>
+#include <memory>
 #include <tuple>
 #include <new>
 #include <string>
@@ -34,6 +36,14 @@ constexpr int64_t kMaxBlocks = int64_t(1) << 24;
 // 256 MiB last-level cache until then.
 constexpr int64_t kNtBytes = int64_t(64) << 20;
 constexpr int64_t kKeepBytes = int64_t(256) << 20;
+// The step rewrites (multicast, reduce-then-broadcast) pay off where they
+// remove a launch from a short phase, or add at most one extra destination;
+// a step storing to many destinations over a large range is store-bound and
+// slower than plain copies whose repeated reads hit the cache.  A rewrite
+// is applied when its step ends with at most kFuseDst destinations or the
+// copies it takes over move at most kFuseBytes (2 * len * e each).
+constexpr int32_t kFuseDst = 2;
+constexpr int64_t kFuseBytes = int64_t(256) << 20;
 
 struct LaunchDesc {
     int32_t phase;
@@ -46,6 +56,8 @@ struct LaunchDesc {
     int64_t tile_off;        // -1, or first entry of the device tile table
     int32_t wpb;             // wavefronts per block
     int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
+    int32_t max_dst;         // most destinations of a step
+    int64_t bytes;           // (k + destinations) * len * e over the steps
 };
 
 struct PtrEntry {
@@ -61,7 +73,7 @@ struct PtrEntry {
 struct DevState {
     int device = -1;
     DevStep* steps = nullptr;
-    int32_t* srcs = nullptr;
+    int32_t* idx = nullptr;  // source and destination indices of the steps
     int2* tiles = nullptr;
     PtrEntry cache[kCache];
     uint64_t clock = 0;
@@ -81,100 +93,265 @@ std::string hip_msg(const char* what, hipError_t e) {
 
 }  // namespace
 
+// An executed step (host form): fold `srcs` over [begin, end) and store the
+// result into every destination.  Plan steps map one to one onto executed
+// steps unless the rewrites below merge them.
+struct XStep {
+    int64_t begin, end;
+    std::vector<int32_t> srcs;
+    std::vector<int32_t> dsts;
+};
+
+struct XPhase {
+    int32_t plan_phase;  // phase of the plan these steps come from
+    std::vector<XStep> steps;
+};
+
 struct ExecState {
+    std::vector<XPhase> phases;  // executed phases, after the rewrites
     std::vector<LaunchDesc> launches;
     std::vector<DevStep> hsteps;
-    std::vector<int32_t> hsrcs;
+    std::vector<int32_t> hidx;   // source and destination indices
     std::vector<int2> htiles;
     std::vector<DevState*> dev;  // indexed by device ordinal
 };
 
-// The element ranges a phase reads, per buffer, merged into disjoint sorted
-// intervals; answers "does the phase read anything of buf in [b, e)?".
-struct ReadSet {
-    std::vector<std::tuple<int32_t, int64_t, int64_t>> iv;  // (buf, begin, end)
-    ReadSet(const Plan& p, int32_t ph) {
-        if (ph >= p.num_phases()) return;
-        std::vector<std::tuple<int32_t, int64_t, int64_t>> raw;
-        for (int64_t i = p.phase_first[size_t(ph)]; i < p.phase_first[size_t(ph) + 1]; ++i) {
-            const Step& st = p.steps[size_t(i)];
+// Every (buffer, range) a phase touches, with the step touching it; answers
+// "does a step other than `self` touch buf within [b, e)?".
+struct Touches {
+    struct Iv { int32_t buf; int64_t b, e; size_t step; };
+    std::vector<Iv> iv;
+    std::vector<int64_t> maxlen;  // longest interval per buffer
+    Touches(const XPhase& ph, int32_t n, bool reads, bool writes) : maxlen(size_t(n), 0) {
+        for (size_t i = 0; i < ph.steps.size(); ++i) {
+            const XStep& st = ph.steps[i];
             if (st.end <= st.begin) continue;
-            for (int32_t t = 0; t < st.nsrc; ++t)
-                raw.emplace_back(p.srcs[size_t(st.src_off + t)], st.begin, st.end);
+            if (reads) for (int32_t q : st.srcs) iv.push_back({q, st.begin, st.end, i});
+            if (writes) for (int32_t q : st.dsts) iv.push_back({q, st.begin, st.end, i});
         }
-        std::sort(raw.begin(), raw.end());
-        for (const auto& r : raw) {
-            if (!iv.empty() && std::get<0>(iv.back()) == std::get<0>(r) &&
-                std::get<1>(r) <= std::get<2>(iv.back()))
-                std::get<2>(iv.back()) = std::max(std::get<2>(iv.back()), std::get<2>(r));
-            else
-                iv.push_back(r);
-        }
+        std::sort(iv.begin(), iv.end(), [](const Iv& x, const Iv& y) {
+            return x.buf != y.buf ? x.buf < y.buf : x.b < y.b;
+        });
+        for (const Iv& x : iv) maxlen[size_t(x.buf)] = std::max(maxlen[size_t(x.buf)], x.e - x.b);
     }
-    bool reads(int32_t buf, int64_t b, int64_t e) const {
+    bool other(int32_t buf, int64_t b, int64_t e, size_t self) const {
         if (e <= b) return false;
-        // first interval of `buf` whose end is past b
-        auto it = std::lower_bound(iv.begin(), iv.end(), std::make_tuple(buf, b, b),
-                                   [](const std::tuple<int32_t, int64_t, int64_t>& a,
-                                      const std::tuple<int32_t, int64_t, int64_t>& k) {
-                                       return std::get<0>(a) != std::get<0>(k)
-                                                  ? std::get<0>(a) < std::get<0>(k)
-                                                  : std::get<2>(a) <= std::get<1>(k);
+        const int64_t from = b - maxlen[size_t(buf)];
+        auto it = std::lower_bound(iv.begin(), iv.end(), std::make_pair(buf, from),
+                                   [](const Iv& x, const std::pair<int32_t, int64_t>& k) {
+                                       return x.buf != k.first ? x.buf < k.first : x.b < k.second;
                                    });
-        return it != iv.end() && std::get<0>(*it) == buf && std::get<1>(*it) < e;
+        for (; it != iv.end() && it->buf == buf && it->b < e; ++it)
+            if (it->e > b && it->step != self) return true;
+        return false;
+    }
+    bool any(int32_t buf, int64_t b, int64_t e) const {
+        return other(buf, b, e, size_t(-1));
     }
 };
 
-// Group the steps of every phase by source count and choose the tiling of
-// each launch.  Host only.
+// Executed phases of a plan.  With `fuse`, two rewrites remove memory
+// traffic or launches without changing any result (subject to kFuseDst /
+// kFuseBytes above):
+//  * multicast: copies in one phase that read the same range of the same
+//    buffer become one step that reads it once and stores it to every
+//    destination;
+//  * reduce-then-broadcast: when every step of phase q+1 copies a range that
+//    a reduce step of phase q has just produced, the copies are absorbed into
+//    those reduce steps, which then store their results to the copies'
+//    destinations as well, and phase q+1 disappears (the last ReduceScatter
+//    phase and the first AllGather phase meet this way).  The absorbed
+//    writes are checked against every read and write of the other steps of
+//    phase q, so the merged phase stays free of hazards.
+static std::vector<XPhase> exec_phases(const Plan& p, bool fuse) {
+    std::vector<XPhase> ph(size_t(p.num_phases()));
+    for (int32_t q = 0; q < p.num_phases(); ++q) {
+        ph[size_t(q)].plan_phase = q;
+        for (int64_t i = p.phase_first[size_t(q)]; i < p.phase_first[size_t(q) + 1]; ++i) {
+            const Step& st = p.steps[size_t(i)];
+            XStep x;
+            x.begin = st.begin;
+            x.end = st.end;
+            x.srcs.assign(p.srcs.begin() + st.src_off, p.srcs.begin() + st.src_off + st.nsrc);
+            x.dsts = {st.dst};
+            ph[size_t(q)].steps.push_back(std::move(x));
+        }
+    }
+    if (!fuse) return ph;
+    auto copy_bytes = [&](const XPhase& xp) {
+        int64_t b = 0;
+        for (const XStep& x : xp.steps)
+            if (x.srcs.size() == 1) b += 2 * int64_t(x.dsts.size()) * (x.end - x.begin) * p.esize;
+        return b;
+    };
+    for (XPhase& xp : ph) {  // multicast
+        const bool small = copy_bytes(xp) <= kFuseBytes;
+        std::map<std::tuple<int32_t, int64_t, int64_t>, size_t> first;
+        std::vector<XStep> kept;
+        for (XStep& x : xp.steps) {
+            if (x.srcs.size() == 1 && x.end > x.begin) {
+                auto key = std::make_tuple(x.srcs[0], x.begin, x.end);
+                auto it = first.find(key);
+                if (it != first.end()) {
+                    XStep& m = kept[it->second];
+                    m.dsts.insert(m.dsts.end(), x.dsts.begin(), x.dsts.end());
+                    continue;
+                }
+                first.emplace(key, kept.size());
+            }
+            kept.push_back(std::move(x));
+        }
+        if (!small) {  // undo groups that grew past kFuseDst destinations
+            std::vector<XStep> undone;
+            for (XStep& x : kept) {
+                if (x.srcs.size() == 1 && int32_t(x.dsts.size()) > kFuseDst) {
+                    for (int32_t d : x.dsts) {
+                        XStep y;
+                        y.begin = x.begin;
+                        y.end = x.end;
+                        y.srcs = x.srcs;
+                        y.dsts = {d};
+                        undone.push_back(std::move(y));
+                    }
+                } else {
+                    undone.push_back(std::move(x));
+                }
+            }
+            kept = std::move(undone);
+        }
+        xp.steps = std::move(kept);
+    }
+    for (size_t q = 0; q + 1 < ph.size(); ++q) {  // reduce-then-broadcast
+        XPhase& cur = ph[q];
+        XPhase& nxt = ph[q + 1];
+        const Touches touched(cur, p.n, true, true);
+        std::map<std::tuple<int32_t, int64_t, int64_t>, size_t> produced;
+        for (size_t i = 0; i < cur.steps.size(); ++i) {
+            const XStep& st = cur.steps[i];
+            if (st.srcs.size() >= 2 && st.end > st.begin)
+                for (int32_t d : st.dsts) produced[std::make_tuple(d, st.begin, st.end)] = i;
+        }
+        // absorb the whole next phase or nothing: only then a launch goes
+        const bool small = copy_bytes(nxt) <= kFuseBytes;
+        std::vector<size_t> into(nxt.steps.size());
+        std::vector<size_t> extra(cur.steps.size(), 0);
+        bool all = !nxt.steps.empty();
+        for (size_t j = 0; j < nxt.steps.size() && all; ++j) {
+            const XStep& c = nxt.steps[j];
+            into[j] = size_t(-1);
+            if (c.end <= c.begin) continue;  // empty step: nothing to move
+            auto it = c.srcs.size() == 1
+                          ? produced.find(std::make_tuple(c.srcs[0], c.begin, c.end))
+                          : produced.end();
+            if (it == produced.end()) {
+                all = false;
+                break;
+            }
+            for (int32_t d : c.dsts)
+                if (touched.other(d, c.begin, c.end, it->second)) all = false;
+            into[j] = it->second;
+            extra[it->second] += c.dsts.size();
+        }
+        for (size_t i = 0; i < cur.steps.size() && all; ++i)
+            if (!small && int32_t(cur.steps[i].dsts.size() + extra[i]) > kFuseDst) all = false;
+        if (!all) continue;
+        for (size_t j = 0; j < nxt.steps.size(); ++j) {
+            if (into[j] == size_t(-1)) continue;
+            XStep& s = cur.steps[into[j]];
+            for (int32_t d : nxt.steps[j].dsts)
+                if (std::find(s.dsts.begin(), s.dsts.end(), d) == s.dsts.end())
+                    s.dsts.push_back(d);
+        }
+        nxt.steps.clear();
+    }
+    std::vector<XPhase> out;
+    for (XPhase& xp : ph)
+        if (!xp.steps.empty()) out.push_back(std::move(xp));
+    return out;
+}
+
+// Is every executed phase free of hazards?  A step may read and write the
+// same positions (each lane loads all sources before storing); otherwise no
+// step may touch what another step of its phase writes.
+static bool exec_phases_hazard_free(const std::vector<XPhase>& ph, int32_t n, std::string& why) {
+    for (size_t q = 0; q < ph.size(); ++q) {
+        const Touches all(ph[q], n, true, true);
+        for (size_t i = 0; i < ph[q].steps.size(); ++i) {
+            const XStep& st = ph[q].steps[i];
+            for (int32_t d : st.dsts)
+                if (all.other(d, st.begin, st.end, i)) {
+                    why = "executed phase " + std::to_string(q) + ": step " + std::to_string(i) +
+                          " writes what another step touches";
+                    return false;
+                }
+        }
+    }
+    return true;
+}
+
+// Group the steps of every executed phase by source count, choose the
+// tiling and the cache mode of each launch.  Host only.
 static void build_launches(const Plan& p, ExecState& ex) {
     const int64_t VEC = 16 / p.esize;
-    for (int32_t ph = 0; ph < p.num_phases(); ++ph) {
-        const int64_t s0 = p.phase_first[size_t(ph)];
-        const int64_t s1 = p.phase_first[size_t(ph) + 1];
-        const ReadSet next(p, ph + 1);
-        std::vector<int64_t> idx;
-        for (int64_t i = s0; i < s1; ++i) idx.push_back(i);
-        auto kof = [&](int64_t i) {
-            const Step& s = p.steps[size_t(i)];
-            return s.op == OP_COPY ? 1 : s.nsrc;
-        };
-        // group by source count; inside a group, steps reading the same
-        // source range become neighbours (their repeated reads share cache)
-        auto src0 = [&](int64_t i) { return p.srcs[size_t(p.steps[size_t(i)].src_off)]; };
-        std::stable_sort(idx.begin(), idx.end(), [&](int64_t a, int64_t b) {
-            if (kof(a) != kof(b)) return kof(a) < kof(b);
-            if (src0(a) != src0(b)) return src0(a) < src0(b);
-            return p.steps[size_t(a)].begin < p.steps[size_t(b)].begin;
+    for (size_t q = 0; q < ex.phases.size(); ++q) {
+        const XPhase& xp = ex.phases[q];
+        std::unique_ptr<Touches> next_reads;
+        if (q + 1 < ex.phases.size())
+            next_reads.reset(new Touches(ex.phases[q + 1], p.n, true, false));
+        std::vector<size_t> idx(xp.steps.size());
+        for (size_t i = 0; i < idx.size(); ++i) idx[i] = i;
+        // group by source count; inside a group, steps reading the same source
+        // become neighbours (their repeated reads share cache)
+        std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) {
+            const XStep& x = xp.steps[a];
+            const XStep& y = xp.steps[b];
+            if (x.srcs.size() != y.srcs.size()) return x.srcs.size() < y.srcs.size();
+            if (x.srcs[0] != y.srcs[0]) return x.srcs[0] < y.srcs[0];
+            return x.begin < y.begin;
         });
         size_t g0 = 0;
         while (g0 < idx.size()) {
             size_t g1 = g0;
-            const int32_t k = kof(idx[g0]);
-            while (g1 < idx.size() && kof(idx[g1]) == k) ++g1;
+            const int32_t k = int32_t(xp.steps[idx[g0]].srcs.size());
+            while (g1 < idx.size() && int32_t(xp.steps[idx[g1]].srcs.size()) == k) ++g1;
             LaunchDesc L{};
-            L.phase = ph;
+            L.phase = xp.plan_phase;
             L.kern_k = kernel_k(k);
             L.first = int64_t(ex.hsteps.size());
             L.count = int64_t(g1 - g0);
-            int64_t maxspan = 0;
+            int64_t maxspan = 0, bytes = 0, written = 0;
+            int32_t maxdst = 0;
             std::vector<int64_t> spans;
+            std::vector<std::tuple<int32_t, int64_t, int64_t>> ranges;
+            bool next_reads_output = false;
             for (size_t g = g0; g < g1; ++g) {
-                const Step& s = p.steps[size_t(idx[g])];
+                const XStep& x = xp.steps[idx[g]];
                 DevStep d{};
-                d.begin = s.begin;
-                d.end = s.end;
-                d.dst = s.dst;
-                d.src_off = int32_t(ex.hsrcs.size());
+                d.begin = x.begin;
+                d.end = x.end;
                 d.k = k;
-                for (int32_t t = 0; t < s.nsrc; ++t)
-                    ex.hsrcs.push_back(p.srcs[size_t(s.src_off + t)]);
+                d.src_off = int32_t(ex.hidx.size());
+                ex.hidx.insert(ex.hidx.end(), x.srcs.begin(), x.srcs.end());
+                d.ndst = int32_t(x.dsts.size());
+                d.dst_off = int32_t(ex.hidx.size());
+                ex.hidx.insert(ex.hidx.end(), x.dsts.begin(), x.dsts.end());
                 ex.hsteps.push_back(d);
-                const int64_t span =
-                    s.end > s.begin ? s.end - (s.begin & ~(VEC - 1)) : 0;
+                const int64_t len = x.end - x.begin;
+                const int64_t span = len > 0 ? x.end - (x.begin & ~(VEC - 1)) : 0;
                 spans.push_back(span);
                 maxspan = std::max(maxspan, span);
+                maxdst = std::max(maxdst, int32_t(x.dsts.size()));
+                bytes += (k + int64_t(x.dsts.size())) * len * p.esize;
+                written += int64_t(x.dsts.size()) * len * p.esize;
+                if (len > 0) {
+                    for (int32_t sidx : x.srcs) ranges.emplace_back(sidx, x.begin, x.end);
+                    if (next_reads)
+                        for (int32_t dd : x.dsts)
+                            next_reads_output = next_reads_output || next_reads->any(dd, x.begin, x.end);
+                }
             }
+            L.bytes = bytes;
+            L.max_dst = maxdst;
             if (maxspan == 0) {  // nothing to move in this group
                 g0 = g1;
                 continue;
@@ -190,27 +367,12 @@ static void build_launches(const Plan& p, ExecState& ex) {
             while (te > tmin && units_for(te) < kMinUnits) te /= 2;
             while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
             L.wpb = cfg.WPB;
-            int64_t bytes = 0, written = 0;
-            std::vector<std::tuple<int32_t, int64_t, int64_t>> ranges;
-            for (size_t g = g0; g < g1; ++g) {
-                const Step& st = p.steps[size_t(idx[g])];
-                bytes += step_bytes(p, st);
-                written += (st.end - st.begin) * p.esize;
-                if (st.end > st.begin)
-                    for (int32_t t = 0; t < st.nsrc; ++t)
-                        ranges.emplace_back(p.srcs[size_t(st.src_off + t)], st.begin, st.end);
-            }
             std::sort(ranges.begin(), ranges.end());
             const bool reuse = std::adjacent_find(ranges.begin(), ranges.end()) != ranges.end();
             L.cm = 0;
             if (bytes >= kNtBytes) {
                 if (!reuse) L.cm |= 1;
-                bool next_reads = false;
-                for (size_t g = g0; g < g1 && !next_reads; ++g) {
-                    const Step& st = p.steps[size_t(idx[g])];
-                    next_reads = next.reads(st.dst, st.begin, st.end);
-                }
-                if (written > kKeepBytes || !next_reads) L.cm |= 2;
+                if (written > kKeepBytes || !next_reads_output) L.cm |= 2;
             }
             L.tile_elems = te;
             L.tiles_per_step = (maxspan + te - 1) / te;
@@ -239,6 +401,7 @@ static ExecState* exec_state(Plan& p) {
     if (!p.exec) {
         ExecState* ex = new ExecState();
         try {
+            ex->phases = exec_phases(p, p.fuse != 0);
             build_launches(p, *ex);
         } catch (...) {
             delete ex;
@@ -255,7 +418,7 @@ static void free_dev(DevState* d) {
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(d->device);
     if (d->steps) (void)hipFree(d->steps);
-    if (d->srcs) (void)hipFree(d->srcs);
+    if (d->idx) (void)hipFree(d->idx);
     if (d->tiles) (void)hipFree(d->tiles);
     for (PtrEntry& e : d->cache) {
         if (e.done) {
@@ -301,7 +464,7 @@ static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
         DevState* d = new DevState();
         d->device = dev;
         ar_status s = upload(&d->steps, ex.hsteps, "step table");
-        if (s == AR_OK) s = upload(&d->srcs, ex.hsrcs, "source table");
+        if (s == AR_OK) s = upload(&d->idx, ex.hidx, "index table");
         if (s == AR_OK) s = upload(&d->tiles, ex.htiles, "tile table");
         if (s != AR_OK) {
             free_dev(d);
@@ -426,7 +589,7 @@ struct ar_timer {
     int64_t cap = 0;
     int64_t count = 0;
     std::vector<hipEvent_t> ev;  // 2 per record, created lazily
-    std::vector<int32_t> phase;
+    std::vector<int32_t> launch;
 };
 
 using namespace arp;
@@ -445,7 +608,8 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
         PtrEntry* pe = nullptr;
         s = pointer_table(*plan, *d, bufs, stream, &pe);
         if (s != AR_OK) return s;
-        for (const LaunchDesc& L : ex->launches) {
+        for (size_t li = 0; li < ex->launches.size(); ++li) {
+            const LaunchDesc& L = ex->launches[li];
             const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
             hipEvent_t e0 = nullptr, e1 = nullptr;
             if (timer) {
@@ -469,15 +633,15 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
             switch (plan->dtype) {
                 case AR_F32:
-                    launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->srcs,
+                    launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
                 case AR_I32:
-                    launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->srcs,
+                    launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
                 default:
-                    launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->srcs,
+                    launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
                                       pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
                     break;
             }
@@ -486,7 +650,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             if (timer) {
                 he = hipEventRecord(e1, stream);
                 if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", he));
-                timer->phase[size_t(timer->count)] = L.phase;
+                timer->launch[size_t(timer->count)] = int32_t(li);
                 ++timer->count;
             }
         }
@@ -539,7 +703,7 @@ AR_EXPORT ar_status ar_timer_create(int64_t capacity, ar_timer** out) {
         ar_timer* t = new ar_timer();
         t->cap = capacity;
         t->ev.assign(size_t(2 * capacity), nullptr);
-        t->phase.assign(size_t(capacity), -1);
+        t->launch.assign(size_t(capacity), -1);
         *out = t;
         return AR_OK;
     } catch (const std::bad_alloc&) {
@@ -555,7 +719,7 @@ AR_EXPORT ar_status ar_timer_reset(ar_timer* timer) {
 }
 
 AR_EXPORT ar_status ar_timer_read(ar_timer* timer, int64_t cap, int64_t* count,
-                                  int32_t* phase, float* ms) {
+                                  int32_t* launch, float* ms) {
     clear_error();
     if (!timer || !count) return fail(AR_ERR_INVALID_ARG, "NULL argument");
     if (cap < 0) return fail(AR_ERR_INVALID_ARG, "cap < 0");
@@ -569,7 +733,7 @@ AR_EXPORT ar_status ar_timer_read(ar_timer* timer, int64_t cap, int64_t* count,
             if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventElapsedTime", e));
             ms[i] = t;
         }
-        if (phase) phase[i] = timer->phase[size_t(i)];
+        if (launch) launch[i] = timer->launch[size_t(i)];
     }
     *count = m;
     return AR_OK;
@@ -584,10 +748,10 @@ AR_EXPORT ar_status ar_timer_destroy(ar_timer* timer) {
     return AR_OK;
 }
 
-// Host-side check of the launch tiling (no GPU): walks every wave tile of
-// every launch with the kernel's own index helpers and verifies that the
-// steps are covered exactly once, in bounds, with 16-byte aligned vector
-// parts.  Declared in csrc/ar_debug.h (test hook, not part of the ABI).
+// Host-side check of the executed phases and the launch tiling (no GPU):
+// every executed phase is free of hazards, and walking every wave tile of
+// every launch with the kernel's own index helpers covers each step exactly
+// once, in bounds, with 16-byte aligned vector parts.  Declared in csrc/ar_debug.h (test hook, not part of the ABI).
 AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                                           char* msg, int64_t msglen) {
     clear_error();
@@ -601,6 +765,8 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
     if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
     try {
         ExecState* ex = exec_state(*plan);
+        std::string why;
+        if (!exec_phases_hazard_free(ex->phases, plan->n, why)) return bad(why);
         const int64_t VEC = 16 / plan->esize;
         std::vector<std::vector<std::pair<int64_t, int64_t>>> cover(ex->hsteps.size());
         std::vector<char> launched(ex->hsteps.size(), 0);
@@ -621,13 +787,20 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 if (s < 0 || s >= L.count || t < 0) return bad("unit maps outside the launch");
                 const DevStep& st = ex->hsteps[size_t(L.first + s)];
                 if (st.k < 1 || st.src_off < 0 ||
-                    int64_t(st.src_off) + st.k > int64_t(ex->hsrcs.size()))
+                    int64_t(st.src_off) + st.k > int64_t(ex->hidx.size()))
                     return bad("source list out of range");
+                if (L.kern_k != 0 && st.k != L.kern_k) return bad("source count differs from the kernel's");
                 for (int32_t q = 0; q < st.k; ++q) {
-                    const int32_t src = ex->hsrcs[size_t(st.src_off + q)];
+                    const int32_t src = ex->hidx[size_t(st.src_off + q)];
                     if (src < 0 || src >= plan->n) return bad("source index out of range");
                 }
-                if (st.dst < 0 || st.dst >= plan->n) return bad("dst out of range");
+                if (st.ndst < 1 || st.dst_off < 0 ||
+                    int64_t(st.dst_off) + st.ndst > int64_t(ex->hidx.size()))
+                    return bad("destination list out of range");
+                for (int32_t q = 0; q < st.ndst; ++q) {
+                    const int32_t dst = ex->hidx[size_t(st.dst_off + q)];
+                    if (dst < 0 || dst >= plan->n) return bad("destination index out of range");
+                }
                 const TileSpan sp = tile_span(st.begin, st.end, t, L.tile_elems, VEC, vecok != 0);
                 if (sp.lo >= sp.hi) continue;
                 if (sp.lo < st.begin || sp.hi > st.end || st.begin < 0 || st.end > plan->N)
@@ -658,5 +831,53 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
         return AR_OK;
     } catch (const std::exception& e) {
         return bad(e.what());
+    }
+}
+
+AR_EXPORT ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value) {
+    clear_error();
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    if (option != AR_OPT_FUSE) return fail(AR_ERR_INVALID_ARG, "unknown option");
+    if (value != 0 && value != 1) return fail(AR_ERR_INVALID_ARG, "AR_OPT_FUSE takes 0 or 1");
+    if (plan->fuse != int32_t(value)) {
+        exec_release(*plan);
+        plan->fuse = int32_t(value);
+    }
+    return AR_OK;
+}
+
+AR_EXPORT ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count) {
+    clear_error();
+    if (!plan || !count) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    try {
+        *count = int32_t(exec_state(const_cast<ar_plan&>(*plan))->launches.size());
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}
+
+AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t* phase,
+                                        int32_t* nsrc, int32_t* max_dst, int64_t* num_steps,
+                                        int64_t* bytes) {
+    clear_error();
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    try {
+        const ExecState* ex = exec_state(const_cast<ar_plan&>(*plan));
+        if (i < 0 || i >= int32_t(ex->launches.size()))
+            return fail(AR_ERR_INVALID_ARG, "launch index out of range");
+        const LaunchDesc& L = ex->launches[size_t(i)];
+        if (phase) *phase = L.phase;
+        if (nsrc) *nsrc = ex->hsteps[size_t(L.first)].k;
+        if (max_dst) *max_dst = L.max_dst;
+        if (num_steps) *num_steps = L.count;
+        if (bytes) *bytes = L.bytes;
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
     }
 }

@@ -1,5 +1,6 @@
 // Batched phase kernel for gfx950: one launch executes every step of one
-// phase that has the same source count k (a copy is the k = 1 case).
+// phase that has the same source count k (a copy is the k = 1 case); a step
+// may store its result into several destinations.
 //
 // Work decomposition.  Each step's element range is cut into wave tiles of
 // `tile_elems` elements, aligned to 16 bytes in the buffer; a 64-lane
@@ -25,13 +26,15 @@ namespace arp {
 
 enum DType : int32_t { DT_F32 = 0, DT_I32 = 1, DT_BF16 = 2 };
 
-struct DevStep {      // 32 bytes, one per step, grouped by launch
+// One executed step: fold the k sources over [begin, end) and store the
+// result into each of the ndst destinations.  32 bytes, grouped by launch.
+struct DevStep {
     int64_t begin;
     int64_t end;
-    int32_t dst;
-    int32_t src_off;  // first source in the device source pool
-    int32_t k;
-    int32_t pad;
+    int32_t src_off;  // first source index in the device index pool
+    int32_t k;        // number of sources
+    int32_t dst_off;  // first destination index in the same pool
+    int32_t ndst;     // number of destinations
 };
 
 // Per source count K (K = 0: source count read at run time):
@@ -219,17 +222,19 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
 // per pass (used for unaligned heads/tails and for unaligned buffers).
 template <int DT, int K>
 __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
-                                            const int32_t* __restrict__ srcl,
-                                            int k, int32_t dst, int64_t lo,
-                                            int64_t hi, int lane) {
+                                            const int32_t* __restrict__ srcl, int k,
+                                            const int32_t* __restrict__ dstl, int ndst,
+                                            int64_t lo, int64_t hi, int lane) {
     using T = typename Elem<DT>::T;
-    constexpr int SU = 4;
-    AR_GLOBAL T* d = as_global<T>(ptrs[dst]);
     if (K == 1 || (K == 0 && k == 1)) {  // copy: move the bits unchanged
         const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[0]]);
-        for (int64_t e = lo + lane; e < hi; e += 64) d[e] = s[e];
+        for (int64_t e = lo + lane; e < hi; e += 64) {
+            const T v = s[e];
+            for (int j = 0; j < ndst; ++j) as_global<T>(ptrs[dstl[j]])[e] = v;
+        }
         return;
     }
+    constexpr int SU = 4;
     for (int64_t e0 = lo; e0 < hi; e0 += 64 * SU) {
         SAcc<DT> acc[SU];
         bool ok[SU];
@@ -248,20 +253,40 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) acc[u].add(s[e0 + u * 64 + lane]);
         }
+        for (int j = 0; j < ndst; ++j) {
+            AR_GLOBAL T* d = as_global<T>(ptrs[dstl[j]]);
 #pragma unroll
-        for (int u = 0; u < SU; ++u)
-            if (ok[u]) d[e0 + u * 64 + lane] = acc[u].out();
+            for (int u = 0; u < SU; ++u)
+                if (ok[u]) d[e0 + u * 64 + lane] = acc[u].out();
+        }
+    }
+}
+
+// Store U vectors per lane (vector offset `at` + u * 64 + lane) into each
+// destination; every load of these positions happened before, so a
+// destination may also be one of the sources.
+template <int U, int CM, bool FULL>
+__device__ __forceinline__ void store_all(void* const* __restrict__ ptrs,
+                                          const int32_t* __restrict__ dstl, int ndst,
+                                          int64_t v0, const u32x4 (&out)[U], const bool (&ok)[U],
+                                          int64_t at, int lane) {
+    for (int j = 0; j < ndst; ++j) {
+        gvec* d = as_global<u32x4>(ptrs[dstl[j]]) + v0 + at + lane;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (FULL || ok[u]) vstore<(CM & 2) != 0>(d + u * 64, out[u]);
     }
 }
 
 // U vectors per lane of K sources at vector offset `at` (+ u * 64 + lane),
-// folded in source order and stored.  FULL: all U vectors are in range, so
-// the loads are issued back to back with no per-vector branch.
-// Cache mode CM of a launch: bit 0 = nontemporal loads, bit 1 = nontemporal
-// stores.
+// folded in source order and stored to every destination.  FULL: all U
+// vectors are in range, so the loads are issued back to back with no
+// per-vector branch.  Cache mode CM of a launch: bit 0 = nontemporal loads,
+// bit 1 = nontemporal stores.
 template <int DT, int K, int U, int CM, bool FULL>
-__device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
-                                             int64_t at, int64_t nv, int lane) {
+__device__ __forceinline__ void fold_vectors(const gvec* const* sp, void* const* __restrict__ ptrs,
+                                             const int32_t* __restrict__ dstl, int ndst,
+                                             int64_t v0, int64_t at, int64_t nv, int lane) {
     bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
@@ -271,10 +296,10 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (ok[u]) x[j][u] = vload<(CM & 1) != 0>(sp[j] + at + u * 64 + lane);
+    u32x4 out[U];
     if constexpr (K == 1) {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (ok[u]) vstore<(CM & 2) != 0>(d + at + u * 64 + lane, x[0][u]);
+        for (int u = 0; u < U; ++u) out[u] = x[0][u];
     } else {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -282,42 +307,51 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, gvec* d,
             acc.init(x[0][u]);
 #pragma unroll
             for (int j = 1; j < K; ++j) acc.add(x[j][u]);
-            if (ok[u]) vstore<(CM & 2) != 0>(d + at + u * 64 + lane, acc.out());
+            out[u] = acc.out();
         }
     }
+    store_all<U, CM, FULL>(ptrs, dstl, ndst, v0, out, ok, at, lane);
 }
 
 // Runtime source count: one source at a time, U vectors in flight.
 template <int DT, int U, int CM, bool FULL>
 __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
-                                                const int32_t* __restrict__ srcl,
-                                                int k, int64_t v0, gvec* d,
-                                                int64_t at, int64_t nv, int lane) {
+                                                const int32_t* __restrict__ srcl, int k,
+                                                const int32_t* __restrict__ dstl, int ndst,
+                                                int64_t v0, int64_t at, int64_t nv, int lane) {
     bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
-    VAcc<DT> acc[U];
-    {
+    u32x4 out[U];
+    if (k == 1) {
         const gvec* s0 = as_global<u32x4>(ptrs[srcl[0]]) + v0;
-        u32x4 x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) x[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
+            if (ok[u]) out[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
+    } else {
+        VAcc<DT> acc[U];
+        {
+            const gvec* s0 = as_global<u32x4>(ptrs[srcl[0]]) + v0;
+            u32x4 x[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc[u].init(x[u]);
+            for (int u = 0; u < U; ++u)
+                if (ok[u]) x[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[u].init(x[u]);
+        }
+        for (int j = 1; j < k; ++j) {
+            const gvec* sj = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+            u32x4 x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (ok[u]) x[u] = vload<(CM & 1) != 0>(sj + at + u * 64 + lane);
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[u].add(x[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) out[u] = acc[u].out();
     }
-    for (int j = 1; j < k; ++j) {
-        const gvec* sj = as_global<u32x4>(ptrs[srcl[j]]) + v0;
-        u32x4 x[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (ok[u]) x[u] = vload<(CM & 1) != 0>(sj + at + u * 64 + lane);
-#pragma unroll
-        for (int u = 0; u < U; ++u) acc[u].add(x[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-        if (ok[u]) vstore<(CM & 2) != 0>(d + at + u * 64 + lane, acc[u].out());
+    store_all<U, CM, FULL>(ptrs, dstl, ndst, v0, out, ok, at, lane);
 }
 
 // One launch: `nunits` wave tiles over the steps steps[0..).  K = 0 means
@@ -342,28 +376,30 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const DevStep st = steps[s];
     const int k = K ? K : st.k;
     const int32_t* srcl = srcs + st.src_off;
+    const int32_t* dstl = srcs + st.dst_off;
+    const int ndst = st.ndst;
 
     const TileSpan sp = tile_span(st.begin, st.end, t, tile_elems, VEC, VECOK);
     if (sp.lo >= sp.hi) return;
-    if (sp.vlo > sp.lo) fold_scalar<DT, K>(ptrs, srcl, k, st.dst, sp.lo, sp.vlo, lane);
-    if (sp.hi > sp.vhi) fold_scalar<DT, K>(ptrs, srcl, k, st.dst, sp.vhi, sp.hi, lane);
+    if (sp.vlo > sp.lo) fold_scalar<DT, K>(ptrs, srcl, k, dstl, ndst, sp.lo, sp.vlo, lane);
+    if (sp.hi > sp.vhi) fold_scalar<DT, K>(ptrs, srcl, k, dstl, ndst, sp.vhi, sp.hi, lane);
     if (!VECOK || sp.vhi <= sp.vlo) return;
 
     const int64_t v0 = sp.vlo / VEC;
     const int64_t nv = (sp.vhi - sp.vlo) / VEC;
-    gvec* d = as_global<u32x4>(ptrs[st.dst]) + v0;
     int64_t at = 0;
     if constexpr (K > 0) {
         const gvec* sv[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(ptrs[srcl[j]]) + v0;
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors<DT, K, U, CM, true>(sv, d, at, nv, lane);
-        if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, d, at, nv, lane);
+            fold_vectors<DT, K, U, CM, true>(sv, ptrs, dstl, ndst, v0, at, nv, lane);
+        if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, ptrs, dstl, ndst, v0, at, nv, lane);
     } else {
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors_rt<DT, U, CM, true>(ptrs, srcl, k, v0, d, at, nv, lane);
-        if (at < nv) fold_vectors_rt<DT, U, CM, false>(ptrs, srcl, k, v0, d, at, nv, lane);
+            fold_vectors_rt<DT, U, CM, true>(ptrs, srcl, k, dstl, ndst, v0, at, nv, lane);
+        if (at < nv)
+            fold_vectors_rt<DT, U, CM, false>(ptrs, srcl, k, dstl, ndst, v0, at, nv, lane);
     }
 }
 

@@ -37,7 +37,8 @@ struct Plan {
     std::vector<int64_t> phase_first;   // num_phases + 1 entries
     std::vector<int64_t> owner_begin;   // per processor (empty: unknown)
     std::vector<int64_t> owner_end;
-    ExecState* exec = nullptr;
+    int32_t fuse = 1;  // AR_OPT_FUSE
+    ExecState* exec = nullptr;  // executor cache, built on first use
 
     int32_t num_phases() const {
         return phase_first.empty() ? 0 : int32_t(phase_first.size() - 1);

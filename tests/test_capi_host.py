@@ -259,3 +259,73 @@ def test_kernel_tiling_uneven_custom_phase():
                 assert st == arplan.AR_OK, msg
         finally:
             arplan.ar_plan_destroy(h)
+
+
+def test_executor_rewrites_launch_structure():
+    # (kind, n, N, fan) -> launches with fusion, and the fused byte total
+    cases = [
+        ("cps", 16, 1 << 20, None, 1),    # reduce + broadcast in one launch
+        ("rhd", 8, 1 << 20, None, 5),     # last halving absorbs the first doubling
+        ("tree", 64, 1 << 16, (8, 8), 3), # RS-L1 absorbs AG-L1; AG-L0 multicast
+        ("tree", 512, 1 << 15, (8, 8, 8), 5),
+        ("ring", 5, 1000, None, 7),       # 2(n-1) - 1
+        ("rb", 6, 999, None, 1),
+    ]
+    for kind, n, N, fan, nl in cases:
+        with arplan.Plan(n, N, "f32", kind, fan) as p:
+            L = p.launches()
+            assert len(L) == nl, (kind, L)
+            p.set_option(arplan.AR_OPT_FUSE, 0)
+            L0 = p.launches()
+            assert len(L0) == p.num_phases
+            # unfused launches move exactly the plan's algorithmic bytes
+            assert sum(x[4] for x in L0) == sum(p.bytes())
+            assert sum(x[4] for x in L) <= sum(x[4] for x in L0)
+            for vecok in (1, 0):
+                st, msg = _check_tiling(p.handle, vecok)
+                assert st == arplan.AR_OK, msg
+            p.set_option(arplan.AR_OPT_FUSE, 1)
+            for vecok in (1, 0):
+                st, msg = _check_tiling(p.handle, vecok)
+                assert st == arplan.AR_OK, msg
+    # co-located PS: every reduce step stores to all n buffers
+    n, N = 16, 1 << 20
+    with arplan.Plan(n, N, "f32", "cps") as p:
+        (ph, k, d, cnt, b), = p.launches()
+        assert (k, d, cnt) == (16, 16, 16)
+        assert b == n * (n + n) * (N // n) * 4
+    with arplan.Plan(64, 1 << 16, "f32", "tree", (8, 8)) as p:
+        L = p.launches()
+        assert [(x[1], x[2], x[3]) for x in L] == [(8, 1, 64), (8, 8, 64), (1, 7, 64)]
+    assert _status(arplan.ar_plan_set_option, 0, 0, 1) == arplan.AR_ERR_INVALID_ARG
+    with arplan.Plan(4, 100, "f32", "ring") as p:
+        assert _status(arplan.ar_plan_set_option, p.handle, 7, 1) == arplan.AR_ERR_INVALID_ARG
+        assert _status(arplan.ar_plan_set_option, p.handle, arplan.AR_OPT_FUSE, 2) == \
+            arplan.AR_ERR_INVALID_ARG
+
+
+def test_fusion_refuses_clashing_absorption():
+    # phase 0: reduce x0[0,4) over {0,1} and copy x1[0,4) -> x2 (reads x1);
+    # phase 1: copy x0[0,4) -> x1.  Absorbing that copy would write x1[0,4)
+    # while phase 0 still reads it, so it must stay a separate launch.
+    steps = [(0, "reduce", 0, [0, 1], 0, 4), (0, "copy", 2, [1], 0, 4),
+             (1, "copy", 1, [0], 0, 4)]
+    h = arplan.ar_plan_create_custom(3, 8, "f32", steps)
+    try:
+        L = [arplan.ar_plan_launch_info(h, i)
+             for i in range(arplan.ar_plan_num_launches(h))]
+        assert [x[0] for x in L] == [0, 0, 1]
+        st, msg = _check_tiling(h, 1)
+        assert st == arplan.AR_OK, msg
+    finally:
+        arplan.ar_plan_destroy(h)
+    # without the clash the copy is absorbed
+    steps = [(0, "reduce", 0, [0, 1], 0, 4), (0, "copy", 2, [1], 4, 8),
+             (1, "copy", 1, [0], 0, 4)]
+    h = arplan.ar_plan_create_custom(3, 8, "f32", steps)
+    try:
+        L = [arplan.ar_plan_launch_info(h, i)
+             for i in range(arplan.ar_plan_num_launches(h))]
+        assert [(x[0], x[1], x[2]) for x in L] == [(0, 1, 1), (0, 2, 2)]
+    finally:
+        arplan.ar_plan_destroy(h)

@@ -25,14 +25,16 @@ if torch.cuda.is_available():
 
 
 def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
-                  pad=0, xs0=None):
-    say("case: %s n=%d N=%d %s fan=%s pad=%d" % (kind, n, N, dtype, fan, pad))
+                  pad=0, xs0=None, fuse=1):
+    say("case: %s n=%d N=%d %s fan=%s pad=%d fuse=%d" % (kind, n, N, dtype, fan,
+                                                        pad, fuse))
     if xs0 is None:
         xs0 = workloads.draw(n, N, dtype, dist, seed)
     ref = oracle.execute(oracle.make_plan(kind, n, N, fan),
                          [x.copy() for x in xs0], dtype)
     ts = to_device(xs0, dtype, pad)
     with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_FUSE, fuse)
         run_plan(p, ts)
     got = to_host(ts, dtype)
     for q in range(n):
@@ -69,9 +71,10 @@ SCALED = [("rhd", 8, (1 << 20) + 13, "f32", None, "uniform"),
           ("rb", 6, 100003, "f32", None, "uniform")]
 
 
+@pytest.mark.parametrize("fuse", [1, 0])
 @pytest.mark.parametrize("kind,n,N,dtype,fan,dist", SCALED)
-def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist):
-    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=5)
+def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist, fuse):
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=5, fuse=fuse)
     if dtype == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
@@ -136,7 +139,8 @@ def test_full_size_configs(name):
 def test_ragged_and_tiny_sizes(kind, n, fan, dtype):
     for N in (1, n - 1, n, n + 1, 2 * n + 3, 4099):
         dist = "int1000" if dtype == "i32" else "uniform"
-        _full_compare(kind, n, N, dtype, fan, dist, seed=N)
+        for fuse in (1, 0):
+            _full_compare(kind, n, N, dtype, fan, dist, seed=N, fuse=fuse)
 
 
 def test_empty_buffers_are_a_no_op():
@@ -150,15 +154,18 @@ def test_empty_buffers_are_a_no_op():
                                        ("bf16", 1), ("bf16", 5)])
 def test_unaligned_buffers(dtype, pad):
     dist = "int1000" if dtype == "i32" else "uniform"
-    _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, pad=pad)
-    _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, pad=pad)
+    for fuse in (1, 0):
+        _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, pad=pad, fuse=fuse)
+        _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, pad=pad, fuse=fuse)
+        _full_compare("cps", 5, 3001, dtype, None, dist, seed=6, pad=pad, fuse=fuse)
 
 
 @pytest.mark.parametrize("n", [3, 5, 16, 32])
 def test_source_counts(n):
     # k = 3 and 16 have unrolled kernels, 5 and 32 use the runtime loop
     for dtype in ("f32", "bf16"):
-        _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n)
+        for fuse in (1, 0):
+            _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n, fuse=fuse)
 
 
 def test_fp32_denormals_are_kept():
@@ -274,7 +281,8 @@ def test_timer_records_each_launch():
             for _ in range(2):
                 p.execute_timed(ts, torch.cuda.current_stream(), t)
             recs = arplan.ar_timer_read(t, 64)
-            assert [ph for ph, _ in recs] == list(range(6)) * 2
+            nl = len(p.launches())
+            assert [li for li, _ in recs] == list(range(nl)) * 2
             assert all(ms > 0 for _, ms in recs)
             arplan.ar_timer_reset(t)
             assert arplan.ar_timer_read(t, 64) == []
