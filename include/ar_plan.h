@@ -190,15 +190,26 @@ ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
  *  With 0, every plan step runs as listed, one launch per phase and source
  *  count.  Changing an option drops the plan's device state; it must not
  *  be done while an execution of the plan may still be running. */
-typedef enum ar_option { AR_OPT_FUSE = 0 } ar_option;
+/*  AR_OPT_SLICE (default 2): run the whole plan as one launch in which each
+ *  wavefront carries a fixed tile of element positions through every phase
+ *  in order, running each step on its tile, so that no barrier or launch
+ *  separates the phases (every step is element-wise and the steps of a
+ *  phase are independent, so a position only depends on what earlier phases
+ *  did at that position).  Every step still reads and writes the buffers in
+ *  memory as listed.  0: never; 1: whenever possible; 2: when the phase
+ *  launches are short (a few MiB each on average).  Possible when every step
+ *  boundary is a multiple of 16 bytes; used only with 16-byte aligned
+ *  buffers (otherwise the phase launches run). */
+typedef enum ar_option { AR_OPT_FUSE = 0, AR_OPT_SLICE = 1 } ar_option;
 ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value);
 
-/* The kernel launches one execution issues (host only, no GPU call): their
- * number, and for launch i the plan phase its steps come from, their
- * source count, the most destinations any of its steps stores to, its
- * number of steps and its algorithmic bytes: (k + destinations) * len * e
- * summed over its steps (each source read once, each destination written
- * once).  Any out-pointer may be NULL. */
+/* The kernel launches one execution on 16-byte aligned buffers issues (host
+ * only, no GPU call): their number, and for launch i the plan phase its
+ * steps come from (-1 for the whole-plan launch), their source count (the
+ * largest, for the whole-plan launch), the most destinations any of its
+ * steps stores to, its number of steps and its algorithmic bytes:
+ * (k + destinations) * len * e summed over its steps (each source read
+ * once, each destination written once).  Any out-pointer may be NULL. */
 ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count);
 ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t* phase,
                               int32_t* nsrc, int32_t* max_dst,

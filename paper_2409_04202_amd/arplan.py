@@ -37,7 +37,7 @@ AR_OK, AR_ERR_INVALID_ARG, AR_ERR_UNSUPPORTED, AR_ERR_OOM, AR_ERR_HIP, \
 AR_F32, AR_I32, AR_BF16 = range(3)
 AR_RING, AR_RHD, AR_CPS, AR_TREE, AR_RB = range(5)
 AR_OP_REDUCE, AR_OP_COPY = range(2)
-AR_OPT_FUSE = 0
+AR_OPT_FUSE, AR_OPT_SLICE = 0, 1
 
 DTYPES = {"f32": AR_F32, "i32": AR_I32, "bf16": AR_BF16}
 KINDS = {"ring": AR_RING, "rhd": AR_RHD, "cps": AR_CPS, "tree": AR_TREE,

@@ -44,6 +44,17 @@ constexpr int64_t kKeepBytes = int64_t(256) << 20;
 // copies it takes over move at most kFuseBytes (2 * len * e each).
 constexpr int32_t kFuseDst = 2;
 constexpr int64_t kFuseBytes = int64_t(256) << 20;
+// Automatic choice of the whole-plan (sliced) launch, for plans whose phase
+// launches are short: it is taken when the phase launches move on average at
+// most kSliceBytes each and a simple cost model predicts it faster.  Model
+// (fitted to MI355X measurements): a phase launch costs kLaunchNs plus its
+// bytes at kBytesPerNs; the sliced launch costs one kLaunchNs plus the larger
+// of its bytes at kBytesPerNs and its longest dependent chain (per phase, the
+// most steps covering one segment, summed over phases) at kChainNs per step.
+constexpr int64_t kSliceBytes = int64_t(32) << 20;
+constexpr double kLaunchNs = 10000.0;
+constexpr double kChainNs = 1000.0;
+constexpr double kBytesPerNs = 5500.0;
 
 struct LaunchDesc {
     int32_t phase;
@@ -75,6 +86,10 @@ struct DevState {
     DevStep* steps = nullptr;
     int32_t* idx = nullptr;  // source and destination indices of the steps
     int2* tiles = nullptr;
+    int64_t* cuts = nullptr;     // sliced launch tables
+    int32_t* sched_off = nullptr;
+    int32_t* sched = nullptr;
+    int2* stiles = nullptr;
     PtrEntry cache[kCache];
     uint64_t clock = 0;
 };
@@ -107,12 +122,31 @@ struct XPhase {
     std::vector<XStep> steps;
 };
 
+// The whole-plan (sliced) launch: segments are the element ranges between
+// consecutive step boundaries; sched lists, per (executed phase, segment),
+// the device steps covering that segment; tiles maps each wavefront to
+// (segment, tile within the segment).
+struct SliceDesc {
+    bool ok = false;
+    std::string why;             // why the plan cannot run sliced
+    int32_t nphases = 0, nseg = 0;
+    int64_t tile_elems = 0, nunits = 0, bytes = 0, nsteps = 0;
+    int64_t chain = 0;           // sum over phases of the most steps on a segment
+    int32_t max_k = 0, max_dst = 0;
+    std::vector<int64_t> cuts;
+    std::vector<int32_t> sched_off, sched;
+    std::vector<int2> tiles;
+};
+
 struct ExecState {
     std::vector<XPhase> phases;  // executed phases, after the rewrites
     std::vector<LaunchDesc> launches;
     std::vector<DevStep> hsteps;
     std::vector<int32_t> hidx;   // source and destination indices
     std::vector<int2> htiles;
+    std::vector<std::vector<int32_t>> dev_of;  // [phase][step] -> hsteps index
+    SliceDesc slice;
+    bool use_slice = false;      // chosen mode for 16-byte aligned buffers
     std::vector<DevState*> dev;  // indexed by device ordinal
 };
 
@@ -293,8 +327,10 @@ static bool exec_phases_hazard_free(const std::vector<XPhase>& ph, int32_t n, st
 // tiling and the cache mode of each launch.  Host only.
 static void build_launches(const Plan& p, ExecState& ex) {
     const int64_t VEC = 16 / p.esize;
+    ex.dev_of.assign(ex.phases.size(), {});
     for (size_t q = 0; q < ex.phases.size(); ++q) {
         const XPhase& xp = ex.phases[q];
+        ex.dev_of[q].assign(xp.steps.size(), -1);
         std::unique_ptr<Touches> next_reads;
         if (q + 1 < ex.phases.size())
             next_reads.reset(new Touches(ex.phases[q + 1], p.n, true, false));
@@ -335,6 +371,7 @@ static void build_launches(const Plan& p, ExecState& ex) {
                 d.ndst = int32_t(x.dsts.size());
                 d.dst_off = int32_t(ex.hidx.size());
                 ex.hidx.insert(ex.hidx.end(), x.dsts.begin(), x.dsts.end());
+                ex.dev_of[q][idx[g]] = int32_t(ex.hsteps.size());
                 ex.hsteps.push_back(d);
                 const int64_t len = x.end - x.begin;
                 const int64_t span = len > 0 ? x.end - (x.begin & ~(VEC - 1)) : 0;
@@ -397,12 +434,104 @@ static void build_launches(const Plan& p, ExecState& ex) {
     }
 }
 
+// The sliced launch of a plan, if every step boundary is 16-byte aligned.
+static void build_slice(const Plan& p, ExecState& ex) {
+    SliceDesc& sd = ex.slice;
+    const int64_t VEC = 16 / p.esize;
+    sd.cuts = {0, p.N};
+    for (const XPhase& xp : ex.phases)
+        for (const XStep& x : xp.steps)
+            if (x.end > x.begin) {
+                sd.cuts.push_back(x.begin);
+                sd.cuts.push_back(x.end);
+            }
+    std::sort(sd.cuts.begin(), sd.cuts.end());
+    sd.cuts.erase(std::unique(sd.cuts.begin(), sd.cuts.end()), sd.cuts.end());
+    for (int64_t c : sd.cuts)
+        if (c % VEC) {
+            sd.why = "a step boundary is not 16-byte aligned";
+            return;
+        }
+    sd.nphases = int32_t(ex.phases.size());
+    sd.nseg = int32_t(sd.cuts.size() - 1);
+    if (sd.nseg < 1 || int64_t(sd.nphases) * sd.nseg > (int64_t(1) << 24)) {
+        sd.why = "too many phases times segments";
+        return;
+    }
+    auto seg_of = [&](int64_t x) {  // segment starting at x
+        return int32_t(std::lower_bound(sd.cuts.begin(), sd.cuts.end(), x) - sd.cuts.begin());
+    };
+    std::vector<std::vector<int32_t>> lists(size_t(sd.nphases) * size_t(sd.nseg));
+    for (size_t q = 0; q < ex.phases.size(); ++q) {
+        const XPhase& xp = ex.phases[q];
+        for (size_t i = 0; i < xp.steps.size(); ++i) {
+            const XStep& x = xp.steps[i];
+            if (x.end <= x.begin) continue;
+            const int32_t di = ex.dev_of[q][i];
+            if (di < 0) {
+                sd.why = "step without a device descriptor";
+                return;
+            }
+            for (int32_t sg = seg_of(x.begin); sg < seg_of(x.end); ++sg)
+                lists[q * size_t(sd.nseg) + size_t(sg)].push_back(di);
+            sd.bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * (x.end - x.begin) * p.esize;
+            sd.max_k = std::max(sd.max_k, int32_t(x.srcs.size()));
+            sd.max_dst = std::max(sd.max_dst, int32_t(x.dsts.size()));
+            ++sd.nsteps;
+        }
+    }
+    for (int32_t q = 0; q < sd.nphases; ++q) {
+        size_t most = 0;
+        for (int32_t sg = 0; sg < sd.nseg; ++sg)
+            most = std::max(most, lists[size_t(q) * size_t(sd.nseg) + size_t(sg)].size());
+        sd.chain += int64_t(most);
+    }
+    sd.sched_off.assign(lists.size() + 1, 0);
+    for (size_t i = 0; i < lists.size(); ++i) {
+        sd.sched_off[i + 1] = sd.sched_off[i] + int32_t(lists[i].size());
+        sd.sched.insert(sd.sched.end(), lists[i].begin(), lists[i].end());
+        if (sd.sched.size() > size_t(1) << 30) {
+            sd.why = "schedule too large";
+            return;
+        }
+    }
+    sd.tile_elems = int64_t(64) * kSliceU * VEC;
+    for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+        const int64_t len = sd.cuts[size_t(sg) + 1] - sd.cuts[size_t(sg)];
+        for (int64_t t = 0; t * sd.tile_elems < len; ++t) sd.tiles.push_back(make_int2(sg, int(t)));
+    }
+    sd.nunits = int64_t(sd.tiles.size());
+    if ((sd.nunits + kSliceWPB - 1) / kSliceWPB > kMaxBlocks) {
+        sd.why = "too many tiles";
+        return;
+    }
+    sd.ok = sd.nunits > 0;
+}
+
 static ExecState* exec_state(Plan& p) {
     if (!p.exec) {
         ExecState* ex = new ExecState();
         try {
             ex->phases = exec_phases(p, p.fuse != 0);
             build_launches(p, *ex);
+            build_slice(p, *ex);
+            if (ex->slice.ok && !ex->launches.empty()) {
+                if (p.slice == 1) {
+                    ex->use_slice = true;
+                } else if (p.slice == 2) {
+                    double t_phase = 0.0;
+                    int64_t total = 0;
+                    for (const LaunchDesc& L : ex->launches) {
+                        t_phase += kLaunchNs + double(L.bytes) / kBytesPerNs;
+                        total += L.bytes;
+                    }
+                    const double t_slice =
+                        kLaunchNs + std::max(double(ex->slice.chain) * kChainNs,
+                                             double(ex->slice.bytes) / kBytesPerNs);
+                    ex->use_slice = total / int64_t(ex->launches.size()) <= kSliceBytes &&
+                                    t_slice < t_phase;
+                }
+            }
         } catch (...) {
             delete ex;
             throw;
@@ -420,6 +549,10 @@ static void free_dev(DevState* d) {
     if (d->steps) (void)hipFree(d->steps);
     if (d->idx) (void)hipFree(d->idx);
     if (d->tiles) (void)hipFree(d->tiles);
+    if (d->cuts) (void)hipFree(d->cuts);
+    if (d->sched_off) (void)hipFree(d->sched_off);
+    if (d->sched) (void)hipFree(d->sched);
+    if (d->stiles) (void)hipFree(d->stiles);
     for (PtrEntry& e : d->cache) {
         if (e.done) {
             (void)hipEventSynchronize(e.done);
@@ -466,6 +599,12 @@ static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
         ar_status s = upload(&d->steps, ex.hsteps, "step table");
         if (s == AR_OK) s = upload(&d->idx, ex.hidx, "index table");
         if (s == AR_OK) s = upload(&d->tiles, ex.htiles, "tile table");
+        if (s == AR_OK && ex.slice.ok) {
+            s = upload(&d->cuts, ex.slice.cuts, "segment table");
+            if (s == AR_OK) s = upload(&d->sched_off, ex.slice.sched_off, "schedule offsets");
+            if (s == AR_OK) s = upload(&d->sched, ex.slice.sched, "schedule");
+            if (s == AR_OK) s = upload(&d->stiles, ex.slice.tiles, "slice tiles");
+        }
         if (s != AR_OK) {
             free_dev(d);
             return s;
@@ -600,59 +739,73 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
         if (plan->N == 0 || plan->num_phases() == 0) return AR_OK;
         ExecState* ex = exec_state(*plan);
         if (ex->launches.empty()) return AR_OK;
-        if (timer && timer->count + int64_t(ex->launches.size()) > timer->cap)
-            return fail(AR_ERR_INVALID_ARG, "timer is full");
         DevState* d = nullptr;
         ar_status s = device_state(*plan, *ex, &d);
         if (s != AR_OK) return s;
         PtrEntry* pe = nullptr;
         s = pointer_table(*plan, *d, bufs, stream, &pe);
         if (s != AR_OK) return s;
-        for (size_t li = 0; li < ex->launches.size(); ++li) {
-            const LaunchDesc& L = ex->launches[li];
-            const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
-            hipEvent_t e0 = nullptr, e1 = nullptr;
-            if (timer) {
-                const int64_t r = timer->count;
-                for (int j = 0; j < 2; ++j) {
-                    hipEvent_t& ev = timer->ev[size_t(2 * r + j)];
-                    if (!ev) {
-                        hipError_t he = hipEventCreate(&ev);
-                        if (he != hipSuccess) {
-                            ev = nullptr;
-                            return fail(AR_ERR_HIP, hip_msg("hipEventCreate", he));
-                        }
-                    }
+        // the whole-plan launch needs 16-byte aligned buffers
+        const bool sliced = ex->use_slice && pe->aligned;
+        const int64_t nlaunch = sliced ? 1 : int64_t(ex->launches.size());
+        if (timer && timer->count + nlaunch > timer->cap)
+            return fail(AR_ERR_INVALID_ARG, "timer is full");
+        auto mark = [&](int j) -> ar_status {  // event j (0 begin, 1 end) of this record
+            if (!timer) return AR_OK;
+            hipEvent_t& ev = timer->ev[size_t(2 * timer->count + j)];
+            if (!ev) {
+                hipError_t he = hipEventCreate(&ev);
+                if (he != hipSuccess) {
+                    ev = nullptr;
+                    return fail(AR_ERR_HIP, hip_msg("hipEventCreate", he));
                 }
-                e0 = timer->ev[size_t(2 * r)];
-                e1 = timer->ev[size_t(2 * r + 1)];
-                hipError_t he = hipEventRecord(e0, stream);
-                if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", he));
             }
-            const DevStep* steps = d->steps + L.first;
-            const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
-            switch (plan->dtype) {
-                case AR_F32:
-                    launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
-                                     pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
-                    break;
-                case AR_I32:
-                    launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
-                                     pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
-                    break;
-                default:
-                    launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
-                                      pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
-                    break;
+            hipError_t he = hipEventRecord(ev, stream);
+            if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", he));
+            return AR_OK;
+        };
+        for (int64_t li = 0; li < nlaunch; ++li) {
+            s = mark(0);
+            if (s != AR_OK) return s;
+            if (sliced) {
+                const SliceDesc& sd = ex->slice;
+                const dim3 grid(static_cast<uint32_t>((sd.nunits + kSliceWPB - 1) / kSliceWPB));
+                const dim3 block(64 * kSliceWPB);
+#define AR_SLICED(DT)                                                                   \
+    hipLaunchKernelGGL((sliced_kernel<DT>), grid, block, 0, stream, d->steps, d->idx,   \
+                       pe->dev, d->sched_off, d->sched, d->cuts, d->stiles, sd.nunits, \
+                       sd.nphases, sd.nseg, sd.tile_elems)
+                switch (plan->dtype) {
+                    case AR_F32: AR_SLICED(DT_F32); break;
+                    case AR_I32: AR_SLICED(DT_I32); break;
+                    default: AR_SLICED(DT_BF16); break;
+                }
+#undef AR_SLICED
+            } else {
+                const LaunchDesc& L = ex->launches[size_t(li)];
+                const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
+                const DevStep* steps = d->steps + L.first;
+                const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
+                switch (plan->dtype) {
+                    case AR_F32:
+                        launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
+                                         pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                        break;
+                    case AR_I32:
+                        launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
+                                         pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                        break;
+                    default:
+                        launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
+                                          pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                        break;
+                }
             }
             hipError_t he = hipGetLastError();
             if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("kernel launch", he));
-            if (timer) {
-                he = hipEventRecord(e1, stream);
-                if (he != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", he));
-                timer->launch[size_t(timer->count)] = int32_t(li);
-                ++timer->count;
-            }
+            s = mark(1);
+            if (s != AR_OK) return s;
+            if (timer) timer->launch[size_t(timer->count++)] = int32_t(li);
         }
         return AR_OK;
     } catch (const std::bad_alloc&) {
@@ -827,6 +980,53 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             if (st.end > st.begin && at != st.end)
                 return bad("step " + std::to_string(i) + " not covered to its end");
         }
+        // the whole-plan launch: tiles cover every segment exactly once with
+        // aligned vectors, and each (phase, segment) lists exactly the steps
+        // of that phase covering the segment
+        const SliceDesc& sd = ex->slice;
+        if (sd.ok) {
+            std::vector<std::vector<std::pair<int64_t, int64_t>>> sc(size_t(sd.nseg));
+            for (int64_t u = 0; u < sd.nunits; ++u) {
+                const int2 e = sd.tiles[size_t(u)];
+                if (e.x < 0 || e.x >= sd.nseg || e.y < 0) return bad("slice tile out of range");
+                const int64_t lo = sd.cuts[size_t(e.x)] + int64_t(e.y) * sd.tile_elems;
+                const int64_t hi = std::min(sd.cuts[size_t(e.x) + 1], lo + sd.tile_elems);
+                if (lo >= hi || lo % VEC || hi % VEC) return bad("slice tile empty or misaligned");
+                if ((hi - lo) / VEC > 64 * kSliceU) return bad("slice tile too long");
+                sc[size_t(e.x)].push_back({lo, hi});
+            }
+            for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+                auto& c = sc[size_t(sg)];
+                std::sort(c.begin(), c.end());
+                int64_t at = sd.cuts[size_t(sg)];
+                for (auto& iv : c) {
+                    if (iv.first != at) return bad("slice tiles leave a gap or overlap");
+                    at = iv.second;
+                }
+                if (at != sd.cuts[size_t(sg) + 1]) return bad("slice tiles do not cover a segment");
+            }
+            if (int64_t(sd.sched_off.size()) != int64_t(sd.nphases) * sd.nseg + 1)
+                return bad("schedule offsets of the wrong size");
+            for (int32_t q = 0; q < sd.nphases; ++q) {
+                const XPhase& xp = ex->phases[size_t(q)];
+                for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+                    std::vector<int32_t> want, got;
+                    for (size_t i = 0; i < xp.steps.size(); ++i) {
+                        const XStep& x = xp.steps[i];
+                        if (x.begin <= sd.cuts[size_t(sg)] && sd.cuts[size_t(sg) + 1] <= x.end)
+                            want.push_back(ex->dev_of[size_t(q)][i]);
+                        else if (x.begin < sd.cuts[size_t(sg) + 1] && sd.cuts[size_t(sg)] < x.end)
+                            return bad("a step cuts a segment");
+                    }
+                    const size_t o = size_t(q) * size_t(sd.nseg) + size_t(sg);
+                    for (int32_t i = sd.sched_off[o]; i < sd.sched_off[o + 1]; ++i)
+                        got.push_back(sd.sched[size_t(i)]);
+                    std::sort(want.begin(), want.end());
+                    std::sort(got.begin(), got.end());
+                    if (want != got) return bad("schedule differs from the steps of a phase");
+                }
+            }
+        }
         if (msg && msglen > 0) msg[0] = 0;
         return AR_OK;
     } catch (const std::exception& e) {
@@ -837,11 +1037,19 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
 AR_EXPORT ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value) {
     clear_error();
     if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
-    if (option != AR_OPT_FUSE) return fail(AR_ERR_INVALID_ARG, "unknown option");
-    if (value != 0 && value != 1) return fail(AR_ERR_INVALID_ARG, "AR_OPT_FUSE takes 0 or 1");
-    if (plan->fuse != int32_t(value)) {
+    int32_t* field = nullptr;
+    if (option == AR_OPT_FUSE) {
+        if (value != 0 && value != 1) return fail(AR_ERR_INVALID_ARG, "AR_OPT_FUSE takes 0 or 1");
+        field = &plan->fuse;
+    } else if (option == AR_OPT_SLICE) {
+        if (value < 0 || value > 2) return fail(AR_ERR_INVALID_ARG, "AR_OPT_SLICE takes 0, 1 or 2");
+        field = &plan->slice;
+    } else {
+        return fail(AR_ERR_INVALID_ARG, "unknown option");
+    }
+    if (*field != int32_t(value)) {
         exec_release(*plan);
-        plan->fuse = int32_t(value);
+        *field = int32_t(value);
     }
     return AR_OK;
 }
@@ -850,7 +1058,8 @@ AR_EXPORT ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count) {
     clear_error();
     if (!plan || !count) return fail(AR_ERR_INVALID_ARG, "NULL argument");
     try {
-        *count = int32_t(exec_state(const_cast<ar_plan&>(*plan))->launches.size());
+        const ExecState* ex = exec_state(const_cast<ar_plan&>(*plan));
+        *count = ex->use_slice ? 1 : int32_t(ex->launches.size());
         return AR_OK;
     } catch (const std::bad_alloc&) {
         return fail(AR_ERR_OOM, "host allocation failed");
@@ -866,6 +1075,16 @@ AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t*
     if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
     try {
         const ExecState* ex = exec_state(const_cast<ar_plan&>(*plan));
+        if (ex->use_slice) {
+            if (i != 0) return fail(AR_ERR_INVALID_ARG, "launch index out of range");
+            const SliceDesc& sd = ex->slice;
+            if (phase) *phase = -1;
+            if (nsrc) *nsrc = sd.max_k;
+            if (max_dst) *max_dst = sd.max_dst;
+            if (num_steps) *num_steps = sd.nsteps;
+            if (bytes) *bytes = sd.bytes;
+            return AR_OK;
+        }
         if (i < 0 || i >= int32_t(ex->launches.size()))
             return fail(AR_ERR_INVALID_ARG, "launch index out of range");
         const LaunchDesc& L = ex->launches[size_t(i)];

@@ -403,4 +403,79 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     }
 }
 
+// ------------------------------------------------------------------------
+// Whole-plan kernel for plans whose launches are too short to fill the chip.
+//
+// Every step is element-wise and the steps of a phase are independent, so
+// the value at an element position depends only on what earlier phases did
+// at that same position.  Here each wavefront owns a fixed tile of element
+// positions (inside one segment: the element ranges between consecutive
+// step boundaries) and carries it through all phases in order: in phase p it
+// runs, for its tile, every step of p that covers the segment, reading and
+// writing the buffers in memory exactly as the phase-by-phase execution
+// does.  A lane always handles the same positions, so it only ever reads
+// back what it wrote itself: no barrier between phases, one launch for the
+// whole plan.
+constexpr int kSliceU = 4;    // vectors per lane in a tile
+constexpr int kSliceWPB = 4;  // wavefronts per block
+
+template <int DT, int K>
+__device__ __forceinline__ void slice_fold(void* const* __restrict__ ptrs,
+                                           const int32_t* __restrict__ srcl,
+                                           const int32_t* __restrict__ dstl, int ndst,
+                                           int64_t v0, int64_t nv, int lane) {
+    const gvec* sv[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+    if (nv == 64 * kSliceU)
+        fold_vectors<DT, K, kSliceU, 0, true>(sv, ptrs, dstl, ndst, v0, 0, nv, lane);
+    else
+        fold_vectors<DT, K, kSliceU, 0, false>(sv, ptrs, dstl, ndst, v0, 0, nv, lane);
+}
+
+template <int DT>
+__global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
+    const DevStep* __restrict__ steps, const int32_t* __restrict__ idx,
+    void* const* __restrict__ ptrs, const int32_t* __restrict__ sched_off,
+    const int32_t* __restrict__ sched, const int64_t* __restrict__ cuts,
+    const int2* __restrict__ tiles, int64_t nunits, int32_t nphases, int32_t nseg,
+    int64_t tile_elems) {
+    constexpr int VEC = Elem<DT>::VEC;
+    const int lane = int(threadIdx.x) & 63;
+    const int64_t unit = int64_t(blockIdx.x) * kSliceWPB +
+                         int64_t(__builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+    if (unit >= nunits) return;
+    const int2 e = tiles[unit];
+    const int32_t seg = __builtin_amdgcn_readfirstlane(e.x);
+    const int64_t t = __builtin_amdgcn_readfirstlane(e.y);
+    const int64_t lo = cuts[seg] + t * tile_elems;
+    const int64_t hi = min(cuts[seg + 1], lo + tile_elems);
+    const int64_t v0 = lo / VEC;
+    const int64_t nv = (hi - lo) / VEC;
+    for (int32_t p = 0; p < nphases; ++p) {
+        const int32_t a = sched_off[int64_t(p) * nseg + seg];
+        const int32_t b = sched_off[int64_t(p) * nseg + seg + 1];
+        for (int32_t i = a; i < b; ++i) {
+            const DevStep st = steps[sched[i]];
+            const int32_t* srcl = idx + st.src_off;
+            const int32_t* dstl = idx + st.dst_off;
+            switch (st.k) {
+                case 1: slice_fold<DT, 1>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
+                case 2: slice_fold<DT, 2>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
+                case 4: slice_fold<DT, 4>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
+                case 8: slice_fold<DT, 8>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
+                default: {
+                    int64_t at = 0;
+                    if (nv == 64 * kSliceU)
+                        fold_vectors_rt<DT, kSliceU, 0, true>(ptrs, srcl, st.k, dstl, st.ndst,
+                                                              v0, at, nv, lane);
+                    else
+                        fold_vectors_rt<DT, kSliceU, 0, false>(ptrs, srcl, st.k, dstl, st.ndst,
+                                                               v0, at, nv, lane);
+                }
+            }
+        }
+    }
+}
+
 }  // namespace arp

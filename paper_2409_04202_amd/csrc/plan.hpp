@@ -37,7 +37,8 @@ struct Plan {
     std::vector<int64_t> phase_first;   // num_phases + 1 entries
     std::vector<int64_t> owner_begin;   // per processor (empty: unknown)
     std::vector<int64_t> owner_end;
-    int32_t fuse = 1;  // AR_OPT_FUSE
+    int32_t fuse = 1;   // AR_OPT_FUSE
+    int32_t slice = 2;  // AR_OPT_SLICE: 0 never, 1 always (if possible), 2 auto
     ExecState* exec = nullptr;  // executor cache, built on first use
 
     int32_t num_phases() const {

@@ -273,6 +273,7 @@ def test_executor_rewrites_launch_structure():
     ]
     for kind, n, N, fan, nl in cases:
         with arplan.Plan(n, N, "f32", kind, fan) as p:
+            p.set_option(arplan.AR_OPT_SLICE, 0)
             L = p.launches()
             assert len(L) == nl, (kind, L)
             p.set_option(arplan.AR_OPT_FUSE, 0)
@@ -291,10 +292,12 @@ def test_executor_rewrites_launch_structure():
     # co-located PS: every reduce step stores to all n buffers
     n, N = 16, 1 << 20
     with arplan.Plan(n, N, "f32", "cps") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 0)
         (ph, k, d, cnt, b), = p.launches()
         assert (k, d, cnt) == (16, 16, 16)
         assert b == n * (n + n) * (N // n) * 4
     with arplan.Plan(64, 1 << 16, "f32", "tree", (8, 8)) as p:
+        p.set_option(arplan.AR_OPT_SLICE, 0)
         L = p.launches()
         assert [(x[1], x[2], x[3]) for x in L] == [(8, 1, 64), (8, 8, 64), (1, 7, 64)]
     assert _status(arplan.ar_plan_set_option, 0, 0, 1) == arplan.AR_ERR_INVALID_ARG
@@ -312,6 +315,7 @@ def test_fusion_refuses_clashing_absorption():
              (1, "copy", 1, [0], 0, 4)]
     h = arplan.ar_plan_create_custom(3, 8, "f32", steps)
     try:
+        arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 0)
         L = [arplan.ar_plan_launch_info(h, i)
              for i in range(arplan.ar_plan_num_launches(h))]
         assert [x[0] for x in L] == [0, 0, 1]
@@ -324,8 +328,35 @@ def test_fusion_refuses_clashing_absorption():
              (1, "copy", 1, [0], 0, 4)]
     h = arplan.ar_plan_create_custom(3, 8, "f32", steps)
     try:
+        arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 0)
         L = [arplan.ar_plan_launch_info(h, i)
              for i in range(arplan.ar_plan_num_launches(h))]
         assert [(x[0], x[1], x[2]) for x in L] == [(0, 1, 1), (0, 2, 2)]
     finally:
         arplan.ar_plan_destroy(h)
+
+
+@pytest.mark.parametrize("kind,n,N,fan", TILING)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_whole_plan_launch_schedule(kind, n, N, fan, dtype):
+    # AR_OPT_SLICE = 1: one launch when every step boundary is 16-byte
+    # aligned; the host check walks its tiles and compares the schedule with
+    # the steps of every phase
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        off = oracle.block_bounds(N, n)
+        vec = 16 // (4 if dtype == "f32" else 2)
+        aligned = all(o % vec == 0 for o in off)
+        L = p.launches()
+        if p.num_phases:
+            sliced = len(L) == 1 and L[0][0] == -1
+            assert sliced == aligned, (L, aligned)
+        for fuse in (1, 0):
+            p.set_option(arplan.AR_OPT_FUSE, fuse)
+            st, msg = _check_tiling(p.handle, 1)
+            assert st == arplan.AR_OK, msg
+        if aligned and p.num_phases:
+            (ph, k, d, cnt, b), = p.launches()
+            assert ph == -1
+            p.set_option(arplan.AR_OPT_SLICE, 0)
+            assert b == sum(x[4] for x in p.launches())

@@ -25,9 +25,9 @@ if torch.cuda.is_available():
 
 
 def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
-                  pad=0, xs0=None, fuse=1):
-    say("case: %s n=%d N=%d %s fan=%s pad=%d fuse=%d" % (kind, n, N, dtype, fan,
-                                                        pad, fuse))
+                  pad=0, xs0=None, fuse=1, slice_=2):
+    say("case: %s n=%d N=%d %s fan=%s pad=%d fuse=%d slice=%d" % (
+        kind, n, N, dtype, fan, pad, fuse, slice_))
     if xs0 is None:
         xs0 = workloads.draw(n, N, dtype, dist, seed)
     ref = oracle.execute(oracle.make_plan(kind, n, N, fan),
@@ -35,6 +35,7 @@ def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
     ts = to_device(xs0, dtype, pad)
     with arplan.Plan(n, N, dtype, kind, fan) as p:
         p.set_option(arplan.AR_OPT_FUSE, fuse)
+        p.set_option(arplan.AR_OPT_SLICE, slice_)
         run_plan(p, ts)
     got = to_host(ts, dtype)
     for q in range(n):
@@ -62,6 +63,8 @@ def test_small_config_bit_exact(name):
 
 
 SCALED = [("rhd", 8, (1 << 20) + 13, "f32", None, "uniform"),
+          ("rhd", 8, 1 << 20, "f32", None, "uniform"),
+          ("cps", 16, 1 << 18, "bf16", None, "uniform"),
           ("cps", 16, (1 << 18) + 7, "f32", None, "normal"),
           ("tree", 64, (1 << 16) + 5, "f32", (8, 8), "uniform"),
           ("tree", 64, (1 << 16) + 5, "i32", (8, 8), "int1000"),
@@ -71,20 +74,25 @@ SCALED = [("rhd", 8, (1 << 20) + 13, "f32", None, "uniform"),
           ("rb", 6, 100003, "f32", None, "uniform")]
 
 
-@pytest.mark.parametrize("fuse", [1, 0])
+MODES = [(1, 2), (0, 0), (1, 1), (0, 1)]   # (AR_OPT_FUSE, AR_OPT_SLICE)
+
+
+@pytest.mark.parametrize("fuse,slice_", MODES)
 @pytest.mark.parametrize("kind,n,N,dtype,fan,dist", SCALED)
-def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist, fuse):
-    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=5, fuse=fuse)
+def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist, fuse, slice_):
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=5, fuse=fuse,
+                             slice_=slice_)
     if dtype == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
+@pytest.mark.parametrize("slice_", [2, 1, 0])
 @pytest.mark.parametrize("name", sorted(k for k in workloads.CONFIGS
                                         if k.startswith("sweep_")))
-def test_sweep_configs_bit_exact(name):
+def test_sweep_configs_bit_exact(name, slice_):
     c = workloads.CONFIGS[name]
     got, xs0 = _full_compare(c["kind"], c["n"], c["N"], c["dtype"],
-                             c["fanin"], c["dist"], c["seed"])
+                             c["fanin"], c["dist"], c["seed"], slice_=slice_)
     if c["dtype"] == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
@@ -137,10 +145,10 @@ def test_full_size_configs(name):
                                         ("rb", 3, None)])
 @pytest.mark.parametrize("dtype", ["f32", "i32", "bf16"])
 def test_ragged_and_tiny_sizes(kind, n, fan, dtype):
-    for N in (1, n - 1, n, n + 1, 2 * n + 3, 4099):
+    for N in (1, n - 1, n, n + 1, 2 * n + 3, 4099, 64 * n):
         dist = "int1000" if dtype == "i32" else "uniform"
-        for fuse in (1, 0):
-            _full_compare(kind, n, N, dtype, fan, dist, seed=N, fuse=fuse)
+        for fuse, sl in MODES:
+            _full_compare(kind, n, N, dtype, fan, dist, seed=N, fuse=fuse, slice_=sl)
 
 
 def test_empty_buffers_are_a_no_op():
@@ -154,18 +162,20 @@ def test_empty_buffers_are_a_no_op():
                                        ("bf16", 1), ("bf16", 5)])
 def test_unaligned_buffers(dtype, pad):
     dist = "int1000" if dtype == "i32" else "uniform"
-    for fuse in (1, 0):
-        _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, pad=pad, fuse=fuse)
-        _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, pad=pad, fuse=fuse)
-        _full_compare("cps", 5, 3001, dtype, None, dist, seed=6, pad=pad, fuse=fuse)
+    for fuse, sl in MODES:
+        _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, pad=pad, fuse=fuse, slice_=sl)
+        _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, pad=pad, fuse=fuse, slice_=sl)
+        _full_compare("cps", 5, 3001, dtype, None, dist, seed=6, pad=pad, fuse=fuse, slice_=sl)
+        _full_compare("ring", 4, 4096, dtype, None, dist, seed=7, pad=pad, fuse=fuse, slice_=sl)
 
 
 @pytest.mark.parametrize("n", [3, 5, 16, 32])
 def test_source_counts(n):
     # k = 3 and 16 have unrolled kernels, 5 and 32 use the runtime loop
     for dtype in ("f32", "bf16"):
-        for fuse in (1, 0):
-            _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n, fuse=fuse)
+        for fuse, sl in MODES:
+            _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n, fuse=fuse, slice_=sl)
+            _full_compare("cps", n, 512 * n, dtype, None, "uniform", seed=n, fuse=fuse, slice_=sl)
 
 
 def test_fp32_denormals_are_kept():
@@ -278,6 +288,7 @@ def test_timer_records_each_launch():
     t = arplan.ar_timer_create(64)
     try:
         with arplan.Plan(n, N, "f32", "rhd") as p:
+            p.set_option(arplan.AR_OPT_SLICE, 0)
             for _ in range(2):
                 p.execute_timed(ts, torch.cuda.current_stream(), t)
             recs = arplan.ar_timer_read(t, 64)
@@ -308,3 +319,30 @@ def test_runs_on_a_side_stream_in_order():
     s.synchronize()
     for q in range(n):
         assert np.array_equal(outs[q].numpy(), ref[q]), q
+
+
+def test_whole_plan_launch_with_timer_and_repeats():
+    n, N = 64, 1 << 14
+    xs0 = workloads.draw(n, N, "f32", "uniform", 15)
+    plan_o = oracle.ring(n, N)
+    ref = oracle.execute(plan_o, [x.copy() for x in xs0], "f32")
+    ref2 = oracle.execute(plan_o, [x.copy() for x in ref], "f32")
+    ts = to_device(xs0, "f32")
+    t = arplan.ar_timer_create(8)
+    try:
+        with arplan.Plan(n, N, "f32", "ring") as p:
+            p.set_option(arplan.AR_OPT_SLICE, 1)
+            (ph, k, d, cnt, b), = p.launches()
+            assert ph == -1
+            p.execute_timed(ts, torch.cuda.current_stream(), t)
+            torch.cuda.synchronize()
+            got = to_host(ts, "f32")
+            assert all(np.array_equal(got[q], ref[q]) for q in range(n))
+            p.execute_timed(ts, torch.cuda.current_stream(), t)
+            torch.cuda.synchronize()
+            got = to_host(ts, "f32")
+            assert all(np.array_equal(got[q], ref2[q]) for q in range(n))
+            recs = arplan.ar_timer_read(t, 8)
+            assert [li for li, _ in recs] == [0, 0] and all(ms > 0 for _, ms in recs)
+    finally:
+        arplan.ar_timer_destroy(t)
