@@ -25,7 +25,8 @@ and rounds of a plan, i.e. the coefficients of GenModel (Section 3.3, Table 2).
 Modules
 -------
 plans    -- Ring, RHD, co-located PS, hierarchical CPS / GenTree tree plans
-gentree  -- the basic-sub-plan block placement of Algorithm 1
+gentree  -- the block placement of Algorithm 1 and the basic plan it gives
+            on arbitrary (also asymmetric) trees
 execute  -- phase-by-phase executor (full and sampled-index forms)
 bf16     -- fp32 <-> bf16 conversion (round to nearest even)
 model    -- per-plan step, byte and round counts (GenModel coefficients)
@@ -35,12 +36,14 @@ from .plans import (Step, Plan, block_bounds, ring, rhd, cps, tree,
                     reduce_broadcast, make_plan)
 from .execute import execute, execute_sampled, fold
 from .bf16 import bf16_to_f32, f32_to_bf16
-from .gentree import server, switch, symmetric_tree, basic_placement
+from .gentree import (server, switch, symmetric_tree, basic_placement,
+                      gentree_plan, from_preorder, preorder_children)
 from . import model
 
 __all__ = [
     "Step", "Plan", "block_bounds", "ring", "rhd", "cps", "tree",
     "reduce_broadcast", "make_plan", "execute", "execute_sampled", "fold",
     "bf16_to_f32", "f32_to_bf16", "server", "switch", "symmetric_tree",
-    "basic_placement", "model",
+    "basic_placement", "gentree_plan", "from_preorder", "preorder_children",
+    "model",
 ]

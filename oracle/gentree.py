@@ -75,11 +75,17 @@ def symmetric_tree(fanin):
     return root
 
 
-def basic_placement(root, n_total=None):
+def basic_placement(root, n_total=None, complete=False):
     """Run the bottom-up placement.
 
     Returns ``{id(node): {server_id: [blocks...]}}`` for every node; for a
     server the map is ``{server_id: [0, ..., n_total - 1]}``.
+
+    On some asymmetric trees the rule leaves a block that no server below a
+    switch takes (every server holding it reached its quota first).  With
+    ``complete``, such a block goes to the server holding it in the first
+    child, in block order (a completion added here; where the rule places
+    every block, nothing changes).
     """
     if n_total is None:
         n_total = number_servers(root)
@@ -109,6 +115,16 @@ def basic_placement(root, n_total=None):
                         got.append(b)
                         want -= 1
                 mine[sid] = got
+        if complete:
+            for b in range(n_total):
+                if taken[b]:
+                    continue
+                for c in node.children:
+                    owner = [sid for sid, bl in place[id(c)].items() if b in bl]
+                    if owner:
+                        mine[owner[0]].append(b)
+                        taken[b] = True
+                        break
         place[id(node)] = mine
 
     visit(root)
@@ -127,3 +143,106 @@ def switch_levels(root):
         return h
     height(root)
     return [levels[h] for h in sorted(levels)]
+
+
+# -- the basic ReduceScatter / AllGather plan on an arbitrary tree ---------
+
+def preorder_children(root):
+    """Child counts of all nodes in preorder (0 for a server)."""
+    out = []
+
+    def walk(node):
+        out.append(len(node.children))
+        for c in node.children:
+            walk(c)
+    walk(root)
+    return out
+
+
+def from_preorder(counts):
+    """Inverse of preorder_children; servers numbered depth-first."""
+    counts = list(counts)
+    pos = [0]
+
+    def build():
+        if pos[0] >= len(counts):
+            raise ValueError("child counts end early")
+        c = counts[pos[0]]
+        pos[0] += 1
+        if c == 0:
+            return server()
+        return switch([build() for _ in range(c)])
+    root = build()
+    if pos[0] != len(counts):
+        raise ValueError("child counts describe more than one tree")
+    number_servers(root)
+    return root
+
+
+def height(node):
+    if node.is_server:
+        return 0
+    return 1 + max(height(c) for c in node.children)
+
+
+def gentree_plan(root, N):
+    """The plan GenTree's basic sub-plans give on the tree `root`.
+
+    Every switch A, bottom-up, runs a ReduceScatter over its children: each
+    block that Algorithm 1 places on server s at A is reduced on s from the
+    copies held, one per child, by the server that owns it at that child
+    (a server child holds every block); sources are taken in child order.
+    Switches of the same height run in the same phase.  The AllGather
+    reverses it top-down: s sends the reduced block back to each of those
+    holders.  Consecutive blocks of one server with the same holders form
+    one step.  With unequal children this is the asymmetric co-located PS.
+    The placement is Algorithm 1 with the completion described in
+    ``basic_placement``.
+    """
+    from .plans import Plan, Step, block_bounds
+
+    n = number_servers(root)
+    off = block_bounds(N, n)
+    place = basic_placement(root, n, complete=True)
+    H = height(root)
+    rs = [[] for _ in range(H)]
+    ag = [[] for _ in range(H)]
+
+    for node_id, pl in place.items():
+        got = sorted(b for blocks in pl.values() for b in blocks)
+        if got != list(range(n)):
+            raise AssertionError("placement does not cover every block")
+
+    def visit(node):
+        if node.is_server:
+            return
+        for c in node.children:
+            visit(c)
+        holder = []          # per child: block -> server holding it there
+        for c in node.children:
+            m = {}
+            for sid, blocks in place[id(c)].items():
+                for b in blocks:
+                    m[b] = sid
+            holder.append(m)
+        h = height(node)
+        for sid, blocks in place[id(node)].items():
+            runs = []        # (first block, last block, holders)
+            for b in blocks:
+                hs = tuple(hm[b] for hm in holder)
+                if runs and runs[-1][1] == b - 1 and runs[-1][2] == hs:
+                    runs[-1][1] = b
+                else:
+                    runs.append([b, b, hs])
+            for b0, b1, hs in runs:
+                if hs == (sid,):
+                    continue           # a single child: nothing to reduce
+                rs[h - 1].append(Step("reduce", sid, hs, off[b0], off[b1 + 1]))
+                for q in hs:
+                    if q != sid:
+                        ag[h - 1].append(Step("copy", q, (sid,), off[b0],
+                                              off[b1 + 1]))
+    visit(root)
+    phases = [ph for ph in rs if ph] + [ph for ph in reversed(ag) if ph]
+    plan = Plan("gentree", n, N, phases)
+    return plan
