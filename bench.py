@@ -59,7 +59,10 @@ def cpu_baseline(name, budget_s=25.0):
     import oracle
     from paper_2409_04202_amd import workloads
     c = workloads.CONFIGS[name]
-    plan = oracle.make_plan(c["kind"], c["n"], c["N"], c["fanin"])
+    if c["kind"] == "gentree":
+        plan = oracle.gentree_plan(oracle.from_preorder(c["fanin"]), c["N"])
+    else:
+        plan = oracle.make_plan(c["kind"], c["n"], c["N"], c["fanin"])
     xs = workloads.inputs(name)
     total = c["n"] * c["N"] * workloads.ESIZE[c["dtype"]]
     runs, spent = 0, 0.0
@@ -178,7 +181,8 @@ def main():
         "dtype": dt,
         "data": "synthetic (seeded %s inputs)" % c["dist"],
         "config": {"workload": name, "plan": c["kind"], "n": n, "N": N,
-                   "fanin": list(c["fanin"]) if c["fanin"] else None,
+                   "fanin": (list(c["fanin"]) if c["kind"] != "gentree"
+                             else "%d-node tree" % len(c["fanin"])) if c["fanin"] else None,
                    "fuse": not args.no_fuse,
                    "parallelism": "emulated %d processors on 1 GPU" % n},
         "plan_bytes_per_step": red_b + cpy_b,

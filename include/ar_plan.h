@@ -96,7 +96,8 @@ typedef enum ar_dtype { AR_F32 = 0, AR_I32 = 1, AR_BF16 = 2 } ar_dtype;
  * one more for the first rem blocks, as in Algorithm 1).
  */
 typedef enum ar_kind {
-    AR_RING = 0, AR_RHD = 1, AR_CPS = 2, AR_TREE = 3, AR_RB = 4
+    AR_RING = 0, AR_RHD = 1, AR_CPS = 2, AR_TREE = 3, AR_RB = 4,
+    AR_GENTREE = 5   /* only through ar_plan_create_gentree */
 } ar_kind;
 
 typedef enum ar_op { AR_OP_REDUCE = 0, AR_OP_COPY = 1 } ar_op;
@@ -132,6 +133,34 @@ typedef struct ar_timer ar_timer;
  * AR_ERR_OOM.  The plan owns all its memory; free it with ar_plan_destroy. */
 ar_status ar_plan_create(int32_t n, int64_t N, int32_t dtype,
                          const ar_topology* topo, ar_plan** out);
+
+/* GenTree's basic plan on an arbitrary tree (Section 4.2, Algorithm 1).  The
+ * tree is given in preorder: nchild[i] is the number of children of node i
+ * (0 for a server), for num_nodes nodes; the list must describe exactly one
+ * tree.  Servers are the processors, numbered in that (depth-first) order;
+ * n is their number (<= 65536).
+ *   Placement: bottom-up, after the ReduceScatter below a switch every
+ *   server under it owns floor(n / s) of the n blocks, s being the number of
+ *   servers under the switch, and the first (n mod s) in child order own one
+ *   more; a server takes, in order, the first blocks of its own list (the
+ *   blocks it owned under its child; a server child's list is every block)
+ *   that no earlier server under the switch took.  Where this leaves a
+ *   block unplaced (it can on asymmetric trees), the block goes to the
+ *   server holding it in the first child that holds it.
+ *   Steps: each switch reduces every block placed on a server over one
+ *   holder per child (in child order) -- a co-located PS when the children
+ *   are alike, the asymmetric co-located PS otherwise -- with consecutive
+ *   blocks of one server and the same holders in one step; switches of one
+ *   height share a phase; the AllGather reverses the ReduceScatter level by
+ *   level.  On a symmetric tree this is exactly AR_TREE.  A switch with one
+ *   child adds nothing.  A plan choice inside a switch (e.g. m x k
+ *   hierarchical CPS) is expressed as an extra level of switches.
+ * ar_plan_owner gives the root-level owner range, or AR_ERR_UNSUPPORTED when
+ * a processor's blocks there are not contiguous.  Errors: AR_ERR_INVALID_ARG
+ * (malformed list, N < 0, unknown dtype, more than 65536 servers),
+ * AR_ERR_UNSUPPORTED (children x servers summed over the nodes > 2^28). */
+ar_status ar_plan_create_gentree(int64_t N, int32_t dtype, int32_t num_nodes,
+                                 const int32_t* nchild, ar_plan** out);
 
 /* Build a plan from an explicit step list (any order; steps are grouped by
  * phase, phases must be numbered 0..P-1 without gaps).  Each step is

@@ -35,13 +35,13 @@ _lib = ctypes.CDLL(LIB_PATH)
 AR_OK, AR_ERR_INVALID_ARG, AR_ERR_UNSUPPORTED, AR_ERR_OOM, AR_ERR_HIP, \
     AR_ERR_INTERNAL = range(6)
 AR_F32, AR_I32, AR_BF16 = range(3)
-AR_RING, AR_RHD, AR_CPS, AR_TREE, AR_RB = range(5)
+AR_RING, AR_RHD, AR_CPS, AR_TREE, AR_RB, AR_GENTREE = range(6)
 AR_OP_REDUCE, AR_OP_COPY = range(2)
 AR_OPT_FUSE, AR_OPT_SLICE = 0, 1
 
 DTYPES = {"f32": AR_F32, "i32": AR_I32, "bf16": AR_BF16}
 KINDS = {"ring": AR_RING, "rhd": AR_RHD, "cps": AR_CPS, "tree": AR_TREE,
-         "rb": AR_RB}
+         "rb": AR_RB, "gentree": AR_GENTREE}
 ESIZE = {AR_F32: 4, AR_I32: 4, AR_BF16: 2}
 
 
@@ -62,6 +62,8 @@ _sig = {
                        POINTER(_P)],
     "ar_plan_create_custom": [c_int32, c_int64, c_int32, POINTER(ar_step),
                               c_int64, POINTER(_P)],
+    "ar_plan_create_gentree": [c_int64, c_int32, c_int32, POINTER(c_int32),
+                               POINTER(_P)],
     "ar_plan_destroy": [_P],
     "ar_plan_execute": [_P, POINTER(c_void_p), c_void_p],
     "ar_plan_execute_strided": [_P, c_void_p, c_int64, c_void_p],
@@ -148,6 +150,17 @@ def ar_plan_create(n, N, dtype, kind, fanin=None):
     out = _P()
     _check(_lib.ar_plan_create(int(n), int(N), _dtype(dtype),
                                ctypes.byref(topo), ctypes.byref(out)))
+    return out.value
+
+
+def ar_plan_create_gentree(N, dtype, nchild):
+    """``nchild``: child counts of the tree's nodes in preorder (0 = server).
+    Returns the plan handle."""
+    counts = list(nchild)
+    arr = (c_int32 * max(1, len(counts)))(*counts)
+    out = _P()
+    _check(_lib.ar_plan_create_gentree(int(N), _dtype(dtype), len(counts), arr,
+                                       ctypes.byref(out)))
     return out.value
 
 
@@ -276,10 +289,14 @@ def ar_timer_destroy(timer):
 # ------------------------------------------------------------ convenience
 
 class Plan:
-    """Owning wrapper around a plan handle."""
+    """Owning wrapper around a plan handle.  ``kind="gentree"`` takes the
+    tree as ``fanin`` = child counts in preorder (``n`` is then ignored)."""
 
     def __init__(self, n, N, dtype, kind, fanin=None):
-        self.handle = ar_plan_create(n, N, dtype, kind, fanin)
+        if kind == "gentree":
+            self.handle = ar_plan_create_gentree(N, dtype, fanin)
+        else:
+            self.handle = ar_plan_create(n, N, dtype, kind, fanin)
         self.n, self.N, self.dtype, self.num_phases, self.num_steps = \
             ar_plan_info(self.handle)
         self.esize = ESIZE[self.dtype]

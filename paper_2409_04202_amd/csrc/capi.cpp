@@ -132,6 +132,49 @@ AR_EXPORT ar_status ar_plan_create(int32_t n, int64_t N, int32_t dtype,
     });
 }
 
+AR_EXPORT ar_status ar_plan_create_gentree(int64_t N, int32_t dtype, int32_t num_nodes,
+                                           const int32_t* nchild, ar_plan** out) {
+    clear_error();
+    if (!out) return fail(AR_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (num_nodes < 1 || !nchild)
+        return fail(AR_ERR_INVALID_ARG, "need num_nodes >= 1 child counts");
+    if (N < 0) return fail(AR_ERR_INVALID_ARG, "N must be >= 0");
+    const int32_t es = esize_of(dtype);
+    if (!es) return fail(AR_ERR_INVALID_ARG, "unknown dtype");
+    if (N > INT64_MAX / es)
+        return fail(AR_ERR_INVALID_ARG, "N * element size overflows");
+    std::vector<int32_t> counts(nchild, nchild + num_nodes);
+    const int64_t n = gentree_servers(counts);
+    if (n < 1)
+        return fail(AR_ERR_INVALID_ARG, "child counts do not describe exactly one tree");
+    if (n > 65536) return fail(AR_ERR_INVALID_ARG, "more than 65536 servers");
+    // size guard: every switch lists, per block, one holder per child
+    {
+        int64_t work = 0;
+        for (int32_t c : counts) work += int64_t(c) * n;
+        if (work > (int64_t(1) << 28))
+            return fail(AR_ERR_UNSUPPORTED, "tree too large (children x servers > 2^28)");
+    }
+    return guarded([&]() -> ar_status {
+        ar_plan* p = new ar_plan();
+        try {
+            p->n = int32_t(n);
+            p->N = N;
+            p->dtype = dtype;
+            p->esize = es;
+            p->kind = AR_GENTREE;
+            expand_gentree(*p, counts);
+            validate_phases(*p);
+        } catch (...) {
+            delete p;
+            throw;
+        }
+        *out = p;
+        return AR_OK;
+    });
+}
+
 AR_EXPORT ar_status ar_plan_create_custom(int32_t n, int64_t N, int32_t dtype,
                                           const ar_step* steps, int64_t nsteps,
                                           ar_plan** out) {
@@ -273,6 +316,8 @@ AR_EXPORT ar_status ar_plan_owner(const ar_plan* plan, int32_t p,
     if (p < 0 || p >= plan->n) return fail(AR_ERR_INVALID_ARG, "p out of range");
     if (plan->owner_begin.empty())
         return fail(AR_ERR_UNSUPPORTED, "custom plans have no owner map");
+    if (plan->owner_begin[size_t(p)] < 0)
+        return fail(AR_ERR_UNSUPPORTED, "this processor's blocks are not contiguous");
     if (begin) *begin = plan->owner_begin[size_t(p)];
     if (end) *end = plan->owner_end[size_t(p)];
     return AR_OK;

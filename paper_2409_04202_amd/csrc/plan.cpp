@@ -280,4 +280,263 @@ void validate_phases(const Plan& p) {
     }
 }
 
+// ---------------------------------------------------------------- GenTree
+
+int64_t gentree_servers(const std::vector<int32_t>& nchild) {
+    // preorder: every node consumes its children; the list must end exactly
+    // when the root is complete
+    int64_t open = 1, servers = 0;
+    for (size_t i = 0; i < nchild.size(); ++i) {
+        if (open == 0 || nchild[i] < 0) return -1;
+        --open;
+        if (nchild[i] == 0) ++servers;
+        open += nchild[i];
+    }
+    return open == 0 ? servers : -1;
+}
+
+namespace {
+
+struct TNode {
+    std::vector<int32_t> kids;  // node indices
+    int32_t server = -1;        // server id for leaves
+    int32_t height = 0;         // 0 for servers
+    // placement after this node's ReduceScatter: servers in order, each
+    // with its blocks in the order taken (leaves: every block, implicit)
+    std::vector<std::pair<int32_t, std::vector<int32_t>>> place;
+};
+
+}  // namespace
+
+// Bottom-up block placement of Algorithm 1 (floor share per server, one
+// more for the first `remain` servers in child order; each server takes the
+// first blocks of its own list that no earlier server below the switch took),
+// completed where the rule leaves a block: the block goes to its holder in
+// the first child.  Each switch reduces every block over one holder per
+// child; switches of one height share a phase; the AllGather reverses it.
+void expand_gentree(Plan& p, const std::vector<int32_t>& nchild) {
+    const int32_t n = p.n;
+    const int64_t N = p.N;
+    const int32_t nn = int32_t(nchild.size());
+    std::vector<TNode> t(static_cast<size_t>(nn));
+    {   // build the tree from the preorder child counts
+        std::vector<std::pair<int32_t, int32_t>> stack;  // (node, kids still to attach)
+        int32_t sid = 0;
+        for (int32_t i = 0; i < nn; ++i) {
+            if (!stack.empty()) {
+                t[size_t(stack.back().first)].kids.push_back(i);
+                if (--stack.back().second == 0) stack.pop_back();
+            }
+            if (nchild[size_t(i)] == 0)
+                t[size_t(i)].server = sid++;
+            else
+                stack.push_back({i, nchild[size_t(i)]});
+            while (!stack.empty() && stack.back().second == 0) stack.pop_back();
+        }
+        if (sid != n) throw std::invalid_argument("server count differs from n");
+    }
+    // post-order (children before parents)
+    std::vector<int32_t> order;
+    {
+        std::vector<std::pair<int32_t, size_t>> st{{0, 0}};
+        while (!st.empty()) {
+            auto& [v, k] = st.back();
+            if (k < t[size_t(v)].kids.size()) {
+                const int32_t c = t[size_t(v)].kids[k++];
+                st.push_back({c, 0});
+            } else {
+                order.push_back(v);
+                st.pop_back();
+            }
+        }
+    }
+    int32_t H = 0;
+    for (int32_t v : order) {
+        TNode& a = t[size_t(v)];
+        if (a.server >= 0) continue;
+        for (int32_t c : a.kids) a.height = std::max(a.height, t[size_t(c)].height + 1);
+        H = std::max(H, a.height);
+    }
+    std::vector<std::vector<Step>> rs(static_cast<size_t>(H)), ag(static_cast<size_t>(H));
+    std::vector<std::vector<int32_t>> rs_srcs(static_cast<size_t>(H)), ag_srcs(static_cast<size_t>(H));
+    auto servers_below = [&](int32_t v) {
+        int64_t c = 0;
+        std::vector<int32_t> st{v};
+        while (!st.empty()) {
+            const int32_t x = st.back();
+            st.pop_back();
+            if (t[size_t(x)].server >= 0) ++c;
+            for (int32_t k : t[size_t(x)].kids) st.push_back(k);
+        }
+        return c;
+    };
+    // next_free[b]: smallest untaken block >= b (path-halving union-find),
+    // so that a server child (whose list is every block) takes its share in
+    // amortised constant time per block
+    std::vector<int32_t> taken(static_cast<size_t>(n)), next_free(static_cast<size_t>(n) + 1);
+    auto find_free = [&](int32_t b) {
+        while (next_free[size_t(b)] != b) {
+            next_free[size_t(b)] = next_free[size_t(next_free[size_t(b)])];
+            b = next_free[size_t(b)];
+        }
+        return b;
+    };
+    auto take = [&](int32_t b) {
+        taken[size_t(b)] = 1;
+        next_free[size_t(b)] = b + 1;
+    };
+    for (int32_t v : order) {
+        TNode& a = t[size_t(v)];
+        if (a.server >= 0) {
+            a.place.push_back({a.server, {}});  // implicit: every block
+            continue;
+        }
+        const int64_t s = servers_below(v);
+        const int64_t quota = n / s;
+        int64_t remain = n % s;
+        std::fill(taken.begin(), taken.end(), 0);
+        for (int32_t b = 0; b <= n; ++b) next_free[size_t(b)] = b;
+        // holder of block b after child i's ReduceScatter: a server child
+        // holds every block; a switch child's placement gives the server
+        const size_t nk = a.kids.size();
+        std::vector<int32_t> const_holder(nk, -1);
+        std::vector<std::vector<int32_t>> holders(nk);
+        for (size_t i = 0; i < nk; ++i) {
+            const TNode& c = t[size_t(a.kids[i])];
+            if (c.server >= 0) {
+                const_holder[i] = c.server;
+            } else {
+                holders[i].assign(size_t(n), -1);
+                for (const auto& pr : c.place)
+                    for (int32_t b : pr.second) holders[i][size_t(b)] = pr.first;
+            }
+        }
+        auto holder = [&](size_t i, int32_t b) {
+            return const_holder[i] >= 0 ? const_holder[i] : holders[i][size_t(b)];
+        };
+        for (size_t i = 0; i < nk; ++i) {
+            const TNode& c = t[size_t(a.kids[i])];
+            for (const auto& pr : c.place) {
+                int64_t want = quota + (remain > 0 ? 1 : 0);
+                if (remain > 0) --remain;
+                std::vector<int32_t> got;
+                if (c.server >= 0) {  // its list is every block, in order
+                    for (int32_t b = find_free(0); want > 0 && b < n; b = find_free(b)) {
+                        take(b);
+                        got.push_back(b);
+                        --want;
+                    }
+                } else {
+                    for (int32_t b : pr.second) {
+                        if (want == 0) break;
+                        if (!taken[size_t(b)]) {
+                            take(b);
+                            got.push_back(b);
+                            --want;
+                        }
+                    }
+                }
+                a.place.push_back({pr.first, std::move(got)});
+            }
+        }
+        for (int32_t b = 0; b < n; ++b) {  // completion
+            if (taken[size_t(b)]) continue;
+            for (size_t i = 0; i < nk; ++i) {
+                const int32_t h = holder(i, b);
+                if (h < 0) continue;
+                for (auto& pr : a.place)
+                    if (pr.first == h) {
+                        pr.second.push_back(b);
+                        break;
+                    }
+                take(b);
+                break;
+            }
+            if (!taken[size_t(b)]) throw std::logic_error("block without holder");
+        }
+        // steps: runs of consecutive blocks of one server with equal holders
+        const size_t lvl = size_t(a.height - 1);
+        for (const auto& [sid, blocks] : a.place) {
+            size_t i0 = 0;
+            while (i0 < blocks.size()) {
+                size_t i1 = i0 + 1;
+                auto same = [&](int32_t x, int32_t y) {
+                    for (size_t k = 0; k < nk; ++k)
+                        if (holder(k, x) != holder(k, y)) return false;
+                    return true;
+                };
+                while (i1 < blocks.size() && blocks[i1] == blocks[i1 - 1] + 1 &&
+                       same(blocks[i1], blocks[i0]))
+                    ++i1;
+                const int32_t b0 = blocks[i0], b1 = blocks[i1 - 1];
+                std::vector<int32_t> hs;
+                for (size_t k = 0; k < nk; ++k) hs.push_back(holder(k, b0));
+                if (!(hs.size() == 1 && hs[0] == sid)) {
+                    const int64_t lo = block_off(N, n, b0), hi = block_off(N, n, int64_t(b1) + 1);
+                    Step st{};
+                    st.op = OP_REDUCE;
+                    st.dst = sid;
+                    st.nsrc = int32_t(hs.size());
+                    st.src_off = int64_t(rs_srcs[lvl].size());
+                    st.begin = lo;
+                    st.end = hi;
+                    rs_srcs[lvl].insert(rs_srcs[lvl].end(), hs.begin(), hs.end());
+                    rs[lvl].push_back(st);
+                    for (int32_t q : hs) {
+                        if (q == sid) continue;
+                        Step c{};
+                        c.op = OP_COPY;
+                        c.dst = q;
+                        c.nsrc = 1;
+                        c.src_off = int64_t(ag_srcs[lvl].size());
+                        c.begin = lo;
+                        c.end = hi;
+                        ag_srcs[lvl].push_back(sid);
+                        ag[lvl].push_back(c);
+                    }
+                }
+                i0 = i1;
+            }
+        }
+        // children's placements are no longer needed
+        for (int32_t c : a.kids)
+            if (t[size_t(c)].server < 0) t[size_t(c)].place.clear();
+    }
+    // phases: ReduceScatter by increasing height, AllGather by decreasing
+    int32_t ph = 0;
+    auto emit = [&](std::vector<Step>& steps, std::vector<int32_t>& pool) {
+        if (steps.empty()) return;
+        for (Step st : steps) {
+            p.add(ph, st.op, st.dst,
+                  std::vector<int32_t>(pool.begin() + st.src_off,
+                                       pool.begin() + st.src_off + st.nsrc),
+                  st.begin, st.end);
+        }
+        ++ph;
+    };
+    for (int32_t h = 0; h < H; ++h) emit(rs[size_t(h)], rs_srcs[size_t(h)]);
+    for (int32_t h = H - 1; h >= 0; --h) emit(ag[size_t(h)], ag_srcs[size_t(h)]);
+    // owner after the last ReduceScatter level: the root's placement
+    p.owner_begin.assign(size_t(n), -1);
+    p.owner_end.assign(size_t(n), -1);
+    if (t[0].server >= 0) {
+        p.owner_begin[0] = 0;
+        p.owner_end[0] = N;
+    } else {
+        for (const auto& [sid, blocks] : t[0].place) {
+            std::vector<int32_t> b = blocks;
+            std::sort(b.begin(), b.end());
+            bool contiguous = true;
+            for (size_t i = 1; i < b.size(); ++i) contiguous = contiguous && b[i] == b[i - 1] + 1;
+            if (b.empty()) {
+                p.owner_begin[size_t(sid)] = p.owner_end[size_t(sid)] = 0;
+            } else if (contiguous) {
+                p.owner_begin[size_t(sid)] = block_off(N, n, b.front());
+                p.owner_end[size_t(sid)] = block_off(N, n, int64_t(b.back()) + 1);
+            }
+        }
+    }
+    p.finish_phases();
+}
+
 }  // namespace arp

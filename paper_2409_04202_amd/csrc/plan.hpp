@@ -68,6 +68,12 @@ void expand_rhd(Plan& p);
 void expand_cps(Plan& p);
 void expand_tree(Plan& p);  // uses p.fanin
 void expand_rb(Plan& p);
+// GenTree basic plan on an arbitrary tree given as child counts in
+// preorder (0 = server); p.n must already be the number of servers.
+void expand_gentree(Plan& p, const std::vector<int32_t>& nchild);
+// Number of servers of a preorder child-count list, or -1 if the list does
+// not describe exactly one tree.
+int64_t gentree_servers(const std::vector<int32_t>& nchild);
 
 // Throws std::invalid_argument naming the first hazard found.
 void validate_phases(const Plan& p);

@@ -41,6 +41,32 @@ CONFIGS = {
                                 BASE_SEED + 5, fanin=(8, 8, 8)),
 }
 
+def preorder(spec):
+    """Child counts in preorder of a tree written as nested lists of server
+    counts: an int k is a switch over k servers, a list is a switch over its
+    elements."""
+    if isinstance(spec, int):
+        return [spec] + [0] * spec
+    out = [len(spec)]
+    for c in spec:
+        out += preorder(c)
+    return out
+
+
+# The paper's asymmetric topologies (Section 5.3) with the per-switch plans
+# GenTree selects for 1e8 floats (Table 6) written as extra switch levels:
+# 8 x 4 hierarchical CPS inside a 32-server middle switch, 8 x 2 inside a
+# 16-server one; asymmetric co-located PS where the children differ.
+ASY384 = [[8] * 4] * 8 + [[8] * 2] * 8
+CDC384 = [[[8] * 4] * 8, [[8] * 2] * 8]
+
+CONFIGS["asy384_gentree_f32"] = _cfg("gentree", 384, 384 * 2048, "f32",
+                                     "uniform", BASE_SEED + 6,
+                                     fanin=preorder(ASY384))
+CONFIGS["cdc384_gentree_f32"] = _cfg("gentree", 384, 384 * 2048, "f32",
+                                     "uniform", BASE_SEED + 7,
+                                     fanin=preorder(CDC384))
+
 SWEEP_N = (1 << 12, 1 << 16, 1 << 20)
 for _i, _N in enumerate(SWEEP_N):
     for _dt in ("f32", "bf16"):

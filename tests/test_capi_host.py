@@ -360,3 +360,89 @@ def test_whole_plan_launch_schedule(kind, n, N, fan, dtype):
             assert ph == -1
             p.set_option(arplan.AR_OPT_SLICE, 0)
             assert b == sum(x[4] for x in p.launches())
+
+
+# -- GenTree plans on arbitrary trees -------------------------------------
+
+def _random_counts(rng, depth=3):
+    def build(d):
+        if d == 0 or rng.random() < 0.3:
+            return [0]
+        k = int(rng.integers(1, 5))
+        out = [k]
+        for _ in range(k):
+            out += build(d - 1)
+        return out
+    while True:
+        c = build(depth)
+        if c != [0]:
+            return c
+
+
+def _gentree_cases():
+    from paper_2409_04202_amd import workloads
+    rng = np.random.default_rng(2024)
+    cases = [_random_counts(rng) for _ in range(40)]
+    cases += [workloads.CONFIGS["asy384_gentree_f32"]["fanin"],
+              workloads.CONFIGS["cdc384_gentree_f32"]["fanin"],
+              [3, 0, 0, 2, 0, 0], [2, 0, 2, 0, 2, 0, 0], [1, 1, 2, 0, 0], [0]]
+    return cases
+
+
+@pytest.mark.parametrize("idx", range(46))
+def test_gentree_steps_match_oracle(idx):
+    counts = _gentree_cases()[idx]
+    root = oracle.from_preorder(counts)
+    n = oracle.gentree.number_servers(root)
+    for N in sorted({0, 1, n, 7 * n + 3}):
+        ref = oracle.gentree_plan(root, N)
+        with arplan.Plan(0, N, "f32", "gentree", counts) as p:
+            assert p.n == n
+            assert _norm(p.phases()) == _norm(_oracle_phases(ref))
+            assert p.bytes() == model.algorithmic_bytes(ref, 4)
+            place = oracle.basic_placement(root, n, complete=True)[id(root)]
+            off = oracle.block_bounds(N, n)
+            if n > 1:
+                for sid, blocks in place.items():
+                    bl = sorted(blocks)
+                    if not bl:
+                        assert p.owner(sid) == (0, 0)
+                    elif bl == list(range(bl[0], bl[-1] + 1)):
+                        assert p.owner(sid) == (off[bl[0]], off[bl[-1] + 1])
+                    else:
+                        assert _status(arplan.ar_plan_owner, p.handle, sid) == \
+                            arplan.AR_ERR_UNSUPPORTED
+            for sl in (0, 1):
+                p.set_option(arplan.AR_OPT_SLICE, sl)
+                for vecok in (1, 0):
+                    st, msg = _check_tiling(p.handle, vecok)
+                    assert st == arplan.AR_OK, msg
+
+
+@pytest.mark.parametrize("fan", [(8, 8), (2, 3, 4), (4, 1, 2), (8, 4, 16)])
+def test_gentree_equals_tree_on_symmetric_trees(fan):
+    counts = oracle.preorder_children(oracle.symmetric_tree(fan))
+    n = int(np.prod(fan))
+    for N in (n, 5 * n + 1):
+        with arplan.Plan(0, N, "bf16", "gentree", counts) as a, \
+                arplan.Plan(n, N, "bf16", "tree", fan) as b:
+            assert _norm(a.phases()) == _norm(b.phases())
+            for p in range(n):
+                assert a.owner(p) == b.owner(p)
+
+
+def test_gentree_errors():
+    E = arplan
+    for bad in ([2, 0], [1, 0, 0], [0, 0], [-1], [2, 0, 0, 0]):
+        assert _status(E.ar_plan_create_gentree, 10, "f32", bad) == E.AR_ERR_INVALID_ARG, bad
+    assert _status(E.ar_plan_create_gentree, 10, "f32", []) == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create_gentree, -1, "f32", [2, 0, 0]) == E.AR_ERR_INVALID_ARG
+    assert _status(E.ar_plan_create_gentree, 10, 9, [2, 0, 0]) == E.AR_ERR_INVALID_ARG
+    # one switch over 20000 servers: 2e4 x 2e4 > 2^28
+    assert _status(E.ar_plan_create_gentree, 10, "f32", [20000] + [0] * 20000) == \
+        E.AR_ERR_UNSUPPORTED
+    h = E.ar_plan_create_gentree(10, "f32", [0])    # a single server
+    try:
+        assert E.ar_plan_info(h)[3:] == (0, 0)
+    finally:
+        E.ar_plan_destroy(h)

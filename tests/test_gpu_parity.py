@@ -24,14 +24,19 @@ if torch.cuda.is_available():
     from paper_2409_04202_amd import arplan
 
 
+def _oracle_plan(kind, n, N, fan):
+    if kind == "gentree":
+        return oracle.gentree_plan(oracle.from_preorder(fan), N)
+    return oracle.make_plan(kind, n, N, fan)
+
+
 def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
                   pad=0, xs0=None, fuse=1, slice_=2):
     say("case: %s n=%d N=%d %s fan=%s pad=%d fuse=%d slice=%d" % (
-        kind, n, N, dtype, fan, pad, fuse, slice_))
+        kind, n, N, dtype, fan if kind != "gentree" else len(fan), pad, fuse, slice_))
     if xs0 is None:
         xs0 = workloads.draw(n, N, dtype, dist, seed)
-    ref = oracle.execute(oracle.make_plan(kind, n, N, fan),
-                         [x.copy() for x in xs0], dtype)
+    ref = oracle.execute(_oracle_plan(kind, n, N, fan), [x.copy() for x in xs0], dtype)
     ts = to_device(xs0, dtype, pad)
     with arplan.Plan(n, N, dtype, kind, fan) as p:
         p.set_option(arplan.AR_OPT_FUSE, fuse)
@@ -112,7 +117,8 @@ def _sample_positions(n, N, rng):
 
 @pytest.mark.parametrize("name", ["rhd_n8_f32", "cps_n16_f32",
                                   "tree8x8_n64_f32", "tree8x8_n64_i32",
-                                  "tree8x8x8_n512_bf16"])
+                                  "tree8x8x8_n512_bf16", "asy384_gentree_f32",
+                                  "cdc384_gentree_f32"])
 def test_full_size_configs(name):
     c = workloads.CONFIGS[name]
     n, N, dt = c["n"], c["N"], c["dtype"]
@@ -123,7 +129,7 @@ def test_full_size_configs(name):
     idx = _sample_positions(n, N, rng)
     with arplan.Plan(n, N, dt, c["kind"], c["fanin"]) as p:
         run_plan(p, ts)
-    plan = oracle.make_plan(c["kind"], n, N, c["fanin"])
+    plan = _oracle_plan(c["kind"], n, N, c["fanin"])
     want = oracle.execute_sampled(plan, [x[idx] for x in xs0], idx, dt)
     it = torch.from_numpy(idx).to("cuda")
     for q in range(n):
@@ -346,3 +352,29 @@ def test_whole_plan_launch_with_timer_and_repeats():
             assert [li for li, _ in recs] == [0, 0] and all(ms > 0 for _, ms in recs)
     finally:
         arplan.ar_timer_destroy(t)
+
+
+GENTREES = [[3, 0, 0, 2, 0, 0], [2, 0, 2, 0, 2, 0, 0],
+            [3, 3, 4, 0, 0, 0, 0, 2, 0, 0, 0, 3, 4, 0, 0, 0, 0, 0, 0, 2, 4, 0,
+             0, 0, 0, 2, 0, 0],
+            workloads.preorder([[4] * 2] * 2 + [[2] * 2] * 2),
+            workloads.preorder([[[4] * 2] * 2, [[2] * 2] * 2])]
+
+
+@pytest.mark.parametrize("counts", GENTREES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+def test_gentree_plans_bit_exact(counts, dtype):
+    n = counts.count(0)
+    dist = "int1000" if dtype == "i32" else "uniform"
+    for N in (n, 64 * n, 64 * n + 5, 40000):
+        for fuse, sl in MODES:
+            _full_compare("gentree", n, N, dtype, counts, dist, seed=N, fuse=fuse,
+                          slice_=sl)
+
+
+@pytest.mark.parametrize("name", ["asy384_gentree_f32", "cdc384_gentree_f32"])
+def test_paper_asymmetric_topologies_scaled(name):
+    c = workloads.CONFIGS[name]
+    for fuse, sl in MODES:
+        _full_compare("gentree", c["n"], 384 * 64 + 17, "f32", c["fanin"], seed=3,
+                      fuse=fuse, slice_=sl)
