@@ -68,12 +68,16 @@ typedef enum ar_dtype { AR_F32 = 0, AR_I32 = 1, AR_BF16 = 2 } ar_dtype;
  *           adds its own block to it (reduce step with srcs {i, i-1}); in
  *           the last n - 1 steps it stores it (copy).  After the
  *           ReduceScatter half processor i owns block (i + 2) mod n.
- *  AR_RHD   Recursive halving-doubling, n a power of two: in halving step j
- *           processor r pairs with r XOR 2^j, keeps the lower half of the
- *           range it holds if bit j of r is 0 and the upper half otherwise,
- *           and reduces it over the pair (2^-(j+1) of the data in step j);
- *           the doubling steps run the halving steps backwards as copies.
- *           Other n: AR_ERR_UNSUPPORTED.
+ *  AR_RHD   Recursive halving-doubling: for n a power of two, in halving
+ *           step j processor r pairs with r XOR 2^j, keeps the lower half of
+ *           the range it holds if bit j of r is 0 and the upper half
+ *           otherwise, and reduces it over the pair (2^-(j+1) of the data in
+ *           step j); the doubling steps run the halving steps backwards as
+ *           copies.  Otherwise, with p the largest power of two below n, two
+ *           steps are added (2 ceil(log2 n) in all): processor q >= p first
+ *           reduces its whole buffer into q - p, ranks 0..p-1 run the
+ *           power-of-two plan on p blocks, and q finally copies the result
+ *           from q - p (ranks >= p then own nothing).
  *  AR_CPS   Co-located PS: processor p reduces block p over all n inputs in
  *           one n-way step, then the n - 1 others copy it.
  *  AR_TREE  Hierarchical co-located PS on a symmetric tree, i.e. the GenTree
@@ -129,8 +133,7 @@ typedef struct ar_timer ar_timer;
  * empty blocks, which are kept as empty steps).  n <= 65536.
  * Errors: AR_ERR_INVALID_ARG (NULL out/topo, n < 1, N < 0, unknown dtype or
  * kind, tree fan-in < 1, missing fan-ins or product != n, N * element size
- * overflowing int64), AR_ERR_UNSUPPORTED (RHD with n not a power of two),
- * AR_ERR_OOM.  The plan owns all its memory; free it with ar_plan_destroy. */
+ * overflowing int64), AR_ERR_UNSUPPORTED (more than 2^26 steps), AR_ERR_OOM.  The plan owns all its memory; free it with ar_plan_destroy. */
 ar_status ar_plan_create(int32_t n, int64_t N, int32_t dtype,
                          const ar_topology* topo, ar_plan** out);
 

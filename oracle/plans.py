@@ -86,18 +86,31 @@ def ring(n, N):
 
 
 def rhd(n, N):
-    """Recursive Halving-Doubling for n a power of two, Section 2.1.
+    """Recursive Halving-Doubling, Section 2.1.
 
-    Halving step j (0 <= j < log2 n): processor r pairs with r XOR 2^j, the
-    two split the range they currently hold into halves, r keeps the lower
-    half when bit j of r is 0 and the upper half otherwise, and reduces its
-    kept half over the pair (ascending rank order).  Step j therefore
-    moves 2^-(j+1) of the data.  The doubling steps run the halving steps
-    backwards: in the step mirroring halving step j, r receives the half
-    that its partner kept there.
+    For n a power of two: halving step j (0 <= j < log2 n): processor r
+    pairs with r XOR 2^j, the two split the range they currently hold into
+    halves, r keeps the lower half when bit j of r is 0 and the upper half
+    otherwise, and reduces its kept half over the pair (ascending rank
+    order).  Step j therefore moves 2^-(j+1) of the data.  The doubling
+    steps run the halving steps backwards: in the step mirroring halving
+    step j, r receives the half that its partner kept there.
+
+    Otherwise the paper adds two steps (2 ceil(log n) in all, Table 1's
+    chi(n) terms: one more full-data transfer each way, S adds and 3S memory
+    operations): with p the largest power of two below n, each processor
+    q >= p first reduces its whole buffer into processor q - p, the first p
+    processors run the power-of-two plan, and q finally copies the result
+    back from q - p.
     """
-    if n & (n - 1) or n < 1:
-        raise ValueError("rhd: n must be a power of two (got %d)" % n)
+    if n < 1:
+        raise ValueError("rhd: n must be >= 1")
+    if n & (n - 1):
+        p = 1 << (n.bit_length() - 1)
+        pre = [Step("reduce", q - p, (q - p, q), 0, N) for q in range(p, n)]
+        post = [Step("copy", q, (q - p,), 0, N) for q in range(p, n)]
+        inner = rhd(p, N)
+        return Plan("rhd", n, N, [pre] + inner.phases + [post])
     off = block_bounds(N, n)
     k = n.bit_length() - 1
     # held[r] = [lo, hi) in blocks currently held by r, per halving step

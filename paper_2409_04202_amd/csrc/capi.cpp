@@ -35,7 +35,7 @@ static int64_t estimate_steps(int32_t kind, int64_t n,
                               const std::vector<int32_t>& fan) {
     switch (kind) {
         case AR_RING: return 2 * (n - 1) * n;
-        case AR_RHD: { int64_t k = 0; while ((int64_t(1) << k) < n) ++k; return 2 * k * n; }
+        case AR_RHD: { int64_t k = 0; while ((int64_t(1) << k) < n) ++k; return 2 * k * n + 2 * n; }
         case AR_CPS: return n * n;
         case AR_RB: return n;
         case AR_TREE: {

@@ -68,12 +68,36 @@ void expand_ring(Plan& p) {
 }
 
 // Recursive halving-doubling, nearest partner (r XOR 1) first; r keeps the
-// lower half when bit j of r is 0.
+// lower half when bit j of r is 0.  For n not a power of two, with p the
+// largest power of two below n: processor q >= p first reduces its whole
+// buffer into q - p, the first p processors run the power-of-two plan, and
+// q copies the result back from q - p (the two extra steps).
+static void rhd_pow2(Plan& p, int32_t n, int32_t ph0);
+
 void expand_rhd(Plan& p) {
     const int32_t n = p.n;
     const int64_t N = p.N;
-    if (n & (n - 1))
-        throw Unsupported("RHD needs a power-of-two processor count");
+    if (n & (n - 1)) {
+        int32_t pw = 1;
+        while (pw * 2 <= n) pw *= 2;
+        for (int32_t q = pw; q < n; ++q) p.add(0, OP_REDUCE, q - pw, {q - pw, q}, 0, N);
+        rhd_pow2(p, pw, 1);
+        const int32_t last = p.steps.empty() ? 1 : p.steps.back().phase + 1;
+        for (int32_t q = pw; q < n; ++q) p.add(last, OP_COPY, q, {q - pw}, 0, N);
+        // owners: the power-of-two part as computed; the extra ones own nothing
+        for (int32_t q = pw; q < n; ++q) {
+            p.owner_begin[size_t(q)] = 0;
+            p.owner_end[size_t(q)] = 0;
+        }
+        p.finish_phases();
+        return;
+    }
+    rhd_pow2(p, n, 0);
+    p.finish_phases();
+}
+
+static void rhd_pow2(Plan& p, int32_t n, int32_t ph0) {
+    const int64_t N = p.N;
     int32_t k = 0;
     while ((1 << k) < n) ++k;
     std::vector<std::pair<int32_t, int32_t>> held(size_t(n), {0, n});
@@ -86,7 +110,7 @@ void expand_rhd(Plan& p) {
             nk[size_t(r)] = ((r >> j) & 1) ? std::make_pair(mid, hi)
                                            : std::make_pair(lo, mid);
             const int32_t q = r ^ (1 << j);
-            p.add(j, OP_REDUCE, r, {std::min(r, q), std::max(r, q)},
+            p.add(ph0 + j, OP_REDUCE, r, {std::min(r, q), std::max(r, q)},
                   block_off(N, n, nk[size_t(r)].first),
                   block_off(N, n, nk[size_t(r)].second));
         }
@@ -98,17 +122,16 @@ void expand_rhd(Plan& p) {
         for (int32_t r = 0; r < n; ++r) {
             const int32_t q = r ^ (1 << j);
             const auto [lo, hi] = kept[size_t(j)][size_t(q)];
-            p.add(k + jj, OP_COPY, r, {q}, block_off(N, n, lo),
+            p.add(ph0 + k + jj, OP_COPY, r, {q}, block_off(N, n, lo),
                   block_off(N, n, hi));
         }
     }
-    p.owner_begin.resize(size_t(n));
-    p.owner_end.resize(size_t(n));
+    p.owner_begin.resize(size_t(p.n));
+    p.owner_end.resize(size_t(p.n));
     for (int32_t r = 0; r < n; ++r) {
         p.owner_begin[size_t(r)] = block_off(N, n, held[size_t(r)].first);
         p.owner_end[size_t(r)] = block_off(N, n, held[size_t(r)].second);
     }
-    p.finish_phases();
 }
 
 // Co-located PS: one n-way reduce per block, then n - 1 copies per block.

@@ -50,8 +50,7 @@ for _n in (1, 2, 3, 4, 5, 7, 8, 12, 16):
         CASES.append(("ring", _n, _N, None))
         CASES.append(("cps", _n, _N, None))
         CASES.append(("rb", _n, _N, None))
-        if _n & (_n - 1) == 0:
-            CASES.append(("rhd", _n, _N, None))
+        CASES.append(("rhd", _n, _N, None))
 for _fan in ((2, 2), (3, 2), (2, 3), (4, 4), (2, 3, 2), (8, 8), (2, 2, 2, 2),
              (1, 4), (4, 1, 2)):
     for _N in (0, 5, 64, 1001):
@@ -77,7 +76,7 @@ def test_steps_match_oracle(kind, n, N, fan):
 
 
 @pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("ring", 8, None),
-                                        ("rhd", 8, None), ("cps", 6, None),
+                                        ("rhd", 8, None), ("rhd", 6, None), ("cps", 6, None),
                                         ("tree", 12, (3, 4)),
                                         ("tree", 64, (8, 8)),
                                         ("tree", 512, (8, 8, 8))])
@@ -127,7 +126,7 @@ def test_create_errors():
     assert _status(E.ar_plan_create, 4, -1, "f32", "ring") == E.AR_ERR_INVALID_ARG
     assert _status(E.ar_plan_create, 4, 10, 7, "ring") == E.AR_ERR_INVALID_ARG
     assert _status(E.ar_plan_create, 4, 10, "f32", 9) == E.AR_ERR_INVALID_ARG
-    assert _status(E.ar_plan_create, 6, 10, "f32", "rhd") == E.AR_ERR_UNSUPPORTED
+    assert _status(E.ar_plan_create, 6, 10, "f32", "rhd") == E.AR_OK
     assert _status(E.ar_plan_create, 6, 10, "f32", "tree", [2, 2]) == E.AR_ERR_INVALID_ARG
     assert _status(E.ar_plan_create, 4, 10, "f32", "tree", [4, 0]) == E.AR_ERR_INVALID_ARG
     assert _status(E.ar_plan_create, 4, 10, "f32", "tree", []) == E.AR_ERR_INVALID_ARG

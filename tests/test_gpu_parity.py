@@ -68,6 +68,8 @@ def test_small_config_bit_exact(name):
 
 
 SCALED = [("rhd", 8, (1 << 20) + 13, "f32", None, "uniform"),
+          ("rhd", 6, (1 << 18) + 3, "f32", None, "uniform"),
+          ("rhd", 12, 1 << 16, "bf16", None, "uniform"),
           ("rhd", 8, 1 << 20, "f32", None, "uniform"),
           ("cps", 16, 1 << 18, "bf16", None, "uniform"),
           ("cps", 16, (1 << 18) + 7, "f32", None, "normal"),
@@ -146,7 +148,7 @@ def test_full_size_configs(name):
 
 # --------------------------------------------------------------- edge cases
 
-@pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("rhd", 4, None),
+@pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("rhd", 4, None), ("rhd", 5, None),
                                         ("cps", 7, None), ("tree", 12, (3, 4)),
                                         ("rb", 3, None)])
 @pytest.mark.parametrize("dtype", ["f32", "i32", "bf16"])

@@ -43,9 +43,8 @@ def _factorizations(n, maxlen=4):
 
 
 def tiny_plans(n, N):
-    plans = [oracle.ring(n, N), oracle.cps(n, N), oracle.reduce_broadcast(n, N)]
-    if n & (n - 1) == 0:
-        plans.append(oracle.rhd(n, N))
+    plans = [oracle.ring(n, N), oracle.cps(n, N), oracle.reduce_broadcast(n, N),
+             oracle.rhd(n, N)]
     for fan in _factorizations(n):
         if len(fan) > 1:
             plans.append(oracle.tree(fan, N))
@@ -333,13 +332,13 @@ def test_rhd_steps_follow_section_2_1(k):
 
 
 def test_round_counts_table_1():
-    # A coefficients: RB 2, CPS 2, Ring 2(n-1), RHD 2 log n, HCPS 2m.
-    for n in (2, 4, 8, 16, 32):
+    # A coefficients: RB 2, CPS 2, Ring 2(n-1), RHD 2 ceil(log n), HCPS 2m.
+    for n in (2, 3, 4, 5, 6, 7, 8, 12, 16, 17, 32):
         N = 4 * n
         assert model.num_phases(oracle.reduce_broadcast(n, N)) == 2
         assert model.num_phases(oracle.cps(n, N)) == 2
         assert model.num_phases(oracle.ring(n, N)) == 2 * (n - 1)
-        assert model.num_phases(oracle.rhd(n, N)) == 2 * (n.bit_length() - 1)
+        assert model.num_phases(oracle.rhd(n, N)) == 2 * (n - 1).bit_length()
     for fan in ((8, 8), (8, 8, 8), (2, 6), (3, 2, 2)):
         assert model.num_phases(oracle.tree(fan, 1000)) == 2 * len(fan)
 
@@ -509,3 +508,29 @@ def test_block_bounds_floor_plus_remainder():
     assert oracle.block_bounds(10, 4) == [0, 3, 6, 8, 10]
     assert oracle.block_bounds(3, 5) == [0, 1, 2, 3, 3, 3]
     assert oracle.block_bounds(0, 3) == [0, 0, 0, 0]
+
+
+@pytest.mark.parametrize("n", [3, 5, 6, 7, 12, 17])
+def test_rhd_non_power_of_two_extra_terms(n):
+    # Tables 1 and 2: with chi(n) = 1 the plan costs 2S beta + S gamma +
+    # 3S delta more than the power-of-two part, on the processor that takes
+    # an extra one in; the inner part is exactly RHD on the first p ranks.
+    N = 8 * n + 3
+    p = 1 << (n.bit_length() - 1)
+    full = oracle.rhd(n, N)
+    inner = oracle.rhd(p, N)
+    assert full.phases[1:-1] == inner.phases
+    pre, post = full.phases[0], full.phases[-1]
+    assert all(st.op == "reduce" and (st.begin, st.end) == (0, N) for st in pre)
+    assert all(st.op == "copy" and (st.begin, st.end) == (0, N) for st in post)
+    assert sorted(st.dst for st in pre) == list(range(n - p))
+    mem = lambda plan, r: sum((len(s.srcs) + 1) * (s.end - s.begin)
+                              for s in plan.steps if s.op == "reduce" and s.dst == r)
+    adds = lambda plan, r: sum((len(s.srcs) - 1) * (s.end - s.begin)
+                               for s in plan.steps if s.op == "reduce" and s.dst == r)
+    for r in range(n - p):      # processors that take an extra one in
+        assert mem(full, r) - mem(inner, r) == 3 * N          # 3S delta
+        assert adds(full, r) - adds(inner, r) == N            # S gamma
+    for q in range(p, n):       # the extra processors: S out, S back in
+        assert model.sent_elements(full)[q] == N
+        assert model.received_elements(full)[q] == N
