@@ -1,0 +1,101 @@
+"""Host-side checks of the single-GPU GenModel fit (features, least squares,
+plan selection).  No GPU: plans are created and inspected on the host only.
+
+The features the library reports are checked against the oracle's own counts
+of the same plans (rounds, and the delta / copy byte terms of Table 2), which
+the oracle pins separately against Table 1 and Table 2.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import model
+
+from paper_2409_04202_amd import arplan, genmodel
+
+
+PLANS = [("ring", n, None) for n in (2, 3, 5, 8)] + \
+        [("rhd", n, None) for n in (2, 6, 8, 12)] + \
+        [("cps", n, None) for n in (2, 7, 16)] + \
+        [("tree", 16, (4, 4)), ("tree", 24, (2, 3, 4)), ("tree", 12, (3, 4))]
+
+
+@pytest.mark.parametrize("kind,n,fan", PLANS)
+@pytest.mark.parametrize("N", [1, 1000, 4099])
+def test_features_match_oracle_counts(kind, n, fan, N):
+    ref = oracle.make_plan(kind, n, N, fan)
+    with arplan.Plan(n, N, "f32", kind, fan) as p:
+        A, D, B = genmodel.features(p)
+    assert A == model.num_phases(ref)
+    assert (D, B) == model.algorithmic_bytes(ref, 4)
+
+
+def test_features_bf16_halve_bytes():
+    with arplan.Plan(8, 4096, "f32", "ring") as p32, \
+            arplan.Plan(8, 4096, "bf16", "ring") as p16:
+        a32, a16 = genmodel.features(p32), genmodel.features(p16)
+    assert a32[0] == a16[0]
+    assert a32[1] == 2 * a16[1] and a32[2] == 2 * a16[2]
+
+
+def _samples(params, plans):
+    out = []
+    for kind, n, fan, N in plans:
+        with arplan.Plan(n, N, "f32", kind, fan) as p:
+            f = genmodel.features(p)
+        out.append((f, genmodel.predict(params, f)))
+    return out
+
+
+def test_fit_recovers_exact_parameters():
+    true = (5e-6, 1.3e-13, 1.2e-13)
+    plans = [("cps", n, None, N) for n in (2, 3, 4, 8, 16)
+             for N in (1 << 10, 1 << 18, 1 << 22)]
+    got = genmodel.fit(_samples(true, plans))
+    assert np.allclose(got, true, rtol=1e-9, atol=0)
+
+
+def test_fit_is_least_squares_in_relative_error():
+    # One sample is off by +10 %; relative weighting spreads the residual
+    # so that no fitted sample is off by more than the perturbation.
+    true = (4e-6, 1e-13, 1e-13)
+    plans = [("cps", n, None, 1 << 20) for n in (2, 4, 8, 16, 32)] + \
+            [("ring", n, None, 1 << 16) for n in (4, 8)]
+    s = _samples(true, plans)
+    s[3] = (s[3][0], s[3][1] * 1.1)
+    got = genmodel.fit(s)
+    rel = [abs(genmodel.predict(got, f) - t) / t for f, t in s]
+    assert max(rel) < 0.1
+
+
+def test_factorizations():
+    assert sorted(genmodel.factorizations(8)) == [(2, 2, 2), (2, 4), (4, 2)]
+    f12 = genmodel.factorizations(12)
+    assert (3, 4) in f12 and (2, 2, 3) in f12 and (12,) not in f12
+    assert all(int(np.prod(f)) == 12 for f in f12)
+    assert genmodel.factorizations(7) == []
+    assert all(len(f) <= 2 for f in genmodel.factorizations(16, max_levels=2))
+
+
+@pytest.mark.parametrize("params", [(1.0, 0.0, 0.0), (0.0, 1e-13, 1e-13),
+                                    (5e-6, 1.3e-13, 1.2e-13)])
+@pytest.mark.parametrize("n,N", [(8, 1 << 12), (12, 1 << 20), (32, 1 << 24)])
+def test_select_is_argmin_of_prediction(params, n, N):
+    t, kind, fan = genmodel.select(params, n, N)
+    preds = []
+    for k, f in genmodel.candidates(n):
+        with arplan.Plan(n, N, "f32", k, f) as p:
+            preds.append(genmodel.predict(params, genmodel.features(p)))
+    assert t == min(preds)
+    if params[1] == 0.0:
+        # Pure round count: a two-round plan (co-located PS) wins.
+        assert kind == "cps"
+    if params[0] == 0.0:
+        # Pure bytes: a plan with no more traffic than any candidate.
+        with arplan.Plan(n, N, "f32", kind, fan) as p:
+            a, d, b = genmodel.features(p)
+        for k, f in genmodel.candidates(n):
+            with arplan.Plan(n, N, "f32", k, f) as p:
+                _, d2, b2 = genmodel.features(p)
+            assert d + b <= d2 + b2
