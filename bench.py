@@ -6,7 +6,11 @@ AllGather phase) over the n input buffers, which are resident in HBM before
 the timed region starts.  The plan runs in place; the inputs are restored
 from a pristine device copy after warm-up, then K steps run back to back
 (values grow by a factor of about n per step, which does not change the
-work: fp32 adds take the same time whatever the operands).
+work: fp32 adds take the same time whatever the operands).  After the timed
+region the inputs are restored again and K more executions record HIP
+events around every kernel launch, for the per-launch durations; events
+between launches would add to the step time, so they stay out of the timed
+region.
 
 Prints one JSON line:
   value       AllReduce algorithm bandwidth n * N * e / time, GB/s
@@ -89,6 +93,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fuse", action="store_true",
                     help="run every plan step as listed (AR_OPT_FUSE = 0)")
+    ap.add_argument("--slice", type=int, choices=(0, 1, 2), default=None,
+                    help="AR_OPT_SLICE (default: the library's, 2)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build executes every emulated processor on one "
@@ -120,6 +126,8 @@ def main():
     plan = arplan.Plan(n, N, dt, c["kind"], c["fanin"])
     if args.no_fuse:
         plan.set_option(arplan.AR_OPT_FUSE, 0)
+    if args.slice is not None:
+        plan.set_option(arplan.AR_OPT_SLICE, args.slice)
     stream = torch.cuda.current_stream()
     launches = plan.launches()          # (phase, nsrc, max_dst, steps, bytes)
     red_b, cpy_b = plan.bytes()
@@ -133,15 +141,23 @@ def main():
         plan.execute(bufs, stream)
     restore()
     K = args.steps
-    cap = max(1, K * len(launches))
-    timer = arplan.ar_timer_create(cap)
+    ptrs = arplan.pointers(bufs)        # marshalled once for the buffer set
+    sh = stream.cuda_stream
     torch.cuda.synchronize()
     print("bench: timing %d steps" % K, file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     for _ in range(K):
-        plan.execute_timed(bufs, stream, timer)
+        plan.execute(ptrs, sh)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    # per-launch durations, outside the timed region
+    restore()
+    cap = max(1, K * len(launches))
+    timer = arplan.ar_timer_create(cap)
+    torch.cuda.synchronize()
+    for _ in range(K):
+        plan.execute_timed(ptrs, sh, timer)
+    torch.cuda.synchronize()
     recs = arplan.ar_timer_read(timer, cap)
     arplan.ar_timer_destroy(timer)
 
@@ -157,12 +173,14 @@ def main():
     red_ms = sum(l_ms[i] for i in red)
     red_bytes = sum(launches[i][4] for i in red)
     achieved = red_bytes / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
-    traffic = load_traffic(name) if not args.no_fuse else None
+    traffic = load_traffic(name) if not args.no_fuse and args.slice is None else None
     roofline = {"bound": "hbm", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
-                "kernel": "phase_kernel, reduce launches (k = %s)" % (
+                "kernel": "%s, reduce launches (k = %s)" % (
+                    " + ".join(sorted({"sliced_kernel" if launches[i][0] < 0
+                                       else "phase_kernel" for i in red})) or "-",
                     sorted({launches[i][1] for i in red}) or "-"),
                 "launches_per_step": len(red),
                 "bytes_per_launch": round(red_bytes / max(1, len(red))),
@@ -184,6 +202,7 @@ def main():
                    "fanin": (list(c["fanin"]) if c["kind"] != "gentree"
                              else "%d-node tree" % len(c["fanin"])) if c["fanin"] else None,
                    "fuse": not args.no_fuse,
+                   "slice": args.slice if args.slice is not None else 2,
                    "parallelism": "emulated %d processors on 1 GPU" % n},
         "plan_bytes_per_step": red_b + cpy_b,
         "plan_gbs": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9, 1),

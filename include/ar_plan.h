@@ -222,23 +222,27 @@ ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
  *  With 0, every plan step runs as listed, one launch per phase and source
  *  count.  Changing an option drops the plan's device state; it must not
  *  be done while an execution of the plan may still be running. */
-/*  AR_OPT_SLICE (default 2): run the whole plan as one launch in which each
- *  wavefront carries a fixed tile of element positions through every phase
- *  in order, running each step on its tile, so that no barrier or launch
- *  separates the phases (every step is element-wise and the steps of a
- *  phase are independent, so a position only depends on what earlier phases
- *  did at that position).  Every step still reads and writes the buffers in
- *  memory as listed.  0: never; 1: whenever possible; 2: when the phase
- *  launches are short (a few MiB each on average).  Possible when every step
- *  boundary is a multiple of 16 bytes; used only with 16-byte aligned
- *  buffers (otherwise the phase launches run). */
+/*  AR_OPT_SLICE (default 2): sliced launches.  A sliced launch runs a run of
+ *  consecutive phases in one launch in which each wavefront carries a fixed
+ *  tile of element positions through those phases in order, running each
+ *  step on its tile, so that no barrier or launch separates the phases
+ *  (every step is element-wise and the steps of a phase are independent, so
+ *  a position only depends on what earlier phases did at that position).
+ *  Every step still reads and writes the buffers in memory as listed.
+ *  0: never; 1: the whole plan as one sliced launch whenever possible;
+ *  2: the runs of phases a cost model predicts faster as sliced launches,
+ *  among phases that each write at most 256 MiB (what one phase hands to the
+ *  next then fits the last-level cache either way).  A run is possible when
+ *  every boundary of its steps is a multiple of 16 bytes; sliced launches
+ *  are used only with 16-byte aligned buffers (otherwise every phase runs
+ *  as its phase launches, those reported with AR_OPT_SLICE = 0). */
 typedef enum ar_option { AR_OPT_FUSE = 0, AR_OPT_SLICE = 1 } ar_option;
 ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value);
 
 /* The kernel launches one execution on 16-byte aligned buffers issues (host
  * only, no GPU call): their number, and for launch i the plan phase its
- * steps come from (-1 for the whole-plan launch), their source count (the
- * largest, for the whole-plan launch), the most destinations any of its
+ * steps come from (-1 for a sliced launch), their source count (the
+ * largest, for a sliced launch), the most destinations any of its
  * steps stores to, its number of steps and its algorithmic bytes:
  * (k + destinations) * len * e summed over its steps (each source read
  * once, each destination written once).  Any out-pointer may be NULL. */

@@ -7,8 +7,10 @@ loads the library and raises ImportError if it has not been built: there is
 no fallback path.
 
 Buffers may be passed as integers (device addresses) or as objects with a
-``data_ptr()`` method (e.g. torch tensors); streams as integers (hipStream_t
-handles, 0 = default stream) or objects with a ``cuda_stream`` attribute.
+``data_ptr()`` method (e.g. torch tensors), or as the pointer array
+``pointers(bufs)`` returns, which repeated executions on the same buffers can
+reuse; streams as integers (hipStream_t handles, 0 = default stream) or
+objects with a ``cuda_stream`` attribute.
 """
 
 import ctypes
@@ -124,6 +126,17 @@ def _ptr(x):
     return int(x)
 
 
+def pointers(bufs):
+    """The C array of device pointers ``ar_plan_execute`` takes, built once
+    for a buffer set (reading ``data_ptr()`` of many tensors per call costs
+    more host time than launching a short plan)."""
+    return (c_void_p * max(1, len(bufs)))(*[_ptr(b) for b in bufs])
+
+
+def _ptr_array(bufs):
+    return bufs if isinstance(bufs, ctypes.Array) else pointers(bufs)
+
+
 def _stream(s):
     if s is None:
         return None
@@ -189,8 +202,7 @@ def ar_plan_destroy(plan):
 
 
 def ar_plan_execute(plan, bufs, stream=None):
-    arr = (c_void_p * max(1, len(bufs)))(*[_ptr(b) for b in bufs])
-    _check(_lib.ar_plan_execute(plan, arr, _stream(stream)))
+    _check(_lib.ar_plan_execute(plan, _ptr_array(bufs), _stream(stream)))
 
 
 def ar_plan_execute_strided(plan, base, stride_bytes, stream=None):
@@ -199,8 +211,7 @@ def ar_plan_execute_strided(plan, base, stride_bytes, stream=None):
 
 
 def ar_plan_execute_timed(plan, bufs, stream, timer):
-    arr = (c_void_p * max(1, len(bufs)))(*[_ptr(b) for b in bufs])
-    _check(_lib.ar_plan_execute_timed(plan, arr, _stream(stream), timer))
+    _check(_lib.ar_plan_execute_timed(plan, _ptr_array(bufs), _stream(stream), timer))
 
 
 def ar_plan_info(plan):
@@ -301,14 +312,19 @@ class Plan:
             ar_plan_info(self.handle)
         self.esize = ESIZE[self.dtype]
 
+    def _bufs(self, bufs):
+        if len(bufs) != self.n:
+            raise ValueError("plan has %d processors, got %d buffers" % (self.n, len(bufs)))
+        return bufs
+
     def execute(self, bufs, stream=None):
-        ar_plan_execute(self.handle, bufs, stream)
+        ar_plan_execute(self.handle, self._bufs(bufs), stream)
 
     def execute_strided(self, base, stride_bytes, stream=None):
         ar_plan_execute_strided(self.handle, base, stride_bytes, stream)
 
     def execute_timed(self, bufs, stream, timer):
-        ar_plan_execute_timed(self.handle, bufs, stream, timer)
+        ar_plan_execute_timed(self.handle, self._bufs(bufs), stream, timer)
 
     def steps(self):
         return [ar_plan_get_step(self.handle, i) for i in range(self.num_steps)]

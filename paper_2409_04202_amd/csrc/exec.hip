@@ -44,20 +44,32 @@ constexpr int64_t kKeepBytes = int64_t(256) << 20;
 // copies it takes over move at most kFuseBytes (2 * len * e each).
 constexpr int32_t kFuseDst = 2;
 constexpr int64_t kFuseBytes = int64_t(256) << 20;
-// Automatic choice of the whole-plan (sliced) launch, for plans whose phase
-// launches are short: it is taken when the phase launches move on average at
-// most kSliceBytes each and a simple cost model predicts it faster.  Model
-// (fitted to MI355X measurements): a phase launch costs kLaunchNs plus its
-// bytes at kBytesPerNs; the sliced launch costs one kLaunchNs plus the larger
-// of its bytes at kBytesPerNs and its longest dependent chain (per phase, the
-// most steps covering one segment, summed over phases) at kChainNs per step.
-constexpr int64_t kSliceBytes = int64_t(32) << 20;
-constexpr double kLaunchNs = 10000.0;
-constexpr double kChainNs = 1000.0;
+// Automatic choice of sliced launches (AR_OPT_SLICE = 2).  A run of
+// consecutive executed phases may become one sliced launch when every phase
+// in it writes at most kKeepBytes (what one phase hands to the next would
+// stay in the last-level cache with phase launches as well) and moves at most
+// kSliceMaxBytes.  The runs are chosen by dynamic programming over the phases
+// with a cost model fitted to MI355X measurements (back-to-back launches, no
+// events between them):
+//  * a phase launch costs kLaunchNs plus its bytes at kBytesPerNs;
+//  * a sliced launch costs kLaunchNs plus, per phase, the larger of its
+//    dependent chain and its streaming time.  The chain is the most steps
+//    covering one element position, which a wavefront runs one after the
+//    other, at kStepNs + k * kStepNsPerSrc{F32,BF16} each (k = the phase's
+//    largest source count); the streaming time is its bytes at kBytesPerNs,
+//    stretched by kMinSliceWaves / waves when the slice has fewer wave tiles
+//    than that (too few waves in flight to reach full bandwidth).
+constexpr double kLaunchNs = 3000.0;
 constexpr double kBytesPerNs = 5500.0;
+constexpr double kStepNs = 350.0;
+constexpr double kStepNsPerSrcF32 = 120.0;
+constexpr double kStepNsPerSrcBF16 = 190.0;
+constexpr double kMinSliceWaves = 256.0;
+constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 
 struct LaunchDesc {
     int32_t phase;
+    int32_t xphase;          // executed phase
     int32_t kern_k;          // template K (0 = runtime source count)
     int64_t first;           // first entry of the device step table
     int64_t count;           // steps in this launch
@@ -86,7 +98,7 @@ struct DevState {
     DevStep* steps = nullptr;
     int32_t* idx = nullptr;  // source and destination indices of the steps
     int2* tiles = nullptr;
-    int64_t* cuts = nullptr;     // sliced launch tables
+    int64_t* cuts = nullptr;     // sliced launch tables, all slices concatenated
     int32_t* sched_off = nullptr;
     int32_t* sched = nullptr;
     int2* stiles = nullptr;
@@ -122,20 +134,30 @@ struct XPhase {
     std::vector<XStep> steps;
 };
 
-// The whole-plan (sliced) launch: segments are the element ranges between
-// consecutive step boundaries; sched lists, per (executed phase, segment),
-// the device steps covering that segment; tiles maps each wavefront to
-// (segment, tile within the segment).
+// A sliced launch runs executed phases [p0, p0 + nphases): segments are the
+// element ranges between consecutive boundaries of those phases' steps;
+// sched lists, per (phase of the slice, segment), the device steps covering
+// that segment; tiles maps each wavefront to (segment, tile within the
+// segment), over the segments some step of the slice covers.
 struct SliceDesc {
     bool ok = false;
-    std::string why;             // why the plan cannot run sliced
-    int32_t nphases = 0, nseg = 0;
+    std::string why;             // why the phases cannot run sliced
+    int32_t p0 = 0, nphases = 0, nseg = 0;
     int64_t tile_elems = 0, nunits = 0, bytes = 0, nsteps = 0;
     int64_t chain = 0;           // sum over phases of the most steps on a segment
     int32_t max_k = 0, max_dst = 0;
     std::vector<int64_t> cuts;
     std::vector<int32_t> sched_off, sched;
     std::vector<int2> tiles;
+    // offsets of this slice's tables in the concatenated device tables
+    int64_t cuts_base = 0, soff_base = 0, sched_base = 0, tiles_base = 0;
+};
+
+// One launch of an execution: a sliced launch (slice >= 0) or the phase
+// launch `launch`.
+struct Stage {
+    int32_t slice;
+    int32_t launch;
 };
 
 struct ExecState {
@@ -145,8 +167,8 @@ struct ExecState {
     std::vector<int32_t> hidx;   // source and destination indices
     std::vector<int2> htiles;
     std::vector<std::vector<int32_t>> dev_of;  // [phase][step] -> hsteps index
-    SliceDesc slice;
-    bool use_slice = false;      // chosen mode for 16-byte aligned buffers
+    std::vector<SliceDesc> slices;
+    std::vector<Stage> stages;   // the launches for 16-byte aligned buffers
     std::vector<DevState*> dev;  // indexed by device ordinal
 };
 
@@ -352,6 +374,7 @@ static void build_launches(const Plan& p, ExecState& ex) {
             while (g1 < idx.size() && int32_t(xp.steps[idx[g1]].srcs.size()) == k) ++g1;
             LaunchDesc L{};
             L.phase = xp.plan_phase;
+            L.xphase = int32_t(q);
             L.kern_k = kernel_k(k);
             L.first = int64_t(ex.hsteps.size());
             L.count = int64_t(g1 - g0);
@@ -434,13 +457,15 @@ static void build_launches(const Plan& p, ExecState& ex) {
     }
 }
 
-// The sliced launch of a plan, if every step boundary is 16-byte aligned.
-static void build_slice(const Plan& p, ExecState& ex) {
-    SliceDesc& sd = ex.slice;
+// The sliced launch of executed phases [p0, p1), if every boundary of their
+// steps is 16-byte aligned.
+static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int32_t p1) {
+    SliceDesc sd;
     const int64_t VEC = 16 / p.esize;
-    sd.cuts = {0, p.N};
-    for (const XPhase& xp : ex.phases)
-        for (const XStep& x : xp.steps)
+    sd.p0 = p0;
+    sd.nphases = p1 - p0;
+    for (int32_t q = p0; q < p1; ++q)
+        for (const XStep& x : ex.phases[size_t(q)].steps)
             if (x.end > x.begin) {
                 sd.cuts.push_back(x.begin);
                 sd.cuts.push_back(x.end);
@@ -450,30 +475,36 @@ static void build_slice(const Plan& p, ExecState& ex) {
     for (int64_t c : sd.cuts)
         if (c % VEC) {
             sd.why = "a step boundary is not 16-byte aligned";
-            return;
+            return sd;
         }
-    sd.nphases = int32_t(ex.phases.size());
+    if (sd.cuts.size() < 2) {
+        sd.why = "nothing to move";
+        return sd;
+    }
     sd.nseg = int32_t(sd.cuts.size() - 1);
-    if (sd.nseg < 1 || int64_t(sd.nphases) * sd.nseg > (int64_t(1) << 24)) {
+    if (int64_t(sd.nphases) * sd.nseg > (int64_t(1) << 24)) {
         sd.why = "too many phases times segments";
-        return;
+        return sd;
     }
     auto seg_of = [&](int64_t x) {  // segment starting at x
         return int32_t(std::lower_bound(sd.cuts.begin(), sd.cuts.end(), x) - sd.cuts.begin());
     };
     std::vector<std::vector<int32_t>> lists(size_t(sd.nphases) * size_t(sd.nseg));
-    for (size_t q = 0; q < ex.phases.size(); ++q) {
-        const XPhase& xp = ex.phases[q];
+    std::vector<char> used(size_t(sd.nseg), 0);
+    for (int32_t q = p0; q < p1; ++q) {
+        const XPhase& xp = ex.phases[size_t(q)];
         for (size_t i = 0; i < xp.steps.size(); ++i) {
             const XStep& x = xp.steps[i];
             if (x.end <= x.begin) continue;
-            const int32_t di = ex.dev_of[q][i];
+            const int32_t di = ex.dev_of[size_t(q)][i];
             if (di < 0) {
                 sd.why = "step without a device descriptor";
-                return;
+                return sd;
             }
-            for (int32_t sg = seg_of(x.begin); sg < seg_of(x.end); ++sg)
-                lists[q * size_t(sd.nseg) + size_t(sg)].push_back(di);
+            for (int32_t sg = seg_of(x.begin); sg < seg_of(x.end); ++sg) {
+                lists[size_t(q - p0) * size_t(sd.nseg) + size_t(sg)].push_back(di);
+                used[size_t(sg)] = 1;
+            }
             sd.bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * (x.end - x.begin) * p.esize;
             sd.max_k = std::max(sd.max_k, int32_t(x.srcs.size()));
             sd.max_dst = std::max(sd.max_dst, int32_t(x.dsts.size()));
@@ -492,20 +523,104 @@ static void build_slice(const Plan& p, ExecState& ex) {
         sd.sched.insert(sd.sched.end(), lists[i].begin(), lists[i].end());
         if (sd.sched.size() > size_t(1) << 30) {
             sd.why = "schedule too large";
-            return;
+            return sd;
         }
     }
     sd.tile_elems = int64_t(64) * kSliceU * VEC;
     for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+        if (!used[size_t(sg)]) continue;
         const int64_t len = sd.cuts[size_t(sg) + 1] - sd.cuts[size_t(sg)];
         for (int64_t t = 0; t * sd.tile_elems < len; ++t) sd.tiles.push_back(make_int2(sg, int(t)));
     }
     sd.nunits = int64_t(sd.tiles.size());
     if ((sd.nunits + kSliceWPB - 1) / kSliceWPB > kMaxBlocks) {
         sd.why = "too many tiles";
-        return;
+        return sd;
     }
     sd.ok = sd.nunits > 0;
+    if (!sd.ok) sd.why = "nothing to move";
+    return sd;
+}
+
+// Per executed phase, what the choice of sliced runs needs: whether every
+// step boundary is 16-byte aligned, the bytes written and moved, the most
+// steps covering one element position, and the predicted phase-launch time.
+struct PhaseCost {
+    bool aligned = true;
+    int64_t written = 0, bytes = 0, cover = 0;
+    int32_t kmax = 0;
+    double t_launch = 0.0;
+};
+
+static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
+    const int64_t VEC = 16 / p.esize;
+    std::vector<PhaseCost> pc(ex.phases.size());
+    for (size_t q = 0; q < ex.phases.size(); ++q) {
+        std::vector<std::pair<int64_t, int32_t>> ev;
+        for (const XStep& x : ex.phases[q].steps) {
+            if (x.end <= x.begin) continue;
+            if (x.begin % VEC || x.end % VEC) pc[q].aligned = false;
+            const int64_t len = x.end - x.begin;
+            pc[q].written += int64_t(x.dsts.size()) * len * p.esize;
+            pc[q].kmax = std::max(pc[q].kmax, int32_t(x.srcs.size()));
+            pc[q].bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * len * p.esize;
+            ev.emplace_back(x.begin, 1);
+            ev.emplace_back(x.end, -1);
+        }
+        std::sort(ev.begin(), ev.end());  // at equal positions ends (-1) first
+        int64_t c = 0;
+        for (const auto& e : ev) {
+            c += e.second;
+            pc[q].cover = std::max(pc[q].cover, c);
+        }
+    }
+    for (const LaunchDesc& L : ex.launches)
+        pc[size_t(L.xphase)].t_launch += kLaunchNs + double(L.bytes) / kBytesPerNs;
+    return pc;
+}
+
+// Sliced runs for AR_OPT_SLICE = 2: phases [a, b), each aligned, writing at
+// most kKeepBytes and moving at most kSliceMaxBytes, chosen to minimise the
+// predicted time.  A run of one phase only pays off when it replaces
+// several launches.
+static std::vector<std::pair<int32_t, int32_t>> choose_runs(const Plan& p, const ExecState& ex,
+                                                            const std::vector<PhaseCost>& pc) {
+    const double per_src = p.dtype == AR_BF16 ? kStepNsPerSrcBF16 : kStepNsPerSrcF32;
+    const double waves = std::max(1.0, double(p.N) * p.esize / (64.0 * kSliceU * 16.0));
+    const double stretch = std::max(1.0, kMinSliceWaves / waves);
+    const int32_t P = int32_t(pc.size());
+    std::vector<int32_t> nl(size_t(P), 0);
+    for (const LaunchDesc& L : ex.launches) ++nl[size_t(L.xphase)];
+    std::vector<double> best(size_t(P) + 1, 0.0);
+    std::vector<int32_t> from(size_t(P) + 1, -1);  // -1: phase launches for phase b - 1
+    for (int32_t b = 1; b <= P; ++b) {
+        best[size_t(b)] = best[size_t(b) - 1] + pc[size_t(b) - 1].t_launch;
+        from[size_t(b)] = -1;
+        double body = 0.0;
+        for (int32_t a = b - 1; a >= 0; --a) {
+            const PhaseCost& c = pc[size_t(a)];
+            if (!c.aligned || c.written > kKeepBytes || c.bytes > kSliceMaxBytes) break;
+            body += std::max(double(c.cover) * (kStepNs + per_src * c.kmax),
+                             stretch * double(c.bytes) / kBytesPerNs);
+            if (b - a == 1 && nl[size_t(a)] < 2) continue;
+            const double t = kLaunchNs + body;
+            if (best[size_t(a)] + t < best[size_t(b)]) {
+                best[size_t(b)] = best[size_t(a)] + t;
+                from[size_t(b)] = a;
+            }
+        }
+    }
+    std::vector<std::pair<int32_t, int32_t>> runs;
+    for (int32_t b = P; b > 0;) {
+        if (from[size_t(b)] < 0) {
+            --b;
+        } else {
+            runs.emplace_back(from[size_t(b)], b);
+            b = from[size_t(b)];
+        }
+    }
+    std::reverse(runs.begin(), runs.end());
+    return runs;
 }
 
 static ExecState* exec_state(Plan& p) {
@@ -514,22 +629,40 @@ static ExecState* exec_state(Plan& p) {
         try {
             ex->phases = exec_phases(p, p.fuse != 0);
             build_launches(p, *ex);
-            build_slice(p, *ex);
-            if (ex->slice.ok && !ex->launches.empty()) {
-                if (p.slice == 1) {
-                    ex->use_slice = true;
-                } else if (p.slice == 2) {
-                    double t_phase = 0.0;
-                    int64_t total = 0;
-                    for (const LaunchDesc& L : ex->launches) {
-                        t_phase += kLaunchNs + double(L.bytes) / kBytesPerNs;
-                        total += L.bytes;
-                    }
-                    const double t_slice =
-                        kLaunchNs + std::max(double(ex->slice.chain) * kChainNs,
-                                             double(ex->slice.bytes) / kBytesPerNs);
-                    ex->use_slice = total / int64_t(ex->launches.size()) <= kSliceBytes &&
-                                    t_slice < t_phase;
+            std::vector<std::pair<int32_t, int32_t>> runs;
+            if (p.slice == 1 && !ex->phases.empty()) {
+                runs.emplace_back(0, int32_t(ex->phases.size()));
+            } else if (p.slice == 2) {
+                runs = choose_runs(p, *ex, phase_costs(p, *ex));
+            }
+            std::vector<int32_t> slice_of(ex->phases.size(), -1);
+            for (const auto& r : runs) {
+                SliceDesc sd = build_slice(p, *ex, r.first, r.second);
+                if (!sd.ok) continue;  // phase launches for these phases
+                sd.cuts_base = ex->slices.empty() ? 0
+                                                  : ex->slices.back().cuts_base +
+                                                        int64_t(ex->slices.back().cuts.size());
+                sd.soff_base = ex->slices.empty() ? 0
+                                                  : ex->slices.back().soff_base +
+                                                        int64_t(ex->slices.back().sched_off.size());
+                sd.sched_base = ex->slices.empty() ? 0
+                                                   : ex->slices.back().sched_base +
+                                                         int64_t(ex->slices.back().sched.size());
+                sd.tiles_base = ex->slices.empty() ? 0
+                                                   : ex->slices.back().tiles_base +
+                                                         int64_t(ex->slices.back().tiles.size());
+                for (int32_t q = r.first; q < r.second; ++q)
+                    slice_of[size_t(q)] = int32_t(ex->slices.size());
+                ex->slices.push_back(std::move(sd));
+            }
+            int32_t last = -1;
+            for (size_t li = 0; li < ex->launches.size(); ++li) {
+                const int32_t sl = slice_of[size_t(ex->launches[li].xphase)];
+                if (sl < 0) {
+                    ex->stages.push_back({-1, int32_t(li)});
+                } else if (sl != last) {
+                    ex->stages.push_back({sl, -1});
+                    last = sl;
                 }
             }
         } catch (...) {
@@ -599,11 +732,20 @@ static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
         ar_status s = upload(&d->steps, ex.hsteps, "step table");
         if (s == AR_OK) s = upload(&d->idx, ex.hidx, "index table");
         if (s == AR_OK) s = upload(&d->tiles, ex.htiles, "tile table");
-        if (s == AR_OK && ex.slice.ok) {
-            s = upload(&d->cuts, ex.slice.cuts, "segment table");
-            if (s == AR_OK) s = upload(&d->sched_off, ex.slice.sched_off, "schedule offsets");
-            if (s == AR_OK) s = upload(&d->sched, ex.slice.sched, "schedule");
-            if (s == AR_OK) s = upload(&d->stiles, ex.slice.tiles, "slice tiles");
+        if (s == AR_OK && !ex.slices.empty()) {
+            std::vector<int64_t> cuts;
+            std::vector<int32_t> soff, sched;
+            std::vector<int2> tiles;
+            for (const SliceDesc& sd : ex.slices) {
+                cuts.insert(cuts.end(), sd.cuts.begin(), sd.cuts.end());
+                soff.insert(soff.end(), sd.sched_off.begin(), sd.sched_off.end());
+                sched.insert(sched.end(), sd.sched.begin(), sd.sched.end());
+                tiles.insert(tiles.end(), sd.tiles.begin(), sd.tiles.end());
+            }
+            s = upload(&d->cuts, cuts, "segment table");
+            if (s == AR_OK) s = upload(&d->sched_off, soff, "schedule offsets");
+            if (s == AR_OK) s = upload(&d->sched, sched, "schedule");
+            if (s == AR_OK) s = upload(&d->stiles, tiles, "slice tiles");
         }
         if (s != AR_OK) {
             free_dev(d);
@@ -745,9 +887,10 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
         PtrEntry* pe = nullptr;
         s = pointer_table(*plan, *d, bufs, stream, &pe);
         if (s != AR_OK) return s;
-        // the whole-plan launch needs 16-byte aligned buffers
-        const bool sliced = ex->use_slice && pe->aligned;
-        const int64_t nlaunch = sliced ? 1 : int64_t(ex->launches.size());
+        // sliced launches need 16-byte aligned buffers; otherwise every
+        // phase runs as its phase launches
+        const bool staged = pe->aligned;
+        const int64_t nlaunch = staged ? int64_t(ex->stages.size()) : int64_t(ex->launches.size());
         if (timer && timer->count + nlaunch > timer->cap)
             return fail(AR_ERR_INVALID_ARG, "timer is full");
         auto mark = [&](int j) -> ar_status {  // event j (0 begin, 1 end) of this record
@@ -767,13 +910,15 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
         for (int64_t li = 0; li < nlaunch; ++li) {
             s = mark(0);
             if (s != AR_OK) return s;
-            if (sliced) {
-                const SliceDesc& sd = ex->slice;
+            const Stage stg = staged ? ex->stages[size_t(li)] : Stage{-1, int32_t(li)};
+            if (stg.slice >= 0) {
+                const SliceDesc& sd = ex->slices[size_t(stg.slice)];
                 const dim3 grid(static_cast<uint32_t>((sd.nunits + kSliceWPB - 1) / kSliceWPB));
                 const dim3 block(64 * kSliceWPB);
 #define AR_SLICED(DT)                                                                   \
     hipLaunchKernelGGL((sliced_kernel<DT>), grid, block, 0, stream, d->steps, d->idx,   \
-                       pe->dev, d->sched_off, d->sched, d->cuts, d->stiles, sd.nunits, \
+                       pe->dev, d->sched_off + sd.soff_base, d->sched + sd.sched_base,  \
+                       d->cuts + sd.cuts_base, d->stiles + sd.tiles_base, sd.nunits,    \
                        sd.nphases, sd.nseg, sd.tile_elems)
                 switch (plan->dtype) {
                     case AR_F32: AR_SLICED(DT_F32); break;
@@ -782,7 +927,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                 }
 #undef AR_SLICED
             } else {
-                const LaunchDesc& L = ex->launches[size_t(li)];
+                const LaunchDesc& L = ex->launches[size_t(stg.launch)];
                 const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
                 const DevStep* steps = d->steps + L.first;
                 const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
@@ -980,11 +1125,41 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             if (st.end > st.begin && at != st.end)
                 return bad("step " + std::to_string(i) + " not covered to its end");
         }
-        // the whole-plan launch: tiles cover every segment exactly once with
-        // aligned vectors, and each (phase, segment) lists exactly the steps
-        // of that phase covering the segment
-        const SliceDesc& sd = ex->slice;
-        if (sd.ok) {
+        // sliced launches: the runs are disjoint and in order, every stage
+        // names a launch or a slice, every launch of a phase outside the
+        // slices runs once; a slice's tiles cover each segment some step of
+        // its phases covers exactly once with aligned vectors, and each
+        // (phase, segment) lists exactly the steps of that phase covering the
+        // segment
+        {
+            std::vector<int32_t> slice_of(ex->phases.size(), -1);
+            int32_t prev_end = 0;
+            for (size_t k = 0; k < ex->slices.size(); ++k) {
+                const SliceDesc& sd = ex->slices[k];
+                if (!sd.ok || sd.nphases < 1 || sd.p0 < prev_end ||
+                    sd.p0 + sd.nphases > int32_t(ex->phases.size()))
+                    return bad("slice phase range out of order");
+                prev_end = sd.p0 + sd.nphases;
+                for (int32_t q = sd.p0; q < prev_end; ++q) slice_of[size_t(q)] = int32_t(k);
+            }
+            std::vector<int32_t> runs_of(ex->launches.size(), 0), seen(ex->slices.size(), 0);
+            for (const Stage& stg : ex->stages) {
+                if (stg.slice >= 0) {
+                    if (stg.slice >= int32_t(ex->slices.size())) return bad("stage names no slice");
+                    ++seen[size_t(stg.slice)];
+                } else {
+                    if (stg.launch < 0 || stg.launch >= int32_t(ex->launches.size()))
+                        return bad("stage names no launch");
+                    ++runs_of[size_t(stg.launch)];
+                }
+            }
+            for (size_t k = 0; k < ex->slices.size(); ++k)
+                if (seen[k] != 1) return bad("slice not run exactly once");
+            for (size_t li = 0; li < ex->launches.size(); ++li)
+                if (runs_of[li] != (slice_of[size_t(ex->launches[li].xphase)] < 0 ? 1 : 0))
+                    return bad("phase launch not run exactly once outside the slices");
+        }
+        for (const SliceDesc& sd : ex->slices) {
             std::vector<std::vector<std::pair<int64_t, int64_t>>> sc(size_t(sd.nseg));
             for (int64_t u = 0; u < sd.nunits; ++u) {
                 const int2 e = sd.tiles[size_t(u)];
@@ -995,8 +1170,19 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 if ((hi - lo) / VEC > 64 * kSliceU) return bad("slice tile too long");
                 sc[size_t(e.x)].push_back({lo, hi});
             }
+            if (int64_t(sd.sched_off.size()) != int64_t(sd.nphases) * sd.nseg + 1)
+                return bad("schedule offsets of the wrong size");
             for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+                bool covered = false;
+                for (int32_t q = 0; q < sd.nphases; ++q) {
+                    const size_t o = size_t(q) * size_t(sd.nseg) + size_t(sg);
+                    if (sd.sched_off[o + 1] > sd.sched_off[o]) covered = true;
+                }
                 auto& c = sc[size_t(sg)];
+                if (!covered) {
+                    if (!c.empty()) return bad("slice tiles on a segment no step covers");
+                    continue;
+                }
                 std::sort(c.begin(), c.end());
                 int64_t at = sd.cuts[size_t(sg)];
                 for (auto& iv : c) {
@@ -1005,16 +1191,15 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 }
                 if (at != sd.cuts[size_t(sg) + 1]) return bad("slice tiles do not cover a segment");
             }
-            if (int64_t(sd.sched_off.size()) != int64_t(sd.nphases) * sd.nseg + 1)
-                return bad("schedule offsets of the wrong size");
             for (int32_t q = 0; q < sd.nphases; ++q) {
-                const XPhase& xp = ex->phases[size_t(q)];
+                const XPhase& xp = ex->phases[size_t(sd.p0 + q)];
                 for (int32_t sg = 0; sg < sd.nseg; ++sg) {
                     std::vector<int32_t> want, got;
                     for (size_t i = 0; i < xp.steps.size(); ++i) {
                         const XStep& x = xp.steps[i];
+                        if (x.end <= x.begin) continue;
                         if (x.begin <= sd.cuts[size_t(sg)] && sd.cuts[size_t(sg) + 1] <= x.end)
-                            want.push_back(ex->dev_of[size_t(q)][i]);
+                            want.push_back(ex->dev_of[size_t(sd.p0 + q)][i]);
                         else if (x.begin < sd.cuts[size_t(sg) + 1] && sd.cuts[size_t(sg)] < x.end)
                             return bad("a step cuts a segment");
                     }
@@ -1026,6 +1211,13 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     if (want != got) return bad("schedule differs from the steps of a phase");
                 }
             }
+            // every step of the slice's phases lies inside the segments
+            for (int32_t q = 0; q < sd.nphases; ++q)
+                for (const XStep& x : ex->phases[size_t(sd.p0 + q)].steps)
+                    if (x.end > x.begin &&
+                        (!std::binary_search(sd.cuts.begin(), sd.cuts.end(), x.begin) ||
+                         !std::binary_search(sd.cuts.begin(), sd.cuts.end(), x.end)))
+                        return bad("a step boundary is not a segment boundary");
         }
         if (msg && msglen > 0) msg[0] = 0;
         return AR_OK;
@@ -1059,7 +1251,7 @@ AR_EXPORT ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count) {
     if (!plan || !count) return fail(AR_ERR_INVALID_ARG, "NULL argument");
     try {
         const ExecState* ex = exec_state(const_cast<ar_plan&>(*plan));
-        *count = ex->use_slice ? 1 : int32_t(ex->launches.size());
+        *count = int32_t(ex->stages.size());
         return AR_OK;
     } catch (const std::bad_alloc&) {
         return fail(AR_ERR_OOM, "host allocation failed");
@@ -1075,9 +1267,11 @@ AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t*
     if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
     try {
         const ExecState* ex = exec_state(const_cast<ar_plan&>(*plan));
-        if (ex->use_slice) {
-            if (i != 0) return fail(AR_ERR_INVALID_ARG, "launch index out of range");
-            const SliceDesc& sd = ex->slice;
+        if (i < 0 || i >= int32_t(ex->stages.size()))
+            return fail(AR_ERR_INVALID_ARG, "launch index out of range");
+        const Stage stg = ex->stages[size_t(i)];
+        if (stg.slice >= 0) {
+            const SliceDesc& sd = ex->slices[size_t(stg.slice)];
             if (phase) *phase = -1;
             if (nsrc) *nsrc = sd.max_k;
             if (max_dst) *max_dst = sd.max_dst;
@@ -1085,9 +1279,7 @@ AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t*
             if (bytes) *bytes = sd.bytes;
             return AR_OK;
         }
-        if (i < 0 || i >= int32_t(ex->launches.size()))
-            return fail(AR_ERR_INVALID_ARG, "launch index out of range");
-        const LaunchDesc& L = ex->launches[size_t(i)];
+        const LaunchDesc& L = ex->launches[size_t(stg.launch)];
         if (phase) *phase = L.phase;
         if (nsrc) *nsrc = ex->hsteps[size_t(L.first)].k;
         if (max_dst) *max_dst = L.max_dst;

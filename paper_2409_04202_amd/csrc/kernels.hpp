@@ -92,11 +92,16 @@ template <> struct Elem<DT_BF16> { using T = uint16_t; static constexpr int VEC 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x0040u;
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// fp32 -> bf16, round to nearest, ties to even; a NaN keeps its sign and
+// upper payload bits and gets the quiet bit.  gfx950 does this in hardware,
+// two values per instruction (v_cvt_pk_bf16_f32), denormals included when
+// fp32 denormals are enabled (they are: -fno-gpu-flush-denormals-to-zero).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
+    const f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 // ---------------------------------------------- 16-byte vector accumulator
@@ -137,10 +142,8 @@ template <> struct VAcc<DT_BF16> {
         v[4] += bf16_lo(x[2]); v[5] += bf16_hi(x[2]); v[6] += bf16_lo(x[3]); v[7] += bf16_hi(x[3]);
     }
     __device__ __forceinline__ u32x4 out() const {
-        return u32x4{f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16),
-                     f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16),
-                     f32_to_bf16_bits(v[4]) | (f32_to_bf16_bits(v[5]) << 16),
-                     f32_to_bf16_bits(v[6]) | (f32_to_bf16_bits(v[7]) << 16)};
+        return u32x4{bf16_pack(v[0], v[1]), bf16_pack(v[2], v[3]),
+                     bf16_pack(v[4], v[5]), bf16_pack(v[6], v[7])};
     }
 };
 
@@ -163,7 +166,7 @@ template <> struct SAcc<DT_BF16> {
     float v;
     __device__ __forceinline__ void init(uint16_t x) { v = __uint_as_float(uint32_t(x) << 16); }
     __device__ __forceinline__ void add(uint16_t x) { v += __uint_as_float(uint32_t(x) << 16); }
-    __device__ __forceinline__ uint16_t out() const { return uint16_t(f32_to_bf16_bits(v)); }
+    __device__ __forceinline__ uint16_t out() const { return uint16_t(bf16_pack(v, 0.0f)); }
 };
 
 // Element ranges of wave tile t of a step [begin, end): the tile is

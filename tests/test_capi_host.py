@@ -411,7 +411,7 @@ def test_gentree_steps_match_oracle(idx):
                     else:
                         assert _status(arplan.ar_plan_owner, p.handle, sid) == \
                             arplan.AR_ERR_UNSUPPORTED
-            for sl in (0, 1):
+            for sl in (0, 1, 2):
                 p.set_option(arplan.AR_OPT_SLICE, sl)
                 for vecok in (1, 0):
                     st, msg = _check_tiling(p.handle, vecok)
@@ -445,3 +445,37 @@ def test_gentree_errors():
         assert E.ar_plan_info(h)[3:] == (0, 0)
     finally:
         E.ar_plan_destroy(h)
+
+
+@pytest.mark.parametrize("name", sorted(__import__(
+    "paper_2409_04202_amd.workloads", fromlist=["CONFIGS"]).CONFIGS))
+def test_sliced_runs_of_workloads(name):
+    # AR_OPT_SLICE = 2 partitions the executed phases into sliced runs and
+    # phase launches: the same executed steps (same bytes) as the phase
+    # launches, every launch tiled exactly, and no sliced launch on the
+    # 2 GiB RHD plan, whose phases each write more than the 256 MiB cache
+    from paper_2409_04202_amd import workloads
+    c = workloads.CONFIGS[name]
+    with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
+        L = p.launches()
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        L0 = p.launches()
+        assert sum(x[4] for x in L) == sum(x[4] for x in L0)
+        assert sum(x[3] for x in L) == sum(x[3] for x in L0)
+        # phase launches kept outside the runs appear in phase order
+        kept = [x for x in L if x[0] >= 0]
+        assert all(x in L0 for x in kept)
+        assert [x[0] for x in kept] == sorted(x[0] for x in kept)
+        p.set_option(arplan.AR_OPT_SLICE, 2)
+        for vecok in (1, 0):
+            st, msg = _check_tiling(p.handle, vecok)
+            assert st == arplan.AR_OK, msg
+        if name == "rhd_n8_f32":
+            assert all(x[0] >= 0 for x in L)
+        if name == "tree8x8x8_n512_bf16":
+            # the last AllGather phase covers each position with 448 copies:
+            # a chain far too long for a sliced launch
+            assert L[-1][0] == 5
+        if name.startswith("sweep_ring"):
+            # 126 phases of short steps: one sliced launch
+            assert len(L) == 1 and L[0][0] == -1

@@ -104,6 +104,22 @@ def test_sweep_configs_bit_exact(name, slice_):
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
+@pytest.mark.parametrize("kind,n,N,dtype,fan", [
+    ("rhd", 16, 1 << 14, "f32", None),
+    ("tree", 64, 1 << 18, "bf16", (4, 4, 4)),
+    ("tree", 128, 1 << 18, "f32", (2, 8, 8)),
+    ("gentree", 384, 384 * 256, "f32",
+     tuple(workloads.CONFIGS["cdc384_gentree_f32"]["fanin"]))])
+def test_sliced_runs_between_phase_launches(kind, n, N, dtype, fan):
+    # the automatic choice mixes sliced runs and phase launches here
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        phases = [x[0] for x in p.launches()]
+    assert -1 in phases and any(ph >= 0 for ph in phases), phases
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, "uniform", seed=11)
+    if dtype == "bf16":
+        assert _normwise_bf16(got[0], xs0) <= 1e-2
+
+
 # ------------------------------------------------- full-size, sampled check
 
 def _sample_positions(n, N, rng):
@@ -214,6 +230,61 @@ def test_bf16_ties_round_to_even():
     got, _ = _full_compare("cps", n, N, "bf16", xs0=[a, b])
     assert np.all(got[0][0::2] == 0x3F80)    # tie to even: 1.0
     assert np.all(got[0][1::2] == 0x3F82)    # 1 + 2^-6 (even mantissa)
+
+
+def _bf16_rounding_inputs(seed):
+    # a: every finite bf16 pattern; b: a value 8 to 10 binades below a (a
+    # random denormal where that underflows), random sign and mantissa, so
+    # that the exact fp32 sum a + b needs rounding: ties, carries into the
+    # exponent, overflow to infinity at the top, cancellation, denormal
+    # results
+    rng = np.random.default_rng(seed)
+    pats = np.arange(65536, dtype=np.uint32)
+    exp = (pats >> 7) & 0xFF
+    a = pats[exp != 0xFF]
+    e = (a >> 7) & 0xFF
+    d = rng.integers(8, 11, a.size).astype(np.uint32)
+    sgn = rng.integers(0, 2, a.size).astype(np.uint32) << 15
+    man = rng.integers(0, 128, a.size).astype(np.uint32)
+    b = np.where(e > d, sgn | ((e - d) << 7) | man, sgn | man)
+    return a.astype(np.uint16), b.astype(np.uint16)
+
+
+@pytest.mark.parametrize("fuse,slice_", MODES)
+def test_bf16_rounding_every_exponent(fuse, slice_):
+    a, b = _bf16_rounding_inputs(3)
+    N = a.size - a.size % 8
+    xs0 = [a[:N].copy(), b[:N].copy()]
+    got, _ = _full_compare("cps", 2, N, "bf16", xs0=xs0, fuse=fuse, slice_=slice_)
+    f = oracle.bf16_to_f32(got[0])
+    assert np.isinf(f).any() and (np.abs(f[f != 0]) < 1.2e-38).any()
+
+
+def test_bf16_nan_and_inf_inputs():
+    # NaN inputs give NaN, infinities add as in IEEE; the NaN payload after
+    # an add is the hardware's choice, so NaNs are compared as NaNs
+    n, N = 4, 4096
+    rng = np.random.default_rng(17)
+    xs0 = [oracle.f32_to_bf16((rng.random(N) * 2 - 1).astype(np.float32))
+           for _ in range(n)]
+    xs0[1][::7] = 0x7FC1                     # quiet NaN, payload 1
+    xs0[2][::11] = 0xFF81                    # signalling NaN, negative
+    xs0[0][::13] = 0x7F80                    # +inf
+    xs0[3][::17] = 0xFF80                    # -inf
+    ref = oracle.execute(oracle.cps(n, N), [x.copy() for x in xs0], "bf16")
+    for fuse, sl in MODES:
+        ts = to_device(xs0, "bf16")
+        with arplan.Plan(n, N, "bf16", "cps") as p:
+            p.set_option(arplan.AR_OPT_FUSE, fuse)
+            p.set_option(arplan.AR_OPT_SLICE, sl)
+            run_plan(p, ts)
+        got = to_host(ts, "bf16")
+        for q in range(n):
+            gf, rf = oracle.bf16_to_f32(got[q]), oracle.bf16_to_f32(ref[q])
+            assert np.array_equal(np.isnan(gf), np.isnan(rf))
+            ok = ~np.isnan(rf)
+            assert np.array_equal(got[q][ok], ref[q][ok])
+            assert np.isnan(rf).any() and np.isinf(rf).any()
 
 
 def test_custom_plan_mixed_sources_and_uneven_steps():
