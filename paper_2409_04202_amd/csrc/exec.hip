@@ -37,11 +37,14 @@ constexpr int64_t kMaxBlocks = int64_t(1) << 24;
 constexpr int64_t kNtBytes = int64_t(64) << 20;
 constexpr int64_t kKeepBytes = int64_t(256) << 20;
 // The step rewrites (multicast, reduce-then-broadcast) pay off where they
-// remove a launch from a short phase, or add at most one extra destination;
-// a step storing to many destinations over a large range is store-bound and
-// slower than plain copies whose repeated reads hit the cache.  A rewrite
-// is applied when its step ends with at most kFuseDst destinations or the
-// copies it takes over move at most kFuseBytes (2 * len * e each).
+// remove a launch from a short phase, add at most one extra destination, or
+// take over copies that read every range once (their reads are saved; a
+// 2-source fold storing to 8 destinations streams at 5.0 TB/s); a step
+// storing to many destinations over a large range is slower than plain
+// copies whose repeated reads hit the cache.  A rewrite is applied when its
+// step ends with at most kFuseDst destinations, the copies it takes over
+// move at most kFuseBytes (2 * len * e each), or (reduce-then-broadcast) no
+// two of those copies read the same range.
 constexpr int32_t kFuseDst = 2;
 constexpr int64_t kFuseBytes = int64_t(256) << 20;
 // Automatic choice of sliced launches (AR_OPT_SLICE = 2).  A run of
@@ -52,18 +55,20 @@ constexpr int64_t kFuseBytes = int64_t(256) << 20;
 // with a cost model fitted to MI355X measurements (back-to-back launches, no
 // events between them):
 //  * a phase launch costs kLaunchNs plus its bytes at kBytesPerNs;
-//  * a sliced launch costs kLaunchNs plus, per phase, the larger of its
-//    dependent chain and its streaming time.  The chain is the most steps
-//    covering one element position, which a wavefront runs one after the
-//    other, at kStepNs + k * kStepNsPerSrc{F32,BF16} each (k = the phase's
-//    largest source count); the streaming time is its bytes at kBytesPerNs,
+//  * a sliced launch costs kLaunchNs plus, per phase, the largest of its
+//    dependent chain, its read time and its write time.  The chain is the
+//    most steps covering one element position, which a wavefront runs one
+//    after the other, at kStepNs + k * kStepNsPerSrc{F32,BF16} +
+//    d * kStepNsPerDst each (k, d = the phase's largest source and
+//    destination counts); reads and writes go at kBytesPerNs, the reads
 //    stretched by kMinSliceWaves / waves when the slice has fewer wave tiles
-//    than that (too few waves in flight to reach full bandwidth).
+//    than that (too few loads in flight to reach full bandwidth).
 constexpr double kLaunchNs = 3000.0;
 constexpr double kBytesPerNs = 5500.0;
 constexpr double kStepNs = 350.0;
 constexpr double kStepNsPerSrcF32 = 120.0;
 constexpr double kStepNsPerSrcBF16 = 190.0;
+constexpr double kStepNsPerDst = 15.0;
 constexpr double kMinSliceWaves = 256.0;
 constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 
@@ -213,12 +218,15 @@ struct Touches {
 //    buffer become one step that reads it once and stores it to every
 //    destination;
 //  * reduce-then-broadcast: when every step of phase q+1 copies a range that
-//    a reduce step of phase q has just produced, the copies are absorbed into
-//    those reduce steps, which then store their results to the copies'
-//    destinations as well, and phase q+1 disappears (the last ReduceScatter
-//    phase and the first AllGather phase meet this way).  The absorbed
-//    writes are checked against every read and write of the other steps of
-//    phase q, so the merged phase stays free of hazards.
+//    is a union of ranges the reduce steps of phase q have just produced,
+//    the copies are absorbed into those reduce steps, which then store their
+//    results to the copies' destinations as well, and phase q+1 disappears
+//    (the last ReduceScatter phase and the first AllGather phase meet this
+//    way).  Applied again with q+2, q+3, ... as long as it succeeds, so that
+//    a whole AllGather can fold into the last reduce phase (RHD: each eighth
+//    is reduced once and stored to all eight buffers).  The absorbed writes
+//    are checked against every read and write of the other steps of phase q,
+//    so the merged phase stays free of hazards.
 static std::vector<XPhase> exec_phases(const Plan& p, bool fuse) {
     std::vector<XPhase> ph(size_t(p.num_phases()));
     for (int32_t q = 0; q < p.num_phases(); ++q) {
@@ -277,48 +285,73 @@ static std::vector<XPhase> exec_phases(const Plan& p, bool fuse) {
         }
         xp.steps = std::move(kept);
     }
-    for (size_t q = 0; q + 1 < ph.size(); ++q) {  // reduce-then-broadcast
-        XPhase& cur = ph[q];
-        XPhase& nxt = ph[q + 1];
+    // reduce-then-broadcast, transitively: phase q absorbs q+1, then q+2, ...
+    // as long as each next phase consists of copies whose source ranges are
+    // exactly unions of ranges the (merged) reduce steps of q write
+    auto absorb = [&](XPhase& cur, const XPhase& nxt) {
         const Touches touched(cur, p.n, true, true);
-        std::map<std::tuple<int32_t, int64_t, int64_t>, size_t> produced;
+        // per buffer, the ranges the reduce steps of cur write, by begin
+        std::map<std::pair<int32_t, int64_t>, std::pair<int64_t, size_t>> produced;
         for (size_t i = 0; i < cur.steps.size(); ++i) {
             const XStep& st = cur.steps[i];
             if (st.srcs.size() >= 2 && st.end > st.begin)
-                for (int32_t d : st.dsts) produced[std::make_tuple(d, st.begin, st.end)] = i;
+                for (int32_t d : st.dsts) produced[{d, st.begin}] = {st.end, i};
         }
-        // absorb the whole next phase or nothing: only then a launch goes
+        // copies whose reads are all distinct move data nobody reads twice:
+        // folding them into the reduce steps saves their reads entirely
         const bool small = copy_bytes(nxt) <= kFuseBytes;
-        std::vector<size_t> into(nxt.steps.size());
-        std::vector<size_t> extra(cur.steps.size(), 0);
-        bool all = !nxt.steps.empty();
-        for (size_t j = 0; j < nxt.steps.size() && all; ++j) {
-            const XStep& c = nxt.steps[j];
-            into[j] = size_t(-1);
-            if (c.end <= c.begin) continue;  // empty step: nothing to move
-            auto it = c.srcs.size() == 1
-                          ? produced.find(std::make_tuple(c.srcs[0], c.begin, c.end))
-                          : produced.end();
-            if (it == produced.end()) {
-                all = false;
-                break;
+        bool distinct = true;
+        {
+            std::vector<std::tuple<int32_t, int64_t, int64_t>> rd;
+            for (const XStep& c : nxt.steps) {
+                if (c.end <= c.begin) continue;
+                if (c.dsts.size() != 1) distinct = false;
+                for (int32_t q : c.srcs) rd.emplace_back(q, c.begin, c.end);
             }
-            for (int32_t d : c.dsts)
-                if (touched.other(d, c.begin, c.end, it->second)) all = false;
-            into[j] = it->second;
-            extra[it->second] += c.dsts.size();
+            std::sort(rd.begin(), rd.end());
+            for (size_t i = 1; i < rd.size() && distinct; ++i)
+                if (std::get<0>(rd[i]) == std::get<0>(rd[i - 1]) &&
+                    std::get<1>(rd[i]) < std::get<2>(rd[i - 1]))
+                    distinct = false;
         }
-        for (size_t i = 0; i < cur.steps.size() && all; ++i)
-            if (!small && int32_t(cur.steps[i].dsts.size() + extra[i]) > kFuseDst) all = false;
-        if (!all) continue;
-        for (size_t j = 0; j < nxt.steps.size(); ++j) {
-            if (into[j] == size_t(-1)) continue;
-            XStep& s = cur.steps[into[j]];
-            for (int32_t d : nxt.steps[j].dsts)
-                if (std::find(s.dsts.begin(), s.dsts.end(), d) == s.dsts.end())
-                    s.dsts.push_back(d);
+        // (producer step, destination) pairs to add
+        std::vector<std::pair<size_t, int32_t>> adds;
+        std::vector<size_t> extra(cur.steps.size(), 0);
+        bool any = false;
+        for (const XStep& c : nxt.steps) {
+            if (c.end <= c.begin) continue;  // empty step: nothing to move
+            if (c.srcs.size() != 1) return false;
+            any = true;
+            int64_t at = c.begin;
+            while (at < c.end) {
+                auto it = produced.find({c.srcs[0], at});
+                if (it == produced.end() || it->second.first > c.end) return false;
+                const size_t i = it->second.second;
+                for (int32_t d : c.dsts) {
+                    if (touched.other(d, at, it->second.first, i)) return false;
+                    adds.emplace_back(i, d);
+                    extra[i] += 1;
+                }
+                at = it->second.first;
+            }
         }
-        nxt.steps.clear();
+        if (!any) return false;
+        if (!small && !distinct)
+            for (size_t i = 0; i < cur.steps.size(); ++i)
+                if (int32_t(cur.steps[i].dsts.size() + extra[i]) > kFuseDst) return false;
+        for (const auto& ad : adds) {
+            XStep& s = cur.steps[ad.first];
+            if (std::find(s.dsts.begin(), s.dsts.end(), ad.second) == s.dsts.end())
+                s.dsts.push_back(ad.second);
+        }
+        return true;
+    };
+    for (size_t q = 0; q + 1 < ph.size(); ++q) {
+        if (ph[q].steps.empty()) continue;
+        for (size_t j = q + 1; j < ph.size(); ++j) {
+            if (!absorb(ph[q], ph[j])) break;
+            ph[j].steps.clear();
+        }
     }
     std::vector<XPhase> out;
     for (XPhase& xp : ph)
@@ -547,8 +580,8 @@ static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int
 // steps covering one element position, and the predicted phase-launch time.
 struct PhaseCost {
     bool aligned = true;
-    int64_t written = 0, bytes = 0, cover = 0;
-    int32_t kmax = 0;
+    int64_t written = 0, read = 0, bytes = 0, cover = 0;
+    int32_t kmax = 0, dmax = 0;
     double t_launch = 0.0;
 };
 
@@ -562,7 +595,9 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
             if (x.begin % VEC || x.end % VEC) pc[q].aligned = false;
             const int64_t len = x.end - x.begin;
             pc[q].written += int64_t(x.dsts.size()) * len * p.esize;
+            pc[q].read += int64_t(x.srcs.size()) * len * p.esize;
             pc[q].kmax = std::max(pc[q].kmax, int32_t(x.srcs.size()));
+            pc[q].dmax = std::max(pc[q].dmax, int32_t(x.dsts.size()));
             pc[q].bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * len * p.esize;
             ev.emplace_back(x.begin, 1);
             ev.emplace_back(x.end, -1);
@@ -600,8 +635,9 @@ static std::vector<std::pair<int32_t, int32_t>> choose_runs(const Plan& p, const
         for (int32_t a = b - 1; a >= 0; --a) {
             const PhaseCost& c = pc[size_t(a)];
             if (!c.aligned || c.written > kKeepBytes || c.bytes > kSliceMaxBytes) break;
-            body += std::max(double(c.cover) * (kStepNs + per_src * c.kmax),
-                             stretch * double(c.bytes) / kBytesPerNs);
+            body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
+                              stretch * double(c.read) / kBytesPerNs,
+                              double(c.written) / kBytesPerNs});
             if (b - a == 1 && nl[size_t(a)] < 2) continue;
             const double t = kLaunchNs + body;
             if (best[size_t(a)] + t < best[size_t(b)]) {

@@ -264,10 +264,10 @@ def test_executor_rewrites_launch_structure():
     # (kind, n, N, fan) -> launches with fusion, and the fused byte total
     cases = [
         ("cps", 16, 1 << 20, None, 1),    # reduce + broadcast in one launch
-        ("rhd", 8, 1 << 20, None, 5),     # last halving absorbs the first doubling
-        ("tree", 64, 1 << 16, (8, 8), 3), # RS-L1 absorbs AG-L1; AG-L0 multicast
-        ("tree", 512, 1 << 15, (8, 8, 8), 5),
-        ("ring", 5, 1000, None, 7),       # 2(n-1) - 1
+        ("rhd", 8, 1 << 20, None, 3),     # last halving absorbs every doubling
+        ("tree", 64, 1 << 16, (8, 8), 2), # RS-L1 absorbs AG-L1, then AG-L0
+        ("tree", 512, 1 << 15, (8, 8, 8), 3),
+        ("ring", 5, 1000, None, 4),       # the AllGather chain folds into the last reduce
         ("rb", 6, 999, None, 1),
     ]
     for kind, n, N, fan, nl in cases:
@@ -298,7 +298,17 @@ def test_executor_rewrites_launch_structure():
     with arplan.Plan(64, 1 << 16, "f32", "tree", (8, 8)) as p:
         p.set_option(arplan.AR_OPT_SLICE, 0)
         L = p.launches()
-        assert [(x[1], x[2], x[3]) for x in L] == [(8, 1, 64), (8, 8, 64), (1, 7, 64)]
+        assert [(x[1], x[2], x[3]) for x in L] == [(8, 1, 64), (8, 64, 64)]
+    # RHD: each eighth is reduced once and stored to all 8 buffers (its
+    # copies read every range once, so the rewrite applies at any size)
+    with arplan.Plan(8, 1 << 26, "f32", "rhd") as p:
+        L = p.launches()
+        assert [(x[0], x[1], x[2], x[3]) for x in L] == [(0, 2, 1, 8), (1, 2, 1, 8), (2, 2, 8, 8)]
+        assert L[2][4] == 8 * (2 + 8) * (1 << 26) // 8 * 4
+    # co-located PS at 1 GiB: the broadcast copies read each range 15 times
+    # (cache hits), so they stay a launch of their own
+    with arplan.Plan(16, 1 << 24, "f32", "cps") as p:
+        assert [(x[1], x[2]) for x in p.launches()] == [(16, 1), (1, 1)]
     assert _status(arplan.ar_plan_set_option, 0, 0, 1) == arplan.AR_ERR_INVALID_ARG
     with arplan.Plan(4, 100, "f32", "ring") as p:
         assert _status(arplan.ar_plan_set_option, p.handle, 7, 1) == arplan.AR_ERR_INVALID_ARG
