@@ -12,6 +12,18 @@ extern "C" {
  * AR_ERR_INTERNAL with the first problem in `msg` (msglen bytes). */
 ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok, char* msg,
                                 int64_t msglen);
+
+/* The executed steps of `plan` under its current options (after the
+ * executor's rewrites), in executed-phase order: step i folds its nsrc[i]
+ * sources over [begin[i], end[i]) and stores the result into its ndst[i]
+ * destinations; its sources and then its destinations are the next
+ * nsrc[i] + ndst[i] entries of idx.  *count / *idx_count receive the totals;
+ * entries are written while they fit in step_cap / idx_cap (any array may be
+ * NULL to query the totals).  Host only. */
+ar_status ar_debug_exec_steps(ar_plan* plan, int64_t step_cap, int32_t* phase,
+                              int64_t* begin, int64_t* end, int32_t* nsrc,
+                              int32_t* ndst, int64_t idx_cap, int32_t* idx,
+                              int64_t* count, int64_t* idx_count);
 #ifdef __cplusplus
 }
 #endif

@@ -18,6 +18,7 @@
 #include <string>
 #include <vector>
 
+#include "ar_debug.h"
 #include "internal.hpp"
 #include "kernels.hpp"
 
@@ -1259,6 +1260,44 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
         return AR_OK;
     } catch (const std::exception& e) {
         return bad(e.what());
+    }
+}
+
+AR_EXPORT ar_status ar_debug_exec_steps(ar_plan* plan, int64_t step_cap, int32_t* phase,
+                                        int64_t* begin, int64_t* end, int32_t* nsrc,
+                                        int32_t* ndst, int64_t idx_cap, int32_t* idx,
+                                        int64_t* count, int64_t* idx_count) {
+    clear_error();
+    if (!plan || !count || !idx_count) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    try {
+        const ExecState* ex = exec_state(*plan);
+        int64_t c = 0, ic = 0;
+        for (size_t q = 0; q < ex->phases.size(); ++q)
+            for (const XStep& x : ex->phases[q].steps) {
+                if (c < step_cap) {
+                    if (phase) phase[c] = int32_t(q);
+                    if (begin) begin[c] = x.begin;
+                    if (end) end[c] = x.end;
+                    if (nsrc) nsrc[c] = int32_t(x.srcs.size());
+                    if (ndst) ndst[c] = int32_t(x.dsts.size());
+                }
+                ++c;
+                for (int32_t v : x.srcs) {
+                    if (idx && ic < idx_cap) idx[ic] = v;
+                    ++ic;
+                }
+                for (int32_t v : x.dsts) {
+                    if (idx && ic < idx_cap) idx[ic] = v;
+                    ++ic;
+                }
+            }
+        *count = c;
+        *idx_count = ic;
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
     }
 }
 

@@ -298,6 +298,38 @@ def test_bf16_nan_and_inf_inputs():
             assert np.isnan(rf).any() and np.isinf(rf).any()
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_random_custom_plans(seed):
+    # random hazard-free plans with copy chains (the same generator as the
+    # host-side rewrite test), every executor mode, bit-exact vs the oracle
+    from test_exec_rewrites_host import _random_plan
+    from oracle.plans import Plan as OPlan, Step as OStep
+    rng = np.random.default_rng(9000 + seed)
+    n = int(rng.integers(2, 7))
+    N = int(rng.integers(8, 4000))
+    phases = _random_plan(rng, n, N)
+    flat = [(q, op, d, s, b, e) for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref_plan = OPlan("custom", n, N, [[OStep(*st) for st in ph] for ph in phases])
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", seed)
+    ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
+    say("case: random custom plan seed=%d n=%d N=%d %s phases=%d" % (seed, n, N, dtype, len(phases)))
+    for fuse, sl in MODES:
+        for pad in (0, 1):
+            ts = to_device(xs0, dtype, pad)
+            h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+            try:
+                arplan.ar_plan_set_option(h, arplan.AR_OPT_FUSE, fuse)
+                arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, sl)
+                arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+                torch.cuda.synchronize()
+            finally:
+                arplan.ar_plan_destroy(h)
+            got = to_host(ts, dtype)
+            for q in range(n):
+                assert np.array_equal(got[q], ref[q]), (seed, fuse, sl, pad, q)
+
+
 def test_custom_plan_mixed_sources_and_uneven_steps():
     # one phase with a 3-way reduce over a long range and 2-way reduces over
     # tiny ranges (explicit tile table), then copies of uneven lengths
