@@ -3,10 +3,12 @@
 //
 // Per phase, the steps are grouped by source count k (copies are k = 1) and
 // each group becomes one launch of phase_kernel<dtype, k, aligned>; the
-// built-in plans have one group per phase.  The step tables are uploaded to
-// the device on the first execute on a device; the n buffer pointers go
-// through a small per-plan cache of device pointer tables, so repeated
-// executes on the same buffers launch kernels only.
+// built-in plans have one group per phase.  Kernels read each step as a
+// record holding its range and its resolved buffer pointers (StepHead);
+// the records of a buffer set are built on the host and uploaded once, and a
+// small per-plan cache keeps them per device, so repeated executes on the
+// same buffers launch kernels only.  The sliced-launch tables are uploaded
+// on the first execute on a device.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -26,7 +28,7 @@ namespace arp {
 
 namespace {
 
-constexpr int kCache = 4;               // pointer tables kept per device
+constexpr int kCache = 4;               // buffer sets whose step records are kept per device
 constexpr int64_t kMinUnits = 2048;     // shrink tiles until a launch has this many
 constexpr int64_t kMaxBlocks = int64_t(1) << 24;
 // Cache policy per launch (measured on MI355X).  Launches moving less than
@@ -77,7 +79,7 @@ struct LaunchDesc {
     int32_t phase;
     int32_t xphase;          // executed phase
     int32_t kern_k;          // template K (0 = runtime source count)
-    int64_t first;           // first entry of the device step table
+    int64_t first;           // first entry of the step table (hsteps)
     int64_t count;           // steps in this launch
     int64_t tile_elems;
     int64_t tiles_per_step;  // arithmetic mapping
@@ -87,12 +89,15 @@ struct LaunchDesc {
     int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
     int32_t max_dst;         // most destinations of a step
     int64_t bytes;           // (k + destinations) * len * e over the steps
+    int64_t rec_off;         // first word of its steps' records
+    int64_t rec_stride;      // words per record
 };
 
+// The step records of one buffer set on one device.
 struct PtrEntry {
     std::vector<void*> key;
-    void** dev = nullptr;
-    void** pinned = nullptr;
+    uint64_t* dev = nullptr;     // records, device
+    uint64_t* pinned = nullptr;  // staging for their upload
     hipEvent_t done = nullptr;
     uint64_t stamp = 0;
     bool valid = false;
@@ -101,8 +106,6 @@ struct PtrEntry {
 
 struct DevState {
     int device = -1;
-    DevStep* steps = nullptr;
-    int32_t* idx = nullptr;  // source and destination indices of the steps
     int2* tiles = nullptr;
     int64_t* cuts = nullptr;     // sliced launch tables, all slices concatenated
     int32_t* sched_off = nullptr;
@@ -142,8 +145,8 @@ struct XPhase {
 
 // A sliced launch runs executed phases [p0, p0 + nphases): segments are the
 // element ranges between consecutive boundaries of those phases' steps;
-// sched lists, per (phase of the slice, segment), the device steps covering
-// that segment; tiles maps each wavefront to (segment, tile within the
+// sched lists, per (phase of the slice, segment), the word offsets of the
+// records of the steps covering that segment; tiles maps each wavefront to (segment, tile within the
 // segment), over the segments some step of the slice covers.
 struct SliceDesc {
     bool ok = false;
@@ -173,6 +176,8 @@ struct ExecState {
     std::vector<int32_t> hidx;   // source and destination indices
     std::vector<int2> htiles;
     std::vector<std::vector<int32_t>> dev_of;  // [phase][step] -> hsteps index
+    std::vector<int64_t> rec_of; // hsteps index -> first word of its record
+    int64_t rec_words = 0;       // words of all records
     std::vector<SliceDesc> slices;
     std::vector<Stage> stages;   // the launches for 16-byte aligned buffers
     std::vector<DevState*> dev;  // indexed by device ordinal
@@ -446,6 +451,12 @@ static void build_launches(const Plan& p, ExecState& ex) {
             }
             L.bytes = bytes;
             L.max_dst = maxdst;
+            L.rec_stride = (kRecHead + k + maxdst + 1) & ~int64_t(1);
+            L.rec_off = ex.rec_words;
+            ex.rec_of.resize(ex.hsteps.size(), -1);
+            for (int64_t j = 0; j < L.count; ++j)
+                ex.rec_of[size_t(L.first + j)] = L.rec_off + j * L.rec_stride;
+            ex.rec_words += L.count * L.rec_stride;
             if (maxspan == 0) {  // nothing to move in this group
                 g0 = g1;
                 continue;
@@ -531,12 +542,13 @@ static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int
             const XStep& x = xp.steps[i];
             if (x.end <= x.begin) continue;
             const int32_t di = ex.dev_of[size_t(q)][i];
-            if (di < 0) {
-                sd.why = "step without a device descriptor";
+            if (di < 0 || ex.rec_of[size_t(di)] < 0 || ex.rec_of[size_t(di)] > INT32_MAX) {
+                sd.why = "step without a record";
                 return sd;
             }
             for (int32_t sg = seg_of(x.begin); sg < seg_of(x.end); ++sg) {
-                lists[size_t(q - p0) * size_t(sd.nseg) + size_t(sg)].push_back(di);
+                lists[size_t(q - p0) * size_t(sd.nseg) + size_t(sg)].push_back(
+                    int32_t(ex.rec_of[size_t(di)]));
                 used[size_t(sg)] = 1;
             }
             sd.bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * (x.end - x.begin) * p.esize;
@@ -716,8 +728,6 @@ static void free_dev(DevState* d) {
     int cur = -1;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(d->device);
-    if (d->steps) (void)hipFree(d->steps);
-    if (d->idx) (void)hipFree(d->idx);
     if (d->tiles) (void)hipFree(d->tiles);
     if (d->cuts) (void)hipFree(d->cuts);
     if (d->sched_off) (void)hipFree(d->sched_off);
@@ -766,9 +776,7 @@ static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
     if (!ex.dev[size_t(dev)]) {
         DevState* d = new DevState();
         d->device = dev;
-        ar_status s = upload(&d->steps, ex.hsteps, "step table");
-        if (s == AR_OK) s = upload(&d->idx, ex.hidx, "index table");
-        if (s == AR_OK) s = upload(&d->tiles, ex.htiles, "tile table");
+        ar_status s = upload(&d->tiles, ex.htiles, "tile table");
         if (s == AR_OK && !ex.slices.empty()) {
             std::vector<int64_t> cuts;
             std::vector<int32_t> soff, sched;
@@ -814,9 +822,11 @@ static ar_status check_buffers(const Plan& p, const std::vector<void*>& bufs) {
     return AR_OK;
 }
 
-static ar_status pointer_table(const Plan& p, DevState& d,
-                               const std::vector<void*>& bufs,
-                               hipStream_t stream, PtrEntry** out) {
+// The step records for buffer set `bufs` on this device (see StepHead):
+// from the per-plan cache, or built on the host and uploaded on `stream`.
+static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
+                              const std::vector<void*>& bufs,
+                              hipStream_t stream, PtrEntry** out) {
     ++d.clock;
     for (PtrEntry& e : d.cache)
         if (e.valid && e.key == bufs) {
@@ -831,18 +841,20 @@ static ar_status pointer_table(const Plan& p, DevState& d,
         if (!e.valid) { v = &e; break; }
         if (e.stamp < v->stamp) v = &e;
     }
-    const size_t nb = bufs.size() * sizeof(void*);
+    const size_t nb = size_t(std::max<int64_t>(ex.rec_words, 1)) * sizeof(uint64_t);
     hipError_t e = hipSuccess;
     if (!v->dev) {
         e = hipMalloc(reinterpret_cast<void**>(&v->dev), nb);
         if (e != hipSuccess) {
             v->dev = nullptr;
-            return fail(AR_ERR_OOM, hip_msg("pointer table", e));
+            (void)hipGetLastError();
+            return fail(e == hipErrorOutOfMemory ? AR_ERR_OOM : AR_ERR_HIP, hip_msg("step records", e));
         }
         e = hipHostMalloc(reinterpret_cast<void**>(&v->pinned), nb, hipHostMallocDefault);
         if (e != hipSuccess) {
             v->pinned = nullptr;
-            return fail(AR_ERR_OOM, hip_msg("pointer staging", e));
+            (void)hipGetLastError();
+            return fail(AR_ERR_OOM, hip_msg("step record staging", e));
         }
         e = hipEventCreateWithFlags(&v->done, hipEventDisableTiming);
         if (e != hipSuccess) {
@@ -855,9 +867,21 @@ static ar_status pointer_table(const Plan& p, DevState& d,
         if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventSynchronize", e));
     }
     v->valid = false;
-    std::memcpy(v->pinned, bufs.data(), nb);
+    uint64_t* w = v->pinned;
+    std::memset(w, 0, nb);
+    for (size_t i = 0; i < ex.hsteps.size(); ++i) {
+        const DevStep& st = ex.hsteps[i];
+        uint64_t* r = w + ex.rec_of[i];
+        StepHead h{st.begin, st.end, st.k, st.ndst, 0};
+        std::memcpy(r, &h, sizeof(h));
+        for (int32_t j = 0; j < st.k; ++j)
+            r[kRecHead + j] = reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.src_off + j)])]);
+        for (int32_t j = 0; j < st.ndst; ++j)
+            r[kRecHead + st.k + j] =
+                reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.dst_off + j)])]);
+    }
     e = hipMemcpyAsync(v->dev, v->pinned, nb, hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("pointer upload", e));
+    if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("step record upload", e));
     e = hipEventRecord(v->done, stream);
     if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventRecord", e));
     v->key = bufs;
@@ -872,12 +896,12 @@ static ar_status pointer_table(const Plan& p, DevState& d,
 
 template <int DT, int K>
 static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
-                      const DevStep* steps, const int32_t* srcs, void* const* ptrs,
-                      const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
+                      const uint64_t* recs, int64_t stride, const int2* tiles,
+                      int64_t nunits, int64_t tps, int64_t te) {
     const dim3 grid(static_cast<uint32_t>(blocks)), block(64 * kcfg(K).WPB);
-#define AR_LAUNCH(V, C)                                                              \
-    hipLaunchKernelGGL((phase_kernel<DT, K, V, C>), grid, block, 0, st, steps, srcs, \
-                       ptrs, tiles, nunits, tps, te)
+#define AR_LAUNCH(V, C)                                                                \
+    hipLaunchKernelGGL((phase_kernel<DT, K, V, C>), grid, block, 0, st, recs, stride, \
+                       tiles, nunits, tps, te)
     if (!vecok) AR_LAUNCH(false, 0);
     else if (cm == 0) AR_LAUNCH(true, 0);
     else if (cm == 1) AR_LAUNCH(true, 1);
@@ -888,16 +912,16 @@ static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
 
 template <int DT>
 static void launch_d(int K, bool vecok, int cm, int64_t blocks, hipStream_t st,
-                     const DevStep* steps, const int32_t* srcs, void* const* ptrs,
-                     const int2* tiles, int64_t nunits, int64_t tps, int64_t te) {
+                     const uint64_t* recs, int64_t stride, const int2* tiles,
+                     int64_t nunits, int64_t tps, int64_t te) {
     switch (K) {
-        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
-        default: launch_dk<DT, 0>(vecok, cm, blocks, st, steps, srcs, ptrs, tiles, nunits, tps, te); break;
+        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
     }
 }
 
@@ -922,7 +946,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
         ar_status s = device_state(*plan, *ex, &d);
         if (s != AR_OK) return s;
         PtrEntry* pe = nullptr;
-        s = pointer_table(*plan, *d, bufs, stream, &pe);
+        s = step_records(*plan, *ex, *d, bufs, stream, &pe);
         if (s != AR_OK) return s;
         // sliced launches need 16-byte aligned buffers; otherwise every
         // phase runs as its phase launches
@@ -953,8 +977,8 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                 const dim3 grid(static_cast<uint32_t>((sd.nunits + kSliceWPB - 1) / kSliceWPB));
                 const dim3 block(64 * kSliceWPB);
 #define AR_SLICED(DT)                                                                   \
-    hipLaunchKernelGGL((sliced_kernel<DT>), grid, block, 0, stream, d->steps, d->idx,   \
-                       pe->dev, d->sched_off + sd.soff_base, d->sched + sd.sched_base,  \
+    hipLaunchKernelGGL((sliced_kernel<DT>), grid, block, 0, stream, pe->dev,             \
+                       d->sched_off + sd.soff_base, d->sched + sd.sched_base,           \
                        d->cuts + sd.cuts_base, d->stiles + sd.tiles_base, sd.nunits,    \
                        sd.nphases, sd.nseg, sd.tile_elems)
                 switch (plan->dtype) {
@@ -966,20 +990,23 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             } else {
                 const LaunchDesc& L = ex->launches[size_t(stg.launch)];
                 const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
-                const DevStep* steps = d->steps + L.first;
+                const uint64_t* recs = pe->dev + L.rec_off;
                 const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
                 switch (plan->dtype) {
                     case AR_F32:
-                        launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
-                                         pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                        launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, recs,
+                                         L.rec_stride, tiles, L.nunits, L.tiles_per_step,
+                                         L.tile_elems);
                         break;
                     case AR_I32:
-                        launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
-                                         pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                        launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, recs,
+                                         L.rec_stride, tiles, L.nunits, L.tiles_per_step,
+                                         L.tile_elems);
                         break;
                     default:
-                        launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, steps, d->idx,
-                                          pe->dev, tiles, L.nunits, L.tiles_per_step, L.tile_elems);
+                        launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, recs,
+                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
+                                          L.tile_elems);
                         break;
                 }
             }
@@ -1149,6 +1176,30 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 cover[size_t(L.first + s)].push_back({sp.lo, sp.hi});
             }
         }
+        // step records: inside the record area, disjoint, long enough for
+        // the step's pointers, at the launch's stride
+        {
+            if (ex->rec_of.size() != ex->hsteps.size()) return bad("a step without a record");
+            std::vector<std::pair<int64_t, int64_t>> iv;
+            for (size_t i = 0; i < ex->hsteps.size(); ++i) {
+                const DevStep& st = ex->hsteps[i];
+                const int64_t o = ex->rec_of[i];
+                if (o < 0 || o + kRecHead + st.k + st.ndst > ex->rec_words)
+                    return bad("step record outside the record area");
+                iv.push_back({o, o + kRecHead + st.k + st.ndst});
+            }
+            std::sort(iv.begin(), iv.end());
+            for (size_t i = 1; i < iv.size(); ++i)
+                if (iv[i].first < iv[i - 1].second) return bad("step records overlap");
+            for (const LaunchDesc& L : ex->launches)
+                for (int64_t j = 0; j < L.count; ++j) {
+                    const DevStep& st = ex->hsteps[size_t(L.first + j)];
+                    if (ex->rec_of[size_t(L.first + j)] != L.rec_off + j * L.rec_stride)
+                        return bad("record not at the launch's stride");
+                    if (L.rec_stride < kRecHead + st.k + st.ndst || L.rec_off % 2 || L.rec_stride % 2)
+                        return bad("record stride too short or misaligned");
+                }
+        }
         for (size_t i = 0; i < ex->hsteps.size(); ++i) {
             const DevStep& st = ex->hsteps[i];
             auto& c = cover[i];
@@ -1236,7 +1287,8 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                         const XStep& x = xp.steps[i];
                         if (x.end <= x.begin) continue;
                         if (x.begin <= sd.cuts[size_t(sg)] && sd.cuts[size_t(sg) + 1] <= x.end)
-                            want.push_back(ex->dev_of[size_t(sd.p0 + q)][i]);
+                            want.push_back(int32_t(
+                                ex->rec_of[size_t(ex->dev_of[size_t(sd.p0 + q)][i])]));
                         else if (x.begin < sd.cuts[size_t(sg) + 1] && sd.cuts[size_t(sg)] < x.end)
                             return bad("a step cuts a segment");
                     }

@@ -15,8 +15,9 @@
 // wrap-around) and stores U vectors.  Loads are nontemporal unless the launch
 // reads some range more than once, stores unless the launch's output is small
 // enough to stay cached for the next phase.  Unaligned head and tail elements of a
-// step are done element-wise.  The step descriptor, its source indices and
-// the buffer pointers are wave-uniform and live in scalar registers.
+// step are done element-wise.  A wave reads its step as one record with the
+// buffer pointers already resolved (see StepRec): wave-uniform, in scalar
+// registers after a single dependent load.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -27,15 +28,29 @@ namespace arp {
 enum DType : int32_t { DT_F32 = 0, DT_I32 = 1, DT_BF16 = 2 };
 
 // One executed step: fold the k sources over [begin, end) and store the
-// result into each of the ndst destinations.  32 bytes, grouped by launch.
+// result into each of the ndst destinations.  Host form, 32 bytes; the
+// indices point into the plan's index pool.
 struct DevStep {
     int64_t begin;
     int64_t end;
-    int32_t src_off;  // first source index in the device index pool
+    int32_t src_off;  // first source index in the index pool
     int32_t k;        // number of sources
     int32_t dst_off;  // first destination index in the same pool
     int32_t ndst;     // number of destinations
 };
+
+// The record a kernel reads for a step, built per buffer set: this header
+// (4 words) followed by k source and ndst destination buffer pointers, one
+// 8-byte word each.  Records of one launch have a common stride, so a wave
+// finds its step's pointers with one dependent load.
+struct StepHead {
+    int64_t begin;
+    int64_t end;
+    int32_t k;
+    int32_t ndst;
+    int64_t pad;
+};
+constexpr int kRecHead = 4;  // header words
 
 // Per source count K (K = 0: source count read at run time):
 //   U   16-byte vectors in flight per lane and source,
@@ -221,19 +236,19 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
     return int64_t((uint64_t(hi) << 32) | lo);
 }
 
-// Fold elements [lo, hi) of `nsrc` sources into dst, one element per lane
-// per pass (used for unaligned heads/tails and for unaligned buffers).
+// Fold elements [lo, hi) of the k sources sp[] into the destinations dp[],
+// one element per lane per pass (used for unaligned heads/tails and for
+// unaligned buffers).
 template <int DT, int K>
-__device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
-                                            const int32_t* __restrict__ srcl, int k,
-                                            const int32_t* __restrict__ dstl, int ndst,
+__device__ __forceinline__ void fold_scalar(void* const* __restrict__ sp, int k,
+                                            void* const* __restrict__ dp, int ndst,
                                             int64_t lo, int64_t hi, int lane) {
     using T = typename Elem<DT>::T;
     if (K == 1 || (K == 0 && k == 1)) {  // copy: move the bits unchanged
-        const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[0]]);
+        const AR_GLOBAL T* s = as_global<T>(sp[0]);
         for (int64_t e = lo + lane; e < hi; e += 64) {
             const T v = s[e];
-            for (int j = 0; j < ndst; ++j) as_global<T>(ptrs[dstl[j]])[e] = v;
+            for (int j = 0; j < ndst; ++j) as_global<T>(dp[j])[e] = v;
         }
         return;
     }
@@ -244,20 +259,20 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
 #pragma unroll
         for (int u = 0; u < SU; ++u) ok[u] = e0 + u * 64 + lane < hi;
         {
-            const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[0]]);
+            const AR_GLOBAL T* s = as_global<T>(sp[0]);
 #pragma unroll
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) acc[u].init(s[e0 + u * 64 + lane]);
         }
         const int kk = K ? K : k;
         for (int t = 1; t < kk; ++t) {
-            const AR_GLOBAL T* s = as_global<T>(ptrs[srcl[t]]);
+            const AR_GLOBAL T* s = as_global<T>(sp[t]);
 #pragma unroll
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) acc[u].add(s[e0 + u * 64 + lane]);
         }
         for (int j = 0; j < ndst; ++j) {
-            AR_GLOBAL T* d = as_global<T>(ptrs[dstl[j]]);
+            AR_GLOBAL T* d = as_global<T>(dp[j]);
 #pragma unroll
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) d[e0 + u * 64 + lane] = acc[u].out();
@@ -265,16 +280,59 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ ptrs,
     }
 }
 
+// Destination pointers of a step, two ways.  Dsts holds the first kRegDst
+// in registers for a whole tile (read once: re-reading them from the record
+// after every store would cost a dependent load per iteration, since the
+// compiler cannot tell the stores from the record) and reads the rest from
+// the record; the phase kernel, which loops over a tile, uses it.  DstMem
+// reads them from the record at the store; the sliced kernel, which stores
+// each step once, uses it.
+constexpr int kRegDst = 8;
+struct Dsts {
+    void* r[kRegDst];
+    void* const* more;  // destinations kRegDst.. (in the record)
+    int n;
+};
+struct DstMem {
+    void* const* p;
+    int n;
+};
+__device__ __forceinline__ Dsts load_dsts(void* const* __restrict__ dp, int ndst) {
+    Dsts d;
+#pragma unroll
+    for (int j = 0; j < kRegDst; ++j) d.r[j] = j < ndst ? dp[j] : nullptr;
+    d.more = dp + kRegDst;
+    d.n = ndst;
+    return d;
+}
+
 // Store U vectors per lane (vector offset `at` + u * 64 + lane) into each
 // destination; every load of these positions happened before, so a
 // destination may also be one of the sources.
 template <int U, int CM, bool FULL>
-__device__ __forceinline__ void store_all(void* const* __restrict__ ptrs,
-                                          const int32_t* __restrict__ dstl, int ndst,
-                                          int64_t v0, const u32x4 (&out)[U], const bool (&ok)[U],
-                                          int64_t at, int lane) {
-    for (int j = 0; j < ndst; ++j) {
-        gvec* d = as_global<u32x4>(ptrs[dstl[j]]) + v0 + at + lane;
+__device__ __forceinline__ void store_all(const Dsts& dst, int64_t v0, const u32x4 (&out)[U],
+                                          const bool (&ok)[U], int64_t at, int lane) {
+#pragma unroll
+    for (int j = 0; j < kRegDst; ++j) {
+        if (j < dst.n) {
+            gvec* d = as_global<u32x4>(dst.r[j]) + v0 + at + lane;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (FULL || ok[u]) vstore<(CM & 2) != 0>(d + u * 64, out[u]);
+        }
+    }
+    for (int j = kRegDst; j < dst.n; ++j) {
+        gvec* d = as_global<u32x4>(dst.more[j - kRegDst]) + v0 + at + lane;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (FULL || ok[u]) vstore<(CM & 2) != 0>(d + u * 64, out[u]);
+    }
+}
+template <int U, int CM, bool FULL>
+__device__ __forceinline__ void store_all(const DstMem& dst, int64_t v0, const u32x4 (&out)[U],
+                                          const bool (&ok)[U], int64_t at, int lane) {
+    for (int j = 0; j < dst.n; ++j) {
+        gvec* d = as_global<u32x4>(dst.p[j]) + v0 + at + lane;
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (FULL || ok[u]) vstore<(CM & 2) != 0>(d + u * 64, out[u]);
@@ -286,9 +344,8 @@ __device__ __forceinline__ void store_all(void* const* __restrict__ ptrs,
 // vectors are in range, so the loads are issued back to back with no
 // per-vector branch.  Cache mode CM of a launch: bit 0 = nontemporal loads,
 // bit 1 = nontemporal stores.
-template <int DT, int K, int U, int CM, bool FULL>
-__device__ __forceinline__ void fold_vectors(const gvec* const* sp, void* const* __restrict__ ptrs,
-                                             const int32_t* __restrict__ dstl, int ndst,
+template <int DT, int K, int U, int CM, bool FULL, class D>
+__device__ __forceinline__ void fold_vectors(const gvec* const* sp, const D& dst,
                                              int64_t v0, int64_t at, int64_t nv, int lane) {
     bool ok[U];
 #pragma unroll
@@ -313,28 +370,27 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, void* const*
             out[u] = acc.out();
         }
     }
-    store_all<U, CM, FULL>(ptrs, dstl, ndst, v0, out, ok, at, lane);
+    store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
 }
 
 // Runtime source count: one source at a time, U vectors in flight.
-template <int DT, int U, int CM, bool FULL>
-__device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
-                                                const int32_t* __restrict__ srcl, int k,
-                                                const int32_t* __restrict__ dstl, int ndst,
-                                                int64_t v0, int64_t at, int64_t nv, int lane) {
+template <int DT, int U, int CM, bool FULL, class D>
+__device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, int k,
+                                                const D& dst, int64_t v0, int64_t at,
+                                                int64_t nv, int lane) {
     bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
     u32x4 out[U];
     if (k == 1) {
-        const gvec* s0 = as_global<u32x4>(ptrs[srcl[0]]) + v0;
+        const gvec* s0 = as_global<u32x4>(srcp[0]) + v0;
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (ok[u]) out[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
     } else {
         VAcc<DT> acc[U];
         {
-            const gvec* s0 = as_global<u32x4>(ptrs[srcl[0]]) + v0;
+            const gvec* s0 = as_global<u32x4>(srcp[0]) + v0;
             u32x4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
@@ -343,7 +399,7 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
             for (int u = 0; u < U; ++u) acc[u].init(x[u]);
         }
         for (int j = 1; j < k; ++j) {
-            const gvec* sj = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+            const gvec* sj = as_global<u32x4>(srcp[j]) + v0;
             u32x4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
@@ -354,16 +410,16 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ ptrs,
 #pragma unroll
         for (int u = 0; u < U; ++u) out[u] = acc[u].out();
     }
-    store_all<U, CM, FULL>(ptrs, dstl, ndst, v0, out, ok, at, lane);
+    store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
 }
 
-// One launch: `nunits` wave tiles over the steps steps[0..).  K = 0 means
-// the source count is read from each step (any k >= 1).  VECOK: every
-// buffer is 16-byte aligned.  CM: cache mode of the vector loads and stores.
+// One launch: `nunits` wave tiles over the steps whose records start at
+// `recs`, `stride` words apart.  K = 0 means the source count is read from
+// each step (any k >= 1).  VECOK: every buffer is 16-byte aligned.  CM:
+// cache mode of the vector loads and stores.
 template <int DT, int K, bool VECOK, int CM>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
-    const DevStep* __restrict__ steps, const int32_t* __restrict__ srcs,
-    void* const* __restrict__ ptrs, const int2* __restrict__ tiles,
+    const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
     int64_t nunits, int64_t tiles_per_step, int64_t tile_elems) {
     constexpr int VEC = Elem<DT>::VEC;
     constexpr int U = kcfg(K).U;
@@ -376,33 +432,35 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     unit_tile(unit, tiles, tiles_per_step, s, t);
     s = uniform64(s);
     t = uniform64(t);
-    const DevStep st = steps[s];
+    const uint64_t* rec = recs + s * stride;
+    const StepHead st = *reinterpret_cast<const StepHead*>(rec);
     const int k = K ? K : st.k;
-    const int32_t* srcl = srcs + st.src_off;
-    const int32_t* dstl = srcs + st.dst_off;
+    void* const* sp = reinterpret_cast<void* const*>(rec + kRecHead);
+    void* const* dp = sp + k;
     const int ndst = st.ndst;
 
-    const TileSpan sp = tile_span(st.begin, st.end, t, tile_elems, VEC, VECOK);
-    if (sp.lo >= sp.hi) return;
-    if (sp.vlo > sp.lo) fold_scalar<DT, K>(ptrs, srcl, k, dstl, ndst, sp.lo, sp.vlo, lane);
-    if (sp.hi > sp.vhi) fold_scalar<DT, K>(ptrs, srcl, k, dstl, ndst, sp.vhi, sp.hi, lane);
-    if (!VECOK || sp.vhi <= sp.vlo) return;
+    const TileSpan ts = tile_span(st.begin, st.end, t, tile_elems, VEC, VECOK);
+    if (ts.lo >= ts.hi) return;
+    if (ts.vlo > ts.lo) fold_scalar<DT, K>(sp, k, dp, ndst, ts.lo, ts.vlo, lane);
+    if (ts.hi > ts.vhi) fold_scalar<DT, K>(sp, k, dp, ndst, ts.vhi, ts.hi, lane);
+    if (!VECOK || ts.vhi <= ts.vlo) return;
 
-    const int64_t v0 = sp.vlo / VEC;
-    const int64_t nv = (sp.vhi - sp.vlo) / VEC;
+    const int64_t v0 = ts.vlo / VEC;
+    const int64_t nv = (ts.vhi - ts.vlo) / VEC;
+    const Dsts dst = load_dsts(dp, ndst);
     int64_t at = 0;
     if constexpr (K > 0) {
         const gvec* sv[K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+        for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(sp[j]) + v0;
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors<DT, K, U, CM, true>(sv, ptrs, dstl, ndst, v0, at, nv, lane);
-        if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, ptrs, dstl, ndst, v0, at, nv, lane);
+            fold_vectors<DT, K, U, CM, true>(sv, dst, v0, at, nv, lane);
+        if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, dst, v0, at, nv, lane);
     } else {
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors_rt<DT, U, CM, true>(ptrs, srcl, k, dstl, ndst, v0, at, nv, lane);
+            fold_vectors_rt<DT, U, CM, true>(sp, k, dst, v0, at, nv, lane);
         if (at < nv)
-            fold_vectors_rt<DT, U, CM, false>(ptrs, srcl, k, dstl, ndst, v0, at, nv, lane);
+            fold_vectors_rt<DT, U, CM, false>(sp, k, dst, v0, at, nv, lane);
     }
 }
 
@@ -423,23 +481,24 @@ constexpr int kSliceU = 4;    // vectors per lane in a tile
 constexpr int kSliceWPB = 4;  // wavefronts per block
 
 template <int DT, int K>
-__device__ __forceinline__ void slice_fold(void* const* __restrict__ ptrs,
-                                           const int32_t* __restrict__ srcl,
-                                           const int32_t* __restrict__ dstl, int ndst,
+__device__ __forceinline__ void slice_fold(void* const* __restrict__ sp,
+                                           void* const* __restrict__ dp, int ndst,
                                            int64_t v0, int64_t nv, int lane) {
     const gvec* sv[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(ptrs[srcl[j]]) + v0;
+    for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(sp[j]) + v0;
+    const DstMem dst{dp, ndst};
     if (nv == 64 * kSliceU)
-        fold_vectors<DT, K, kSliceU, 0, true>(sv, ptrs, dstl, ndst, v0, 0, nv, lane);
+        fold_vectors<DT, K, kSliceU, 0, true>(sv, dst, v0, 0, nv, lane);
     else
-        fold_vectors<DT, K, kSliceU, 0, false>(sv, ptrs, dstl, ndst, v0, 0, nv, lane);
+        fold_vectors<DT, K, kSliceU, 0, false>(sv, dst, v0, 0, nv, lane);
 }
 
+// sched lists, per (phase of the slice, segment), the word offsets in
+// `recs` of the records of the steps covering the segment.
 template <int DT>
 __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
-    const DevStep* __restrict__ steps, const int32_t* __restrict__ idx,
-    void* const* __restrict__ ptrs, const int32_t* __restrict__ sched_off,
+    const uint64_t* __restrict__ recs, const int32_t* __restrict__ sched_off,
     const int32_t* __restrict__ sched, const int64_t* __restrict__ cuts,
     const int2* __restrict__ tiles, int64_t nunits, int32_t nphases, int32_t nseg,
     int64_t tile_elems) {
@@ -459,22 +518,21 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
         const int32_t a = sched_off[int64_t(p) * nseg + seg];
         const int32_t b = sched_off[int64_t(p) * nseg + seg + 1];
         for (int32_t i = a; i < b; ++i) {
-            const DevStep st = steps[sched[i]];
-            const int32_t* srcl = idx + st.src_off;
-            const int32_t* dstl = idx + st.dst_off;
+            const uint64_t* rec = recs + sched[i];
+            const StepHead st = *reinterpret_cast<const StepHead*>(rec);
+            void* const* sp = reinterpret_cast<void* const*>(rec + kRecHead);
+            void* const* dp = sp + st.k;
             switch (st.k) {
-                case 1: slice_fold<DT, 1>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
-                case 2: slice_fold<DT, 2>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
-                case 4: slice_fold<DT, 4>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
-                case 8: slice_fold<DT, 8>(ptrs, srcl, dstl, st.ndst, v0, nv, lane); break;
+                case 1: slice_fold<DT, 1>(sp, dp, st.ndst, v0, nv, lane); break;
+                case 2: slice_fold<DT, 2>(sp, dp, st.ndst, v0, nv, lane); break;
+                case 4: slice_fold<DT, 4>(sp, dp, st.ndst, v0, nv, lane); break;
+                case 8: slice_fold<DT, 8>(sp, dp, st.ndst, v0, nv, lane); break;
                 default: {
-                    int64_t at = 0;
+                    const DstMem dst{dp, st.ndst};
                     if (nv == 64 * kSliceU)
-                        fold_vectors_rt<DT, kSliceU, 0, true>(ptrs, srcl, st.k, dstl, st.ndst,
-                                                              v0, at, nv, lane);
+                        fold_vectors_rt<DT, kSliceU, 0, true>(sp, st.k, dst, v0, 0, nv, lane);
                     else
-                        fold_vectors_rt<DT, kSliceU, 0, false>(ptrs, srcl, st.k, dstl, st.ndst,
-                                                               v0, at, nv, lane);
+                        fold_vectors_rt<DT, kSliceU, 0, false>(sp, st.k, dst, v0, 0, nv, lane);
                 }
             }
         }
