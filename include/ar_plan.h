@@ -192,10 +192,15 @@ ar_status ar_plan_destroy(ar_plan* plan);
  * the result of running the steps phase by phase as listed.  The
  * pointer array is read during the call only.  Any pointer alignment works;
  * 16-byte-aligned buffers take the vector path.  The first call on a device
- * uploads the plan's step tables (device memory owned by the plan).
- * Executions of one plan must be ordered (one stream, or synchronised): the
- * plan keeps one device copy of recently used pointer tables.  Distinct plans
- * are independent.  Errors: AR_ERR_INVALID_ARG, AR_ERR_OOM, AR_ERR_HIP. */
+ * uploads the plan's tile tables; the first call with a new buffer set
+ * builds that set's step records (each executed step's range and resolved
+ * buffer pointers, (4 + k + d) * 8 bytes rounded up to 16 for a step with
+ * k sources and d destinations) on the host and uploads them; the plan keeps
+ * the records of its 4 most recently used buffer sets per device (device and
+ * pinned host memory owned by the plan), so repeated executes on the same
+ * buffers only launch kernels.  Executions of one plan must be ordered (one
+ * stream, or synchronised).  Distinct plans are independent.  Errors:
+ * AR_ERR_INVALID_ARG, AR_ERR_OOM, AR_ERR_HIP. */
 ar_status ar_plan_execute(ar_plan* plan, void* const* bufs, void* stream);
 
 /* Same, with buffer p at (char*)base + p * stride_bytes; stride_bytes must
