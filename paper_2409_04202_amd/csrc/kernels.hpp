@@ -465,18 +465,19 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
 }
 
 // ------------------------------------------------------------------------
-// Whole-plan kernel for plans whose launches are too short to fill the chip.
+// Sliced kernel: one launch for a run of consecutive phases whose launches
+// would be too short to fill the chip.
 //
 // Every step is element-wise and the steps of a phase are independent, so
 // the value at an element position depends only on what earlier phases did
 // at that same position.  Here each wavefront owns a fixed tile of element
 // positions (inside one segment: the element ranges between consecutive
-// step boundaries) and carries it through all phases in order: in phase p it
-// runs, for its tile, every step of p that covers the segment, reading and
-// writing the buffers in memory exactly as the phase-by-phase execution
-// does.  A lane always handles the same positions, so it only ever reads
-// back what it wrote itself: no barrier between phases, one launch for the
-// whole plan.
+// step boundaries of the run) and carries it through the run's phases in
+// order: in phase p it runs, for its tile, every step of p that covers the
+// segment, reading and writing the buffers in memory exactly as the
+// phase-by-phase execution does.  A lane always handles the same positions,
+// so it only ever reads back what it wrote itself: no barrier between
+// phases, one launch for the run.
 constexpr int kSliceU = 4;    // vectors per lane in a tile
 constexpr int kSliceWPB = 4;  // wavefronts per block
 
