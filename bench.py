@@ -19,6 +19,11 @@ Prints one JSON line:
               destinations) over their mean duration (HIP events on the
               launch stream), against MI355X's 8 TB/s HBM peak
   cpu_baseline  the CPU oracle executing the same plan on the host
+and, beside the contract's fields: the step time's median and minimum over
+individually timed executions, the whole plan's and the copy launches'
+fractions of the peak, a practical ceiling measured in the same run (a plain
+device copy and a two-source fold through the library, 2 GiB each), and the
+oracle with the steps of each phase spread over a thread pool.
 """
 
 import argparse
@@ -57,6 +62,107 @@ def load_traffic(workload):
     return d.get("reduce_bytes_per_launch")
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def parallel_execute(plan, bufs, dtype, pool):
+    """oracle.execute with the steps of each phase on a thread pool (numpy's
+    ufuncs release the GIL): every step reads the phase's starting state,
+    the phase's writes are committed after all its steps."""
+    import numpy as np
+    import oracle
+
+    def one(st):
+        if st.op == "reduce":
+            return oracle.fold(dtype, [bufs[q][st.begin:st.end] for q in st.srcs])
+        return np.array(bufs[st.srcs[0]][st.begin:st.end], copy=True)
+
+    for phase in plan.phases:
+        vals = list(pool.map(one, phase))
+        for st, v in zip(phase, vals):
+            bufs[st.dst][st.begin:st.end] = v
+    return bufs
+
+
+def cpu_parallel(name, budget_s=10.0):
+    """The oracle's plan with the steps of each phase spread over a thread
+    pool (see parallel_execute)."""
+    from concurrent.futures import ThreadPoolExecutor
+    import oracle
+    from paper_2409_04202_amd import workloads
+    c = workloads.CONFIGS[name]
+    if c["kind"] == "gentree":
+        plan = oracle.gentree_plan(oracle.from_preorder(c["fanin"]), c["N"])
+    else:
+        plan = oracle.make_plan(c["kind"], c["n"], c["N"], c["fanin"])
+    xs = workloads.inputs(name)
+    dt = c["dtype"]
+    total = c["n"] * c["N"] * workloads.ESIZE[dt]
+    workers = os.cpu_count() or 1
+    runs, spent = 0, 0.0
+    with ThreadPoolExecutor(max_workers=workers) as pool:
+        while spent < budget_s * 0.5 and runs < 20:
+            bufs = [x.copy() for x in xs]
+            t0 = time.perf_counter()
+            parallel_execute(plan, bufs, dt, pool)
+            spent += time.perf_counter() - t0
+            runs += 1
+    return {"value": round(total * runs / spent / 1e9, 4), "unit": "GB/s",
+            "cores": workers, "cpu": cpu_model(), "kind": "oracle, phase steps on a thread pool",
+            "sample": "%d full executions" % runs, "seconds": round(spent, 3)}
+
+
+def ceiling(torch, arplan):
+    """Practical HBM ceiling in this run: a plain device copy (torch's copy
+    kernel) and a two-source fold through the library, 2 GiB of traffic per
+    repetition each (copy: 1 GiB read + 1 GiB written; fold: 2 x 683 MiB
+    read + 683 MiB written)."""
+    reps = 10
+    out = {}
+    a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")    # 1 GiB
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    for _ in range(2):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    out["copy_gbs"] = round(2 * a.numel() * 4 / (ms * 1e-3) / 1e9, 1)
+    del a, b
+    N = (2 << 30) // 12                     # 3 x N x 4 bytes = 2 GiB
+    N -= N % 64
+    xs = [torch.ones(N, dtype=torch.float32, device="cuda") for _ in range(3)]
+    h = arplan.ar_plan_create_custom(3, N, "f32", [(0, "reduce", 2, (0, 1), 0, N)])
+    try:
+        ptrs = arplan.pointers(xs)
+        sh = torch.cuda.current_stream().cuda_stream
+        for _ in range(2):
+            arplan.ar_plan_execute(h, ptrs, sh)
+        e0.record()
+        for _ in range(reps):
+            arplan.ar_plan_execute(h, ptrs, sh)
+        e1.record()
+        e1.synchronize()
+    finally:
+        arplan.ar_plan_destroy(h)
+    ms = e0.elapsed_time(e1) / reps
+    out["fold2_gbs"] = round(3 * N * 4 / (ms * 1e-3) / 1e9, 1)
+    del xs
+    return out
+
+
 def cpu_baseline(name, budget_s=25.0):
     """The oracle, as written, on the same workload (single thread)."""
     import numpy as np  # noqa: F401
@@ -81,6 +187,7 @@ def cpu_baseline(name, budget_s=25.0):
             "sample": "%d full executions of the %s plan (n=%d, N=%d %s), "
                       "numpy, one thread" % (runs, c["kind"], c["n"], c["N"],
                                              c["dtype"]),
+            "cpu": cpu_model(),
             "seconds": round(spent, 3)}
 
 
@@ -91,6 +198,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default=DEFAULT)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the copy / two-source fold ceiling measurement")
     ap.add_argument("--no-fuse", action="store_true",
                     help="run every plan step as listed (AR_OPT_FUSE = 0)")
     ap.add_argument("--slice", type=int, choices=(0, 1, 2), default=None,
@@ -160,6 +269,17 @@ def main():
     torch.cuda.synchronize()
     recs = arplan.ar_timer_read(timer, cap)
     arplan.ar_timer_destroy(timer)
+    # step time distribution: each execution between two events
+    restore()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(K)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record(stream)
+        plan.execute(ptrs, sh)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
 
     ms_step = (t1 - t0) * 1e3 / K
     total = n * N * esize
@@ -172,6 +292,9 @@ def main():
     red = [i for i, L in enumerate(launches) if L[1] >= 2]
     red_ms = sum(l_ms[i] for i in red)
     red_bytes = sum(launches[i][4] for i in red)
+    cpy = [i for i, L in enumerate(launches) if L[1] == 1]
+    cpy_ms = sum(l_ms[i] for i in cpy)
+    cpy_bytes = sum(launches[i][4] for i in cpy)
     achieved = red_bytes / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
     traffic = load_traffic(name) if not args.no_fuse and args.slice is None else None
     roofline = {"bound": "hbm", "achieved": round(achieved, 1),
@@ -209,6 +332,11 @@ def main():
         "kernel_bytes_per_step": sum(L[4] for L in launches),
         "kernel_gbs": round(sum(L[4] for L in launches) / (ms_step * 1e-3) / 1e9, 1),
         "kernel_ms_per_step": round(sum(l_ms), 5),
+        "step_ms": {"median": round(step_ms[len(step_ms) // 2], 5),
+                    "min": round(step_ms[0], 5)},
+        "plan_frac": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "copy_frac": (round(cpy_bytes / (cpy_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+                      if cpy_ms > 0 else None),
         "launches": [{"phase": L[0], "k": L[1], "max_dst": L[2], "steps": L[3],
                       "bytes": L[4], "ms": round(m, 5),
                       "gbs": round(L[4] / (m * 1e-3) / 1e9, 1) if m > 0 else None}
@@ -217,10 +345,14 @@ def main():
         "cpu_baseline": None,
     }
     plan.close()
+    del bufs, pristine
+    if not args.no_ceiling:
+        print("bench: practical ceiling", file=sys.stderr, flush=True)
+        out["ceiling"] = ceiling(torch, arplan)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
-        del bufs, pristine
         out["cpu_baseline"] = cpu_baseline(name)
+        out["cpu_parallel"] = cpu_parallel(name)
     print(json.dumps(out), flush=True)
 
 

@@ -1,0 +1,43 @@
+"""Host-side checks of bench.py: the multi-GPU refusal and the thread-pool
+form of the oracle used for the parallel CPU baseline."""
+
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2409_04202_amd import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+@pytest.mark.parametrize("name,N", [("ring_n4_f32", None), ("ring_n4_i32", None),
+                                    ("tree8x8_n64_f32", 4096 + 64),
+                                    ("tree8x8x8_n512_bf16", 2048 + 512),
+                                    ("cdc384_gentree_f32", 384 * 3 + 1)])
+def test_parallel_oracle_equals_oracle(name, N):
+    c = workloads.CONFIGS[name]
+    N = c["N"] if N is None else N
+    if c["kind"] == "gentree":
+        plan = oracle.gentree_plan(oracle.from_preorder(c["fanin"]), N)
+    else:
+        plan = oracle.make_plan(c["kind"], c["n"], N, c["fanin"])
+    xs = workloads.inputs(name, N=N)
+    want = oracle.execute(plan, [x.copy() for x in xs], c["dtype"])
+    with ThreadPoolExecutor(max_workers=4) as pool:
+        got = bench.parallel_execute(plan, [x.copy() for x in xs], c["dtype"], pool)
+    for q in range(len(xs)):
+        assert np.array_equal(got[q], want[q])
