@@ -1,9 +1,11 @@
 """Build the HIP library ``lib/libarplan.so`` for gfx950 with hipcc.
 
 Run ``python -m paper_2409_04202_amd.build`` (or ``__graft_entry__.build()``).
-Host-only translation units are compiled with the host compiler, the HIP
-translation unit with ``hipcc --offload-arch=gfx950``, and hipcc links the
-shared library.  Always recompiles.
+The plan library and the C ABI (plan.cpp, capi.cpp) are compiled with the
+host compiler; the executor (exec.hip, and its host-side planning in
+rewrite.cpp and schedule.cpp, which share its HIP types) with
+``hipcc --offload-arch=gfx950``; hipcc links the shared library.  Always
+recompiles.
 """
 
 import os
@@ -19,7 +21,7 @@ LIB = os.path.join(LIBDIR, "libarplan.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HOST_SRCS = ["plan.cpp", "capi.cpp"]
-HIP_SRCS = ["exec.hip"]
+HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
           "-Wextra", "-Wno-unused-parameter"]

@@ -1,0 +1,209 @@
+// Host-side state of the executor, shared by its translation units: the
+// executed phases after the rewrites (rewrite.cpp), their launches and
+// sliced runs (schedule.cpp), and the per-device state and launching
+// (exec.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "../../include/ar_plan.h"
+#include "plan.hpp"
+
+namespace arp {
+
+
+constexpr int kCache = 4;               // buffer sets whose step records are kept per device
+constexpr int64_t kMinUnits = 2048;     // shrink tiles until a launch has this many
+constexpr int64_t kMaxBlocks = int64_t(1) << 24;
+// Cache policy per launch (measured on MI355X).  Launches moving less than
+// kNtBytes keep everything cached.  Larger ones load nontemporally unless a
+// source range is read by more than one step of the launch (then the repeated
+// reads hit the cache), and store nontemporally unless the next phase reads
+// what they write and it is at most kKeepBytes, small enough to stay in the
+// 256 MiB last-level cache until then.
+constexpr int64_t kNtBytes = int64_t(64) << 20;
+constexpr int64_t kKeepBytes = int64_t(256) << 20;
+// The step rewrites (multicast, reduce-then-broadcast) pay off where they
+// remove a launch from a short phase, add at most one extra destination, or
+// take over copies that read every range once (their reads are saved; a
+// 2-source fold storing to 8 destinations streams at 5.0 TB/s); a step
+// storing to many destinations over a large range is slower than plain
+// copies whose repeated reads hit the cache.  A rewrite is applied when its
+// step ends with at most kFuseDst destinations, the copies it takes over
+// move at most kFuseBytes (2 * len * e each), or (reduce-then-broadcast) no
+// two of those copies read the same range.
+constexpr int32_t kFuseDst = 2;
+constexpr int64_t kFuseBytes = int64_t(256) << 20;
+// Automatic choice of sliced launches (AR_OPT_SLICE = 2).  A run of
+// consecutive executed phases may become one sliced launch when every phase
+// in it writes at most kKeepBytes (what one phase hands to the next would
+// stay in the last-level cache with phase launches as well) and moves at most
+// kSliceMaxBytes.  The runs are chosen by dynamic programming over the phases
+// with a cost model fitted to MI355X measurements (back-to-back launches, no
+// events between them):
+//  * a phase launch costs kLaunchNs plus its bytes at kBytesPerNs;
+//  * a sliced launch costs kLaunchNs plus, per phase, the largest of its
+//    dependent chain, its read time and its write time.  The chain is the
+//    most steps covering one element position, which a wavefront runs one
+//    after the other, at kStepNs + k * kStepNsPerSrc{F32,BF16} +
+//    d * kStepNsPerDst each (k, d = the phase's largest source and
+//    destination counts); reads and writes go at kBytesPerNs, the reads
+//    stretched by kMinSliceWaves / waves when the slice has fewer wave tiles
+//    than that (too few loads in flight to reach full bandwidth).
+constexpr double kLaunchNs = 3000.0;
+constexpr double kBytesPerNs = 5500.0;
+constexpr double kStepNs = 350.0;
+constexpr double kStepNsPerSrcF32 = 120.0;
+constexpr double kStepNsPerSrcBF16 = 190.0;
+constexpr double kStepNsPerDst = 15.0;
+constexpr double kMinSliceWaves = 256.0;
+constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
+
+struct LaunchDesc {
+    int32_t phase;
+    int32_t xphase;          // executed phase
+    int32_t kern_k;          // template K (0 = runtime source count)
+    int64_t first;           // first entry of the step table (hsteps)
+    int64_t count;           // steps in this launch
+    int64_t tile_elems;
+    int64_t tiles_per_step;  // arithmetic mapping
+    int64_t nunits;          // wave tiles
+    int64_t tile_off;        // -1, or first entry of the device tile table
+    int32_t wpb;             // wavefronts per block
+    int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
+    int32_t max_dst;         // most destinations of a step
+    int64_t bytes;           // (k + destinations) * len * e over the steps
+    int64_t rec_off;         // first word of its steps' records
+    int64_t rec_stride;      // words per record
+};
+
+// The step records of one buffer set on one device.
+struct PtrEntry {
+    std::vector<void*> key;
+    uint64_t* dev = nullptr;     // records, device
+    uint64_t* pinned = nullptr;  // staging for their upload
+    hipEvent_t done = nullptr;
+    uint64_t stamp = 0;
+    bool valid = false;
+    bool aligned = false;
+};
+
+struct DevState {
+    int device = -1;
+    int2* tiles = nullptr;
+    int64_t* cuts = nullptr;     // sliced launch tables, all slices concatenated
+    int32_t* sched_off = nullptr;
+    int32_t* sched = nullptr;
+    int2* stiles = nullptr;
+    PtrEntry cache[kCache];
+    uint64_t clock = 0;
+};
+
+// An executed step (host form): fold `srcs` over [begin, end) and store the
+// result into every destination.  Plan steps map one to one onto executed
+// steps unless the rewrites below merge them.
+struct XStep {
+    int64_t begin, end;
+    std::vector<int32_t> srcs;
+    std::vector<int32_t> dsts;
+};
+
+struct XPhase {
+    int32_t plan_phase;  // phase of the plan these steps come from
+    std::vector<XStep> steps;
+};
+
+// A sliced launch runs executed phases [p0, p0 + nphases): segments are the
+// element ranges between consecutive boundaries of those phases' steps;
+// sched lists, per (phase of the slice, segment), the word offsets of the
+// records of the steps covering that segment; tiles maps each wavefront to (segment, tile within the
+// segment), over the segments some step of the slice covers.
+struct SliceDesc {
+    bool ok = false;
+    std::string why;             // why the phases cannot run sliced
+    int32_t p0 = 0, nphases = 0, nseg = 0;
+    int64_t tile_elems = 0, nunits = 0, bytes = 0, nsteps = 0;
+    int64_t chain = 0;           // sum over phases of the most steps on a segment
+    int32_t max_k = 0, max_dst = 0;
+    std::vector<int64_t> cuts;
+    std::vector<int32_t> sched_off, sched;
+    std::vector<int2> tiles;
+    // offsets of this slice's tables in the concatenated device tables
+    int64_t cuts_base = 0, soff_base = 0, sched_base = 0, tiles_base = 0;
+};
+
+// One launch of an execution: a sliced launch (slice >= 0) or the phase
+// launch `launch`.
+struct Stage {
+    int32_t slice;
+    int32_t launch;
+};
+
+struct ExecState {
+    std::vector<XPhase> phases;  // executed phases, after the rewrites
+    std::vector<LaunchDesc> launches;
+    std::vector<DevStep> hsteps;
+    std::vector<int32_t> hidx;   // source and destination indices
+    std::vector<int2> htiles;
+    std::vector<std::vector<int32_t>> dev_of;  // [phase][step] -> hsteps index
+    std::vector<int64_t> rec_of; // hsteps index -> first word of its record
+    int64_t rec_words = 0;       // words of all records
+    std::vector<SliceDesc> slices;
+    std::vector<Stage> stages;   // the launches for 16-byte aligned buffers
+    std::vector<DevState*> dev;  // indexed by device ordinal
+};
+
+// Every (buffer, range) a phase touches, with the step touching it; answers
+// "does a step other than `self` touch buf within [b, e)?".
+struct Touches {
+    struct Iv { int32_t buf; int64_t b, e; size_t step; };
+    std::vector<Iv> iv;
+    std::vector<int64_t> maxlen;  // longest interval per buffer
+    Touches(const XPhase& ph, int32_t n, bool reads, bool writes) : maxlen(size_t(n), 0) {
+        for (size_t i = 0; i < ph.steps.size(); ++i) {
+            const XStep& st = ph.steps[i];
+            if (st.end <= st.begin) continue;
+            if (reads) for (int32_t q : st.srcs) iv.push_back({q, st.begin, st.end, i});
+            if (writes) for (int32_t q : st.dsts) iv.push_back({q, st.begin, st.end, i});
+        }
+        std::sort(iv.begin(), iv.end(), [](const Iv& x, const Iv& y) {
+            return x.buf != y.buf ? x.buf < y.buf : x.b < y.b;
+        });
+        for (const Iv& x : iv) maxlen[size_t(x.buf)] = std::max(maxlen[size_t(x.buf)], x.e - x.b);
+    }
+    bool other(int32_t buf, int64_t b, int64_t e, size_t self) const {
+        if (e <= b) return false;
+        const int64_t from = b - maxlen[size_t(buf)];
+        auto it = std::lower_bound(iv.begin(), iv.end(), std::make_pair(buf, from),
+                                   [](const Iv& x, const std::pair<int32_t, int64_t>& k) {
+                                       return x.buf != k.first ? x.buf < k.first : x.b < k.second;
+                                   });
+        for (; it != iv.end() && it->buf == buf && it->b < e; ++it)
+            if (it->e > b && it->step != self) return true;
+        return false;
+    }
+    bool any(int32_t buf, int64_t b, int64_t e) const {
+        return other(buf, b, e, size_t(-1));
+    }
+};
+
+// Template source count of the phase kernel for k sources (0: read at run
+// time).
+int kernel_k(int32_t k);
+
+// Executed phases of a plan, after the rewrites when `fuse` (rewrite.cpp).
+std::vector<XPhase> exec_phases(const Plan& p, bool fuse);
+
+// Is every executed phase free of hazards?  (rewrite.cpp)
+bool exec_phases_hazard_free(const std::vector<XPhase>& ph, int32_t n, std::string& why);
+
+// The plan's executor state under its current options, built on first use
+// (schedule.cpp).  Host only.
+ExecState* exec_state(Plan& p);
+
+}  // namespace arp

@@ -1,0 +1,360 @@
+// Launch scheduling: executed phases become phase launches (steps grouped by
+// source count, tiled, cache mode chosen) and sliced runs (chosen by a cost
+// model).  Host only.
+#include <algorithm>
+#include <map>
+#include <memory>
+#include <tuple>
+#include <vector>
+
+#include "exec_state.hpp"
+
+namespace arp {
+
+int kernel_k(int32_t k) {
+    switch (k) {
+        case 1: case 2: case 3: case 4: case 8: case 16: return k;
+        default: return 0;
+    }
+}
+
+// Group the steps of every executed phase by source count, choose the
+// tiling and the cache mode of each launch.  Host only.
+static void build_launches(const Plan& p, ExecState& ex) {
+    const int64_t VEC = 16 / p.esize;
+    ex.dev_of.assign(ex.phases.size(), {});
+    for (size_t q = 0; q < ex.phases.size(); ++q) {
+        const XPhase& xp = ex.phases[q];
+        ex.dev_of[q].assign(xp.steps.size(), -1);
+        std::unique_ptr<Touches> next_reads;
+        if (q + 1 < ex.phases.size())
+            next_reads.reset(new Touches(ex.phases[q + 1], p.n, true, false));
+        std::vector<size_t> idx(xp.steps.size());
+        for (size_t i = 0; i < idx.size(); ++i) idx[i] = i;
+        // group by source count; inside a group, steps reading the same source
+        // become neighbours (their repeated reads share cache)
+        std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) {
+            const XStep& x = xp.steps[a];
+            const XStep& y = xp.steps[b];
+            if (x.srcs.size() != y.srcs.size()) return x.srcs.size() < y.srcs.size();
+            if (x.srcs[0] != y.srcs[0]) return x.srcs[0] < y.srcs[0];
+            return x.begin < y.begin;
+        });
+        size_t g0 = 0;
+        while (g0 < idx.size()) {
+            size_t g1 = g0;
+            const int32_t k = int32_t(xp.steps[idx[g0]].srcs.size());
+            while (g1 < idx.size() && int32_t(xp.steps[idx[g1]].srcs.size()) == k) ++g1;
+            LaunchDesc L{};
+            L.phase = xp.plan_phase;
+            L.xphase = int32_t(q);
+            L.kern_k = kernel_k(k);
+            L.first = int64_t(ex.hsteps.size());
+            L.count = int64_t(g1 - g0);
+            int64_t maxspan = 0, bytes = 0, written = 0;
+            int32_t maxdst = 0;
+            std::vector<int64_t> spans;
+            std::vector<std::tuple<int32_t, int64_t, int64_t>> ranges;
+            bool next_reads_output = false;
+            for (size_t g = g0; g < g1; ++g) {
+                const XStep& x = xp.steps[idx[g]];
+                DevStep d{};
+                d.begin = x.begin;
+                d.end = x.end;
+                d.k = k;
+                d.src_off = int32_t(ex.hidx.size());
+                ex.hidx.insert(ex.hidx.end(), x.srcs.begin(), x.srcs.end());
+                d.ndst = int32_t(x.dsts.size());
+                d.dst_off = int32_t(ex.hidx.size());
+                ex.hidx.insert(ex.hidx.end(), x.dsts.begin(), x.dsts.end());
+                ex.dev_of[q][idx[g]] = int32_t(ex.hsteps.size());
+                ex.hsteps.push_back(d);
+                const int64_t len = x.end - x.begin;
+                const int64_t span = len > 0 ? x.end - (x.begin & ~(VEC - 1)) : 0;
+                spans.push_back(span);
+                maxspan = std::max(maxspan, span);
+                maxdst = std::max(maxdst, int32_t(x.dsts.size()));
+                bytes += (k + int64_t(x.dsts.size())) * len * p.esize;
+                written += int64_t(x.dsts.size()) * len * p.esize;
+                if (len > 0) {
+                    for (int32_t sidx : x.srcs) ranges.emplace_back(sidx, x.begin, x.end);
+                    if (next_reads)
+                        for (int32_t dd : x.dsts)
+                            next_reads_output = next_reads_output || next_reads->any(dd, x.begin, x.end);
+                }
+            }
+            L.bytes = bytes;
+            L.max_dst = maxdst;
+            L.rec_stride = (kRecHead + k + maxdst + 1) & ~int64_t(1);
+            L.rec_off = ex.rec_words;
+            ex.rec_of.resize(ex.hsteps.size(), -1);
+            for (int64_t j = 0; j < L.count; ++j)
+                ex.rec_of[size_t(L.first + j)] = L.rec_off + j * L.rec_stride;
+            ex.rec_words += L.count * L.rec_stride;
+            if (maxspan == 0) {  // nothing to move in this group
+                g0 = g1;
+                continue;
+            }
+            // wave tile: the measured best size for this source count,
+            // halved while the launch has too few tiles to fill the chip
+            const KCfg cfg = kcfg(L.kern_k);
+            const int64_t tmin = int64_t(64) * cfg.U * VEC;
+            int64_t te = int64_t(cfg.TE) * VEC;
+            auto units_for = [&](int64_t t) {
+                return L.count * ((maxspan + t - 1) / t);
+            };
+            while (te > tmin && units_for(te) < kMinUnits) te /= 2;
+            while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
+            L.wpb = cfg.WPB;
+            std::sort(ranges.begin(), ranges.end());
+            const bool reuse = std::adjacent_find(ranges.begin(), ranges.end()) != ranges.end();
+            L.cm = 0;
+            if (bytes >= kNtBytes) {
+                if (!reuse) L.cm |= 1;
+                if (written > kKeepBytes || !next_reads_output) L.cm |= 2;
+            }
+            L.tile_elems = te;
+            L.tiles_per_step = (maxspan + te - 1) / te;
+            int64_t used = 0;
+            for (int64_t sp : spans) used += (sp + te - 1) / te;
+            if (used * 5 < L.count * L.tiles_per_step * 4) {
+                // uneven steps: explicit tile table
+                L.tile_off = int64_t(ex.htiles.size());
+                for (int64_t j = 0; j < L.count; ++j) {
+                    const int64_t nt = (spans[size_t(j)] + te - 1) / te;
+                    for (int64_t t = 0; t < nt; ++t)
+                        ex.htiles.push_back(make_int2(int(j), int(t)));
+                }
+                L.nunits = used;
+            } else {
+                L.tile_off = -1;
+                L.nunits = L.count * L.tiles_per_step;
+            }
+            ex.launches.push_back(L);
+            g0 = g1;
+        }
+    }
+}
+
+// The sliced launch of executed phases [p0, p1), if every boundary of their
+// steps is 16-byte aligned.
+static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int32_t p1) {
+    SliceDesc sd;
+    const int64_t VEC = 16 / p.esize;
+    sd.p0 = p0;
+    sd.nphases = p1 - p0;
+    for (int32_t q = p0; q < p1; ++q)
+        for (const XStep& x : ex.phases[size_t(q)].steps)
+            if (x.end > x.begin) {
+                sd.cuts.push_back(x.begin);
+                sd.cuts.push_back(x.end);
+            }
+    std::sort(sd.cuts.begin(), sd.cuts.end());
+    sd.cuts.erase(std::unique(sd.cuts.begin(), sd.cuts.end()), sd.cuts.end());
+    for (int64_t c : sd.cuts)
+        if (c % VEC) {
+            sd.why = "a step boundary is not 16-byte aligned";
+            return sd;
+        }
+    if (sd.cuts.size() < 2) {
+        sd.why = "nothing to move";
+        return sd;
+    }
+    sd.nseg = int32_t(sd.cuts.size() - 1);
+    if (int64_t(sd.nphases) * sd.nseg > (int64_t(1) << 24)) {
+        sd.why = "too many phases times segments";
+        return sd;
+    }
+    auto seg_of = [&](int64_t x) {  // segment starting at x
+        return int32_t(std::lower_bound(sd.cuts.begin(), sd.cuts.end(), x) - sd.cuts.begin());
+    };
+    std::vector<std::vector<int32_t>> lists(size_t(sd.nphases) * size_t(sd.nseg));
+    std::vector<char> used(size_t(sd.nseg), 0);
+    for (int32_t q = p0; q < p1; ++q) {
+        const XPhase& xp = ex.phases[size_t(q)];
+        for (size_t i = 0; i < xp.steps.size(); ++i) {
+            const XStep& x = xp.steps[i];
+            if (x.end <= x.begin) continue;
+            const int32_t di = ex.dev_of[size_t(q)][i];
+            if (di < 0 || ex.rec_of[size_t(di)] < 0 || ex.rec_of[size_t(di)] > INT32_MAX) {
+                sd.why = "step without a record";
+                return sd;
+            }
+            for (int32_t sg = seg_of(x.begin); sg < seg_of(x.end); ++sg) {
+                lists[size_t(q - p0) * size_t(sd.nseg) + size_t(sg)].push_back(
+                    int32_t(ex.rec_of[size_t(di)]));
+                used[size_t(sg)] = 1;
+            }
+            sd.bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * (x.end - x.begin) * p.esize;
+            sd.max_k = std::max(sd.max_k, int32_t(x.srcs.size()));
+            sd.max_dst = std::max(sd.max_dst, int32_t(x.dsts.size()));
+            ++sd.nsteps;
+        }
+    }
+    for (int32_t q = 0; q < sd.nphases; ++q) {
+        size_t most = 0;
+        for (int32_t sg = 0; sg < sd.nseg; ++sg)
+            most = std::max(most, lists[size_t(q) * size_t(sd.nseg) + size_t(sg)].size());
+        sd.chain += int64_t(most);
+    }
+    sd.sched_off.assign(lists.size() + 1, 0);
+    for (size_t i = 0; i < lists.size(); ++i) {
+        sd.sched_off[i + 1] = sd.sched_off[i] + int32_t(lists[i].size());
+        sd.sched.insert(sd.sched.end(), lists[i].begin(), lists[i].end());
+        if (sd.sched.size() > size_t(1) << 30) {
+            sd.why = "schedule too large";
+            return sd;
+        }
+    }
+    sd.tile_elems = int64_t(64) * kSliceU * VEC;
+    for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+        if (!used[size_t(sg)]) continue;
+        const int64_t len = sd.cuts[size_t(sg) + 1] - sd.cuts[size_t(sg)];
+        for (int64_t t = 0; t * sd.tile_elems < len; ++t) sd.tiles.push_back(make_int2(sg, int(t)));
+    }
+    sd.nunits = int64_t(sd.tiles.size());
+    if ((sd.nunits + kSliceWPB - 1) / kSliceWPB > kMaxBlocks) {
+        sd.why = "too many tiles";
+        return sd;
+    }
+    sd.ok = sd.nunits > 0;
+    if (!sd.ok) sd.why = "nothing to move";
+    return sd;
+}
+
+// Per executed phase, what the choice of sliced runs needs: whether every
+// step boundary is 16-byte aligned, the bytes written and moved, the most
+// steps covering one element position, and the predicted phase-launch time.
+struct PhaseCost {
+    bool aligned = true;
+    int64_t written = 0, read = 0, bytes = 0, cover = 0;
+    int32_t kmax = 0, dmax = 0;
+    double t_launch = 0.0;
+};
+
+static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
+    const int64_t VEC = 16 / p.esize;
+    std::vector<PhaseCost> pc(ex.phases.size());
+    for (size_t q = 0; q < ex.phases.size(); ++q) {
+        std::vector<std::pair<int64_t, int32_t>> ev;
+        for (const XStep& x : ex.phases[q].steps) {
+            if (x.end <= x.begin) continue;
+            if (x.begin % VEC || x.end % VEC) pc[q].aligned = false;
+            const int64_t len = x.end - x.begin;
+            pc[q].written += int64_t(x.dsts.size()) * len * p.esize;
+            pc[q].read += int64_t(x.srcs.size()) * len * p.esize;
+            pc[q].kmax = std::max(pc[q].kmax, int32_t(x.srcs.size()));
+            pc[q].dmax = std::max(pc[q].dmax, int32_t(x.dsts.size()));
+            pc[q].bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * len * p.esize;
+            ev.emplace_back(x.begin, 1);
+            ev.emplace_back(x.end, -1);
+        }
+        std::sort(ev.begin(), ev.end());  // at equal positions ends (-1) first
+        int64_t c = 0;
+        for (const auto& e : ev) {
+            c += e.second;
+            pc[q].cover = std::max(pc[q].cover, c);
+        }
+    }
+    for (const LaunchDesc& L : ex.launches)
+        pc[size_t(L.xphase)].t_launch += kLaunchNs + double(L.bytes) / kBytesPerNs;
+    return pc;
+}
+
+// Sliced runs for AR_OPT_SLICE = 2: phases [a, b), each aligned, writing at
+// most kKeepBytes and moving at most kSliceMaxBytes, chosen to minimise the
+// predicted time.  A run of one phase only pays off when it replaces
+// several launches.
+static std::vector<std::pair<int32_t, int32_t>> choose_runs(const Plan& p, const ExecState& ex,
+                                                            const std::vector<PhaseCost>& pc) {
+    const double per_src = p.dtype == AR_BF16 ? kStepNsPerSrcBF16 : kStepNsPerSrcF32;
+    const double waves = std::max(1.0, double(p.N) * p.esize / (64.0 * kSliceU * 16.0));
+    const double stretch = std::max(1.0, kMinSliceWaves / waves);
+    const int32_t P = int32_t(pc.size());
+    std::vector<int32_t> nl(size_t(P), 0);
+    for (const LaunchDesc& L : ex.launches) ++nl[size_t(L.xphase)];
+    std::vector<double> best(size_t(P) + 1, 0.0);
+    std::vector<int32_t> from(size_t(P) + 1, -1);  // -1: phase launches for phase b - 1
+    for (int32_t b = 1; b <= P; ++b) {
+        best[size_t(b)] = best[size_t(b) - 1] + pc[size_t(b) - 1].t_launch;
+        from[size_t(b)] = -1;
+        double body = 0.0;
+        for (int32_t a = b - 1; a >= 0; --a) {
+            const PhaseCost& c = pc[size_t(a)];
+            if (!c.aligned || c.written > kKeepBytes || c.bytes > kSliceMaxBytes) break;
+            body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
+                              stretch * double(c.read) / kBytesPerNs,
+                              double(c.written) / kBytesPerNs});
+            if (b - a == 1 && nl[size_t(a)] < 2) continue;
+            const double t = kLaunchNs + body;
+            if (best[size_t(a)] + t < best[size_t(b)]) {
+                best[size_t(b)] = best[size_t(a)] + t;
+                from[size_t(b)] = a;
+            }
+        }
+    }
+    std::vector<std::pair<int32_t, int32_t>> runs;
+    for (int32_t b = P; b > 0;) {
+        if (from[size_t(b)] < 0) {
+            --b;
+        } else {
+            runs.emplace_back(from[size_t(b)], b);
+            b = from[size_t(b)];
+        }
+    }
+    std::reverse(runs.begin(), runs.end());
+    return runs;
+}
+
+ExecState* exec_state(Plan& p) {
+    if (!p.exec) {
+        ExecState* ex = new ExecState();
+        try {
+            ex->phases = exec_phases(p, p.fuse != 0);
+            build_launches(p, *ex);
+            std::vector<std::pair<int32_t, int32_t>> runs;
+            if (p.slice == 1 && !ex->phases.empty()) {
+                runs.emplace_back(0, int32_t(ex->phases.size()));
+            } else if (p.slice == 2) {
+                runs = choose_runs(p, *ex, phase_costs(p, *ex));
+            }
+            std::vector<int32_t> slice_of(ex->phases.size(), -1);
+            for (const auto& r : runs) {
+                SliceDesc sd = build_slice(p, *ex, r.first, r.second);
+                if (!sd.ok) continue;  // phase launches for these phases
+                sd.cuts_base = ex->slices.empty() ? 0
+                                                  : ex->slices.back().cuts_base +
+                                                        int64_t(ex->slices.back().cuts.size());
+                sd.soff_base = ex->slices.empty() ? 0
+                                                  : ex->slices.back().soff_base +
+                                                        int64_t(ex->slices.back().sched_off.size());
+                sd.sched_base = ex->slices.empty() ? 0
+                                                   : ex->slices.back().sched_base +
+                                                         int64_t(ex->slices.back().sched.size());
+                sd.tiles_base = ex->slices.empty() ? 0
+                                                   : ex->slices.back().tiles_base +
+                                                         int64_t(ex->slices.back().tiles.size());
+                for (int32_t q = r.first; q < r.second; ++q)
+                    slice_of[size_t(q)] = int32_t(ex->slices.size());
+                ex->slices.push_back(std::move(sd));
+            }
+            int32_t last = -1;
+            for (size_t li = 0; li < ex->launches.size(); ++li) {
+                const int32_t sl = slice_of[size_t(ex->launches[li].xphase)];
+                if (sl < 0) {
+                    ex->stages.push_back({-1, int32_t(li)});
+                } else if (sl != last) {
+                    ex->stages.push_back({sl, -1});
+                    last = sl;
+                }
+            }
+        } catch (...) {
+            delete ex;
+            throw;
+        }
+        p.exec = ex;
+    }
+    return p.exec;
+}
+
+}  // namespace arp
