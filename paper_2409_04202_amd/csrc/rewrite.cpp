@@ -10,9 +10,63 @@
 
 namespace arp {
 
+// What the reads and writes of one executed phase touch, kept up to date
+// while copies of later phases are folded into its reduce steps (each fold
+// adds writes only): per buffer, the touched intervals by begin, with the
+// step that touches them and whether it writes them.  Folding phase after
+// phase then costs the added writes only.
+struct Merged {
+    struct Touch { int64_t end; size_t step; bool write; };
+    std::vector<std::multimap<int64_t, Touch>> iv;  // per buffer
+    std::vector<int64_t> maxlen;                    // longest interval per buffer
+    std::vector<bool> reduce;                       // per step: two or more sources
+    std::vector<int32_t> extra;                     // per step: destinations one fold adds
+
+    Merged(const XPhase& ph, int32_t n)
+        : iv(size_t(n)), maxlen(size_t(n), 0), extra(ph.steps.size(), 0) {
+        for (size_t i = 0; i < ph.steps.size(); ++i) {
+            const XStep& st = ph.steps[i];
+            reduce.push_back(st.srcs.size() >= 2);
+            if (st.end <= st.begin) continue;
+            for (int32_t q : st.srcs) touch(q, st.begin, st.end, i, false);
+            for (int32_t d : st.dsts) touch(d, st.begin, st.end, i, true);
+        }
+    }
+    void touch(int32_t buf, int64_t b, int64_t e, size_t step, bool write) {
+        iv[size_t(buf)].insert({b, Touch{e, step, write}});
+        maxlen[size_t(buf)] = std::max(maxlen[size_t(buf)], e - b);
+    }
+    // the reduce step that writes `buf` from position b on (its end in
+    // `end`), or -1
+    int64_t producer(int32_t buf, int64_t b, int64_t& end) const {
+        const auto r = iv[size_t(buf)].equal_range(b);
+        for (auto it = r.first; it != r.second; ++it)
+            if (it->second.write && reduce[it->second.step]) {
+                end = it->second.end;
+                return int64_t(it->second.step);
+            }
+        return -1;
+    }
+    // does `step` already write `buf` (from its begin b on)?
+    bool writes(int32_t buf, int64_t b, size_t step) const {
+        const auto r = iv[size_t(buf)].equal_range(b);
+        for (auto it = r.first; it != r.second; ++it)
+            if (it->second.write && it->second.step == step) return true;
+        return false;
+    }
+    // does a step other than `self` touch positions [b, e) of `buf`?
+    bool other(int32_t buf, int64_t b, int64_t e, size_t self) const {
+        if (e <= b) return false;
+        const auto& m = iv[size_t(buf)];
+        for (auto it = m.lower_bound(b - maxlen[size_t(buf)]); it != m.end() && it->first < e; ++it)
+            if (it->second.end > b && it->second.step != self) return true;
+        return false;
+    }
+};
+
 // Executed phases of a plan.  With `fuse`, two rewrites remove memory
 // traffic or launches without changing any result (subject to kFuseDst /
-// kFuseBytes above):
+// kFuseBytes of exec_state.hpp):
 //  * multicast: copies in one phase that read the same range of the same
 //    buffer become one step that reads it once and stores it to every
 //    destination;
@@ -87,15 +141,7 @@ std::vector<XPhase> exec_phases(const Plan& p, bool fuse) {
     // reduce-then-broadcast, transitively: phase q absorbs q+1, then q+2, ...
     // as long as each next phase consists of copies whose source ranges are
     // exactly unions of ranges the (merged) reduce steps of q write
-    auto absorb = [&](XPhase& cur, const XPhase& nxt) {
-        const Touches touched(cur, p.n, true, true);
-        // per buffer, the ranges the reduce steps of cur write, by begin
-        std::map<std::pair<int32_t, int64_t>, std::pair<int64_t, size_t>> produced;
-        for (size_t i = 0; i < cur.steps.size(); ++i) {
-            const XStep& st = cur.steps[i];
-            if (st.srcs.size() >= 2 && st.end > st.begin)
-                for (int32_t d : st.dsts) produced[{d, st.begin}] = {st.end, i};
-        }
+    auto absorb = [&](XPhase& cur, Merged& m, const XPhase& nxt) {
         // copies whose reads are all distinct move data nobody reads twice:
         // folding them into the reduce steps saves their reads entirely
         const bool small = copy_bytes(nxt) <= kFuseBytes;
@@ -113,9 +159,14 @@ std::vector<XPhase> exec_phases(const Plan& p, bool fuse) {
                     std::get<1>(rd[i]) < std::get<2>(rd[i - 1]))
                     distinct = false;
         }
-        // (producer step, destination) pairs to add
+        // (producer step, destination) pairs to add, checked against the
+        // merged phase as it stands before this fold
         std::vector<std::pair<size_t, int32_t>> adds;
-        std::vector<size_t> extra(cur.steps.size(), 0);
+        struct Reset {  // leaves m.extra all zero on every return
+            Merged& m;
+            const std::vector<std::pair<size_t, int32_t>>& adds;
+            ~Reset() { for (const auto& ad : adds) m.extra[ad.first] = 0; }
+        } reset{m, adds};
         bool any = false;
         for (const XStep& c : nxt.steps) {
             if (c.end <= c.begin) continue;  // empty step: nothing to move
@@ -123,32 +174,45 @@ std::vector<XPhase> exec_phases(const Plan& p, bool fuse) {
             any = true;
             int64_t at = c.begin;
             while (at < c.end) {
-                auto it = produced.find({c.srcs[0], at});
-                if (it == produced.end() || it->second.first > c.end) return false;
-                const size_t i = it->second.second;
+                int64_t end = 0;
+                const int64_t i = m.producer(c.srcs[0], at, end);
+                if (i < 0 || end > c.end) return false;
                 for (int32_t d : c.dsts) {
-                    if (touched.other(d, at, it->second.first, i)) return false;
-                    adds.emplace_back(i, d);
-                    extra[i] += 1;
+                    if (m.other(d, at, end, size_t(i))) return false;
+                    adds.emplace_back(size_t(i), d);
+                    m.extra[size_t(i)] += 1;
                 }
-                at = it->second.first;
+                at = end;
             }
         }
         if (!any) return false;
         if (!small && !distinct)
-            for (size_t i = 0; i < cur.steps.size(); ++i)
-                if (int32_t(cur.steps[i].dsts.size() + extra[i]) > kFuseDst) return false;
+            for (const auto& ad : adds)
+                if (int32_t(cur.steps[ad.first].dsts.size()) + m.extra[ad.first] > kFuseDst)
+                    return false;
         for (const auto& ad : adds) {
             XStep& s = cur.steps[ad.first];
-            if (std::find(s.dsts.begin(), s.dsts.end(), ad.second) == s.dsts.end())
+            if (!m.writes(ad.second, s.begin, ad.first)) {
                 s.dsts.push_back(ad.second);
+                m.touch(ad.second, s.begin, s.end, ad.first, true);
+            }
         }
         return true;
     };
     for (size_t q = 0; q + 1 < ph.size(); ++q) {
         if (ph[q].steps.empty()) continue;
+        bool copies = false;  // only a phase of copies can be folded
+        for (const XStep& c : ph[q + 1].steps) {
+            if (c.srcs.size() != 1 && c.end > c.begin) {
+                copies = false;
+                break;
+            }
+            copies = copies || c.end > c.begin;
+        }
+        if (!copies) continue;
+        Merged m(ph[q], p.n);
         for (size_t j = q + 1; j < ph.size(); ++j) {
-            if (!absorb(ph[q], ph[j])) break;
+            if (!absorb(ph[q], m, ph[j])) break;
             ph[j].steps.clear();
         }
     }
