@@ -37,6 +37,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# kernel of a launch by its phase field in ar_plan_launch_info
+KERNEL_OF = {-1: "sliced_kernel", -2: "resident_kernel"}
 DEFAULT = "rhd_n8_f32"
 
 
@@ -204,6 +206,8 @@ def main():
                     help="run every plan step as listed (AR_OPT_FUSE = 0)")
     ap.add_argument("--slice", type=int, choices=(0, 1, 2), default=None,
                     help="AR_OPT_SLICE (default: the library's, 2)")
+    ap.add_argument("--resident", type=int, choices=(0, 1), default=None,
+                    help="AR_OPT_RESIDENT (default: the library's, 1)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build executes every emulated processor on one "
@@ -237,6 +241,8 @@ def main():
         plan.set_option(arplan.AR_OPT_FUSE, 0)
     if args.slice is not None:
         plan.set_option(arplan.AR_OPT_SLICE, args.slice)
+    if args.resident is not None:
+        plan.set_option(arplan.AR_OPT_RESIDENT, args.resident)
     stream = torch.cuda.current_stream()
     launches = plan.launches()          # (phase, nsrc, max_dst, steps, bytes)
     red_b, cpy_b = plan.bytes()
@@ -296,14 +302,15 @@ def main():
     cpy_ms = sum(l_ms[i] for i in cpy)
     cpy_bytes = sum(launches[i][4] for i in cpy)
     achieved = red_bytes / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
-    traffic = load_traffic(name) if not args.no_fuse and args.slice is None else None
+    traffic = load_traffic(name) if (not args.no_fuse and args.slice is None
+                                     and args.resident is None) else None
     roofline = {"bound": "hbm", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
                 "kernel": "%s, reduce launches (k = %s)" % (
-                    " + ".join(sorted({"sliced_kernel" if launches[i][0] < 0
-                                       else "phase_kernel" for i in red})) or "-",
+                    " + ".join(sorted({KERNEL_OF.get(launches[i][0], "phase_kernel")
+                                       for i in red})) or "-",
                     sorted({launches[i][1] for i in red}) or "-"),
                 "launches_per_step": len(red),
                 "bytes_per_launch": round(red_bytes / max(1, len(red))),
@@ -326,6 +333,7 @@ def main():
                              else "%d-node tree" % len(c["fanin"])) if c["fanin"] else None,
                    "fuse": not args.no_fuse,
                    "slice": args.slice if args.slice is not None else 2,
+                   "resident": args.resident if args.resident is not None else 1,
                    "parallelism": "emulated %d processors on 1 GPU" % n},
         "plan_bytes_per_step": red_b + cpy_b,
         "plan_gbs": round((red_b + cpy_b) / (ms_step * 1e-3) / 1e9, 1),

@@ -241,16 +241,29 @@ ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
  *  every boundary of its steps is a multiple of 16 bytes; sliced launches
  *  are used only with 16-byte aligned buffers (otherwise every phase runs
  *  as its phase launches, those reported with AR_OPT_SLICE = 0). */
-typedef enum ar_option { AR_OPT_FUSE = 0, AR_OPT_SLICE = 1 } ar_option;
+/*  AR_OPT_RESIDENT (default 1): a sliced launch of a plan with n <= 64
+ *  buffers may run resident instead: each wavefront keeps its tile of
+ *  element positions of every buffer in on-chip memory (LDS) for the whole
+ *  run, loading each buffer's tile before the run's first read of it and
+ *  storing each tile the run writes after its last phase, so that the
+ *  run's intermediate values stay on chip; every step is still run in
+ *  order with the plan's sources in their listed order, so results are the
+ *  same bits.  With AR_OPT_SLICE = 2 the cost model picks the plain or the
+ *  resident form per run; with AR_OPT_SLICE = 1 the whole plan runs
+ *  resident when n <= 64.  0: sliced launches always run plain. */
+typedef enum ar_option { AR_OPT_FUSE = 0, AR_OPT_SLICE = 1, AR_OPT_RESIDENT = 2 } ar_option;
 ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value);
 
 /* The kernel launches one execution on 16-byte aligned buffers issues (host
  * only, no GPU call): their number, and for launch i the plan phase its
- * steps come from (-1 for a sliced launch), their source count (the
+ * steps come from (-1 for a sliced launch, -2 for a resident one), their
+ * source count (the
  * largest, for a sliced launch), the most destinations any of its
  * steps stores to, its number of steps and its algorithmic bytes:
  * (k + destinations) * len * e summed over its steps (each source read
- * once, each destination written once).  Any out-pointer may be NULL. */
+ * once, each destination written once); for a resident launch, the bytes
+ * of the buffer tiles it loads and stores (each once; a whole AllReduce
+ * run resident moves 2 * n * N * e).  Any out-pointer may be NULL. */
 ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count);
 ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t* phase,
                               int32_t* nsrc, int32_t* max_dst,

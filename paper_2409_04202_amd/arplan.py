@@ -39,7 +39,7 @@ AR_OK, AR_ERR_INVALID_ARG, AR_ERR_UNSUPPORTED, AR_ERR_OOM, AR_ERR_HIP, \
 AR_F32, AR_I32, AR_BF16 = range(3)
 AR_RING, AR_RHD, AR_CPS, AR_TREE, AR_RB, AR_GENTREE = range(6)
 AR_OP_REDUCE, AR_OP_COPY = range(2)
-AR_OPT_FUSE, AR_OPT_SLICE = 0, 1
+AR_OPT_FUSE, AR_OPT_SLICE, AR_OPT_RESIDENT = 0, 1, 2
 
 DTYPES = {"f32": AR_F32, "i32": AR_I32, "bf16": AR_BF16}
 KINDS = {"ring": AR_RING, "rhd": AR_RHD, "cps": AR_CPS, "tree": AR_TREE,

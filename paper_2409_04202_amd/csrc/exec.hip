@@ -45,6 +45,8 @@ static void free_dev(DevState* d) {
     if (d->sched_off) (void)hipFree(d->sched_off);
     if (d->sched) (void)hipFree(d->sched);
     if (d->stiles) (void)hipFree(d->stiles);
+    if (d->runits) (void)hipFree(d->runits);
+    if (d->prog) (void)hipFree(d->prog);
     for (PtrEntry& e : d->cache) {
         if (e.done) {
             (void)hipEventSynchronize(e.done);
@@ -93,16 +95,22 @@ static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
             std::vector<int64_t> cuts;
             std::vector<int32_t> soff, sched;
             std::vector<int2> tiles;
+            std::vector<ResUnit> runits;
+            std::vector<uint32_t> prog;
             for (const SliceDesc& sd : ex.slices) {
                 cuts.insert(cuts.end(), sd.cuts.begin(), sd.cuts.end());
                 soff.insert(soff.end(), sd.sched_off.begin(), sd.sched_off.end());
                 sched.insert(sched.end(), sd.sched.begin(), sd.sched.end());
                 tiles.insert(tiles.end(), sd.tiles.begin(), sd.tiles.end());
+                runits.insert(runits.end(), sd.runits.begin(), sd.runits.end());
+                prog.insert(prog.end(), sd.prog.begin(), sd.prog.end());
             }
             s = upload(&d->cuts, cuts, "segment table");
             if (s == AR_OK) s = upload(&d->sched_off, soff, "schedule offsets");
             if (s == AR_OK) s = upload(&d->sched, sched, "schedule");
             if (s == AR_OK) s = upload(&d->stiles, tiles, "slice tiles");
+            if (s == AR_OK) s = upload(&d->runits, runits, "resident units");
+            if (s == AR_OK) s = upload(&d->prog, prog, "resident programs");
         }
         if (s != AR_OK) {
             free_dev(d);
@@ -134,8 +142,9 @@ static ar_status check_buffers(const Plan& p, const std::vector<void*>& bufs) {
     return AR_OK;
 }
 
-// The step records for buffer set `bufs` on this device (see StepHead):
-// from the per-plan cache, or built on the host and uploaded on `stream`.
+// The step records for buffer set `bufs` on this device (see StepHead),
+// followed by the n buffer pointers: from the per-plan cache, or built on
+// the host and uploaded on `stream`.
 static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
                               const std::vector<void*>& bufs,
                               hipStream_t stream, PtrEntry** out) {
@@ -153,7 +162,7 @@ static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
         if (!e.valid) { v = &e; break; }
         if (e.stamp < v->stamp) v = &e;
     }
-    const size_t nb = size_t(std::max<int64_t>(ex.rec_words, 1)) * sizeof(uint64_t);
+    const size_t nb = size_t(ex.rec_words + p.n) * sizeof(uint64_t);
     hipError_t e = hipSuccess;
     if (!v->dev) {
         e = hipMalloc(reinterpret_cast<void**>(&v->dev), nb);
@@ -192,6 +201,7 @@ static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
             r[kRecHead + st.k + j] =
                 reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.dst_off + j)])]);
     }
+    for (size_t i = 0; i < bufs.size(); ++i) w[ex.rec_words + int64_t(i)] = reinterpret_cast<uint64_t>(bufs[i]);
     e = hipMemcpyAsync(v->dev, v->pinned, nb, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("step record upload", e));
     e = hipEventRecord(v->done, stream);
@@ -284,7 +294,20 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             s = mark(0);
             if (s != AR_OK) return s;
             const Stage stg = staged ? ex->stages[size_t(li)] : Stage{-1, int32_t(li)};
-            if (stg.slice >= 0) {
+            if (stg.slice >= 0 && ex->slices[size_t(stg.slice)].resident) {
+                const SliceDesc& sd = ex->slices[size_t(stg.slice)];
+                const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(64);
+                const size_t lds = size_t(plan->n) * 1024;
+#define AR_RESIDENT(DT)                                                                    \
+    hipLaunchKernelGGL((resident_kernel<DT>), grid, block, lds, stream, pe->dev + ex->rec_words, \
+                       plan->n, d->runits + sd.runit_base, d->prog + sd.prog_base, sd.nunits)
+                switch (plan->dtype) {
+                    case AR_F32: AR_RESIDENT(DT_F32); break;
+                    case AR_I32: AR_RESIDENT(DT_I32); break;
+                    default: AR_RESIDENT(DT_BF16); break;
+                }
+#undef AR_RESIDENT
+            } else if (stg.slice >= 0) {
                 const SliceDesc& sd = ex->slices[size_t(stg.slice)];
                 const dim3 grid(static_cast<uint32_t>((sd.nunits + kSliceWPB - 1) / kSliceWPB));
                 const dim3 block(64 * kSliceWPB);
@@ -567,7 +590,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 const int64_t lo = sd.cuts[size_t(e.x)] + int64_t(e.y) * sd.tile_elems;
                 const int64_t hi = std::min(sd.cuts[size_t(e.x) + 1], lo + sd.tile_elems);
                 if (lo >= hi || lo % VEC || hi % VEC) return bad("slice tile empty or misaligned");
-                if ((hi - lo) / VEC > 64 * kSliceU) return bad("slice tile too long");
+                if ((hi - lo) / VEC > (sd.resident ? 64 : 64 * kSliceU)) return bad("slice tile too long");
                 sc[size_t(e.x)].push_back({lo, hi});
             }
             if (int64_t(sd.sched_off.size()) != int64_t(sd.nphases) * sd.nseg + 1)
@@ -610,6 +633,100 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     std::sort(want.begin(), want.end());
                     std::sort(got.begin(), got.end());
                     if (want != got) return bad("schedule differs from the steps of a phase");
+                }
+            }
+            if (sd.resident) {
+                // per segment: the step records decode to the steps covering
+                // it in phase order, no record across a 64-word chunk, rows in
+                // range; per unit: its tile, and the rows to load (read before
+                // written) and to store (written) of its segment
+                if (plan->n > kResMaxN) return bad("resident launch with too many buffers");
+                if (int64_t(sd.runits.size()) != sd.nunits || int64_t(sd.tiles.size()) != sd.nunits ||
+                    int64_t(sd.rec_off.size()) != sd.nseg)
+                    return bad("resident table sizes");
+                std::vector<uint64_t> wload(size_t(sd.nseg), 0), wstore(size_t(sd.nseg), 0);
+                std::vector<int32_t> words(size_t(sd.nseg), 0);
+                for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+                    std::vector<std::pair<std::vector<int32_t>, std::vector<int32_t>>> want;
+                    uint64_t seen = 0;
+                    for (int32_t q = 0; q < sd.nphases; ++q)
+                        for (const XStep& x : ex->phases[size_t(sd.p0 + q)].steps)
+                            if (x.end > x.begin && x.begin <= sd.cuts[size_t(sg)] &&
+                                sd.cuts[size_t(sg) + 1] <= x.end) {
+                                want.push_back({x.srcs, x.dsts});
+                                for (int32_t b : x.srcs)
+                                    if (!(seen >> b & 1)) wload[size_t(sg)] |= uint64_t(1) << b;
+                                for (int32_t b : x.srcs) seen |= uint64_t(1) << b;
+                                for (int32_t b : x.dsts) {
+                                    seen |= uint64_t(1) << b;
+                                    wstore[size_t(sg)] |= uint64_t(1) << b;
+                                }
+                            }
+                    const int32_t off = sd.rec_off[size_t(sg)];
+                    if (want.empty()) {
+                        if (off != -1) return bad("resident records on an idle segment");
+                        continue;
+                    }
+                    if (off < 0 || off > int64_t(sd.prog.size())) return bad("resident records outside the table");
+                    std::vector<std::pair<std::vector<int32_t>, std::vector<int32_t>>> got;
+                    const uint32_t* sp = sd.prog.data() + off;
+                    const int64_t avail = int64_t(sd.prog.size()) - off;
+                    int32_t nw = 0;
+                    for (int32_t c0 = 0; got.size() < want.size(); c0 += 64) {
+                        int32_t c = 0;
+                        while (c < 64 && got.size() < want.size()) {
+                            if (c0 + c >= avail) return bad("resident records run past the table");
+                            const uint32_t h = sp[c0 + c];
+                            const uint32_t op = h & 0xFF;
+                            if (op == kResAdd2 || op == kResCopy) {
+                                const int32_t r0 = int32_t((h >> 8) & 0xFF), r1 = int32_t((h >> 16) & 0xFF);
+                                const int32_t d = int32_t(h >> 24);
+                                if (r0 >= plan->n || r1 >= plan->n || d >= plan->n)
+                                    return bad("resident row out of range");
+                                if (op == kResCopy && r1 != r0) return bad("resident copy record malformed");
+                                got.push_back({op == kResAdd2 ? std::vector<int32_t>{r0, r1}
+                                                              : std::vector<int32_t>{r0},
+                                               std::vector<int32_t>{d}});
+                                c += 1;
+                                nw = c0 + c;
+                                continue;
+                            }
+                            const int k = int(op), nd = int((h >> 8) & 0xFF);
+                            if (k > kResMaxN) return bad("resident record header malformed");
+                            if (k == 0) {
+                                for (int32_t j = c; j < 64 && c0 + j < avail; ++j)
+                                    if (sp[c0 + j]) return bad("resident chunk padding not zero");
+                                break;
+                            }
+                            if (nd < 1 || c + res_words(k, nd) > 64 || c0 + c + res_words(k, nd) > avail)
+                                return bad("resident record across a chunk");
+                            std::vector<int32_t> rows;
+                            for (int j = 0; j < k + nd; ++j) {
+                                const uint32_t wd = j < 2 ? h >> (16 + 8 * j)
+                                                          : sp[c0 + c + 1 + (j - 2) / 4] >> (8 * ((j - 2) % 4));
+                                rows.push_back(int32_t(wd & 0xFF));
+                                if (rows.back() >= plan->n) return bad("resident row out of range");
+                            }
+                            got.push_back({std::vector<int32_t>(rows.begin(), rows.begin() + k),
+                                           std::vector<int32_t>(rows.begin() + k, rows.end())});
+                            c += res_words(k, nd);
+                            nw = c0 + c;
+                        }
+                    }
+                    if (got != want) return bad("resident steps differ from the phases' steps");
+                    words[size_t(sg)] = nw;
+                }
+                for (int64_t i = 0; i < sd.nunits; ++i) {
+                    const ResUnit& u = sd.runits[size_t(i)];
+                    const int2 e = sd.tiles[size_t(i)];
+                    const size_t sg = size_t(e.x);
+                    const int64_t lo = sd.cuts[sg] + int64_t(e.y) * sd.tile_elems;
+                    const int64_t nv = std::min(sd.tile_elems, sd.cuts[sg + 1] - lo) / VEC;
+                    if (u.lo != lo || u.nv != nv || nv < 1 || nv > 64) return bad("resident unit tile");
+                    if (u.load != wload[sg] || u.store != wstore[sg]) return bad("resident unit rows");
+                    if (u.off != sd.rec_off[sg] || u.nw < words[sg] ||
+                        int64_t(u.off) + u.nw > int64_t(sd.prog.size()))
+                        return bad("resident unit records");
                 }
             }
             // every step of the slice's phases lies inside the segments
@@ -665,6 +782,40 @@ AR_EXPORT ar_status ar_debug_exec_steps(ar_plan* plan, int64_t step_cap, int32_t
     }
 }
 
+AR_EXPORT ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* info,
+                                      int64_t* units, uint32_t* prog) {
+    clear_error();
+    if (!plan || !info) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    try {
+        const ExecState* ex = exec_state(*plan);
+        if (stage < 0 || stage >= int32_t(ex->stages.size()) || ex->stages[size_t(stage)].slice < 0 ||
+            !ex->slices[size_t(ex->stages[size_t(stage)].slice)].resident)
+            return fail(AR_ERR_INVALID_ARG, "not a resident launch");
+        const SliceDesc& sd = ex->slices[size_t(ex->stages[size_t(stage)].slice)];
+        info[0] = sd.p0;
+        info[1] = sd.nphases;
+        info[2] = sd.nunits;
+        info[3] = int64_t(sd.prog.size());
+        if (units)
+            for (size_t i = 0; i < sd.runits.size(); ++i) {
+                const ResUnit& u = sd.runits[i];
+                int64_t* o = units + 6 * i;
+                o[0] = u.lo;
+                o[1] = int64_t(u.load);
+                o[2] = int64_t(u.store);
+                o[3] = u.nv;
+                o[4] = u.off;
+                o[5] = u.nw;
+            }
+        if (prog) std::copy(sd.prog.begin(), sd.prog.end(), prog);
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}
+
 AR_EXPORT ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value) {
     clear_error();
     if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
@@ -675,6 +826,9 @@ AR_EXPORT ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t va
     } else if (option == AR_OPT_SLICE) {
         if (value < 0 || value > 2) return fail(AR_ERR_INVALID_ARG, "AR_OPT_SLICE takes 0, 1 or 2");
         field = &plan->slice;
+    } else if (option == AR_OPT_RESIDENT) {
+        if (value != 0 && value != 1) return fail(AR_ERR_INVALID_ARG, "AR_OPT_RESIDENT takes 0 or 1");
+        field = &plan->resident;
     } else {
         return fail(AR_ERR_INVALID_ARG, "unknown option");
     }
@@ -711,11 +865,11 @@ AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t*
         const Stage stg = ex->stages[size_t(i)];
         if (stg.slice >= 0) {
             const SliceDesc& sd = ex->slices[size_t(stg.slice)];
-            if (phase) *phase = -1;
+            if (phase) *phase = sd.resident ? -2 : -1;
             if (nsrc) *nsrc = sd.max_k;
             if (max_dst) *max_dst = sd.max_dst;
             if (num_steps) *num_steps = sd.nsteps;
-            if (bytes) *bytes = sd.bytes;
+            if (bytes) *bytes = sd.resident ? sd.res_bytes : sd.bytes;
             return AR_OK;
         }
         const LaunchDesc& L = ex->launches[size_t(stg.launch)];

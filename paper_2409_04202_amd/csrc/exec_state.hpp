@@ -63,6 +63,27 @@ constexpr double kStepNsPerSrcBF16 = 190.0;
 constexpr double kStepNsPerDst = 15.0;
 constexpr double kMinSliceWaves = 256.0;
 constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
+// A sliced run may instead run resident (resident_kernel, AR_OPT_RESIDENT):
+// a wave per 64 vectors of a segment, the plan's n <= kResMaxN buffers in
+// LDS rows of 1 KiB.  Its predicted time is kLaunchNs plus the larger of its
+// HBM traffic (each row read and written once) at kBytesPerNs and its waves'
+// time: per wave kResWaveNs, kResRowNs per row loaded or stored, and per
+// step of its chain kResFastNs for a one-word record (two sources or a copy,
+// one destination) or kResStepNs + k * kResStepNsPerSrc + d *
+// kResStepNsPerDst otherwise; waves run kResWavesPerCU per compute unit at a
+// time, or fewer when their LDS rows do not fit (kLdsBytesPerCU), and waves
+// sharing a unit slow each other by kResShare per extra wave.  Fitted to
+// MI355X measurements of chains of 2-source steps, Ring and tree plans.
+constexpr double kResWaveNs = 1250.0;
+constexpr double kResRowNs = 60.0;
+constexpr double kResFastNs = 210.0;
+constexpr double kResStepNs = 150.0;
+constexpr double kResStepNsPerSrc = 80.0;
+constexpr double kResStepNsPerDst = 20.0;
+constexpr double kResShare = 0.1;
+constexpr int64_t kResWavesPerCU = 16;
+constexpr int64_t kLdsBytesPerCU = int64_t(160) << 10;
+constexpr int64_t kNumCUs = 256;
 
 struct LaunchDesc {
     int32_t phase;
@@ -100,6 +121,8 @@ struct DevState {
     int32_t* sched_off = nullptr;
     int32_t* sched = nullptr;
     int2* stiles = nullptr;
+    ResUnit* runits = nullptr;   // resident units and records, all slices concatenated
+    uint32_t* prog = nullptr;
     PtrEntry cache[kCache];
     uint64_t clock = 0;
 };
@@ -135,6 +158,16 @@ struct SliceDesc {
     std::vector<int2> tiles;
     // offsets of this slice's tables in the concatenated device tables
     int64_t cuts_base = 0, soff_base = 0, sched_base = 0, tiles_base = 0;
+    // resident form (resident_kernel): one ResUnit per wave and, per
+    // segment, its step records in `prog` (rec_off[s]: first word, -1 for a
+    // segment no step covers); `tiles` and `tile_elems` are then the
+    // resident kernel's tiles (one vector per lane), unit i = tiles[i]
+    bool resident = false;
+    std::vector<ResUnit> runits;
+    std::vector<uint32_t> prog;
+    std::vector<int32_t> rec_off;
+    int64_t runit_base = 0, prog_base = 0;
+    int64_t res_bytes = 0;       // bytes the resident launch loads and stores
 };
 
 // One launch of an execution: a sliced launch (slice >= 0) or the phase
@@ -152,7 +185,8 @@ struct ExecState {
     std::vector<int2> htiles;
     std::vector<std::vector<int32_t>> dev_of;  // [phase][step] -> hsteps index
     std::vector<int64_t> rec_of; // hsteps index -> first word of its record
-    int64_t rec_words = 0;       // words of all records
+    int64_t rec_words = 0;       // words of all records; the n buffer
+                                 // pointers follow them (resident launches)
     std::vector<SliceDesc> slices;
     std::vector<Stage> stages;   // the launches for 16-byte aligned buffers
     std::vector<DevState*> dev;  // indexed by device ordinal

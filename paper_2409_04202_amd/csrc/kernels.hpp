@@ -78,6 +78,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // (vector memory counter only) instead of flat instructions.
 #define AR_GLOBAL __attribute__((address_space(1)))
 typedef AR_GLOBAL u32x4 gvec;
+#define AR_LDS __attribute__((address_space(3)))
 
 template <class T>
 __device__ __forceinline__ AR_GLOBAL T* as_global(void* p) {
@@ -536,6 +537,173 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
                         fold_vectors_rt<DT, kSliceU, 0, false>(sp, st.k, dst, v0, 0, nv, lane);
                 }
             }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------
+// Resident sliced kernel: the same runs of phases, with the element
+// positions a wave owns kept on chip for the whole run.  A wavefront owns up
+// to one 16-byte vector per lane inside one segment and holds it, for every
+// buffer, in a 1 KiB LDS row (row b, lane l at rows[b * 64 + l]).  It loads
+// the rows the run reads before writing them (global_load_lds_dwordx4:
+// straight into LDS, all in flight at once), runs the steps of every phase
+// of the run on the rows, then stores the rows the run wrote.  A phase costs
+// a few LDS accesses instead of a round trip through the memory hierarchy,
+// and each buffer position is read and written once per run.  A lane only
+// touches its own row entries: no barrier.
+//
+// Each wave reads one ResUnit: its tile, the rows to load and to store (bit
+// b = buffer b), and where its segment's step records start.  The records
+// are the steps of the run's phases covering the segment, in phase order;
+// steps of one phase touch disjoint positions written by others (the phases
+// are hazard-free), so running them one after the other per lane gives the
+// phase's result.  Records (32-bit words, first byte the opcode):
+//  * kResAdd2 | r0 << 8 | r1 << 16 | d << 24: d = r0 + r1 (fold order r0, r1);
+//  * kResCopy | r0 << 8 | r0 << 16 | d << 24: d = r0;
+//  * otherwise a header k | nd << 8 | r0 << 16 | r1 << 24 (1 <= k <= 64)
+//    followed by ceil((k + nd - 2) / 4) words of four row bytes each (row
+//    j >= 2 in byte (j - 2) % 4 of word 1 + (j - 2) / 4): rows 0..k-1 are the
+//    sources in fold order, rows k..k+nd-1 the destinations.
+// The records are read 64 words at a time (one word per lane, broadcast with
+// v_readlane; the next chunk is loaded while one is run), so no record
+// straddles a 64-word chunk; a word 0 ends a chunk early.  The one-word
+// records run pipelined: the previous record's result stays in registers
+// (a read of the row it wrote takes it from there), so the next record's LDS
+// reads go out before the previous result is written to LDS.
+constexpr int kResMaxN = 64;  // buffers of a plan the resident kernel takes
+
+struct ResUnit {
+    int64_t lo;      // first element of the tile
+    uint64_t load;   // rows to load
+    uint64_t store;  // rows to store
+    int32_t nv;      // 16-byte vectors in the tile, 1..64
+    int32_t off;     // first word of the segment's step records
+    int32_t nw;      // words of step records (chunk padding included)
+    int32_t pad;
+};
+
+constexpr uint32_t kResAdd2 = 0xFE;
+constexpr uint32_t kResCopy = 0xFD;
+
+// words of a record with k sources and nd destinations
+__host__ __device__ constexpr int res_words(int k, int nd) {
+    return (k == 2 || k == 1) && nd == 1 ? 1 : 1 + (k + nd > 2 ? (k + nd - 2 + 3) / 4 : 0);
+}
+
+// row j of the record whose header h sits at chunk word c (w: the chunk, one
+// word per lane)
+__device__ __forceinline__ int res_row(uint32_t w, uint32_t h, int c, int j) {
+    if (j < 2) return int((h >> (16 + 8 * j)) & 0xFFu);
+    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + ((j - 2) >> 2)));
+    return int((x >> (8 * ((j - 2) & 3))) & 0xFFu);
+}
+
+template <int DT>
+__global__ __launch_bounds__(64) void resident_kernel(
+    const uint64_t* __restrict__ bufs, int32_t n, const ResUnit* __restrict__ units,
+    const uint32_t* __restrict__ prog, int64_t nunits) {
+    extern __shared__ u32x4 rows[];
+    constexpr int VEC = Elem<DT>::VEC;
+    const int lane = int(threadIdx.x);
+    const int64_t unit = int64_t(blockIdx.x);
+    if (unit >= nunits) return;
+    const ResUnit u = units[unit];
+    const bool act = lane < u.nv;
+    // lanes past the tile's end read the tile's first vector and store nothing
+    const int64_t v = u.lo / VEC + (act ? lane : 0);
+    const uint32_t* sp = prog + u.off;
+    uint32_t w = lane < u.nw ? sp[lane] : 0u;  // first chunk of step records
+    const uint64_t mine = lane < n ? bufs[lane] : 0;
+    const uint32_t plo = uint32_t(mine), phi = uint32_t(mine >> 32);
+    // the pointers (and the first records) have arrived: the row loads
+    // below then go out back to back, with no wait between them
+    __builtin_amdgcn_s_waitcnt(0);
+    auto at = [&](int b) {
+        const uint64_t a =
+            (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(phi), b))) << 32) |
+            uint32_t(__builtin_amdgcn_readlane(int(plo), b));
+        return reinterpret_cast<gvec*>(a) + v;
+    };
+    for (uint64_t m = u.load; m; m &= m - 1) {
+        const int b = __builtin_ctzll(m);
+        __builtin_amdgcn_global_load_lds((const AR_GLOBAL void*)(at(b)),
+                                         (AR_LDS void*)(rows + b * 64), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    u32x4 last = {0u, 0u, 0u, 0u};  // result of the previous one-word record
+    int last_row = -1;               // the row it went to (-1: none)
+    for (int c0 = 0; c0 < u.nw; c0 += 64) {
+        const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
+        const int m = min(64, u.nw - c0);
+        int c = 0;
+        uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(w), 0));
+        u32x4 pa = last, pb = last;  // LDS reads issued for a one-word record
+        auto issue = [&]() {
+            const uint32_t op = h & 0xFFu;
+            if (op == kResAdd2 || op == kResCopy) {
+                pa = rows[int((h >> 8) & 0xFFu) * 64 + lane];
+                pb = rows[int((h >> 16) & 0xFFu) * 64 + lane];
+            }
+        };
+        issue();
+        while (c < m) {
+            const uint32_t op = h & 0xFFu;
+            if (op == 0) break;
+            if (op == kResAdd2 || op == kResCopy) {
+                const int r0 = int((h >> 8) & 0xFFu), r1 = int((h >> 16) & 0xFFu);
+                const int d = int(h >> 24);
+                const u32x4 a = r0 == last_row ? last : pa;
+                u32x4 out = a;
+                if (op == kResAdd2) {
+                    const u32x4 b = r1 == last_row ? last : pb;
+                    VAcc<DT> acc;
+                    acc.init(a);
+                    acc.add(b);
+                    out = acc.out();
+                }
+                c += 1;
+                h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                issue();  // the next record's reads, before this write
+                rows[d * 64 + lane] = out;
+                last = out;
+                last_row = d;
+            } else {
+                const int k = int(op), nd = int((h >> 8) & 0xFFu);
+                u32x4 out;
+                if (k == 1) {
+                    out = rows[res_row(w, h, c, 0) * 64 + lane];
+                } else {
+                    VAcc<DT> acc;
+                    acc.init(rows[res_row(w, h, c, 0) * 64 + lane]);
+                    for (int j = 1; j < k; ++j) acc.add(rows[res_row(w, h, c, j) * 64 + lane]);
+                    out = acc.out();
+                }
+                // `out` has arrived; the stores below then go out back to back
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only
+                for (int j = 0; j < nd; ++j) rows[res_row(w, h, c, k + j) * 64 + lane] = out;
+                last_row = -1;
+                c += res_words(k, nd);
+                h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                issue();
+            }
+        }
+        w = wn;
+    }
+    uint64_t m = u.store;
+    while (m) {
+        int b[8];
+        u32x4 x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            b[j] = m ? __builtin_ctzll(m) : -1;
+            m &= m - 1;
+            if (b[j] >= 0) x[j] = rows[b[j] * 64 + lane];
+        }
+        if (act) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (b[j] >= 0) *at(b[j]) = x[j];
         }
     }
 }

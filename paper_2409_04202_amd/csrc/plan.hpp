@@ -39,6 +39,7 @@ struct Plan {
     std::vector<int64_t> owner_end;
     int32_t fuse = 1;   // AR_OPT_FUSE
     int32_t slice = 2;  // AR_OPT_SLICE: 0 never, 1 always (if possible), 2 auto
+    int32_t resident = 1;  // AR_OPT_RESIDENT: sliced runs may keep their state in LDS
     ExecState* exec = nullptr;  // executor cache, built on first use
 
     int32_t num_phases() const {

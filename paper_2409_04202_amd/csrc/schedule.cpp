@@ -2,6 +2,7 @@
 // source count, tiled, cache mode chosen) and sliced runs (chosen by a cost
 // model).  Host only.
 #include <algorithm>
+#include <cmath>
 #include <map>
 #include <memory>
 #include <tuple>
@@ -222,6 +223,95 @@ static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int
     return sd;
 }
 
+// The resident form of sliced run `sd` (resident_kernel): per segment some
+// step covers, the records of the steps covering it in phase order, the
+// buffers whose first touch in the run reads them and the buffers the run
+// writes there; one unit per 64 vectors of such a segment.  Leaves `sd` in
+// its plain form when the plan has more than kResMaxN buffers or a table
+// would overflow.
+static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
+    if (p.n > kResMaxN || sd.nseg < 1) return;
+    const int64_t VEC = 16 / p.esize;
+    const size_t nseg = size_t(sd.nseg);
+    auto seg_of = [&](int64_t x) {
+        return size_t(std::lower_bound(sd.cuts.begin(), sd.cuts.end(), x) - sd.cuts.begin());
+    };
+    std::vector<std::vector<uint32_t>> recs(nseg);
+    // per segment: buffers touched, read before any write, written
+    std::vector<uint64_t> seen(nseg, 0), load(nseg, 0), store(nseg, 0);
+    std::vector<uint32_t> rec;
+    for (int32_t q = sd.p0; q < sd.p0 + sd.nphases; ++q) {
+        for (const XStep& x : ex.phases[size_t(q)].steps) {
+            if (x.end <= x.begin) continue;
+            const int k = int(x.srcs.size()), nd = int(x.dsts.size());
+            if (k < 1 || nd < 1 || k > kResMaxN || nd > 255 || res_words(k, nd) > 64) return;
+            std::vector<int32_t> r(x.srcs);
+            r.insert(r.end(), x.dsts.begin(), x.dsts.end());
+            rec.assign(size_t(res_words(k, nd)), 0u);
+            if (k == 2 && nd == 1) {
+                rec[0] = kResAdd2 | uint32_t(r[0]) << 8 | uint32_t(r[1]) << 16 | uint32_t(r[2]) << 24;
+            } else if (k == 1 && nd == 1) {
+                rec[0] = kResCopy | uint32_t(r[0]) << 8 | uint32_t(r[0]) << 16 | uint32_t(r[1]) << 24;
+            } else {
+                rec[0] = uint32_t(k) | uint32_t(nd) << 8;
+                for (size_t j = 0; j < r.size(); ++j) {
+                    const uint32_t b = uint32_t(r[j]);
+                    if (j < 2) rec[0] |= b << (16 + 8 * j);
+                    else rec[1 + (j - 2) / 4] |= b << (8 * ((j - 2) % 4));
+                }
+            }
+            uint64_t rd = 0, wr = 0;
+            for (int32_t b : x.srcs) rd |= uint64_t(1) << b;
+            for (int32_t b : x.dsts) wr |= uint64_t(1) << b;
+            for (size_t sg = seg_of(x.begin); sg < seg_of(x.end); ++sg) {
+                load[sg] |= rd & ~seen[sg];
+                seen[sg] |= rd | wr;
+                store[sg] |= wr;
+                std::vector<uint32_t>& w = recs[sg];
+                if (w.size() % 64 + rec.size() > 64) w.resize((w.size() + 63) / 64 * 64, 0u);
+                w.insert(w.end(), rec.begin(), rec.end());
+            }
+        }
+    }
+    std::vector<uint32_t> prog;
+    std::vector<int32_t> rec_off(nseg, -1);
+    for (size_t sg = 0; sg < nseg; ++sg) {
+        if (recs[sg].empty()) continue;
+        rec_off[sg] = int32_t(prog.size());
+        prog.insert(prog.end(), recs[sg].begin(), recs[sg].end());
+        if (prog.size() > size_t(INT32_MAX)) return;
+    }
+    const int64_t te = int64_t(64) * VEC;
+    std::vector<int2> tiles;
+    std::vector<ResUnit> units;
+    int64_t bytes = 0;
+    for (size_t sg = 0; sg < nseg; ++sg) {
+        if (recs[sg].empty()) continue;
+        const int64_t len = sd.cuts[sg + 1] - sd.cuts[sg];
+        bytes += int64_t(__builtin_popcountll(load[sg]) + __builtin_popcountll(store[sg])) * len * p.esize;
+        for (int64_t t = 0; t * te < len; ++t) {
+            tiles.push_back(make_int2(int(sg), int(t)));
+            ResUnit u{};
+            u.lo = sd.cuts[sg] + t * te;
+            u.load = load[sg];
+            u.store = store[sg];
+            u.nv = int32_t(std::min(te, sd.cuts[sg + 1] - u.lo) / VEC);
+            u.off = rec_off[sg];
+            u.nw = int32_t(recs[sg].size());
+            units.push_back(u);
+        }
+    }
+    if (units.empty() || int64_t(units.size()) > kMaxBlocks) return;
+    sd.resident = true;
+    sd.runits = std::move(units);
+    sd.prog = std::move(prog);
+    sd.rec_off = std::move(rec_off);
+    sd.tiles = std::move(tiles);
+    sd.tile_elems = te;
+    sd.nunits = int64_t(sd.tiles.size());
+    sd.res_bytes = bytes;
+}
+
 // Per executed phase, what the choice of sliced runs needs: whether every
 // step boundary is 16-byte aligned, the bytes written and moved, the most
 // steps covering one element position, and the predicted phase-launch time.
@@ -229,6 +319,7 @@ struct PhaseCost {
     bool aligned = true;
     int64_t written = 0, read = 0, bytes = 0, cover = 0;
     int32_t kmax = 0, dmax = 0;
+    uint64_t touched = 0;  // buffers the phase touches (n <= kResMaxN)
     double t_launch = 0.0;
 };
 
@@ -246,6 +337,10 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
             pc[q].kmax = std::max(pc[q].kmax, int32_t(x.srcs.size()));
             pc[q].dmax = std::max(pc[q].dmax, int32_t(x.dsts.size()));
             pc[q].bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * len * p.esize;
+            if (p.n <= kResMaxN) {
+                for (int32_t b : x.srcs) pc[q].touched |= uint64_t(1) << b;
+                for (int32_t b : x.dsts) pc[q].touched |= uint64_t(1) << b;
+            }
             ev.emplace_back(x.begin, 1);
             ev.emplace_back(x.end, -1);
         }
@@ -263,42 +358,74 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
 
 // Sliced runs for AR_OPT_SLICE = 2: phases [a, b), each aligned, writing at
 // most kKeepBytes and moving at most kSliceMaxBytes, chosen to minimise the
-// predicted time.  A run of one phase only pays off when it replaces
-// several launches.
-static std::vector<std::pair<int32_t, int32_t>> choose_runs(const Plan& p, const ExecState& ex,
-                                                            const std::vector<PhaseCost>& pc) {
+// predicted time, each in its plain or (AR_OPT_RESIDENT, n <= kResMaxN) its
+// resident form, whichever is predicted faster.  A run of one phase only
+// pays off when it replaces several launches.
+struct Run {
+    int32_t a, b;
+    bool resident;
+};
+
+static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
+                                    const std::vector<PhaseCost>& pc) {
     const double per_src = p.dtype == AR_BF16 ? kStepNsPerSrcBF16 : kStepNsPerSrcF32;
     const double waves = std::max(1.0, double(p.N) * p.esize / (64.0 * kSliceU * 16.0));
     const double stretch = std::max(1.0, kMinSliceWaves / waves);
+    const bool res_ok = p.resident != 0 && p.n <= kResMaxN;
+    // resident waves (one vector per lane) and how many run at once
+    const double res_waves = std::max(1.0, double(p.N) * p.esize / (64.0 * 16.0));
+    const int64_t per_cu = std::max<int64_t>(
+        1, std::min<int64_t>(kResWavesPerCU, kLdsBytesPerCU / (int64_t(p.n) * 1024)));
+    const double rounds = std::ceil(res_waves / double(kNumCUs * per_cu)) *
+                          (1.0 + kResShare * double(per_cu - 1));
     const int32_t P = int32_t(pc.size());
     std::vector<int32_t> nl(size_t(P), 0);
     for (const LaunchDesc& L : ex.launches) ++nl[size_t(L.xphase)];
     std::vector<double> best(size_t(P) + 1, 0.0);
     std::vector<int32_t> from(size_t(P) + 1, -1);  // -1: phase launches for phase b - 1
+    std::vector<char> res_of(size_t(P) + 1, 0);
     for (int32_t b = 1; b <= P; ++b) {
         best[size_t(b)] = best[size_t(b) - 1] + pc[size_t(b) - 1].t_launch;
         from[size_t(b)] = -1;
-        double body = 0.0;
+        double body = 0.0, chain = 0.0;
+        uint64_t touched = 0;
         for (int32_t a = b - 1; a >= 0; --a) {
             const PhaseCost& c = pc[size_t(a)];
             if (!c.aligned || c.written > kKeepBytes || c.bytes > kSliceMaxBytes) break;
             body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
                               stretch * double(c.read) / kBytesPerNs,
                               double(c.written) / kBytesPerNs});
+            chain += double(c.cover) *
+                     (c.kmax <= 2 && c.dmax == 1
+                          ? kResFastNs
+                          : kResStepNs + kResStepNsPerSrc * c.kmax + kResStepNsPerDst * c.dmax);
+            touched |= c.touched;
             if (b - a == 1 && nl[size_t(a)] < 2) continue;
-            const double t = kLaunchNs + body;
+            double t = kLaunchNs + body;
+            bool res = false;
+            if (res_ok) {
+                const double rows = 2.0 * double(__builtin_popcountll(touched));
+                const double t_res =
+                    kLaunchNs + std::max(rounds * (kResWaveNs + kResRowNs * rows + chain),
+                                         rows * double(p.N) * p.esize / kBytesPerNs);
+                if (t_res < t) {
+                    t = t_res;
+                    res = true;
+                }
+            }
             if (best[size_t(a)] + t < best[size_t(b)]) {
                 best[size_t(b)] = best[size_t(a)] + t;
                 from[size_t(b)] = a;
+                res_of[size_t(b)] = res;
             }
         }
     }
-    std::vector<std::pair<int32_t, int32_t>> runs;
+    std::vector<Run> runs;
     for (int32_t b = P; b > 0;) {
         if (from[size_t(b)] < 0) {
             --b;
         } else {
-            runs.emplace_back(from[size_t(b)], b);
+            runs.push_back({from[size_t(b)], b, res_of[size_t(b)] != 0});
             b = from[size_t(b)];
         }
     }
@@ -312,16 +439,17 @@ ExecState* exec_state(Plan& p) {
         try {
             ex->phases = exec_phases(p, p.fuse != 0);
             build_launches(p, *ex);
-            std::vector<std::pair<int32_t, int32_t>> runs;
+            std::vector<Run> runs;
             if (p.slice == 1 && !ex->phases.empty()) {
-                runs.emplace_back(0, int32_t(ex->phases.size()));
+                runs.push_back({0, int32_t(ex->phases.size()), p.resident != 0});
             } else if (p.slice == 2) {
                 runs = choose_runs(p, *ex, phase_costs(p, *ex));
             }
             std::vector<int32_t> slice_of(ex->phases.size(), -1);
-            for (const auto& r : runs) {
-                SliceDesc sd = build_slice(p, *ex, r.first, r.second);
+            for (const Run& r : runs) {
+                SliceDesc sd = build_slice(p, *ex, r.a, r.b);
                 if (!sd.ok) continue;  // phase launches for these phases
+                if (r.resident) build_resident(p, *ex, sd);
                 sd.cuts_base = ex->slices.empty() ? 0
                                                   : ex->slices.back().cuts_base +
                                                         int64_t(ex->slices.back().cuts.size());
@@ -334,7 +462,13 @@ ExecState* exec_state(Plan& p) {
                 sd.tiles_base = ex->slices.empty() ? 0
                                                    : ex->slices.back().tiles_base +
                                                          int64_t(ex->slices.back().tiles.size());
-                for (int32_t q = r.first; q < r.second; ++q)
+                sd.runit_base = ex->slices.empty() ? 0
+                                                   : ex->slices.back().runit_base +
+                                                         int64_t(ex->slices.back().runits.size());
+                sd.prog_base = ex->slices.empty() ? 0
+                                                  : ex->slices.back().prog_base +
+                                                        int64_t(ex->slices.back().prog.size());
+                for (int32_t q = r.a; q < r.b; ++q)
                     slice_of[size_t(q)] = int32_t(ex->slices.size());
                 ex->slices.push_back(std::move(sd));
             }

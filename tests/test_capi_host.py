@@ -356,17 +356,28 @@ def test_whole_plan_launch_schedule(kind, n, N, fan, dtype):
         off = oracle.block_bounds(N, n)
         vec = 16 // (4 if dtype == "f32" else 2)
         aligned = all(o % vec == 0 for o in off)
+        # plans of at most 64 buffers run resident (-2) unless that is off
+        marker = -2 if n <= 64 else -1
         L = p.launches()
         if p.num_phases:
-            sliced = len(L) == 1 and L[0][0] == -1
+            sliced = len(L) == 1 and L[0][0] == marker
             assert sliced == aligned, (L, aligned)
-        for fuse in (1, 0):
-            p.set_option(arplan.AR_OPT_FUSE, fuse)
-            st, msg = _check_tiling(p.handle, 1)
-            assert st == arplan.AR_OK, msg
+        for res in (1, 0):
+            p.set_option(arplan.AR_OPT_RESIDENT, res)
+            for fuse in (1, 0):
+                p.set_option(arplan.AR_OPT_FUSE, fuse)
+                st, msg = _check_tiling(p.handle, 1)
+                assert st == arplan.AR_OK, msg
+        p.set_option(arplan.AR_OPT_FUSE, 1)
         if aligned and p.num_phases:
             (ph, k, d, cnt, b), = p.launches()
             assert ph == -1
+            p.set_option(arplan.AR_OPT_RESIDENT, 1)
+            (ph, k, d, cnt, b2), = p.launches()
+            assert ph == marker
+            # resident: every buffer position loaded once and stored once
+            esize = 4 if dtype == "f32" else 2
+            assert b2 == (2 * n * N * esize if marker == -2 else b)
             p.set_option(arplan.AR_OPT_SLICE, 0)
             assert b == sum(x[4] for x in p.launches())
 
@@ -466,12 +477,19 @@ def test_sliced_runs_of_workloads(name):
     # 2 GiB RHD plan, whose phases each write more than the 256 MiB cache
     from paper_2409_04202_amd import workloads
     c = workloads.CONFIGS[name]
+    esize = 2 if c["dtype"] == "bf16" else 4
     with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
         L = p.launches()
         p.set_option(arplan.AR_OPT_SLICE, 0)
         L0 = p.launches()
-        assert sum(x[4] for x in L) == sum(x[4] for x in L0)
         assert sum(x[3] for x in L) == sum(x[3] for x in L0)
+        # a resident launch moves each buffer position of its run at most
+        # once in and once out; the plain forms move the steps' bytes
+        assert all(x[4] <= 2 * c["n"] * c["N"] * esize for x in L if x[0] == -2)
+        p.set_option(arplan.AR_OPT_RESIDENT, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 2)
+        assert sum(x[4] for x in p.launches()) == sum(x[4] for x in L0)
+        p.set_option(arplan.AR_OPT_RESIDENT, 1)
         # phase launches kept outside the runs appear in phase order
         kept = [x for x in L if x[0] >= 0]
         assert all(x in L0 for x in kept)
@@ -488,4 +506,4 @@ def test_sliced_runs_of_workloads(name):
             assert L[-1][0] == 5
         if name.startswith("sweep_ring"):
             # 126 phases of short steps: one sliced launch
-            assert len(L) == 1 and L[0][0] == -1
+            assert len(L) == 1 and L[0][0] in (-1, -2)

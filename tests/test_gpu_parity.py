@@ -31,9 +31,10 @@ def _oracle_plan(kind, n, N, fan):
 
 
 def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
-                  pad=0, xs0=None, fuse=1, slice_=2):
-    say("case: %s n=%d N=%d %s fan=%s pad=%d fuse=%d slice=%d" % (
-        kind, n, N, dtype, fan if kind != "gentree" else len(fan), pad, fuse, slice_))
+                  pad=0, xs0=None, fuse=1, slice_=2, resident=1):
+    say("case: %s n=%d N=%d %s fan=%s pad=%d fuse=%d slice=%d resident=%d" % (
+        kind, n, N, dtype, fan if kind != "gentree" else len(fan), pad, fuse, slice_,
+        resident))
     if xs0 is None:
         xs0 = workloads.draw(n, N, dtype, dist, seed)
     ref = oracle.execute(_oracle_plan(kind, n, N, fan), [x.copy() for x in xs0], dtype)
@@ -41,6 +42,7 @@ def _full_compare(kind, n, N, dtype, fan=None, dist="uniform", seed=1,
     with arplan.Plan(n, N, dtype, kind, fan) as p:
         p.set_option(arplan.AR_OPT_FUSE, fuse)
         p.set_option(arplan.AR_OPT_SLICE, slice_)
+        p.set_option(arplan.AR_OPT_RESIDENT, resident)
         run_plan(p, ts)
     got = to_host(ts, dtype)
     for q in range(n):
@@ -81,25 +83,28 @@ SCALED = [("rhd", 8, (1 << 20) + 13, "f32", None, "uniform"),
           ("rb", 6, 100003, "f32", None, "uniform")]
 
 
-MODES = [(1, 2), (0, 0), (1, 1), (0, 1)]   # (AR_OPT_FUSE, AR_OPT_SLICE)
+# (AR_OPT_FUSE, AR_OPT_SLICE, AR_OPT_RESIDENT); whole-plan sliced launches
+# run resident for n <= 64 unless resident is 0
+MODES = [(1, 2, 1), (0, 0, 1), (1, 1, 1), (0, 1, 1), (1, 1, 0), (0, 2, 0)]
 
 
-@pytest.mark.parametrize("fuse,slice_", MODES)
+@pytest.mark.parametrize("fuse,slice_,resident", MODES)
 @pytest.mark.parametrize("kind,n,N,dtype,fan,dist", SCALED)
-def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist, fuse, slice_):
+def test_scaled_configs_bit_exact(kind, n, N, dtype, fan, dist, fuse, slice_, resident):
     got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=5, fuse=fuse,
-                             slice_=slice_)
+                             slice_=slice_, resident=resident)
     if dtype == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
-@pytest.mark.parametrize("slice_", [2, 1, 0])
+@pytest.mark.parametrize("slice_,resident", [(2, 1), (1, 1), (2, 0), (1, 0), (0, 1)])
 @pytest.mark.parametrize("name", sorted(k for k in workloads.CONFIGS
                                         if k.startswith("sweep_")))
-def test_sweep_configs_bit_exact(name, slice_):
+def test_sweep_configs_bit_exact(name, slice_, resident):
     c = workloads.CONFIGS[name]
     got, xs0 = _full_compare(c["kind"], c["n"], c["N"], c["dtype"],
-                             c["fanin"], c["dist"], c["seed"], slice_=slice_)
+                             c["fanin"], c["dist"], c["seed"], slice_=slice_,
+                             resident=resident)
     if c["dtype"] == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
@@ -122,7 +127,7 @@ def test_sliced_runs_between_phase_launches():
     for kind, n, N, dtype, fan in _MIXED_CANDIDATES:
         with arplan.Plan(n, N, dtype, kind, fan) as p:
             ph = [x[0] for x in p.launches()]
-        if -1 in ph and any(x >= 0 for x in ph):
+        if any(x < 0 for x in ph) and any(x >= 0 for x in ph):
             mixed.append((kind, n, N, dtype, fan))
     assert len(mixed) >= 2, mixed
     for kind, n, N, dtype, fan in mixed[:3]:
@@ -182,8 +187,9 @@ def test_full_size_configs(name):
 def test_ragged_and_tiny_sizes(kind, n, fan, dtype):
     for N in (1, n - 1, n, n + 1, 2 * n + 3, 4099, 64 * n):
         dist = "int1000" if dtype == "i32" else "uniform"
-        for fuse, sl in MODES:
-            _full_compare(kind, n, N, dtype, fan, dist, seed=N, fuse=fuse, slice_=sl)
+        for fuse, sl, res in MODES:
+            _full_compare(kind, n, N, dtype, fan, dist, seed=N, fuse=fuse, slice_=sl,
+                          resident=res)
 
 
 def test_empty_buffers_are_a_no_op():
@@ -197,20 +203,22 @@ def test_empty_buffers_are_a_no_op():
                                        ("bf16", 1), ("bf16", 5)])
 def test_unaligned_buffers(dtype, pad):
     dist = "int1000" if dtype == "i32" else "uniform"
-    for fuse, sl in MODES:
-        _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, pad=pad, fuse=fuse, slice_=sl)
-        _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, pad=pad, fuse=fuse, slice_=sl)
-        _full_compare("cps", 5, 3001, dtype, None, dist, seed=6, pad=pad, fuse=fuse, slice_=sl)
-        _full_compare("ring", 4, 4096, dtype, None, dist, seed=7, pad=pad, fuse=fuse, slice_=sl)
+    for fuse, sl, res in MODES:
+        kw = dict(pad=pad, fuse=fuse, slice_=sl, resident=res)
+        _full_compare("tree", 8, 10007, dtype, (4, 2), dist, seed=3, **kw)
+        _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, **kw)
+        _full_compare("cps", 5, 3001, dtype, None, dist, seed=6, **kw)
+        _full_compare("ring", 4, 4096, dtype, None, dist, seed=7, **kw)
 
 
 @pytest.mark.parametrize("n", [3, 5, 16, 32])
 def test_source_counts(n):
     # k = 3 and 16 have unrolled kernels, 5 and 32 use the runtime loop
     for dtype in ("f32", "bf16"):
-        for fuse, sl in MODES:
-            _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n, fuse=fuse, slice_=sl)
-            _full_compare("cps", n, 512 * n, dtype, None, "uniform", seed=n, fuse=fuse, slice_=sl)
+        for fuse, sl, res in MODES:
+            kw = dict(fuse=fuse, slice_=sl, resident=res)
+            _full_compare("cps", n, 50021, dtype, None, "uniform", seed=n, **kw)
+            _full_compare("cps", n, 512 * n, dtype, None, "uniform", seed=n, **kw)
 
 
 def test_fp32_denormals_are_kept():
@@ -261,12 +269,13 @@ def _bf16_rounding_inputs(seed):
     return a.astype(np.uint16), b.astype(np.uint16)
 
 
-@pytest.mark.parametrize("fuse,slice_", MODES)
-def test_bf16_rounding_every_exponent(fuse, slice_):
+@pytest.mark.parametrize("fuse,slice_,resident", MODES)
+def test_bf16_rounding_every_exponent(fuse, slice_, resident):
     a, b = _bf16_rounding_inputs(3)
     N = a.size - a.size % 8
     xs0 = [a[:N].copy(), b[:N].copy()]
-    got, _ = _full_compare("cps", 2, N, "bf16", xs0=xs0, fuse=fuse, slice_=slice_)
+    got, _ = _full_compare("cps", 2, N, "bf16", xs0=xs0, fuse=fuse, slice_=slice_,
+                           resident=resident)
     f = oracle.bf16_to_f32(got[0])
     assert np.isinf(f).any() and (np.abs(f[f != 0]) < 1.2e-38).any()
 
@@ -283,11 +292,12 @@ def test_bf16_nan_and_inf_inputs():
     xs0[0][::13] = 0x7F80                    # +inf
     xs0[3][::17] = 0xFF80                    # -inf
     ref = oracle.execute(oracle.cps(n, N), [x.copy() for x in xs0], "bf16")
-    for fuse, sl in MODES:
+    for fuse, sl, res in MODES:
         ts = to_device(xs0, "bf16")
         with arplan.Plan(n, N, "bf16", "cps") as p:
             p.set_option(arplan.AR_OPT_FUSE, fuse)
             p.set_option(arplan.AR_OPT_SLICE, sl)
+            p.set_option(arplan.AR_OPT_RESIDENT, res)
             run_plan(p, ts)
         got = to_host(ts, "bf16")
         for q in range(n):
@@ -314,13 +324,14 @@ def test_random_custom_plans(seed):
     xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", seed)
     ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
     say("case: random custom plan seed=%d n=%d N=%d %s phases=%d" % (seed, n, N, dtype, len(phases)))
-    for fuse, sl in MODES:
+    for fuse, sl, res in MODES:
         for pad in (0, 1):
             ts = to_device(xs0, dtype, pad)
             h = arplan.ar_plan_create_custom(n, N, dtype, flat)
             try:
                 arplan.ar_plan_set_option(h, arplan.AR_OPT_FUSE, fuse)
                 arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, sl)
+                arplan.ar_plan_set_option(h, arplan.AR_OPT_RESIDENT, res)
                 arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
                 torch.cuda.synchronize()
             finally:
@@ -328,6 +339,56 @@ def test_random_custom_plans(seed):
             got = to_host(ts, dtype)
             for q in range(n):
                 assert np.array_equal(got[q], ref[q]), (seed, fuse, sl, pad, q)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_aligned_custom_plans_resident(seed):
+    # random hazard-free plans whose boundaries are whole 16-byte vectors, so
+    # that the whole plan runs as one resident launch (ragged tiles, several
+    # 64-word program chunks); against the oracle and the plain sliced launch
+    from test_exec_rewrites_host import _random_plan
+    from oracle.plans import Plan as OPlan, Step as OStep
+    rng = np.random.default_rng(9500 + seed)
+    n = int(rng.integers(2, 7))
+    M = int(rng.integers(40, 3000))
+    phases = _random_plan(rng, n, M)
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    vec = 8 if dtype == "bf16" else 4
+    N = M * vec
+    flat = [(q, op, d, s, b * vec, e * vec)
+            for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref_plan = OPlan("custom", n, N, [[OStep(op, d, s, b * vec, e * vec)
+                                       for (op, d, s, b, e) in ph] for ph in phases])
+    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", seed)
+    ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
+    say("case: aligned custom plan seed=%d n=%d N=%d %s phases=%d" % (seed, n, N, dtype, len(phases)))
+    for res in (1, 0):
+        ts = to_device(xs0, dtype)
+        h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+        try:
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 1)
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_RESIDENT, res)
+            assert arplan.ar_plan_launch_info(h, 0)[0] == (-2 if res else -1)
+            arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+        finally:
+            arplan.ar_plan_destroy(h)
+        got = to_host(ts, dtype)
+        for q in range(n):
+            assert np.array_equal(got[q], ref[q]), (seed, res, q)
+
+
+@pytest.mark.parametrize("kind,n,fan", [("ring", 64, None), ("tree", 64, (8, 8)),
+                                        ("tree", 64, (4, 4, 4)), ("rhd", 32, None),
+                                        ("cps", 64, None), ("ring", 2, None)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+def test_whole_plan_resident_bit_exact(kind, n, fan, dtype):
+    # every built-in plan kind as one resident launch, at sizes with ragged
+    # last tiles per segment
+    vec = 8 if dtype == "bf16" else 4
+    dist = "int1000" if dtype == "i32" else "uniform"
+    for N in (n * vec, n * vec * 37, n * vec * 301):
+        _full_compare(kind, n, N, dtype, fan, dist, seed=N + n, slice_=1, resident=1)
 
 
 def test_custom_plan_mixed_sources_and_uneven_steps():
@@ -443,7 +504,8 @@ def test_runs_on_a_side_stream_in_order():
         assert np.array_equal(outs[q].numpy(), ref[q]), q
 
 
-def test_whole_plan_launch_with_timer_and_repeats():
+@pytest.mark.parametrize("resident", [1, 0])
+def test_whole_plan_launch_with_timer_and_repeats(resident):
     n, N = 64, 1 << 14
     xs0 = workloads.draw(n, N, "f32", "uniform", 15)
     plan_o = oracle.ring(n, N)
@@ -454,8 +516,9 @@ def test_whole_plan_launch_with_timer_and_repeats():
     try:
         with arplan.Plan(n, N, "f32", "ring") as p:
             p.set_option(arplan.AR_OPT_SLICE, 1)
+            p.set_option(arplan.AR_OPT_RESIDENT, resident)
             (ph, k, d, cnt, b), = p.launches()
-            assert ph == -1
+            assert ph == (-2 if resident else -1)
             p.execute_timed(ts, torch.cuda.current_stream(), t)
             torch.cuda.synchronize()
             got = to_host(ts, "f32")
@@ -483,14 +546,14 @@ def test_gentree_plans_bit_exact(counts, dtype):
     n = counts.count(0)
     dist = "int1000" if dtype == "i32" else "uniform"
     for N in (n, 64 * n, 64 * n + 5, 40000):
-        for fuse, sl in MODES:
+        for fuse, sl, res in MODES:
             _full_compare("gentree", n, N, dtype, counts, dist, seed=N, fuse=fuse,
-                          slice_=sl)
+                          slice_=sl, resident=res)
 
 
 @pytest.mark.parametrize("name", ["asy384_gentree_f32", "cdc384_gentree_f32"])
 def test_paper_asymmetric_topologies_scaled(name):
     c = workloads.CONFIGS[name]
-    for fuse, sl in MODES:
+    for fuse, sl, res in MODES:
         _full_compare("gentree", c["n"], 384 * 64 + 17, "f32", c["fanin"], seed=3,
-                      fuse=fuse, slice_=sl)
+                      fuse=fuse, slice_=sl, resident=res)

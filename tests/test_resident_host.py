@@ -1,0 +1,180 @@
+"""Resident sliced launches, checked on the host (no GPU).
+
+A resident launch runs, per segment of element positions, a program the
+library builds on the host: the buffers to load into on-chip rows, the step
+records of the run's phases in phase order, the buffers to store back.  Here
+the programs are read back through the library's test hook and interpreted
+with numpy on random inputs: a row read before it was loaded or written is
+an error, the folds use the oracle's arithmetic, and the result must equal,
+bit for bit, the oracle's phase-by-phase run of the plan as written.  This
+pins the program semantics (which rows are loaded and stored, the step
+order, the record encoding) independently of the GPU.
+"""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.execute import fold
+from oracle.plans import Plan as OPlan, Step as OStep
+
+from paper_2409_04202_amd import arplan, workloads
+
+from test_exec_rewrites_host import _random_plan
+
+
+def _resident_tables(handle, stage):
+    f = arplan._lib.ar_debug_resident
+    I64 = ctypes.POINTER(ctypes.c_int64)
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int32, I64, I64, ctypes.POINTER(ctypes.c_uint32)]
+    f.restype = ctypes.c_int32
+    info = (ctypes.c_int64 * 4)()
+    st = f(handle, stage, info, None, None)
+    if st != arplan.AR_OK:
+        return None
+    nunits, nw = info[2], info[3]
+    units = (ctypes.c_int64 * (6 * nunits))()
+    prog = (ctypes.c_uint32 * max(1, nw))()
+    assert f(handle, stage, info, units, prog) == arplan.AR_OK
+    return ([tuple(units[6 * i:6 * i + 6]) for i in range(nunits)],
+            np.array(prog[:nw], dtype=np.uint32))
+
+
+def _decode(words):
+    """Step records of one segment: [(srcs, dsts)], per the documented
+    encoding (one word 0xFE | r0 << 8 | r1 << 16 | d << 24 for d = r0 + r1,
+    0xFD | r0 << 8 | r0 << 16 | d << 24 for d = r0; otherwise a header
+    k | nd << 8 | r0 << 16 | r1 << 24, then four row bytes per word; 64-word
+    chunks, a zero word ends a chunk)."""
+    out = []
+    for c0 in range(0, len(words), 64):
+        chunk = [int(w) for w in words[c0:c0 + 64]]
+        c = 0
+        while c < len(chunk):
+            h = chunk[c]
+            if h & 0xFF in (0xFE, 0xFD):      # one-word add of two rows, copy
+                r0, r1, d = (h >> 8) & 0xFF, (h >> 16) & 0xFF, h >> 24
+                out.append(([r0, r1] if h & 0xFF == 0xFE else [r0], [d]))
+                c += 1
+                continue
+            k, nd = h & 0xFF, (h >> 8) & 0xFF
+            if k == 0:
+                assert not any(chunk[c:]), "padding must be zero"
+                break
+            rows = []
+            for j in range(k + nd):
+                w = h >> (16 + 8 * j) if j < 2 else \
+                    chunk[c + 1 + (j - 2) // 4] >> (8 * ((j - 2) % 4))
+                rows.append(w & 0xFF)
+            out.append((rows[:k], rows[k:]))
+            c += 1 + ((k + nd - 2 + 3) // 4 if k + nd > 2 else 0)
+    return out
+
+
+def _bits(mask):
+    mask &= (1 << 64) - 1
+    return [b for b in range(64) if mask >> b & 1]
+
+
+def _interpret(tables, bufs, dtype):
+    """Run every unit (wave) of a resident launch: its tile of every buffer
+    it loads becomes a row, the records run on the rows, the rows it stores
+    go back.  Units of one launch own disjoint positions."""
+    units, prog = tables
+    vec = 8 if dtype == "bf16" else 4
+    out = [b.copy() for b in bufs]
+    for lo, load, store, nv, off, nw in units:
+        hi = lo + nv * vec
+        rows = {}
+        for b in _bits(load):
+            rows[b] = bufs[b][lo:hi].copy()
+        for srcs, dsts in _decode(prog[off:off + nw]):
+            for s in srcs:
+                assert s in rows, "row %d read before it was loaded or written" % s
+            val = rows[srcs[0]].copy() if len(srcs) == 1 else \
+                fold(dtype, [rows[s] for s in srcs])
+            for d in dsts:
+                rows[d] = val.copy()
+        for b in _bits(store):
+            out[b][lo:hi] = rows[b]
+    return out
+
+
+def _check_whole_plan(handle, ref_plan, n, N, dtype, seed):
+    arplan.ar_plan_set_option(handle, arplan.AR_OPT_SLICE, 1)
+    assert arplan.ar_plan_num_launches(handle) == 1
+    assert arplan.ar_plan_launch_info(handle, 0)[0] == -2
+    tables = _resident_tables(handle, 0)
+    assert tables is not None
+    dist = "int1000" if dtype == "i32" else "uniform"
+    xs = workloads.draw(n, N, dtype, dist, seed)
+    want = oracle.execute(ref_plan, [x.copy() for x in xs], dtype)
+    got = _interpret(tables, [x.copy() for x in xs], dtype)
+    for q in range(n):
+        assert np.array_equal(got[q], want[q]), q
+
+
+BUILTIN = [("ring", n, None) for n in (2, 3, 4, 8)] + \
+          [("rhd", n, None) for n in (2, 4, 6, 8)] + \
+          [("cps", n, None) for n in (3, 16)] + [("rb", 5, None)] + \
+          [("tree", 16, (4, 4)), ("tree", 24, (2, 3, 4)), ("tree", 64, (8, 8))]
+
+
+@pytest.mark.parametrize("kind,n,fan", BUILTIN)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("fuse", [1, 0])
+def test_whole_plan_resident_program(kind, n, fan, dtype, fuse):
+    vec = 8 if dtype == "bf16" else 4
+    N = n * vec * 8  # every block boundary 16-byte aligned
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_FUSE, fuse)
+        _check_whole_plan(p.handle, oracle.make_plan(kind, n, N, fan), n, N, dtype, seed=n)
+
+
+def test_resident_needs_at_most_64_buffers():
+    with arplan.Plan(128, 128 * 4, "f32", "ring") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        L = p.launches()
+        assert len(L) == 1 and L[0][0] == -1
+        assert _resident_tables(p.handle, 0) is None
+    with arplan.Plan(64, 64 * 4, "f32", "ring") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        assert p.launches()[0][0] == -2
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_custom_plans_resident_program(seed):
+    # random hazard-free plans on positions scaled to whole 16-byte vectors
+    rng = np.random.default_rng(9100 + seed)
+    n = int(rng.integers(2, 7))
+    M = int(rng.integers(4, 100))
+    phases = _random_plan(rng, n, M)
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    vec = 8 if dtype == "bf16" else 4
+    N = M * vec
+    flat = [(q, op, d, s, b * vec, e * vec)
+            for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref = OPlan("custom", n, N, [[OStep(op, d, s, b * vec, e * vec)
+                                  for (op, d, s, b, e) in ph] for ph in phases])
+    h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+    try:
+        _check_whole_plan(h, ref, n, N, dtype, seed=seed)
+    finally:
+        arplan.ar_plan_destroy(h)
+
+
+@pytest.mark.parametrize("name", ["sweep_ring_n64_f32_N4096", "sweep_ring_n64_bf16_N4096"])
+def test_workload_runs_resident_by_default(name):
+    # the small-message workloads run as one resident launch by default; the
+    # program is checked at a reduced N with the same block structure
+    c = workloads.CONFIGS[name]
+    n = c["n"]
+    with arplan.Plan(n, c["N"], c["dtype"], c["kind"], c.get("fanin")) as p:
+        L = p.launches()
+        assert len(L) == 1 and L[0][0] == -2, L
+    N = n * 4 * 5
+    with arplan.Plan(n, N, "f32", c["kind"], c.get("fanin")) as p:
+        _check_whole_plan(p.handle, oracle.make_plan(c["kind"], n, N, c.get("fanin")),
+                          n, N, "f32", seed=5)
