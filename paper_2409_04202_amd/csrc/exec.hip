@@ -636,9 +636,14 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 }
             }
             if (sd.resident) {
-                // per segment: the step records decode to the steps covering
-                // it in phase order, no record across a 64-word chunk, rows in
-                // range; per unit: its tile, and the rows to load (read before
+                // per segment: running its records symbolically (each value a
+                // term: an input row, an unordered 2-operand add, the rounding
+                // at the end of a fold) gives, for every row it stores, the
+                // term the executed steps give (phase by phase, each phase
+                // reading the state it started with), and leaves every other
+                // row's term the input; no record reads a row that is neither
+                // loaded nor written before, no record crosses a 64-word chunk;
+                // per unit: its tile, and the rows to load (read before
                 // written) and to store (written) of its segment
                 if (plan->n > kResMaxN) return bad("resident launch with too many buffers");
                 if (int64_t(sd.runits.size()) != sd.nunits || int64_t(sd.tiles.size()) != sd.nunits ||
@@ -647,73 +652,136 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 std::vector<uint64_t> wload(size_t(sd.nseg), 0), wstore(size_t(sd.nseg), 0);
                 std::vector<int32_t> words(size_t(sd.nseg), 0);
                 for (int32_t sg = 0; sg < sd.nseg; ++sg) {
-                    std::vector<std::pair<std::vector<int32_t>, std::vector<int32_t>>> want;
+                    std::map<std::tuple<int, int64_t, int64_t>, int64_t> terms;
+                    auto term = [&](int kind, int64_t x, int64_t y) {
+                        if (kind == 1 && x > y) std::swap(x, y);  // add: unordered
+                        auto it = terms.emplace(std::make_tuple(kind, x, y), int64_t(terms.size())).first;
+                        return it->second;
+                    };
+                    auto fold = [&](const std::vector<int64_t>& v) {  // k >= 1 operand terms
+                        if (v.size() == 1) return v[0];
+                        int64_t t = v[0];
+                        for (size_t j = 1; j < v.size(); ++j) t = term(1, t, v[j]);
+                        return term(2, t, 0);
+                    };
+                    const size_t n = size_t(plan->n);
+                    std::vector<int64_t> want(n), input(n);
+                    for (size_t b = 0; b < n; ++b) want[b] = input[b] = term(0, int64_t(b), 0);
                     uint64_t seen = 0;
-                    for (int32_t q = 0; q < sd.nphases; ++q)
-                        for (const XStep& x : ex->phases[size_t(sd.p0 + q)].steps)
-                            if (x.end > x.begin && x.begin <= sd.cuts[size_t(sg)] &&
-                                sd.cuts[size_t(sg) + 1] <= x.end) {
-                                want.push_back({x.srcs, x.dsts});
-                                for (int32_t b : x.srcs)
-                                    if (!(seen >> b & 1)) wload[size_t(sg)] |= uint64_t(1) << b;
-                                for (int32_t b : x.srcs) seen |= uint64_t(1) << b;
-                                for (int32_t b : x.dsts) {
-                                    seen |= uint64_t(1) << b;
-                                    wstore[size_t(sg)] |= uint64_t(1) << b;
-                                }
+                    bool covered = false;
+                    for (int32_t q = 0; q < sd.nphases; ++q) {
+                        std::vector<std::pair<int32_t, int64_t>> outs;
+                        for (const XStep& x : ex->phases[size_t(sd.p0 + q)].steps) {
+                            if (!(x.end > x.begin && x.begin <= sd.cuts[size_t(sg)] &&
+                                  sd.cuts[size_t(sg) + 1] <= x.end))
+                                continue;
+                            covered = true;
+                            std::vector<int64_t> v;
+                            for (int32_t b : x.srcs) {
+                                v.push_back(want[size_t(b)]);
+                                if (!(seen >> b & 1)) wload[size_t(sg)] |= uint64_t(1) << b;
                             }
+                            for (int32_t b : x.srcs) seen |= uint64_t(1) << b;
+                            const int64_t t = fold(v);
+                            for (int32_t b : x.dsts) {
+                                outs.push_back({b, t});
+                                seen |= uint64_t(1) << b;
+                                wstore[size_t(sg)] |= uint64_t(1) << b;
+                            }
+                        }
+                        for (const auto& o : outs) want[size_t(o.first)] = o.second;
+                    }
                     const int32_t off = sd.rec_off[size_t(sg)];
-                    if (want.empty()) {
+                    if (!covered) {
                         if (off != -1) return bad("resident records on an idle segment");
                         continue;
                     }
-                    if (off < 0 || off > int64_t(sd.prog.size())) return bad("resident records outside the table");
-                    std::vector<std::pair<std::vector<int32_t>, std::vector<int32_t>>> got;
+                    // the segment's unit records give its record count
+                    int32_t nw = -1;
+                    for (int64_t i = 0; i < sd.nunits; ++i)
+                        if (sd.tiles[size_t(i)].x == sg) {
+                            nw = sd.runits[size_t(i)].nw;
+                            break;
+                        }
+                    if (off < 0 || nw < 1 || int64_t(off) + nw > int64_t(sd.prog.size()))
+                        return bad("resident records outside the table");
+                    std::vector<int64_t> have(n, -1);
+                    for (size_t b = 0; b < n; ++b)
+                        if (wload[size_t(sg)] >> b & 1) have[b] = input[b];
+                    auto get = [&](uint32_t r, int64_t& t) {
+                        if (r >= n || have[r] < 0) return false;
+                        t = have[r];
+                        return true;
+                    };
                     const uint32_t* sp = sd.prog.data() + off;
-                    const int64_t avail = int64_t(sd.prog.size()) - off;
-                    int32_t nw = 0;
-                    for (int32_t c0 = 0; got.size() < want.size(); c0 += 64) {
+                    for (int32_t c0 = 0; c0 < nw; c0 += 64) {
+                        const int32_t m = std::min(64, nw - c0);
                         int32_t c = 0;
-                        while (c < 64 && got.size() < want.size()) {
-                            if (c0 + c >= avail) return bad("resident records run past the table");
+                        while (c < m) {
                             const uint32_t h = sp[c0 + c];
                             const uint32_t op = h & 0xFF;
-                            if (op == kResAdd2 || op == kResCopy) {
-                                const int32_t r0 = int32_t((h >> 8) & 0xFF), r1 = int32_t((h >> 16) & 0xFF);
-                                const int32_t d = int32_t(h >> 24);
-                                if (r0 >= plan->n || r1 >= plan->n || d >= plan->n)
-                                    return bad("resident row out of range");
-                                if (op == kResCopy && r1 != r0) return bad("resident copy record malformed");
-                                got.push_back({op == kResAdd2 ? std::vector<int32_t>{r0, r1}
-                                                              : std::vector<int32_t>{r0},
-                                               std::vector<int32_t>{d}});
-                                c += 1;
-                                nw = c0 + c;
-                                continue;
-                            }
-                            const int k = int(op), nd = int((h >> 8) & 0xFF);
-                            if (k > kResMaxN) return bad("resident record header malformed");
-                            if (k == 0) {
-                                for (int32_t j = c; j < 64 && c0 + j < avail; ++j)
+                            if (op == 0) {
+                                for (int32_t j = c; j < m; ++j)
                                     if (sp[c0 + j]) return bad("resident chunk padding not zero");
                                 break;
                             }
-                            if (nd < 1 || c + res_words(k, nd) > 64 || c0 + c + res_words(k, nd) > avail)
-                                return bad("resident record across a chunk");
-                            std::vector<int32_t> rows;
-                            for (int j = 0; j < k + nd; ++j) {
-                                const uint32_t wd = j < 2 ? h >> (16 + 8 * j)
-                                                          : sp[c0 + c + 1 + (j - 2) / 4] >> (8 * ((j - 2) % 4));
-                                rows.push_back(int32_t(wd & 0xFF));
-                                if (rows.back() >= plan->n) return bad("resident row out of range");
+                            std::vector<int64_t> v;
+                            std::vector<uint32_t> dsts;
+                            int64_t t = 0;
+                            int32_t len = 1;
+                            if (op == kResAdd2 || op == kResCopy) {
+                                const uint32_t r0 = (h >> 8) & 0xFF, r1 = (h >> 16) & 0xFF;
+                                if (op == kResCopy && r1 != r0) return bad("resident copy record malformed");
+                                if (!get(r0, t)) return bad("resident record reads an unloaded row");
+                                v.push_back(t);
+                                if (op == kResAdd2) {
+                                    if (!get(r1, t)) return bad("resident record reads an unloaded row");
+                                    v.push_back(t);
+                                }
+                                dsts.push_back(h >> 24);
+                                t = fold(v);
+                            } else if (op == kResChain) {
+                                const int32_t mm = int32_t((h >> 8) & 0xFF);
+                                len = 1 + (mm + 3) / 4;
+                                if (mm < 1 || c + len > m) return bad("resident record across a chunk");
+                                if (!get((h >> 16) & 0xFF, t)) return bad("resident chain reads an unloaded row");
+                                for (int32_t i = 0; i < mm; ++i) {
+                                    int64_t y = 0;
+                                    const uint32_t r = (sp[c0 + c + 1 + i / 4] >> (8 * (i % 4))) & 0xFF;
+                                    if (!get(r, y)) return bad("resident chain reads an unloaded row");
+                                    t = fold({t, y});
+                                }
+                                dsts.push_back(h >> 24);
+                            } else {
+                                const int k = int(op), nd = int((h >> 8) & 0xFF);
+                                len = res_words(k, nd);
+                                if (k > kResMaxN || nd < 1 || c + len > m) return bad("resident record across a chunk");
+                                for (int j = 0; j < k + nd; ++j) {
+                                    const uint32_t r = (j < 2 ? h >> (16 + 8 * j)
+                                                              : sp[c0 + c + 1 + (j - 2) / 4] >> (8 * ((j - 2) % 4))) & 0xFF;
+                                    if (j < k) {
+                                        if (!get(r, t)) return bad("resident record reads an unloaded row");
+                                        v.push_back(t);
+                                    } else {
+                                        dsts.push_back(r);
+                                    }
+                                }
+                                t = fold(v);
                             }
-                            got.push_back({std::vector<int32_t>(rows.begin(), rows.begin() + k),
-                                           std::vector<int32_t>(rows.begin() + k, rows.end())});
-                            c += res_words(k, nd);
-                            nw = c0 + c;
+                            for (uint32_t d : dsts) {
+                                if (d >= n) return bad("resident row out of range");
+                                have[d] = t;
+                            }
+                            c += len;
                         }
                     }
-                    if (got != want) return bad("resident steps differ from the phases' steps");
+                    for (size_t b = 0; b < n; ++b) {
+                        if (wstore[size_t(sg)] >> b & 1) {
+                            if (have[b] != want[b]) return bad("resident result differs from the phases' steps");
+                        } else if (want[b] != input[b]) {
+                            return bad("resident launch leaves a written row unstored");
+                        }
+                    }
                     words[size_t(sg)] = nw;
                 }
                 for (int64_t i = 0; i < sd.nunits; ++i) {
@@ -724,7 +792,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     const int64_t nv = std::min(sd.tile_elems, sd.cuts[sg + 1] - lo) / VEC;
                     if (u.lo != lo || u.nv != nv || nv < 1 || nv > 64) return bad("resident unit tile");
                     if (u.load != wload[sg] || u.store != wstore[sg]) return bad("resident unit rows");
-                    if (u.off != sd.rec_off[sg] || u.nw < words[sg] ||
+                    if (u.off != sd.rec_off[sg] || u.nw != words[sg] ||
                         int64_t(u.off) + u.nw > int64_t(sd.prog.size()))
                         return bad("resident unit records");
                 }

@@ -67,20 +67,25 @@ constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 // a wave per 64 vectors of a segment, the plan's n <= kResMaxN buffers in
 // LDS rows of 1 KiB.  Its predicted time is kLaunchNs plus the larger of its
 // HBM traffic (each row read and written once) at kBytesPerNs and its waves'
-// time: per wave kResWaveNs, kResRowNs per row loaded or stored, and per
-// step of its chain kResFastNs for a one-word record (two sources or a copy,
-// one destination) or kResStepNs + k * kResStepNsPerSrc + d *
-// kResStepNsPerDst otherwise; waves run kResWavesPerCU per compute unit at a
+// time, plus kResOverlap times the smaller (with few waves per compute unit
+// the two overlap only in part); the waves' time is, per wave kResWaveNs, kResRowNs per row loaded or stored, and per
+// step of its chain kResChainNs for a 2-source, 1-destination step that is
+// the only one on its positions in its phase and follows another such phase
+// of the run (these form chain records), kResFastNs for other one-word
+// records (two sources or a copy, one destination), or kResStepNs + k *
+// kResStepNsPerSrc + d * kResStepNsPerDst; waves run kResWavesPerCU per compute unit at a
 // time, or fewer when their LDS rows do not fit (kLdsBytesPerCU), and waves
 // sharing a unit slow each other by kResShare per extra wave.  Fitted to
 // MI355X measurements of chains of 2-source steps, Ring and tree plans.
 constexpr double kResWaveNs = 1250.0;
 constexpr double kResRowNs = 60.0;
 constexpr double kResFastNs = 210.0;
+constexpr double kResChainNs = 45.0;
 constexpr double kResStepNs = 150.0;
 constexpr double kResStepNsPerSrc = 80.0;
 constexpr double kResStepNsPerDst = 20.0;
 constexpr double kResShare = 0.1;
+constexpr double kResOverlap = 0.5;
 constexpr int64_t kResWavesPerCU = 16;
 constexpr int64_t kLdsBytesPerCU = int64_t(160) << 10;
 constexpr int64_t kNumCUs = 256;

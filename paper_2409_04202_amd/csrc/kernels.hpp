@@ -561,6 +561,11 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
 // phase's result.  Records (32-bit words, first byte the opcode):
 //  * kResAdd2 | r0 << 8 | r1 << 16 | d << 24: d = r0 + r1 (fold order r0, r1);
 //  * kResCopy | r0 << 8 | r0 << 16 | d << 24: d = r0;
+//  * kResChain | m << 8 | s << 16 | d << 24, then ceil(m / 4) words of four
+//    row bytes y1..ym: a chain of m 2-source steps each folding the previous
+//    result with the next row (acc = s, acc = fold(acc, yi) rounded per step,
+//    then d = acc); the intermediate results, which nothing reads later,
+//    stay in registers;
 //  * otherwise a header k | nd << 8 | r0 << 16 | r1 << 24 (1 <= k <= 64)
 //    followed by ceil((k + nd - 2) / 4) words of four row bytes each (row
 //    j >= 2 in byte (j - 2) % 4 of word 1 + (j - 2) / 4): rows 0..k-1 are the
@@ -585,6 +590,7 @@ struct ResUnit {
 
 constexpr uint32_t kResAdd2 = 0xFE;
 constexpr uint32_t kResCopy = 0xFD;
+constexpr uint32_t kResChain = 0xFC;
 
 // words of a record with k sources and nd destinations
 __host__ __device__ constexpr int res_words(int k, int nd) {
@@ -667,6 +673,33 @@ __global__ __launch_bounds__(64) void resident_kernel(
                 issue();  // the next record's reads, before this write
                 rows[d * 64 + lane] = out;
                 last = out;
+                last_row = d;
+            } else if (op == kResChain) {
+                const int mm = int((h >> 8) & 0xFFu), d = int(h >> 24);
+                u32x4 cur = rows[int((h >> 16) & 0xFFu) * 64 + lane];
+                for (int i0 = 0; i0 < mm; i0 += 8) {
+                    const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
+                    const uint32_t wb =
+                        i0 + 4 < mm ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
+                    u32x4 y[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        if (i0 + u < mm)
+                            y[u] = rows[int(((u < 4 ? wa : wb) >> (8 * (u & 3))) & 0xFFu) * 64 + lane];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        if (i0 + u < mm) {
+                            VAcc<DT> acc;
+                            acc.init(cur);
+                            acc.add(y[u]);
+                            cur = acc.out();
+                        }
+                }
+                c += 1 + (mm + 3) / 4;
+                h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                issue();  // the next record's reads, before this write
+                rows[d * 64 + lane] = cur;
+                last = cur;
                 last_row = d;
             } else {
                 const int k = int(op), nd = int((h >> 8) & 0xFFu);

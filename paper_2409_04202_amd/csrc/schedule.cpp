@@ -223,6 +223,84 @@ static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int
     return sd;
 }
 
+// Resident records of the steps covering one segment, in phase order
+// (encoding: resident_kernel).  Two-source steps that each fold the previous
+// one's result, whose intermediate results nothing reads later (the next
+// touch of such a row after the step that consumes it overwrites it), become
+// one chain record that keeps the running result in registers and writes
+// only the last one.
+static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint32_t>& w) {
+    const size_t L = st.size();
+    std::vector<uint64_t> rd(L, 0), wr(L, 0);
+    for (size_t j = 0; j < L; ++j) {
+        for (int32_t b : st[j]->srcs) rd[j] |= uint64_t(1) << b;
+        for (int32_t b : st[j]->dsts) wr[j] |= uint64_t(1) << b;
+    }
+    // next[j * 64 + r]: the first record after j touching row r, or -1
+    std::vector<int32_t> next(L * 64, -1);
+    for (size_t j = L; j-- > 0;) {
+        if (j + 1 < L) {
+            std::copy(next.begin() + (j + 1) * 64, next.begin() + (j + 2) * 64, next.begin() + j * 64);
+            for (int r = 0; r < 64; ++r)
+                if ((rd[j + 1] | wr[j + 1]) >> r & 1) next[j * 64 + r] = int32_t(j + 1);
+        }
+    }
+    auto add2 = [&](size_t j) { return st[j]->srcs.size() == 2 && st[j]->dsts.size() == 1; };
+    // can record j's result stay in registers for record j + 1 only?
+    auto chained = [&](size_t j) {
+        if (j + 1 >= L || !add2(j) || !add2(j + 1)) return false;
+        const int32_t d = st[j]->dsts[0];
+        const XStep& x = *st[j + 1];
+        if ((x.srcs[0] == d) == (x.srcs[1] == d)) return false;  // exactly one operand
+        if (wr[j + 1] >> d & 1) return true;                      // overwritten at once
+        const int32_t t = next[(j + 1) * 64 + size_t(d)];
+        return t >= 0 && (wr[size_t(t)] >> d & 1) && !(rd[size_t(t)] >> d & 1);
+    };
+    auto put = [&](const std::vector<uint32_t>& rec) {
+        if (w.size() % 64 + rec.size() > 64) w.resize((w.size() + 63) / 64 * 64, 0u);
+        w.insert(w.end(), rec.begin(), rec.end());
+    };
+    std::vector<uint32_t> rec;
+    for (size_t j = 0; j < L;) {
+        if (chained(j)) {
+            size_t j1 = j + 1;  // the chain is records j..j1
+            while (j1 - j + 1 < 64 && chained(j1)) ++j1;
+            const size_t m = j1 - j + 1;
+            std::vector<int32_t> ys{st[j]->srcs[1]};
+            for (size_t i = j + 1; i <= j1; ++i) {
+                const int32_t prev = st[i - 1]->dsts[0];
+                ys.push_back(st[i]->srcs[0] == prev ? st[i]->srcs[1] : st[i]->srcs[0]);
+            }
+            rec.assign(1 + (m + 3) / 4, 0u);
+            rec[0] = kResChain | uint32_t(m) << 8 | uint32_t(st[j]->srcs[0]) << 16 |
+                     uint32_t(st[j1]->dsts[0]) << 24;
+            for (size_t i = 0; i < m; ++i) rec[1 + i / 4] |= uint32_t(ys[i]) << (8 * (i % 4));
+            put(rec);
+            j = j1 + 1;
+            continue;
+        }
+        const XStep& x = *st[j];
+        const int k = int(x.srcs.size()), nd = int(x.dsts.size());
+        std::vector<int32_t> r(x.srcs);
+        r.insert(r.end(), x.dsts.begin(), x.dsts.end());
+        rec.assign(size_t(res_words(k, nd)), 0u);
+        if (k == 2 && nd == 1) {
+            rec[0] = kResAdd2 | uint32_t(r[0]) << 8 | uint32_t(r[1]) << 16 | uint32_t(r[2]) << 24;
+        } else if (k == 1 && nd == 1) {
+            rec[0] = kResCopy | uint32_t(r[0]) << 8 | uint32_t(r[0]) << 16 | uint32_t(r[1]) << 24;
+        } else {
+            rec[0] = uint32_t(k) | uint32_t(nd) << 8;
+            for (size_t i = 0; i < r.size(); ++i) {
+                const uint32_t b = uint32_t(r[i]);
+                if (i < 2) rec[0] |= b << (16 + 8 * i);
+                else rec[1 + (i - 2) / 4] |= b << (8 * ((i - 2) % 4));
+            }
+        }
+        put(rec);
+        ++j;
+    }
+}
+
 // The resident form of sliced run `sd` (resident_kernel): per segment some
 // step covers, the records of the steps covering it in phase order, the
 // buffers whose first touch in the run reads them and the buffers the run
@@ -236,30 +314,14 @@ static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
     auto seg_of = [&](int64_t x) {
         return size_t(std::lower_bound(sd.cuts.begin(), sd.cuts.end(), x) - sd.cuts.begin());
     };
-    std::vector<std::vector<uint32_t>> recs(nseg);
+    std::vector<std::vector<const XStep*>> steps(nseg);
     // per segment: buffers touched, read before any write, written
     std::vector<uint64_t> seen(nseg, 0), load(nseg, 0), store(nseg, 0);
-    std::vector<uint32_t> rec;
     for (int32_t q = sd.p0; q < sd.p0 + sd.nphases; ++q) {
         for (const XStep& x : ex.phases[size_t(q)].steps) {
             if (x.end <= x.begin) continue;
             const int k = int(x.srcs.size()), nd = int(x.dsts.size());
             if (k < 1 || nd < 1 || k > kResMaxN || nd > 255 || res_words(k, nd) > 64) return;
-            std::vector<int32_t> r(x.srcs);
-            r.insert(r.end(), x.dsts.begin(), x.dsts.end());
-            rec.assign(size_t(res_words(k, nd)), 0u);
-            if (k == 2 && nd == 1) {
-                rec[0] = kResAdd2 | uint32_t(r[0]) << 8 | uint32_t(r[1]) << 16 | uint32_t(r[2]) << 24;
-            } else if (k == 1 && nd == 1) {
-                rec[0] = kResCopy | uint32_t(r[0]) << 8 | uint32_t(r[0]) << 16 | uint32_t(r[1]) << 24;
-            } else {
-                rec[0] = uint32_t(k) | uint32_t(nd) << 8;
-                for (size_t j = 0; j < r.size(); ++j) {
-                    const uint32_t b = uint32_t(r[j]);
-                    if (j < 2) rec[0] |= b << (16 + 8 * j);
-                    else rec[1 + (j - 2) / 4] |= b << (8 * ((j - 2) % 4));
-                }
-            }
             uint64_t rd = 0, wr = 0;
             for (int32_t b : x.srcs) rd |= uint64_t(1) << b;
             for (int32_t b : x.dsts) wr |= uint64_t(1) << b;
@@ -267,12 +329,13 @@ static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
                 load[sg] |= rd & ~seen[sg];
                 seen[sg] |= rd | wr;
                 store[sg] |= wr;
-                std::vector<uint32_t>& w = recs[sg];
-                if (w.size() % 64 + rec.size() > 64) w.resize((w.size() + 63) / 64 * 64, 0u);
-                w.insert(w.end(), rec.begin(), rec.end());
+                steps[sg].push_back(&x);
             }
         }
     }
+    std::vector<std::vector<uint32_t>> recs(nseg);
+    for (size_t sg = 0; sg < nseg; ++sg)
+        if (!steps[sg].empty()) encode_segment(steps[sg], recs[sg]);
     std::vector<uint32_t> prog;
     std::vector<int32_t> rec_off(nseg, -1);
     for (size_t sg = 0; sg < nseg; ++sg) {
@@ -389,25 +452,32 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
         from[size_t(b)] = -1;
         double body = 0.0, chain = 0.0;
         uint64_t touched = 0;
+        bool next_link = false;
         for (int32_t a = b - 1; a >= 0; --a) {
             const PhaseCost& c = pc[size_t(a)];
             if (!c.aligned || c.written > kKeepBytes || c.bytes > kSliceMaxBytes) break;
             body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
                               stretch * double(c.read) / kBytesPerNs,
                               double(c.written) / kBytesPerNs});
-            chain += double(c.cover) *
-                     (c.kmax <= 2 && c.dmax == 1
-                          ? kResFastNs
-                          : kResStepNs + kResStepNsPerSrc * c.kmax + kResStepNsPerDst * c.dmax);
+            // a run is priced from its last phase down: phase a chains into
+            // phase a + 1 when both have one 2-source step per position
+            const bool link = c.cover == 1 && c.kmax == 2 && c.dmax == 1;
+            chain += link && next_link ? kResChainNs
+                     : double(c.cover) *
+                           (c.kmax <= 2 && c.dmax == 1
+                                ? kResFastNs
+                                : kResStepNs + kResStepNsPerSrc * c.kmax + kResStepNsPerDst * c.dmax);
+            next_link = link;
             touched |= c.touched;
             if (b - a == 1 && nl[size_t(a)] < 2) continue;
             double t = kLaunchNs + body;
             bool res = false;
             if (res_ok) {
                 const double rows = 2.0 * double(__builtin_popcountll(touched));
-                const double t_res =
-                    kLaunchNs + std::max(rounds * (kResWaveNs + kResRowNs * rows + chain),
-                                         rows * double(p.N) * p.esize / kBytesPerNs);
+                const double t_waves = rounds * (kResWaveNs + kResRowNs * rows + chain);
+                const double t_bytes = rows * double(p.N) * p.esize / kBytesPerNs;
+                const double t_res = kLaunchNs + std::max(t_waves, t_bytes) +
+                                     kResOverlap * std::min(t_waves, t_bytes);
                 if (t_res < t) {
                     t = t_res;
                     res = true;

@@ -22,6 +22,7 @@ from oracle.plans import Plan as OPlan, Step as OStep
 
 from paper_2409_04202_amd import arplan, workloads
 
+from test_capi_host import _check_tiling
 from test_exec_rewrites_host import _random_plan
 
 
@@ -59,6 +60,13 @@ def _decode(words):
                 out.append(([r0, r1] if h & 0xFF == 0xFE else [r0], [d]))
                 c += 1
                 continue
+            if h & 0xFF == 0xFC:              # chain: acc = s, acc = fold(acc, y_i), d = acc
+                m, s0, d = (h >> 8) & 0xFF, (h >> 16) & 0xFF, h >> 24
+                ys = [(chunk[c + 1 + i // 4] >> (8 * (i % 4))) & 0xFF for i in range(m)]
+                assert c + 1 + (m + 3) // 4 <= len(chunk), "chain across a chunk"
+                out.append((("chain", s0, ys), [d]))
+                c += 1 + (m + 3) // 4
+                continue
             k, nd = h & 0xFF, (h >> 8) & 0xFF
             if k == 0:
                 assert not any(chunk[c:]), "padding must be zero"
@@ -91,6 +99,15 @@ def _interpret(tables, bufs, dtype):
         for b in _bits(load):
             rows[b] = bufs[b][lo:hi].copy()
         for srcs, dsts in _decode(prog[off:off + nw]):
+            if srcs[0] == "chain":
+                _, s0, ys = srcs
+                for r in [s0] + ys:
+                    assert r in rows, "row %d read before it was loaded or written" % r
+                val = rows[s0].copy()
+                for y in ys:
+                    val = fold(dtype, [val, rows[y]])
+                rows[dsts[0]] = val
+                continue
             for s in srcs:
                 assert s in rows, "row %d read before it was loaded or written" % s
             val = rows[srcs[0]].copy() if len(srcs) == 1 else \
@@ -108,6 +125,10 @@ def _check_whole_plan(handle, ref_plan, n, N, dtype, seed):
     assert arplan.ar_plan_launch_info(handle, 0)[0] == -2
     tables = _resident_tables(handle, 0)
     assert tables is not None
+    # the library's own check: each segment's records, run symbolically, give
+    # the executed steps' result terms for every stored row
+    st, msg = _check_tiling(handle, 1)
+    assert st == arplan.AR_OK, msg
     dist = "int1000" if dtype == "i32" else "uniform"
     xs = workloads.draw(n, N, dtype, dist, seed)
     want = oracle.execute(ref_plan, [x.copy() for x in xs], dtype)
@@ -178,3 +199,17 @@ def test_workload_runs_resident_by_default(name):
     with arplan.Plan(n, N, "f32", c["kind"], c.get("fanin")) as p:
         _check_whole_plan(p.handle, oracle.make_plan(c["kind"], n, N, c.get("fanin")),
                           n, N, "f32", seed=5)
+
+
+def test_ring_program_is_one_chain_and_a_broadcast():
+    # Ring n = 64: the 62 ReduceScatter steps of a block each fold the previous
+    # partial sum, whose row is overwritten by the final broadcast: one chain
+    # record of 62 adds, then the last step storing to every buffer
+    n, N = 64, 64 * 64 * 4
+    with arplan.Plan(n, N, "f32", "ring") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        units, prog = _resident_tables(p.handle, 0)
+        for lo, load, store, nv, off, nw in units:
+            recs = _decode(prog[off:off + nw])
+            assert [r[0][0] for r in recs[:1]] == ["chain"] and len(recs) == 2
+            assert len(recs[0][0][2]) == 62 and len(recs[1][1]) == 64
