@@ -296,15 +296,16 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             const Stage stg = staged ? ex->stages[size_t(li)] : Stage{-1, int32_t(li)};
             if (stg.slice >= 0 && ex->slices[size_t(stg.slice)].resident) {
                 const SliceDesc& sd = ex->slices[size_t(stg.slice)];
-                const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(64);
+                const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(64 * sd.res_waves);
                 const size_t lds = size_t(plan->n) * 1024;
-#define AR_RESIDENT(DT)                                                                    \
-    hipLaunchKernelGGL((resident_kernel<DT>), grid, block, lds, stream, pe->dev + ex->rec_words, \
+#define AR_RESIDENT(DT, W)                                                                    \
+    hipLaunchKernelGGL((resident_kernel<DT, W>), grid, block, lds, stream, pe->dev + ex->rec_words, \
                        plan->n, d->runits + sd.runit_base, d->prog + sd.prog_base, sd.nunits)
+                const bool four = sd.res_waves == 4;
                 switch (plan->dtype) {
-                    case AR_F32: AR_RESIDENT(DT_F32); break;
-                    case AR_I32: AR_RESIDENT(DT_I32); break;
-                    default: AR_RESIDENT(DT_BF16); break;
+                    case AR_F32: if (four) AR_RESIDENT(DT_F32, 4); else AR_RESIDENT(DT_F32, 1); break;
+                    case AR_I32: if (four) AR_RESIDENT(DT_I32, 4); else AR_RESIDENT(DT_I32, 1); break;
+                    default: if (four) AR_RESIDENT(DT_BF16, 4); else AR_RESIDENT(DT_BF16, 1); break;
                 }
 #undef AR_RESIDENT
             } else if (stg.slice >= 0) {
@@ -646,6 +647,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 // per unit: its tile, and the rows to load (read before
                 // written) and to store (written) of its segment
                 if (plan->n > kResMaxN) return bad("resident launch with too many buffers");
+                if (sd.res_waves != 1 && sd.res_waves != 4) return bad("resident workgroup size");
                 if (int64_t(sd.runits.size()) != sd.nunits || int64_t(sd.tiles.size()) != sd.nunits ||
                     int64_t(sd.rec_off.size()) != sd.nseg)
                     return bad("resident table sizes");
@@ -755,17 +757,16 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                             } else {
                                 const int k = int(op), nd = int((h >> 8) & 0xFF);
                                 len = res_words(k, nd);
-                                if (k > kResMaxN || nd < 1 || c + len > m) return bad("resident record across a chunk");
-                                for (int j = 0; j < k + nd; ++j) {
-                                    const uint32_t r = (j < 2 ? h >> (16 + 8 * j)
-                                                              : sp[c0 + c + 1 + (j - 2) / 4] >> (8 * ((j - 2) % 4))) & 0xFF;
-                                    if (j < k) {
-                                        if (!get(r, t)) return bad("resident record reads an unloaded row");
-                                        v.push_back(t);
-                                    } else {
-                                        dsts.push_back(r);
-                                    }
+                                if (k > kResMaxN || nd < 1 || (h >> 16) || c + len > m)
+                                    return bad("resident record malformed or across a chunk");
+                                const int ks = (k + 3) / 4;
+                                for (int j = 0; j < k; ++j) {
+                                    const uint32_t r = (sp[c0 + c + 1 + j / 4] >> (8 * (j % 4))) & 0xFF;
+                                    if (!get(r, t)) return bad("resident record reads an unloaded row");
+                                    v.push_back(t);
                                 }
+                                for (int j = 0; j < nd; ++j)
+                                    dsts.push_back((sp[c0 + c + 1 + ks + j / 4] >> (8 * (j % 4))) & 0xFF);
                                 t = fold(v);
                             }
                             for (uint32_t d : dsts) {

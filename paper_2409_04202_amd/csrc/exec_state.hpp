@@ -64,19 +64,22 @@ constexpr double kStepNsPerDst = 15.0;
 constexpr double kMinSliceWaves = 256.0;
 constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 // A sliced run may instead run resident (resident_kernel, AR_OPT_RESIDENT):
-// a wave per 64 vectors of a segment, the plan's n <= kResMaxN buffers in
-// LDS rows of 1 KiB.  Its predicted time is kLaunchNs plus the larger of its
-// HBM traffic (each row read and written once) at kBytesPerNs and its waves'
-// time, plus kResOverlap times the smaller (with few waves per compute unit
-// the two overlap only in part); the waves' time is, per wave kResWaveNs, kResRowNs per row loaded or stored, and per
-// step of its chain kResChainNs for a 2-source, 1-destination step that is
-// the only one on its positions in its phase and follows another such phase
-// of the run (these form chain records), kResFastNs for other one-word
-// records (two sources or a copy, one destination), or kResStepNs + k *
-// kResStepNsPerSrc + d * kResStepNsPerDst; waves run kResWavesPerCU per compute unit at a
-// time, or fewer when their LDS rows do not fit (kLdsBytesPerCU), and waves
-// sharing a unit slow each other by kResShare per extra wave.  Fitted to
-// MI355X measurements of chains of 2-source steps, Ring and tree plans.
+// a workgroup of W waves (res_waves in schedule.cpp) per 64 vectors of a
+// segment, the plan's n <= kResMaxN buffers in LDS rows of 1 KiB.  Its
+// predicted time is kLaunchNs plus the larger of its HBM traffic (each row
+// read and written once) at kBytesPerNs and its workgroups' time, plus
+// kResOverlap times the smaller (with few workgroups per compute unit the
+// two overlap only in part).  A workgroup takes kResWaveNs, kResRowNs / W
+// per row loaded or stored, and per step of its chain kResChainNs for a
+// 2-source, 1-destination step that is the only one on its positions in its
+// phase and follows another such phase of the run (these form chain
+// records), kResFastNs for other one-word records (two sources or a copy,
+// one destination), or kResStepNs + k * kResStepNsPerSrc + d *
+// kResStepNsPerDst.  Workgroups run kResWavesPerCU (one wave) or 8 (four
+// waves) per compute unit at a time, or fewer when their LDS rows do not fit
+// (kLdsBytesPerCU), and those sharing a unit slow each other by kResShare
+// per extra one.  Fitted to MI355X measurements of chains of 2-source
+// steps, Ring and tree plans.
 constexpr double kResWaveNs = 1250.0;
 constexpr double kResRowNs = 60.0;
 constexpr double kResFastNs = 210.0;
@@ -168,6 +171,7 @@ struct SliceDesc {
     // segment no step covers); `tiles` and `tile_elems` are then the
     // resident kernel's tiles (one vector per lane), unit i = tiles[i]
     bool resident = false;
+    int32_t res_waves = 1;       // wavefronts per resident workgroup (1 or 4)
     std::vector<ResUnit> runits;
     std::vector<uint32_t> prog;
     std::vector<int32_t> rec_off;

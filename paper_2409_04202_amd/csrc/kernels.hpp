@@ -543,22 +543,25 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
 
 // ------------------------------------------------------------------------
 // Resident sliced kernel: the same runs of phases, with the element
-// positions a wave owns kept on chip for the whole run.  A wavefront owns up
-// to one 16-byte vector per lane inside one segment and holds it, for every
-// buffer, in a 1 KiB LDS row (row b, lane l at rows[b * 64 + l]).  It loads
-// the rows the run reads before writing them (global_load_lds_dwordx4:
-// straight into LDS, all in flight at once), runs the steps of every phase
-// of the run on the rows, then stores the rows the run wrote.  A phase costs
-// a few LDS accesses instead of a round trip through the memory hierarchy,
-// and each buffer position is read and written once per run.  A lane only
-// touches its own row entries: no barrier.
+// positions a workgroup owns kept on chip for the whole run.  A workgroup
+// owns up to one 16-byte vector per lane inside one segment and holds it,
+// for every buffer, in a 1 KiB LDS row (row b, lane l at rows[b * 64 + l]).
+// Its W wavefronts (1 or 4) load the rows the run reads before writing them
+// (global_load_lds_dwordx4: straight into LDS, all in flight at once; wave w
+// takes the rows b with b % W == w), wave 0 runs the steps of every phase of
+// the run on the rows, and all waves store the rows the run wrote.  Four
+// waves issue the row loads and stores four times as fast; one wave per
+// workgroup lets a compute unit hold more tiles when LDS does not limit it.
+// A phase costs a few LDS accesses instead of a round trip through the
+// memory hierarchy, and each buffer position is read and written once per
+// run.
 //
-// Each wave reads one ResUnit: its tile, the rows to load and to store (bit
-// b = buffer b), and where its segment's step records start.  The records
-// are the steps of the run's phases covering the segment, in phase order;
-// steps of one phase touch disjoint positions written by others (the phases
-// are hazard-free), so running them one after the other per lane gives the
-// phase's result.  Records (32-bit words, first byte the opcode):
+// Each workgroup reads one ResUnit: its tile, the rows to load and to store
+// (bit b = buffer b), and where its segment's step records start.  The
+// records are the steps of the run's phases covering the segment, in phase
+// order; steps of one phase touch disjoint positions written by others (the
+// phases are hazard-free), so running them one after the other per lane
+// gives the phase's result.  Records (32-bit words, first byte the opcode):
 //  * kResAdd2 | r0 << 8 | r1 << 16 | d << 24: d = r0 + r1 (fold order r0, r1);
 //  * kResCopy | r0 << 8 | r0 << 16 | d << 24: d = r0;
 //  * kResChain | m << 8 | s << 16 | d << 24, then ceil(m / 4) words of four
@@ -566,15 +569,14 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
 //    result with the next row (acc = s, acc = fold(acc, yi) rounded per step,
 //    then d = acc); the intermediate results, which nothing reads later,
 //    stay in registers;
-//  * otherwise a header k | nd << 8 | r0 << 16 | r1 << 24 (1 <= k <= 64)
-//    followed by ceil((k + nd - 2) / 4) words of four row bytes each (row
-//    j >= 2 in byte (j - 2) % 4 of word 1 + (j - 2) / 4): rows 0..k-1 are the
-//    sources in fold order, rows k..k+nd-1 the destinations.
+//  * otherwise a header k | nd << 8 (1 <= k <= 64), then ceil(k / 4) words of
+//    the source rows in fold order and ceil(nd / 4) words of the destination
+//    rows, four row bytes per word.
 // The records are read 64 words at a time (one word per lane, broadcast with
 // v_readlane; the next chunk is loaded while one is run), so no record
 // straddles a 64-word chunk; a word 0 ends a chunk early.  The one-word
-// records run pipelined: the previous record's result stays in registers
-// (a read of the row it wrote takes it from there), so the next record's LDS
+// records run pipelined: the previous record's result stays in registers (a
+// read of the row it wrote takes it from there), so the next record's LDS
 // reads go out before the previous result is written to LDS.
 constexpr int kResMaxN = 64;  // buffers of a plan the resident kernel takes
 
@@ -594,26 +596,21 @@ constexpr uint32_t kResChain = 0xFC;
 
 // words of a record with k sources and nd destinations
 __host__ __device__ constexpr int res_words(int k, int nd) {
-    return (k == 2 || k == 1) && nd == 1 ? 1 : 1 + (k + nd > 2 ? (k + nd - 2 + 3) / 4 : 0);
+    return (k == 2 || k == 1) && nd == 1 ? 1 : 1 + (k + 3) / 4 + (nd + 3) / 4;
 }
 
-// row j of the record whose header h sits at chunk word c (w: the chunk, one
-// word per lane)
-__device__ __forceinline__ int res_row(uint32_t w, uint32_t h, int c, int j) {
-    if (j < 2) return int((h >> (16 + 8 * j)) & 0xFFu);
-    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + ((j - 2) >> 2)));
-    return int((x >> (8 * ((j - 2) & 3))) & 0xFFu);
-}
+__device__ __forceinline__ int res_byte(uint32_t x, int i) { return int((x >> (8 * i)) & 0xFFu); }
 
-template <int DT>
-__global__ __launch_bounds__(64) void resident_kernel(
+template <int DT, int W>
+__global__ __launch_bounds__(64 * W) void resident_kernel(
     const uint64_t* __restrict__ bufs, int32_t n, const ResUnit* __restrict__ units,
     const uint32_t* __restrict__ prog, int64_t nunits) {
     extern __shared__ u32x4 rows[];
     constexpr int VEC = Elem<DT>::VEC;
-    const int lane = int(threadIdx.x);
+    const int lane = int(threadIdx.x) & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
     const int64_t unit = int64_t(blockIdx.x);
-    if (unit >= nunits) return;
+    if (unit >= nunits) return;  // the same for the whole workgroup
     const ResUnit u = units[unit];
     const bool act = lane < u.nv;
     // lanes past the tile's end read the tile's first vector and store nothing
@@ -631,99 +628,122 @@ __global__ __launch_bounds__(64) void resident_kernel(
             uint32_t(__builtin_amdgcn_readlane(int(plo), b));
         return reinterpret_cast<gvec*>(a) + v;
     };
-    for (uint64_t m = u.load; m; m &= m - 1) {
+    // rows b with b % W == wv
+    const uint64_t mine_rows = W == 1 ? ~uint64_t(0) : 0x1111111111111111ull << wv;
+    for (uint64_t m = u.load & mine_rows; m; m &= m - 1) {
         const int b = __builtin_ctzll(m);
         __builtin_amdgcn_global_load_lds((const AR_GLOBAL void*)(at(b)),
                                          (AR_LDS void*)(rows + b * 64), 16, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    u32x4 last = {0u, 0u, 0u, 0u};  // result of the previous one-word record
-    int last_row = -1;               // the row it went to (-1: none)
-    for (int c0 = 0; c0 < u.nw; c0 += 64) {
-        const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
-        const int m = min(64, u.nw - c0);
-        int c = 0;
-        uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(w), 0));
-        u32x4 pa = last, pb = last;  // LDS reads issued for a one-word record
-        auto issue = [&]() {
-            const uint32_t op = h & 0xFFu;
-            if (op == kResAdd2 || op == kResCopy) {
-                pa = rows[int((h >> 8) & 0xFFu) * 64 + lane];
-                pb = rows[int((h >> 16) & 0xFFu) * 64 + lane];
-            }
-        };
-        issue();
-        while (c < m) {
-            const uint32_t op = h & 0xFFu;
-            if (op == 0) break;
-            if (op == kResAdd2 || op == kResCopy) {
-                const int r0 = int((h >> 8) & 0xFFu), r1 = int((h >> 16) & 0xFFu);
-                const int d = int(h >> 24);
-                const u32x4 a = r0 == last_row ? last : pa;
-                u32x4 out = a;
-                if (op == kResAdd2) {
-                    const u32x4 b = r1 == last_row ? last : pb;
-                    VAcc<DT> acc;
-                    acc.init(a);
-                    acc.add(b);
-                    out = acc.out();
+    if (W == 1) __builtin_amdgcn_s_waitcnt(0);
+    else __syncthreads();  // waits for this wave's loads, then for every wave
+    if (wv == 0) {
+        u32x4 last = {0u, 0u, 0u, 0u};  // result of the previous one-word record
+        int last_row = -1;               // the row it went to (-1: none)
+        for (int c0 = 0; c0 < u.nw; c0 += 64) {
+            const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
+            const int m = min(64, u.nw - c0);
+            int c = 0;
+            uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(w), 0));
+            u32x4 pa = last, pb = last;  // LDS reads issued for a one-word record
+            auto issue = [&]() {
+                const uint32_t op = h & 0xFFu;
+                if (op == kResAdd2 || op == kResCopy) {
+                    pa = rows[res_byte(h, 1) * 64 + lane];
+                    pb = rows[res_byte(h, 2) * 64 + lane];
                 }
-                c += 1;
-                h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
-                issue();  // the next record's reads, before this write
-                rows[d * 64 + lane] = out;
-                last = out;
-                last_row = d;
-            } else if (op == kResChain) {
-                const int mm = int((h >> 8) & 0xFFu), d = int(h >> 24);
-                u32x4 cur = rows[int((h >> 16) & 0xFFu) * 64 + lane];
-                for (int i0 = 0; i0 < mm; i0 += 8) {
-                    const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
-                    const uint32_t wb =
-                        i0 + 4 < mm ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
-                    u32x4 y[8];
+            };
+            issue();
+            while (c < m) {
+                const uint32_t op = h & 0xFFu;
+                if (op == 0) break;
+                if (op == kResAdd2 || op == kResCopy) {
+                    const int r0 = res_byte(h, 1), r1 = res_byte(h, 2), d = res_byte(h, 3);
+                    const u32x4 a = r0 == last_row ? last : pa;
+                    u32x4 out = a;
+                    if (op == kResAdd2) {
+                        const u32x4 b = r1 == last_row ? last : pb;
+                        VAcc<DT> acc;
+                        acc.init(a);
+                        acc.add(b);
+                        out = acc.out();
+                    }
+                    c += 1;
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();  // the next record's reads, before this write
+                    rows[d * 64 + lane] = out;
+                    last = out;
+                    last_row = d;
+                } else if (op == kResChain) {
+                    const int mm = res_byte(h, 1), d = res_byte(h, 3);
+                    u32x4 cur = rows[res_byte(h, 2) * 64 + lane];
+                    for (int i0 = 0; i0 < mm; i0 += 8) {
+                        const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
+                        const uint32_t wb =
+                            i0 + 4 < mm ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
+                        u32x4 y[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u)
-                        if (i0 + u < mm)
-                            y[u] = rows[int(((u < 4 ? wa : wb) >> (8 * (u & 3))) & 0xFFu) * 64 + lane];
+                        for (int j = 0; j < 8; ++j)
+                            if (i0 + j < mm) y[j] = rows[res_byte(j < 4 ? wa : wb, j & 3) * 64 + lane];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u)
-                        if (i0 + u < mm) {
-                            VAcc<DT> acc;
-                            acc.init(cur);
-                            acc.add(y[u]);
-                            cur = acc.out();
-                        }
-                }
-                c += 1 + (mm + 3) / 4;
-                h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
-                issue();  // the next record's reads, before this write
-                rows[d * 64 + lane] = cur;
-                last = cur;
-                last_row = d;
-            } else {
-                const int k = int(op), nd = int((h >> 8) & 0xFFu);
-                u32x4 out;
-                if (k == 1) {
-                    out = rows[res_row(w, h, c, 0) * 64 + lane];
+                        for (int j = 0; j < 8; ++j)
+                            if (i0 + j < mm) {
+                                VAcc<DT> acc;
+                                acc.init(cur);
+                                acc.add(y[j]);
+                                cur = acc.out();
+                            }
+                    }
+                    c += 1 + (mm + 3) / 4;
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();  // the next record's reads, before this write
+                    rows[d * 64 + lane] = cur;
+                    last = cur;
+                    last_row = d;
                 } else {
-                    VAcc<DT> acc;
-                    acc.init(rows[res_row(w, h, c, 0) * 64 + lane]);
-                    for (int j = 1; j < k; ++j) acc.add(rows[res_row(w, h, c, j) * 64 + lane]);
-                    out = acc.out();
+                    const int k = int(op), nd = res_byte(h, 1);
+                    const int ks = (k + 3) >> 2;
+                    u32x4 out;
+                    if (k == 1) {
+                        out = rows[res_byte(uint32_t(__builtin_amdgcn_readlane(int(w), c + 1)), 0) * 64 + lane];
+                    } else {
+                        VAcc<DT> acc;
+                        for (int i0 = 0; i0 < k; i0 += 8) {
+                            const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
+                            const uint32_t wb =
+                                i0 + 4 < k ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
+                            u32x4 y[8];
+#pragma unroll
+                            for (int j = 0; j < 8; ++j)
+                                if (i0 + j < k) y[j] = rows[res_byte(j < 4 ? wa : wb, j & 3) * 64 + lane];
+#pragma unroll
+                            for (int j = 0; j < 8; ++j)
+                                if (i0 + j < k) {
+                                    if (i0 + j == 0) acc.init(y[j]);
+                                    else acc.add(y[j]);
+                                }
+                        }
+                        out = acc.out();
+                    }
+                    // `out` has arrived; the stores below then go out back to back
+                    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only
+                    for (int j0 = 0; j0 < nd; j0 += 4) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + ks + (j0 >> 2)));
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            if (j0 + j < nd) rows[res_byte(x, j) * 64 + lane] = out;
+                    }
+                    last_row = -1;
+                    c += res_words(k, nd);
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();
                 }
-                // `out` has arrived; the stores below then go out back to back
-                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only
-                for (int j = 0; j < nd; ++j) rows[res_row(w, h, c, k + j) * 64 + lane] = out;
-                last_row = -1;
-                c += res_words(k, nd);
-                h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
-                issue();
             }
+            w = wn;
         }
-        w = wn;
     }
-    uint64_t m = u.store;
+    if (W > 1) __syncthreads();  // the rows are final
+    uint64_t m = u.store & mine_rows;
     while (m) {
         int b[8];
         u32x4 x[8];

@@ -223,6 +223,15 @@ static SliceDesc build_slice(const Plan& p, const ExecState& ex, int32_t p0, int
     return sd;
 }
 
+// Wavefronts per resident workgroup: four issue a tile's row loads and
+// stores in parallel, which pays when LDS already limits a compute unit to
+// at most eight tiles (32 waves) or when there are too few tiles to fill the
+// chip; otherwise one wave per tile lets a unit hold more tiles.
+static int32_t res_waves(int32_t n, int64_t units) {
+    const int64_t by_lds = kLdsBytesPerCU / (int64_t(n) * 1024);
+    return by_lds <= 8 || units <= 4 * kNumCUs ? 4 : 1;
+}
+
 // Resident records of the steps covering one segment, in phase order
 // (encoding: resident_kernel).  Two-source steps that each fold the previous
 // one's result, whose intermediate results nothing reads later (the next
@@ -290,11 +299,10 @@ static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint
             rec[0] = kResCopy | uint32_t(r[0]) << 8 | uint32_t(r[0]) << 16 | uint32_t(r[1]) << 24;
         } else {
             rec[0] = uint32_t(k) | uint32_t(nd) << 8;
-            for (size_t i = 0; i < r.size(); ++i) {
-                const uint32_t b = uint32_t(r[i]);
-                if (i < 2) rec[0] |= b << (16 + 8 * i);
-                else rec[1 + (i - 2) / 4] |= b << (8 * ((i - 2) % 4));
-            }
+            for (int i = 0; i < k; ++i) rec[1 + i / 4] |= uint32_t(x.srcs[size_t(i)]) << (8 * (i % 4));
+            const int ks = (k + 3) / 4;
+            for (int i = 0; i < nd; ++i)
+                rec[1 + ks + i / 4] |= uint32_t(x.dsts[size_t(i)]) << (8 * (i % 4));
         }
         put(rec);
         ++j;
@@ -321,7 +329,7 @@ static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
         for (const XStep& x : ex.phases[size_t(q)].steps) {
             if (x.end <= x.begin) continue;
             const int k = int(x.srcs.size()), nd = int(x.dsts.size());
-            if (k < 1 || nd < 1 || k > kResMaxN || nd > 255 || res_words(k, nd) > 64) return;
+            if (k < 1 || nd < 1 || k > kResMaxN || nd > kResMaxN) return;
             uint64_t rd = 0, wr = 0;
             for (int32_t b : x.srcs) rd |= uint64_t(1) << b;
             for (int32_t b : x.dsts) wr |= uint64_t(1) << b;
@@ -366,6 +374,7 @@ static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
     }
     if (units.empty() || int64_t(units.size()) > kMaxBlocks) return;
     sd.resident = true;
+    sd.res_waves = res_waves(p.n, int64_t(units.size()));
     sd.runits = std::move(units);
     sd.prog = std::move(prog);
     sd.rec_off = std::move(rec_off);
@@ -435,11 +444,13 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
     const double waves = std::max(1.0, double(p.N) * p.esize / (64.0 * kSliceU * 16.0));
     const double stretch = std::max(1.0, kMinSliceWaves / waves);
     const bool res_ok = p.resident != 0 && p.n <= kResMaxN;
-    // resident waves (one vector per lane) and how many run at once
-    const double res_waves = std::max(1.0, double(p.N) * p.esize / (64.0 * 16.0));
+    // resident tiles (one vector per lane), their workgroup size, and how
+    // many run at once
+    const double tiles = std::max(1.0, double(p.N) * p.esize / (64.0 * 16.0));
+    const int32_t W = res_waves(p.n, int64_t(tiles));
     const int64_t per_cu = std::max<int64_t>(
-        1, std::min<int64_t>(kResWavesPerCU, kLdsBytesPerCU / (int64_t(p.n) * 1024)));
-    const double rounds = std::ceil(res_waves / double(kNumCUs * per_cu)) *
+        1, std::min<int64_t>(W == 4 ? 8 : kResWavesPerCU, kLdsBytesPerCU / (int64_t(p.n) * 1024)));
+    const double rounds = std::ceil(tiles / double(kNumCUs * per_cu)) *
                           (1.0 + kResShare * double(per_cu - 1));
     const int32_t P = int32_t(pc.size());
     std::vector<int32_t> nl(size_t(P), 0);
@@ -474,7 +485,7 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             bool res = false;
             if (res_ok) {
                 const double rows = 2.0 * double(__builtin_popcountll(touched));
-                const double t_waves = rounds * (kResWaveNs + kResRowNs * rows + chain);
+                const double t_waves = rounds * (kResWaveNs + kResRowNs / W * rows + chain);
                 const double t_bytes = rows * double(p.N) * p.esize / kBytesPerNs;
                 const double t_res = kLaunchNs + std::max(t_waves, t_bytes) +
                                      kResOverlap * std::min(t_waves, t_bytes);

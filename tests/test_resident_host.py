@@ -46,9 +46,10 @@ def _resident_tables(handle, stage):
 def _decode(words):
     """Step records of one segment: [(srcs, dsts)], per the documented
     encoding (one word 0xFE | r0 << 8 | r1 << 16 | d << 24 for d = r0 + r1,
-    0xFD | r0 << 8 | r0 << 16 | d << 24 for d = r0; otherwise a header
-    k | nd << 8 | r0 << 16 | r1 << 24, then four row bytes per word; 64-word
-    chunks, a zero word ends a chunk)."""
+    0xFD | r0 << 8 | r0 << 16 | d << 24 for d = r0, a chain 0xFC | m << 8 |
+    s << 16 | d << 24 with m row bytes; otherwise a header k | nd << 8, then
+    the k source rows and the nd destination rows, each from a new word, four
+    row bytes per word; 64-word chunks, a zero word ends a chunk)."""
     out = []
     for c0 in range(0, len(words), 64):
         chunk = [int(w) for w in words[c0:c0 + 64]]
@@ -71,13 +72,12 @@ def _decode(words):
             if k == 0:
                 assert not any(chunk[c:]), "padding must be zero"
                 break
-            rows = []
-            for j in range(k + nd):
-                w = h >> (16 + 8 * j) if j < 2 else \
-                    chunk[c + 1 + (j - 2) // 4] >> (8 * ((j - 2) % 4))
-                rows.append(w & 0xFF)
-            out.append((rows[:k], rows[k:]))
-            c += 1 + ((k + nd - 2 + 3) // 4 if k + nd > 2 else 0)
+            ks, ds = (k + 3) // 4, (nd + 3) // 4
+            assert c + 1 + ks + ds <= len(chunk), "record across a chunk"
+            srcs = [(chunk[c + 1 + j // 4] >> (8 * (j % 4))) & 0xFF for j in range(k)]
+            dsts = [(chunk[c + 1 + ks + j // 4] >> (8 * (j % 4))) & 0xFF for j in range(nd)]
+            out.append((srcs, dsts))
+            c += 1 + ks + ds
     return out
 
 
