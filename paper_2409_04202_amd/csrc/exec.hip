@@ -715,6 +715,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                         t = have[r];
                         return true;
                     };
+                    int64_t last = -1;  // the previous record's result
                     const uint32_t* sp = sd.prog.data() + off;
                     for (int32_t c0 = 0; c0 < nw; c0 += 64) {
                         const int32_t m = std::min(64, nw - c0);
@@ -727,52 +728,58 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                                     if (sp[c0 + j]) return bad("resident chunk padding not zero");
                                 break;
                             }
-                            std::vector<int64_t> v;
+                            auto row = [&](int32_t i) {  // row byte i after the header
+                                return (sp[c0 + c + 1 + i / 4] >> (8 * (i % 4))) & 0xFF;
+                            };
                             std::vector<uint32_t> dsts;
-                            int64_t t = 0;
+                            int64_t t = 0, y = 0;
                             int32_t len = 1;
                             if (op == kResAdd2 || op == kResCopy) {
                                 const uint32_t r0 = (h >> 8) & 0xFF, r1 = (h >> 16) & 0xFF;
                                 if (op == kResCopy && r1 != r0) return bad("resident copy record malformed");
                                 if (!get(r0, t)) return bad("resident record reads an unloaded row");
-                                v.push_back(t);
                                 if (op == kResAdd2) {
-                                    if (!get(r1, t)) return bad("resident record reads an unloaded row");
-                                    v.push_back(t);
-                                }
-                                dsts.push_back(h >> 24);
-                                t = fold(v);
-                            } else if (op == kResChain) {
-                                const int32_t mm = int32_t((h >> 8) & 0xFF);
-                                len = 1 + (mm + 3) / 4;
-                                if (mm < 1 || c + len > m) return bad("resident record across a chunk");
-                                if (!get((h >> 16) & 0xFF, t)) return bad("resident chain reads an unloaded row");
-                                for (int32_t i = 0; i < mm; ++i) {
-                                    int64_t y = 0;
-                                    const uint32_t r = (sp[c0 + c + 1 + i / 4] >> (8 * (i % 4))) & 0xFF;
-                                    if (!get(r, y)) return bad("resident chain reads an unloaded row");
+                                    if (!get(r1, y)) return bad("resident record reads an unloaded row");
                                     t = fold({t, y});
                                 }
                                 dsts.push_back(h >> 24);
-                            } else {
-                                const int k = int(op), nd = int((h >> 8) & 0xFF);
-                                len = res_words(k, nd);
-                                if (k > kResMaxN || nd < 1 || (h >> 16) || c + len > m)
+                            } else if (op == kResChain || op == kResFold) {
+                                const int32_t k = int32_t((h >> 8) & 0xFF);
+                                len = 1 + (k + 3) / 4;
+                                if (k < 1 || (op == kResFold && (k < 2 || (h >> 24))) || c + len > m)
                                     return bad("resident record malformed or across a chunk");
-                                const int ks = (k + 3) / 4;
-                                for (int j = 0; j < k; ++j) {
-                                    const uint32_t r = (sp[c0 + c + 1 + j / 4] >> (8 * (j % 4))) & 0xFF;
-                                    if (!get(r, t)) return bad("resident record reads an unloaded row");
-                                    v.push_back(t);
+                                std::vector<int64_t> v;
+                                if (op == kResChain) {
+                                    if (!get((h >> 16) & 0xFF, t)) return bad("resident chain reads an unloaded row");
+                                    for (int32_t i = 0; i < k; ++i) {
+                                        if (!get(row(i), y)) return bad("resident chain reads an unloaded row");
+                                        t = fold({t, y});
+                                    }
+                                    dsts.push_back(h >> 24);
+                                } else {
+                                    for (int32_t i = 0; i < k; ++i) {
+                                        if (!get(row(i), y)) return bad("resident fold reads an unloaded row");
+                                        v.push_back(y);
+                                    }
+                                    t = fold(v);
+                                    dsts.push_back((h >> 16) & 0xFF);
                                 }
-                                for (int j = 0; j < nd; ++j)
-                                    dsts.push_back((sp[c0 + c + 1 + ks + j / 4] >> (8 * (j % 4))) & 0xFF);
-                                t = fold(v);
+                            } else if (op == kResStore) {
+                                const int32_t nd = int32_t((h >> 8) & 0xFF);
+                                len = 1 + nd / 4;
+                                if (nd < 4 || nd % 4 || (h >> 16) || c + len > m)
+                                    return bad("resident store record malformed or across a chunk");
+                                if (last < 0) return bad("resident store without a result before it");
+                                t = last;
+                                for (int32_t i = 0; i < nd; ++i) dsts.push_back(row(i));
+                            } else {
+                                return bad("resident record with an unknown opcode");
                             }
                             for (uint32_t d : dsts) {
                                 if (d >= n) return bad("resident row out of range");
                                 have[d] = t;
                             }
+                            last = t;
                             c += len;
                         }
                     }

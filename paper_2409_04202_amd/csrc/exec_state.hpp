@@ -85,8 +85,8 @@ constexpr double kResRowNs = 60.0;
 constexpr double kResFastNs = 210.0;
 constexpr double kResChainNs = 45.0;
 constexpr double kResStepNs = 150.0;
-constexpr double kResStepNsPerSrc = 80.0;
-constexpr double kResStepNsPerDst = 20.0;
+constexpr double kResStepNsPerSrc = 40.0;
+constexpr double kResStepNsPerDst = 27.0;
 constexpr double kResShare = 0.1;
 constexpr double kResOverlap = 0.5;
 constexpr int64_t kResWavesPerCU = 16;

@@ -569,9 +569,13 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
 //    result with the next row (acc = s, acc = fold(acc, yi) rounded per step,
 //    then d = acc); the intermediate results, which nothing reads later,
 //    stay in registers;
-//  * otherwise a header k | nd << 8 (1 <= k <= 64), then ceil(k / 4) words of
-//    the source rows in fold order and ceil(nd / 4) words of the destination
-//    rows, four row bytes per word.
+//  * kResFold | k << 8 | d << 16, then ceil(k / 4) words of the k >= 2
+//    source rows in fold order: d = fold(rows);
+//  * kResStore | nd << 8, then nd / 4 words of destination rows (nd a
+//    multiple of 4; a list is padded by repeating its last row): each gets
+//    the previous record's result (a step with several destinations is its
+//    fold, add or copy into the first, then a store into the others).
+// Row bytes are packed four per word.
 // The records are read 64 words at a time (one word per lane, broadcast with
 // v_readlane; the next chunk is loaded while one is run), so no record
 // straddles a 64-word chunk; a word 0 ends a chunk early.  The one-word
@@ -593,11 +597,8 @@ struct ResUnit {
 constexpr uint32_t kResAdd2 = 0xFE;
 constexpr uint32_t kResCopy = 0xFD;
 constexpr uint32_t kResChain = 0xFC;
-
-// words of a record with k sources and nd destinations
-__host__ __device__ constexpr int res_words(int k, int nd) {
-    return (k == 2 || k == 1) && nd == 1 ? 1 : 1 + (k + 3) / 4 + (nd + 3) / 4;
-}
+constexpr uint32_t kResFold = 0xFB;
+constexpr uint32_t kResStore = 0xFA;
 
 __device__ __forceinline__ int res_byte(uint32_t x, int i) { return int((x >> (8 * i)) & 0xFFu); }
 
@@ -700,41 +701,50 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
                     rows[d * 64 + lane] = cur;
                     last = cur;
                     last_row = d;
-                } else {
-                    const int k = int(op), nd = res_byte(h, 1);
-                    const int ks = (k + 3) >> 2;
-                    u32x4 out;
-                    if (k == 1) {
-                        out = rows[res_byte(uint32_t(__builtin_amdgcn_readlane(int(w), c + 1)), 0) * 64 + lane];
-                    } else {
-                        VAcc<DT> acc;
-                        for (int i0 = 0; i0 < k; i0 += 8) {
-                            const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
-                            const uint32_t wb =
-                                i0 + 4 < k ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
-                            u32x4 y[8];
-#pragma unroll
-                            for (int j = 0; j < 8; ++j)
-                                if (i0 + j < k) y[j] = rows[res_byte(j < 4 ? wa : wb, j & 3) * 64 + lane];
-#pragma unroll
-                            for (int j = 0; j < 8; ++j)
-                                if (i0 + j < k) {
-                                    if (i0 + j == 0) acc.init(y[j]);
-                                    else acc.add(y[j]);
-                                }
-                        }
-                        out = acc.out();
+                } else if (op == kResFold) {
+                    const int k = res_byte(h, 1), d = res_byte(h, 2);
+                    VAcc<DT> acc;
+                    const int kg = k >> 2;  // full groups of four sources
+                    for (int g = 0; g < kg; ++g) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + g));
+                        const u32x4 a0 = rows[res_byte(x, 0) * 64 + lane];
+                        const u32x4 a1 = rows[res_byte(x, 1) * 64 + lane];
+                        const u32x4 a2 = rows[res_byte(x, 2) * 64 + lane];
+                        const u32x4 a3 = rows[res_byte(x, 3) * 64 + lane];
+                        if (g == 0) acc.init(a0);
+                        else acc.add(a0);
+                        acc.add(a1);
+                        acc.add(a2);
+                        acc.add(a3);
                     }
-                    // `out` has arrived; the stores below then go out back to back
-                    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only
-                    for (int j0 = 0; j0 < nd; j0 += 4) {
-                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + ks + (j0 >> 2)));
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            if (j0 + j < nd) rows[res_byte(x, j) * 64 + lane] = out;
+                    const int rem = k & 3;
+                    if (rem) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + kg));
+                        const u32x4 a0 = rows[res_byte(x, 0) * 64 + lane];
+                        const u32x4 a1 = rows[res_byte(x, rem > 1 ? 1 : 0) * 64 + lane];
+                        const u32x4 a2 = rows[res_byte(x, rem > 2 ? 2 : 0) * 64 + lane];
+                        if (kg == 0) acc.init(a0);
+                        else acc.add(a0);
+                        if (rem > 1) acc.add(a1);
+                        if (rem > 2) acc.add(a2);
                     }
-                    last_row = -1;
-                    c += res_words(k, nd);
+                    const u32x4 out = acc.out();
+                    c += 1 + ((k + 3) >> 2);
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();  // the next record's reads, before this write
+                    rows[d * 64 + lane] = out;
+                    last = out;
+                    last_row = d;
+                } else {  // kResStore: the previous result into nd rows
+                    const int nq = res_byte(h, 1) >> 2;
+                    for (int j = 0; j < nq; ++j) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + j));
+                        rows[res_byte(x, 0) * 64 + lane] = last;
+                        rows[res_byte(x, 1) * 64 + lane] = last;
+                        rows[res_byte(x, 2) * 64 + lane] = last;
+                        rows[res_byte(x, 3) * 64 + lane] = last;
+                    }
+                    c += 1 + nq;
                     h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
                     issue();
                 }

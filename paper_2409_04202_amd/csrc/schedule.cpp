@@ -289,22 +289,30 @@ static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint
             continue;
         }
         const XStep& x = *st[j];
-        const int k = int(x.srcs.size()), nd = int(x.dsts.size());
-        std::vector<int32_t> r(x.srcs);
-        r.insert(r.end(), x.dsts.begin(), x.dsts.end());
-        rec.assign(size_t(res_words(k, nd)), 0u);
-        if (k == 2 && nd == 1) {
-            rec[0] = kResAdd2 | uint32_t(r[0]) << 8 | uint32_t(r[1]) << 16 | uint32_t(r[2]) << 24;
-        } else if (k == 1 && nd == 1) {
-            rec[0] = kResCopy | uint32_t(r[0]) << 8 | uint32_t(r[0]) << 16 | uint32_t(r[1]) << 24;
+        const size_t k = x.srcs.size();
+        // the fold, add or copy into the first destination
+        if (k == 2) {
+            rec.assign(1, kResAdd2 | uint32_t(x.srcs[0]) << 8 | uint32_t(x.srcs[1]) << 16 |
+                              uint32_t(x.dsts[0]) << 24);
+        } else if (k == 1) {
+            rec.assign(1, kResCopy | uint32_t(x.srcs[0]) << 8 | uint32_t(x.srcs[0]) << 16 |
+                              uint32_t(x.dsts[0]) << 24);
         } else {
-            rec[0] = uint32_t(k) | uint32_t(nd) << 8;
-            for (int i = 0; i < k; ++i) rec[1 + i / 4] |= uint32_t(x.srcs[size_t(i)]) << (8 * (i % 4));
-            const int ks = (k + 3) / 4;
-            for (int i = 0; i < nd; ++i)
-                rec[1 + ks + i / 4] |= uint32_t(x.dsts[size_t(i)]) << (8 * (i % 4));
+            rec.assign(1 + (k + 3) / 4, 0u);
+            rec[0] = kResFold | uint32_t(k) << 8 | uint32_t(x.dsts[0]) << 16;
+            for (size_t i = 0; i < k; ++i) rec[1 + i / 4] |= uint32_t(x.srcs[i]) << (8 * (i % 4));
         }
         put(rec);
+        // then the same value into the other destinations, the list padded
+        // to a multiple of four by repeating its last row
+        if (x.dsts.size() > 1) {
+            std::vector<int32_t> ds(x.dsts.begin() + 1, x.dsts.end());
+            while (ds.size() % 4) ds.push_back(ds.back());
+            rec.assign(1 + ds.size() / 4, 0u);
+            rec[0] = kResStore | uint32_t(ds.size()) << 8;
+            for (size_t i = 0; i < ds.size(); ++i) rec[1 + i / 4] |= uint32_t(ds[i]) << (8 * (i % 4));
+            put(rec);
+        }
         ++j;
     }
 }

@@ -44,40 +44,44 @@ def _resident_tables(handle, stage):
 
 
 def _decode(words):
-    """Step records of one segment: [(srcs, dsts)], per the documented
-    encoding (one word 0xFE | r0 << 8 | r1 << 16 | d << 24 for d = r0 + r1,
-    0xFD | r0 << 8 | r0 << 16 | d << 24 for d = r0, a chain 0xFC | m << 8 |
-    s << 16 | d << 24 with m row bytes; otherwise a header k | nd << 8, then
-    the k source rows and the nd destination rows, each from a new word, four
-    row bytes per word; 64-word chunks, a zero word ends a chunk)."""
+    """Records of one segment, per the documented encoding: ("add", [r0, r1],
+    d), ("copy", [r0], d), ("chain", [s, y1..ym], d), ("fold", rows, d),
+    ("store", rows, None); four row bytes per word after a header, 64-word
+    chunks, a zero word ends a chunk."""
     out = []
     for c0 in range(0, len(words), 64):
         chunk = [int(w) for w in words[c0:c0 + 64]]
         c = 0
         while c < len(chunk):
             h = chunk[c]
-            if h & 0xFF in (0xFE, 0xFD):      # one-word add of two rows, copy
-                r0, r1, d = (h >> 8) & 0xFF, (h >> 16) & 0xFF, h >> 24
-                out.append(([r0, r1] if h & 0xFF == 0xFE else [r0], [d]))
-                c += 1
-                continue
-            if h & 0xFF == 0xFC:              # chain: acc = s, acc = fold(acc, y_i), d = acc
-                m, s0, d = (h >> 8) & 0xFF, (h >> 16) & 0xFF, h >> 24
-                ys = [(chunk[c + 1 + i // 4] >> (8 * (i % 4))) & 0xFF for i in range(m)]
-                assert c + 1 + (m + 3) // 4 <= len(chunk), "chain across a chunk"
-                out.append((("chain", s0, ys), [d]))
-                c += 1 + (m + 3) // 4
-                continue
-            k, nd = h & 0xFF, (h >> 8) & 0xFF
-            if k == 0:
+            op, b1, b2, b3 = h & 0xFF, (h >> 8) & 0xFF, (h >> 16) & 0xFF, h >> 24
+            if op == 0:
                 assert not any(chunk[c:]), "padding must be zero"
                 break
-            ks, ds = (k + 3) // 4, (nd + 3) // 4
-            assert c + 1 + ks + ds <= len(chunk), "record across a chunk"
-            srcs = [(chunk[c + 1 + j // 4] >> (8 * (j % 4))) & 0xFF for j in range(k)]
-            dsts = [(chunk[c + 1 + ks + j // 4] >> (8 * (j % 4))) & 0xFF for j in range(nd)]
-            out.append((srcs, dsts))
-            c += 1 + ks + ds
+
+            def rows(m):
+                assert c + 1 + (m + 3) // 4 <= len(chunk), "record across a chunk"
+                return [(chunk[c + 1 + i // 4] >> (8 * (i % 4))) & 0xFF for i in range(m)]
+            if op == 0xFE:
+                out.append(("add", [b1, b2], b3))
+                c += 1
+            elif op == 0xFD:
+                assert b2 == b1
+                out.append(("copy", [b1], b3))
+                c += 1
+            elif op == 0xFC:
+                out.append(("chain", [b2] + rows(b1), b3))
+                c += 1 + (b1 + 3) // 4
+            elif op == 0xFB:
+                assert b1 >= 2 and b3 == 0
+                out.append(("fold", rows(b1), b2))
+                c += 1 + (b1 + 3) // 4
+            elif op == 0xFA:
+                assert b1 % 4 == 0 and b1 > 0 and b2 == 0 and b3 == 0
+                out.append(("store", rows(b1), None))
+                c += 1 + b1 // 4
+            else:
+                raise AssertionError("unknown opcode %#x" % op)
     return out
 
 
@@ -98,22 +102,25 @@ def _interpret(tables, bufs, dtype):
         rows = {}
         for b in _bits(load):
             rows[b] = bufs[b][lo:hi].copy()
-        for srcs, dsts in _decode(prog[off:off + nw]):
-            if srcs[0] == "chain":
-                _, s0, ys = srcs
-                for r in [s0] + ys:
-                    assert r in rows, "row %d read before it was loaded or written" % r
-                val = rows[s0].copy()
-                for y in ys:
+        last = None
+        for kind, rs, d in _decode(prog[off:off + nw]):
+            for r in (rs if kind != "store" else []):
+                assert r in rows, "row %d read before it was loaded or written" % r
+            if kind == "copy":
+                val = rows[rs[0]].copy()
+            elif kind == "add" or kind == "fold":
+                val = fold(dtype, [rows[r] for r in rs])
+            elif kind == "chain":
+                val = rows[rs[0]].copy()
+                for y in rs[1:]:
                     val = fold(dtype, [val, rows[y]])
-                rows[dsts[0]] = val
+            else:  # store: the previous record's result into every listed row
+                assert last is not None
+                for r in rs:
+                    rows[r] = last.copy()
                 continue
-            for s in srcs:
-                assert s in rows, "row %d read before it was loaded or written" % s
-            val = rows[srcs[0]].copy() if len(srcs) == 1 else \
-                fold(dtype, [rows[s] for s in srcs])
-            for d in dsts:
-                rows[d] = val.copy()
+            rows[d] = val
+            last = val
         for b in _bits(store):
             out[b][lo:hi] = rows[b]
     return out
@@ -204,12 +211,13 @@ def test_workload_runs_resident_by_default(name):
 def test_ring_program_is_one_chain_and_a_broadcast():
     # Ring n = 64: the 62 ReduceScatter steps of a block each fold the previous
     # partial sum, whose row is overwritten by the final broadcast: one chain
-    # record of 62 adds, then the last step storing to every buffer
+    # record of 62 adds (start row and 62 rows), then the last step: its add
+    # into one buffer and a store into the 63 others (padded to 64)
     n, N = 64, 64 * 64 * 4
     with arplan.Plan(n, N, "f32", "ring") as p:
         p.set_option(arplan.AR_OPT_SLICE, 1)
         units, prog = _resident_tables(p.handle, 0)
         for lo, load, store, nv, off, nw in units:
             recs = _decode(prog[off:off + nw])
-            assert [r[0][0] for r in recs[:1]] == ["chain"] and len(recs) == 2
-            assert len(recs[0][0][2]) == 62 and len(recs[1][1]) == 64
+            assert [r[0] for r in recs] == ["chain", "add", "store"]
+            assert len(recs[0][1]) == 63 and len(recs[2][1]) == 64
