@@ -378,6 +378,42 @@ def test_random_aligned_custom_plans_resident(seed):
             assert np.array_equal(got[q], ref[q]), (seed, res, q)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_wide_random_plans_resident(seed):
+    # 8-64 buffers, folds of up to 16 sources, copies into up to 40 buffers
+    # (fold and store records); whole plan resident, plain sliced and the
+    # default choice, against the oracle
+    from test_resident_host import _wide_random_plan
+    from oracle.plans import Plan as OPlan, Step as OStep
+    rng = np.random.default_rng(9600 + seed)
+    n = int(rng.choice([8, 17, 33, 64]))
+    M = int(rng.integers(3, 600))
+    phases = _wide_random_plan(rng, n, M)
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    vec = 8 if dtype == "bf16" else 4
+    N = M * vec
+    flat = [(q, op, d, s, b * vec, e * vec)
+            for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref_plan = OPlan("custom", n, N, [[OStep(op, d, s, b * vec, e * vec)
+                                       for (op, d, s, b, e) in ph] for ph in phases])
+    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", seed)
+    ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
+    say("case: wide custom plan seed=%d n=%d N=%d %s phases=%d" % (seed, n, N, dtype, len(phases)))
+    for sl, res in ((1, 1), (1, 0), (2, 1)):
+        ts = to_device(xs0, dtype)
+        h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+        try:
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, sl)
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_RESIDENT, res)
+            arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+        finally:
+            arplan.ar_plan_destroy(h)
+        got = to_host(ts, dtype)
+        for q in range(n):
+            assert np.array_equal(got[q], ref[q]), (seed, sl, res, q)
+
+
 @pytest.mark.parametrize("kind,n,fan", [("ring", 64, None), ("tree", 64, (8, 8)),
                                         ("tree", 64, (4, 4, 4)), ("rhd", 32, None),
                                         ("cps", 64, None), ("ring", 2, None)])

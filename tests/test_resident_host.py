@@ -221,3 +221,71 @@ def test_ring_program_is_one_chain_and_a_broadcast():
             recs = _decode(prog[off:off + nw])
             assert [r[0] for r in recs] == ["chain", "add", "store"]
             assert len(recs[0][1]) == 63 and len(recs[2][1]) == 64
+
+
+def _wide_random_plan(rng, n, M):
+    """Random hazard-free phases over n buffers on M positions: per phase the
+    positions are cut into blocks and each block gets one reduce of 3..16
+    distinct sources (its destination may be one of them) or copies of one
+    source into several destinations (the executor merges them into one step
+    with many destinations)."""
+    phases = []
+    for q in range(int(rng.integers(2, 6))):
+        cuts = np.unique(np.concatenate([[0, M], rng.integers(1, M, size=rng.integers(1, 6))]))
+        steps = []
+        for b, e in zip(cuts[:-1], cuts[1:]):
+            if rng.random() < 0.5:
+                k = int(rng.integers(3, min(n, 16) + 1))
+                srcs = [int(x) for x in rng.choice(n, size=k, replace=False)]
+                dst = int(rng.choice(srcs)) if rng.random() < 0.5 else int(rng.integers(n))
+                steps.append(("reduce", dst, srcs, int(b), int(e)))
+            else:
+                src = int(rng.integers(n))
+                others = [x for x in range(n) if x != src]
+                m = int(rng.integers(1, min(n - 1, 40) + 1))
+                for d in rng.choice(others, size=m, replace=False):
+                    steps.append(("copy", int(d), [src], int(b), int(e)))
+        phases.append(steps)
+    return phases
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_wide_random_plans_resident_program(seed):
+    # 8-64 buffers, folds of up to 16 sources and copies into up to 40
+    # buffers: fold records, store records with padded lists, many rows
+    rng = np.random.default_rng(9300 + seed)
+    n = int(rng.choice([8, 17, 33, 64]))
+    M = int(rng.integers(3, 120))
+    phases = _wide_random_plan(rng, n, M)
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    vec = 8 if dtype == "bf16" else 4
+    N = M * vec
+    flat = [(q, op, d, s, b * vec, e * vec)
+            for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref = OPlan("custom", n, N, [[OStep(op, d, s, b * vec, e * vec)
+                                  for (op, d, s, b, e) in ph] for ph in phases])
+    h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+    try:
+        _check_whole_plan(h, ref, n, N, dtype, seed=seed)
+    finally:
+        arplan.ar_plan_destroy(h)
+
+
+def test_wide_random_plans_use_every_record_kind():
+    kinds = set()
+    for seed in range(40):
+        rng = np.random.default_rng(9300 + seed)
+        n = int(rng.choice([8, 17, 33, 64]))
+        M = int(rng.integers(3, 120))
+        phases = _wide_random_plan(rng, n, M)
+        flat = [(q, op, d, s, b * 4, e * 4)
+                for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+        h = arplan.ar_plan_create_custom(n, M * 4, "f32", flat)
+        try:
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 1)
+            units, prog = _resident_tables(h, 0)
+            for lo, load, store, nv, off, nw in units:
+                kinds |= {r[0] for r in _decode(prog[off:off + nw])}
+        finally:
+            arplan.ar_plan_destroy(h)
+    assert {"fold", "store", "copy"} <= kinds, kinds
