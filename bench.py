@@ -44,7 +44,8 @@ DEFAULT = "rhd_n8_f32"
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("kernels.hpp", "exec.hip", "exec_state.hpp", "rewrite.cpp", "schedule.cpp"):
+    for f in ("kernels.hpp", "resident.hpp", "exec.hip", "exec_state.hpp", "rewrite.cpp",
+              "schedule.cpp"):
         with open(os.path.join(ROOT, "paper_2409_04202_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -21,7 +21,7 @@ LIB = os.path.join(LIBDIR, "libarplan.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HOST_SRCS = ["plan.cpp", "capi.cpp"]
-HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp"]
+HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp", "debug.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
           "-Wextra", "-Wno-unused-parameter"]

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "kernels.hpp"
+#include "resident.hpp"
 #include "../../include/ar_plan.h"
 #include "plan.hpp"
 

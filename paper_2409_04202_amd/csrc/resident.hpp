@@ -1,0 +1,239 @@
+// Resident sliced kernel for gfx950 (see below); it shares the vector
+// types and the fold arithmetic of the phase and sliced kernels.
+#pragma once
+
+#include "kernels.hpp"
+
+namespace arp {
+
+// ------------------------------------------------------------------------
+// Resident sliced kernel: the same runs of phases, with the element
+// positions a workgroup owns kept on chip for the whole run.  A workgroup
+// owns up to one 16-byte vector per lane inside one segment and holds it,
+// for every buffer, in a 1 KiB LDS row (row b, lane l at rows[b * 64 + l]).
+// Its W wavefronts (1 or 4) load the rows the run reads before writing them
+// (global_load_lds_dwordx4: straight into LDS, all in flight at once; wave w
+// takes the rows b with b % W == w), wave 0 runs the steps of every phase of
+// the run on the rows, and all waves store the rows the run wrote.  Four
+// waves issue the row loads and stores four times as fast; one wave per
+// workgroup lets a compute unit hold more tiles when LDS does not limit it.
+// A phase costs a few LDS accesses instead of a round trip through the
+// memory hierarchy, and each buffer position is read and written once per
+// run.
+//
+// Each workgroup reads one ResUnit: its tile, the rows to load and to store
+// (bit b = buffer b), and where its segment's step records start.  The
+// records are the steps of the run's phases covering the segment, in phase
+// order; steps of one phase touch disjoint positions written by others (the
+// phases are hazard-free), so running them one after the other per lane
+// gives the phase's result.  Records (32-bit words, first byte the opcode):
+//  * kResAdd2 | r0 << 8 | r1 << 16 | d << 24: d = r0 + r1 (fold order r0, r1);
+//  * kResCopy | r0 << 8 | r0 << 16 | d << 24: d = r0;
+//  * kResChain | m << 8 | s << 16 | d << 24, then ceil(m / 4) words of four
+//    row bytes y1..ym: a chain of m 2-source steps each folding the previous
+//    result with the next row (acc = s, acc = fold(acc, yi) rounded per step,
+//    then d = acc); the intermediate results, which nothing reads later,
+//    stay in registers;
+//  * kResFold | k << 8 | d << 16, then ceil(k / 4) words of the k >= 2
+//    source rows in fold order: d = fold(rows);
+//  * kResStore | nd << 8, then nd / 4 words of destination rows (nd a
+//    multiple of 4; a list is padded by repeating its last row): each gets
+//    the previous record's result (a step with several destinations is its
+//    fold, add or copy into the first, then a store into the others).
+// Row bytes are packed four per word.
+// The records are read 64 words at a time (one word per lane, broadcast with
+// v_readlane; the next chunk is loaded while one is run), so no record
+// straddles a 64-word chunk; a word 0 ends a chunk early.  The one-word
+// records run pipelined: the previous record's result stays in registers (a
+// read of the row it wrote takes it from there), so the next record's LDS
+// reads go out before the previous result is written to LDS.
+constexpr int kResMaxN = 64;  // buffers of a plan the resident kernel takes
+
+struct ResUnit {
+    int64_t lo;      // first element of the tile
+    uint64_t load;   // rows to load
+    uint64_t store;  // rows to store
+    int32_t nv;      // 16-byte vectors in the tile, 1..64
+    int32_t off;     // first word of the segment's step records
+    int32_t nw;      // words of step records (chunk padding included)
+    int32_t pad;
+};
+
+constexpr uint32_t kResAdd2 = 0xFE;
+constexpr uint32_t kResCopy = 0xFD;
+constexpr uint32_t kResChain = 0xFC;
+constexpr uint32_t kResFold = 0xFB;
+constexpr uint32_t kResStore = 0xFA;
+
+__device__ __forceinline__ int res_byte(uint32_t x, int i) { return int((x >> (8 * i)) & 0xFFu); }
+
+template <int DT, int W>
+__global__ __launch_bounds__(64 * W) void resident_kernel(
+    const uint64_t* __restrict__ bufs, int32_t n, const ResUnit* __restrict__ units,
+    const uint32_t* __restrict__ prog, int64_t nunits) {
+    extern __shared__ u32x4 rows[];
+    constexpr int VEC = Elem<DT>::VEC;
+    const int lane = int(threadIdx.x) & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+    const int64_t unit = int64_t(blockIdx.x);
+    if (unit >= nunits) return;  // the same for the whole workgroup
+    const ResUnit u = units[unit];
+    const bool act = lane < u.nv;
+    // lanes past the tile's end read the tile's first vector and store nothing
+    const int64_t v = u.lo / VEC + (act ? lane : 0);
+    const uint32_t* sp = prog + u.off;
+    uint32_t w = lane < u.nw ? sp[lane] : 0u;  // first chunk of step records
+    const uint64_t mine = lane < n ? bufs[lane] : 0;
+    const uint32_t plo = uint32_t(mine), phi = uint32_t(mine >> 32);
+    // the pointers (and the first records) have arrived: the row loads
+    // below then go out back to back, with no wait between them
+    __builtin_amdgcn_s_waitcnt(0);
+    auto at = [&](int b) {
+        const uint64_t a =
+            (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(phi), b))) << 32) |
+            uint32_t(__builtin_amdgcn_readlane(int(plo), b));
+        return reinterpret_cast<gvec*>(a) + v;
+    };
+    // rows b with b % W == wv
+    const uint64_t mine_rows = W == 1 ? ~uint64_t(0) : 0x1111111111111111ull << wv;
+    for (uint64_t m = u.load & mine_rows; m; m &= m - 1) {
+        const int b = __builtin_ctzll(m);
+        __builtin_amdgcn_global_load_lds((const AR_GLOBAL void*)(at(b)),
+                                         (AR_LDS void*)(rows + b * 64), 16, 0, 0);
+    }
+    if (W == 1) __builtin_amdgcn_s_waitcnt(0);
+    else __syncthreads();  // waits for this wave's loads, then for every wave
+    if (wv == 0) {
+        u32x4 last = {0u, 0u, 0u, 0u};  // result of the previous one-word record
+        int last_row = -1;               // the row it went to (-1: none)
+        for (int c0 = 0; c0 < u.nw; c0 += 64) {
+            const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
+            const int m = min(64, u.nw - c0);
+            int c = 0;
+            uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(w), 0));
+            u32x4 pa = last, pb = last;  // LDS reads issued for a one-word record
+            auto issue = [&]() {
+                const uint32_t op = h & 0xFFu;
+                if (op == kResAdd2 || op == kResCopy) {
+                    pa = rows[res_byte(h, 1) * 64 + lane];
+                    pb = rows[res_byte(h, 2) * 64 + lane];
+                }
+            };
+            issue();
+            while (c < m) {
+                const uint32_t op = h & 0xFFu;
+                if (op == 0) break;
+                if (op == kResAdd2 || op == kResCopy) {
+                    const int r0 = res_byte(h, 1), r1 = res_byte(h, 2), d = res_byte(h, 3);
+                    const u32x4 a = r0 == last_row ? last : pa;
+                    u32x4 out = a;
+                    if (op == kResAdd2) {
+                        const u32x4 b = r1 == last_row ? last : pb;
+                        VAcc<DT> acc;
+                        acc.init(a);
+                        acc.add(b);
+                        out = acc.out();
+                    }
+                    c += 1;
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();  // the next record's reads, before this write
+                    rows[d * 64 + lane] = out;
+                    last = out;
+                    last_row = d;
+                } else if (op == kResChain) {
+                    const int mm = res_byte(h, 1), d = res_byte(h, 3);
+                    u32x4 cur = rows[res_byte(h, 2) * 64 + lane];
+                    for (int i0 = 0; i0 < mm; i0 += 8) {
+                        const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
+                        const uint32_t wb =
+                            i0 + 4 < mm ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
+                        u32x4 y[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j)
+                            if (i0 + j < mm) y[j] = rows[res_byte(j < 4 ? wa : wb, j & 3) * 64 + lane];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j)
+                            if (i0 + j < mm) {
+                                VAcc<DT> acc;
+                                acc.init(cur);
+                                acc.add(y[j]);
+                                cur = acc.out();
+                            }
+                    }
+                    c += 1 + (mm + 3) / 4;
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();  // the next record's reads, before this write
+                    rows[d * 64 + lane] = cur;
+                    last = cur;
+                    last_row = d;
+                } else if (op == kResFold) {
+                    const int k = res_byte(h, 1), d = res_byte(h, 2);
+                    VAcc<DT> acc;
+                    const int kg = k >> 2;  // full groups of four sources
+                    for (int g = 0; g < kg; ++g) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + g));
+                        const u32x4 a0 = rows[res_byte(x, 0) * 64 + lane];
+                        const u32x4 a1 = rows[res_byte(x, 1) * 64 + lane];
+                        const u32x4 a2 = rows[res_byte(x, 2) * 64 + lane];
+                        const u32x4 a3 = rows[res_byte(x, 3) * 64 + lane];
+                        if (g == 0) acc.init(a0);
+                        else acc.add(a0);
+                        acc.add(a1);
+                        acc.add(a2);
+                        acc.add(a3);
+                    }
+                    const int rem = k & 3;
+                    if (rem) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + kg));
+                        const u32x4 a0 = rows[res_byte(x, 0) * 64 + lane];
+                        const u32x4 a1 = rows[res_byte(x, rem > 1 ? 1 : 0) * 64 + lane];
+                        const u32x4 a2 = rows[res_byte(x, rem > 2 ? 2 : 0) * 64 + lane];
+                        if (kg == 0) acc.init(a0);
+                        else acc.add(a0);
+                        if (rem > 1) acc.add(a1);
+                        if (rem > 2) acc.add(a2);
+                    }
+                    const u32x4 out = acc.out();
+                    c += 1 + ((k + 3) >> 2);
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();  // the next record's reads, before this write
+                    rows[d * 64 + lane] = out;
+                    last = out;
+                    last_row = d;
+                } else {  // kResStore: the previous result into nd rows
+                    const int nq = res_byte(h, 1) >> 2;
+                    for (int j = 0; j < nq; ++j) {
+                        const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + j));
+                        rows[res_byte(x, 0) * 64 + lane] = last;
+                        rows[res_byte(x, 1) * 64 + lane] = last;
+                        rows[res_byte(x, 2) * 64 + lane] = last;
+                        rows[res_byte(x, 3) * 64 + lane] = last;
+                    }
+                    c += 1 + nq;
+                    h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
+                    issue();
+                }
+            }
+            w = wn;
+        }
+    }
+    if (W > 1) __syncthreads();  // the rows are final
+    uint64_t m = u.store & mine_rows;
+    while (m) {
+        int b[8];
+        u32x4 x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            b[j] = m ? __builtin_ctzll(m) : -1;
+            m &= m - 1;
+            if (b[j] >= 0) x[j] = rows[b[j] * 64 + lane];
+        }
+        if (act) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (b[j] >= 0) *at(b[j]) = x[j];
+        }
+    }
+}
+
+}  // namespace arp
