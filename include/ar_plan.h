@@ -198,9 +198,12 @@ ar_status ar_plan_destroy(ar_plan* plan);
  * k sources and d destinations) on the host and uploads them; the plan keeps
  * the records of its 4 most recently used buffer sets per device (device and
  * pinned host memory owned by the plan), so repeated executes on the same
- * buffers only launch kernels.  Executions of one plan must be ordered (one
- * stream, or synchronised).  Distinct plans are independent.  Errors:
- * AR_ERR_INVALID_ARG, AR_ERR_OOM, AR_ERR_HIP. */
+ * buffers only launch kernels.  Such a call may therefore be captured in a
+ * HIP graph (stream capture records its kernel launches only); the first
+ * call on a device or with a new buffer set allocates, copies and records
+ * an event, so it must run before capture starts.  Executions of one plan
+ * must be ordered (one stream, or synchronised).  Distinct plans are
+ * independent.  Errors: AR_ERR_INVALID_ARG, AR_ERR_OOM, AR_ERR_HIP. */
 ar_status ar_plan_execute(ar_plan* plan, void* const* bufs, void* stream);
 
 /* Same, with buffer p at (char*)base + p * stride_bytes; stride_bytes must

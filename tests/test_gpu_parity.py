@@ -540,6 +540,44 @@ def test_runs_on_a_side_stream_in_order():
         assert np.array_equal(outs[q].numpy(), ref[q]), q
 
 
+@pytest.mark.parametrize("kind,n,N,fan,slice_,resident", [
+    ("ring", 8, 8 * 1024, None, 1, 1),           # one resident launch
+    ("ring", 8, 8 * 1024, None, 1, 0),           # one plain sliced launch
+    ("rhd", 8, 1 << 20, None, 0, 1),             # phase launches
+    ("tree", 64, 64 * 256, (8, 8), 2, 1)])       # the default choice
+def test_graph_capture_replays(kind, n, N, fan, slice_, resident):
+    # an execution captured in a HIP graph after a first eager execution (which
+    # uploads the step records, so that capture records kernel launches only)
+    # replays the same work: every replay, with eager work and a
+    # synchronisation between replays, matches the oracle applied once more
+    xs0 = workloads.draw(n, N, "i32", "int1000", 21)
+    plan_o = _oracle_plan(kind, n, N, fan)
+    want = oracle.execute(plan_o, [x.copy() for x in xs0], "i32")
+    say("case: graph capture %s n=%d N=%d slice=%d resident=%d" % (kind, n, N, slice_, resident))
+    ts = to_device(xs0, "i32")
+    with arplan.Plan(n, N, "i32", kind, fan) as p:
+        p.set_option(arplan.AR_OPT_SLICE, slice_)
+        p.set_option(arplan.AR_OPT_RESIDENT, resident)
+        run_plan(p, ts)
+        got = to_host(ts, "i32")
+        assert all(np.array_equal(got[q], want[q]) for q in range(n))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            p.execute(ts, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        got = to_host(ts, "i32")   # capture does not run the work
+        assert all(np.array_equal(got[q], want[q]) for q in range(n))
+        for r in range(3):
+            g.replay()
+            torch.cuda.synchronize()
+            want = oracle.execute(plan_o, want, "i32")
+            got = to_host(ts, "i32")
+            assert all(np.array_equal(got[q], want[q]) for q in range(n)), r
+            extra = (ts[0].to(torch.int64) + 1).sum()   # eager work between replays
+            torch.cuda.synchronize()
+            assert int(extra.item()) == int(want[0].astype(np.int64).sum()) + N
+
+
 @pytest.mark.parametrize("resident", [1, 0])
 def test_whole_plan_launch_with_timer_and_repeats(resident):
     n, N = 64, 1 << 14
