@@ -268,14 +268,28 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                         continue;
                     }
                     // the segment's unit records give its record count
-                    int32_t nw = -1;
+                    int32_t nw = -1, aoff = -1;
                     for (int64_t i = 0; i < sd.nunits; ++i)
                         if (sd.tiles[size_t(i)].x == sg) {
                             nw = sd.runits[size_t(i)].nw;
+                            aoff = sd.runits[size_t(i)].alias;
                             break;
                         }
                     if (off < 0 || nw < 1 || int64_t(off) + nw > int64_t(sd.prog.size()))
                         return bad("resident records outside the table");
+                    // the row each stored buffer takes its value from
+                    std::vector<uint32_t> src_row(n);
+                    for (size_t b = 0; b < n; ++b) src_row[b] = uint32_t(b);
+                    if (aoff >= 0) {
+                        if (int64_t(aoff) + 16 > int64_t(sd.prog.size())) return bad("resident alias table outside the table");
+                        for (size_t b = 0; b < 64; ++b) {
+                            const uint32_t a = (sd.prog[size_t(aoff) + b / 4] >> (8 * (b % 4))) & 0xFF;
+                            if (a == 0xFF) continue;
+                            if (b >= n || a >= n || !(wstore[size_t(sg)] >> b & 1))
+                                return bad("resident alias entry out of range or not stored");
+                            src_row[b] = a;
+                        }
+                    }
                     std::vector<int64_t> have(n, -1);
                     for (size_t b = 0; b < n; ++b)
                         if (wload[size_t(sg)] >> b & 1) have[b] = input[b];
@@ -354,13 +368,16 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     }
                     for (size_t b = 0; b < n; ++b) {
                         if (wstore[size_t(sg)] >> b & 1) {
-                            if (have[b] != want[b]) return bad("resident result differs from the phases' steps");
+                            if (have[src_row[b]] != want[b])
+                                return bad("resident result differs from the phases' steps");
                         } else if (want[b] != input[b]) {
                             return bad("resident launch leaves a written row unstored");
                         }
                     }
                     words[size_t(sg)] = nw;
                 }
+                std::vector<int64_t> first_unit(size_t(sd.nseg), -1);
+                for (int64_t i = sd.nunits; i-- > 0;) first_unit[size_t(sd.tiles[size_t(i)].x)] = i;
                 for (int64_t i = 0; i < sd.nunits; ++i) {
                     const ResUnit& u = sd.runits[size_t(i)];
                     const int2 e = sd.tiles[size_t(i)];
@@ -372,6 +389,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     if (u.off != sd.rec_off[sg] || u.nw != words[sg] ||
                         int64_t(u.off) + u.nw > int64_t(sd.prog.size()))
                         return bad("resident unit records");
+                    if (u.alias != sd.runits[size_t(first_unit[sg])].alias) return bad("resident unit alias table");
                 }
             }
             // every step of the slice's phases lies inside the segments
@@ -444,13 +462,14 @@ AR_EXPORT ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* inf
         if (units)
             for (size_t i = 0; i < sd.runits.size(); ++i) {
                 const ResUnit& u = sd.runits[i];
-                int64_t* o = units + 6 * i;
+                int64_t* o = units + 7 * i;
                 o[0] = u.lo;
                 o[1] = int64_t(u.load);
                 o[2] = int64_t(u.store);
                 o[3] = u.nv;
                 o[4] = u.off;
                 o[5] = u.nw;
+                o[6] = u.alias;
             }
         if (prog) std::copy(sd.prog.begin(), sd.prog.end(), prog);
         return AR_OK;

@@ -47,7 +47,8 @@ constexpr int64_t kFuseBytes = int64_t(256) << 20;
 // kSliceMaxBytes.  The runs are chosen by dynamic programming over the phases
 // with a cost model fitted to MI355X measurements (back-to-back launches, no
 // events between them):
-//  * a phase launch costs kLaunchNs plus its bytes at kBytesPerNs;
+//  * a phase launch costs kLaunchNs plus its bytes at kBytesPerNs, at least
+//    kKernelMinNs (one dependent load and store through memory);
 //  * a sliced launch costs kLaunchNs plus, per phase, the largest of its
 //    dependent chain, its read time and its write time.  The chain is the
 //    most steps covering one element position, which a wavefront runs one
@@ -57,6 +58,7 @@ constexpr int64_t kFuseBytes = int64_t(256) << 20;
 //    stretched by kMinSliceWaves / waves when the slice has fewer wave tiles
 //    than that (too few loads in flight to reach full bandwidth).
 constexpr double kLaunchNs = 3000.0;
+constexpr double kKernelMinNs = 2000.0;
 constexpr double kBytesPerNs = 5500.0;
 constexpr double kStepNs = 350.0;
 constexpr double kStepNsPerSrcF32 = 120.0;
@@ -70,18 +72,19 @@ constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 // predicted time is kLaunchNs plus the larger of its HBM traffic (each row
 // read and written once) at kBytesPerNs and its workgroups' time, plus
 // kResOverlap times the smaller (with few workgroups per compute unit the
-// two overlap only in part).  A workgroup takes kResWaveNs, kResRowNs / W
-// per row loaded or stored, and per step of its chain kResChainNs for a
-// 2-source, 1-destination step that is the only one on its positions in its
-// phase and follows another such phase of the run (these form chain
-// records), kResFastNs for other one-word records (two sources or a copy,
-// one destination), or kResStepNs + k * kResStepNsPerSrc + d *
-// kResStepNsPerDst.  Workgroups run kResWavesPerCU (one wave) or 8 (four
-// waves) per compute unit at a time, or fewer when their LDS rows do not fit
-// (kLdsBytesPerCU), and those sharing a unit slow each other by kResShare
-// per extra one.  Fitted to MI355X measurements of chains of 2-source
-// steps, Ring and tree plans.
-constexpr double kResWaveNs = 1250.0;
+// two overlap only in part).  A workgroup takes kResRowNs / W per row
+// loaded or stored, and per step of its chain kResChainNs for a 2-source,
+// 1-destination step that is the only one on its positions in its phase and
+// follows another such phase of the run (these form chain records),
+// kResFastNs for other one-word records (two sources or a copy, one
+// destination), or kResStepNs + k * kResStepNsPerSrc + d * kResStepNsPerDst
+// (d = 1 in the run's last phase, whose further destinations the store pass
+// writes through the alias table).  Workgroups run kResWavesPerCU (one
+// wave) or 8 (four waves) per compute unit at a time, or fewer when their
+// LDS rows do not fit (kLdsBytesPerCU), and those sharing a unit (when there
+// are more tiles than units) slow each other by kResShare per extra one.
+// Fitted to MI355X measurements of chains of one-step phases, Ring and tree
+// plans.
 constexpr double kResRowNs = 60.0;
 constexpr double kResFastNs = 210.0;
 constexpr double kResChainNs = 45.0;

@@ -22,7 +22,11 @@ namespace arp {
 // run.
 //
 // Each workgroup reads one ResUnit: its tile, the rows to load and to store
-// (bit b = buffer b), and where its segment's step records start.  The
+// (bit b = buffer b), where its segment's step records start, and optionally
+// an alias table: 64 bytes, byte b the row whose final value buffer b gets
+// (0xFF: its own row).  A step's further destinations whose values nothing
+// touches afterwards are stored that way, from the first destination's row,
+// instead of by a store record.  The
 // records are the steps of the run's phases covering the segment, in phase
 // order; steps of one phase touch disjoint positions written by others (the
 // phases are hazard-free), so running them one after the other per lane
@@ -56,7 +60,7 @@ struct ResUnit {
     int32_t nv;      // 16-byte vectors in the tile, 1..64
     int32_t off;     // first word of the segment's step records
     int32_t nw;      // words of step records (chunk padding included)
-    int32_t pad;
+    int32_t alias;   // first word of the segment's alias table, or -1
 };
 
 constexpr uint32_t kResAdd2 = 0xFE;
@@ -85,6 +89,7 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
     uint32_t w = lane < u.nw ? sp[lane] : 0u;  // first chunk of step records
     const uint64_t mine = lane < n ? bufs[lane] : 0;
     const uint32_t plo = uint32_t(mine), phi = uint32_t(mine >> 32);
+    const uint32_t aw = u.alias >= 0 && lane < 16 ? prog[u.alias + lane] : 0xFFFFFFFFu;
     // the pointers (and the first records) have arrived: the row loads
     // below then go out back to back, with no wait between them
     __builtin_amdgcn_s_waitcnt(0);
@@ -226,7 +231,10 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
         for (int j = 0; j < 8; ++j) {
             b[j] = m ? __builtin_ctzll(m) : -1;
             m &= m - 1;
-            if (b[j] >= 0) x[j] = rows[b[j] * 64 + lane];
+            if (b[j] >= 0) {
+                const int r = res_byte(uint32_t(__builtin_amdgcn_readlane(int(aw), b[j] >> 2)), b[j] & 3);
+                x[j] = rows[(r == 0xFF ? b[j] : r) * 64 + lane];
+            }
         }
         if (act) {
 #pragma unroll

@@ -238,7 +238,9 @@ static int32_t res_waves(int32_t n, int64_t units) {
 // touch of such a row after the step that consumes it overwrites it), become
 // one chain record that keeps the running result in registers and writes
 // only the last one.
-static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint32_t>& w) {
+static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint32_t>& w,
+                           std::vector<uint8_t>& alias) {
+    alias.assign(64, 0xFF);
     const size_t L = st.size();
     std::vector<uint64_t> rd(L, 0), wr(L, 0);
     for (size_t j = 0; j < L; ++j) {
@@ -303,9 +305,18 @@ static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint
             for (size_t i = 0; i < k; ++i) rec[1 + i / 4] |= uint32_t(x.srcs[i]) << (8 * (i % 4));
         }
         put(rec);
-        // then the same value into the other destinations, the list padded
-        // to a multiple of four by repeating its last row
-        if (x.dsts.size() > 1) {
+        // then the same value into the other destinations: when nothing
+        // touches them afterwards and nothing writes the first one, the
+        // store pass takes their values from the first one's row (alias);
+        // otherwise a store record, its list padded to a multiple of four by
+        // repeating its last row
+        bool aliased = x.dsts.size() > 1;
+        for (size_t i = 1; i < x.dsts.size() && aliased; ++i)
+            aliased = next[j * 64 + size_t(x.dsts[i])] < 0;
+        for (size_t i = j + 1; i < L && aliased; ++i) aliased = !(wr[i] >> x.dsts[0] & 1);
+        if (aliased) {
+            for (size_t i = 1; i < x.dsts.size(); ++i) alias[size_t(x.dsts[i])] = uint8_t(x.dsts[0]);
+        } else if (x.dsts.size() > 1) {
             std::vector<int32_t> ds(x.dsts.begin() + 1, x.dsts.end());
             while (ds.size() % 4) ds.push_back(ds.back());
             rec.assign(1 + ds.size() / 4, 0u);
@@ -350,14 +361,21 @@ static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
         }
     }
     std::vector<std::vector<uint32_t>> recs(nseg);
+    std::vector<std::vector<uint8_t>> alias(nseg);
     for (size_t sg = 0; sg < nseg; ++sg)
-        if (!steps[sg].empty()) encode_segment(steps[sg], recs[sg]);
+        if (!steps[sg].empty()) encode_segment(steps[sg], recs[sg], alias[sg]);
     std::vector<uint32_t> prog;
-    std::vector<int32_t> rec_off(nseg, -1);
+    std::vector<int32_t> rec_off(nseg, -1), alias_off(nseg, -1);
     for (size_t sg = 0; sg < nseg; ++sg) {
         if (recs[sg].empty()) continue;
         rec_off[sg] = int32_t(prog.size());
         prog.insert(prog.end(), recs[sg].begin(), recs[sg].end());
+        if (std::any_of(alias[sg].begin(), alias[sg].end(), [](uint8_t a) { return a != 0xFF; })) {
+            alias_off[sg] = int32_t(prog.size());
+            for (size_t i = 0; i < 64; i += 4)
+                prog.push_back(uint32_t(alias[sg][i]) | uint32_t(alias[sg][i + 1]) << 8 |
+                               uint32_t(alias[sg][i + 2]) << 16 | uint32_t(alias[sg][i + 3]) << 24);
+        }
         if (prog.size() > size_t(INT32_MAX)) return;
     }
     const int64_t te = int64_t(64) * VEC;
@@ -377,6 +395,7 @@ static void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd) {
             u.nv = int32_t(std::min(te, sd.cuts[sg + 1] - u.lo) / VEC);
             u.off = rec_off[sg];
             u.nw = int32_t(recs[sg].size());
+            u.alias = alias_off[sg];
             units.push_back(u);
         }
     }
@@ -432,7 +451,7 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
         }
     }
     for (const LaunchDesc& L : ex.launches)
-        pc[size_t(L.xphase)].t_launch += kLaunchNs + double(L.bytes) / kBytesPerNs;
+        pc[size_t(L.xphase)].t_launch += kLaunchNs + std::max(kKernelMinNs, double(L.bytes) / kBytesPerNs);
     return pc;
 }
 
@@ -458,8 +477,10 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
     const int32_t W = res_waves(p.n, int64_t(tiles));
     const int64_t per_cu = std::max<int64_t>(
         1, std::min<int64_t>(W == 4 ? 8 : kResWavesPerCU, kLdsBytesPerCU / (int64_t(p.n) * 1024)));
+    // workgroups sharing a compute unit when the tiles are spread evenly
+    const double sharing = std::min(double(per_cu), std::ceil(tiles / double(kNumCUs)));
     const double rounds = std::ceil(tiles / double(kNumCUs * per_cu)) *
-                          (1.0 + kResShare * double(per_cu - 1));
+                          (1.0 + kResShare * (sharing - 1.0));
     const int32_t P = int32_t(pc.size());
     std::vector<int32_t> nl(size_t(P), 0);
     for (const LaunchDesc& L : ex.launches) ++nl[size_t(L.xphase)];
@@ -481,11 +502,14 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             // a run is priced from its last phase down: phase a chains into
             // phase a + 1 when both have one 2-source step per position
             const bool link = c.cover == 1 && c.kmax == 2 && c.dmax == 1;
+            // the run's last phase stores its further destinations through
+            // the alias table, at no step cost
+            const int32_t d = a == b - 1 ? 1 : c.dmax;
             chain += link && next_link ? kResChainNs
                      : double(c.cover) *
-                           (c.kmax <= 2 && c.dmax == 1
+                           (c.kmax <= 2 && d == 1
                                 ? kResFastNs
-                                : kResStepNs + kResStepNsPerSrc * c.kmax + kResStepNsPerDst * c.dmax);
+                                : kResStepNs + kResStepNsPerSrc * c.kmax + kResStepNsPerDst * d);
             next_link = link;
             touched |= c.touched;
             if (b - a == 1 && nl[size_t(a)] < 2) continue;
@@ -493,7 +517,7 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             bool res = false;
             if (res_ok) {
                 const double rows = 2.0 * double(__builtin_popcountll(touched));
-                const double t_waves = rounds * (kResWaveNs + kResRowNs / W * rows + chain);
+                const double t_waves = rounds * (kResRowNs / W * rows + chain);
                 const double t_bytes = rows * double(p.N) * p.esize / kBytesPerNs;
                 const double t_res = kLaunchNs + std::max(t_waves, t_bytes) +
                                      kResOverlap * std::min(t_waves, t_bytes);

@@ -36,10 +36,10 @@ def _resident_tables(handle, stage):
     if st != arplan.AR_OK:
         return None
     nunits, nw = info[2], info[3]
-    units = (ctypes.c_int64 * (6 * nunits))()
+    units = (ctypes.c_int64 * (7 * nunits))()
     prog = (ctypes.c_uint32 * max(1, nw))()
     assert f(handle, stage, info, units, prog) == arplan.AR_OK
-    return ([tuple(units[6 * i:6 * i + 6]) for i in range(nunits)],
+    return ([tuple(units[7 * i:7 * i + 7]) for i in range(nunits)],
             np.array(prog[:nw], dtype=np.uint32))
 
 
@@ -97,8 +97,15 @@ def _interpret(tables, bufs, dtype):
     units, prog = tables
     vec = 8 if dtype == "bf16" else 4
     out = [b.copy() for b in bufs]
-    for lo, load, store, nv, off, nw in units:
+    for lo, load, store, nv, off, nw, alias in units:
         hi = lo + nv * vec
+        # buffer b takes its stored value from row src[b] (the alias table)
+        src = list(range(64))
+        if alias >= 0:
+            for b in range(64):
+                a = (int(prog[alias + b // 4]) >> (8 * (b % 4))) & 0xFF
+                if a != 0xFF:
+                    src[b] = a
         rows = {}
         for b in _bits(load):
             rows[b] = bufs[b][lo:hi].copy()
@@ -122,7 +129,7 @@ def _interpret(tables, bufs, dtype):
             rows[d] = val
             last = val
         for b in _bits(store):
-            out[b][lo:hi] = rows[b]
+            out[b][lo:hi] = rows[src[b]]
     return out
 
 
@@ -212,15 +219,16 @@ def test_ring_program_is_one_chain_and_a_broadcast():
     # Ring n = 64: the 62 ReduceScatter steps of a block each fold the previous
     # partial sum, whose row is overwritten by the final broadcast: one chain
     # record of 62 adds (start row and 62 rows), then the last step: its add
-    # into one buffer and a store into the 63 others (padded to 64)
+    # into one buffer, whose row the other 63 buffers take their values from
+    # (alias table)
     n, N = 64, 64 * 64 * 4
     with arplan.Plan(n, N, "f32", "ring") as p:
         p.set_option(arplan.AR_OPT_SLICE, 1)
         units, prog = _resident_tables(p.handle, 0)
-        for lo, load, store, nv, off, nw in units:
+        for lo, load, store, nv, off, nw, alias in units:
             recs = _decode(prog[off:off + nw])
-            assert [r[0] for r in recs] == ["chain", "add", "store"]
-            assert len(recs[0][1]) == 63 and len(recs[2][1]) == 64
+            assert [r[0] for r in recs] == ["chain", "add"] and alias >= 0
+            assert len(recs[0][1]) == 63
 
 
 def _wide_random_plan(rng, n, M):
@@ -284,7 +292,7 @@ def test_wide_random_plans_use_every_record_kind():
         try:
             arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 1)
             units, prog = _resident_tables(h, 0)
-            for lo, load, store, nv, off, nw in units:
+            for lo, load, store, nv, off, nw, alias in units:
                 kinds |= {r[0] for r in _decode(prog[off:off + nw])}
         finally:
             arplan.ar_plan_destroy(h)
