@@ -1,14 +1,17 @@
-// Executor: turns a plan's phases into batched kernel launches on a HIP
-// stream, plus the timing API.
+// Executor: turns a plan's executed phases into kernel launches on a HIP
+// stream, plus the timing API and the executor options.
 //
-// Per phase, the steps are grouped by source count k (copies are k = 1) and
-// each group becomes one launch of phase_kernel<dtype, k, aligned>; the
-// built-in plans have one group per phase.  Kernels read each step as a
-// record holding its range and its resolved buffer pointers (StepHead);
-// the records of a buffer set are built on the host and uploaded once, and a
-// small per-plan cache keeps them per device, so repeated executes on the
-// same buffers launch kernels only.  The sliced-launch tables are uploaded
-// on the first execute on a device.
+// An execution is a list of stages (schedule.cpp): phase launches, where the
+// steps of one phase with the same source count k (copies are k = 1) run as
+// one launch of phase_kernel<dtype, k, aligned, cache mode>, and sliced
+// launches of runs of phases (sliced_kernel, or resident_kernel).  Kernels
+// read each step as a record holding its range and its resolved buffer
+// pointers (StepHead); the records of a buffer set, followed by its n buffer
+// pointers, are built on the host and uploaded once, and a small per-plan
+// cache keeps them per device, so repeated executes on the same buffers
+// launch kernels only.  The tile, sliced and resident tables are uploaded on
+// the first execute on a device.  Buffers that are not 16-byte aligned run
+// every phase as its phase launches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

@@ -16,7 +16,7 @@
 // reads some range more than once, stores unless the launch's output is small
 // enough to stay cached for the next phase.  Unaligned head and tail elements of a
 // step are done element-wise.  A wave reads its step as one record with the
-// buffer pointers already resolved (see StepRec): wave-uniform, in scalar
+// buffer pointers already resolved (see StepHead): wave-uniform, in scalar
 // registers after a single dependent load.
 #pragma once
 

@@ -1,6 +1,7 @@
 // Launch scheduling: executed phases become phase launches (steps grouped by
-// source count, tiled, cache mode chosen) and sliced runs (chosen by a cost
-// model).  Host only.
+// source count, tiled, cache mode chosen) and sliced runs, plain or resident
+// (their tables, and the resident programs), chosen by a cost model.  Host
+// only.
 #include <algorithm>
 #include <cmath>
 #include <map>
