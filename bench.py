@@ -30,6 +30,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -42,12 +43,22 @@ KERNEL_OF = {-1: "sliced_kernel", -2: "resident_kernel"}
 DEFAULT = "rhd_n8_f32"
 
 
+def _code_only(text):
+    """C/C++ source without comments and blank space, so that a hash of it
+    changes with the code only (the sources hold no string with // or /*)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash():
+    """Hash of the code of the kernels and of the host code that decides
+    their launches (comments and layout excluded)."""
     h = hashlib.sha256()
     for f in ("kernels.hpp", "resident.hpp", "exec.hip", "exec_state.hpp", "rewrite.cpp",
               "schedule.cpp"):
-        with open(os.path.join(ROOT, "paper_2409_04202_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2409_04202_amd", "csrc", f)) as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

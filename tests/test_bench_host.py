@@ -41,3 +41,21 @@ def test_parallel_oracle_equals_oracle(name, N):
         got = bench.parallel_execute(plan, [x.copy() for x in xs], c["dtype"], pool)
     for q in range(len(xs)):
         assert np.array_equal(got[q], want[q])
+
+
+def test_kernel_source_hash_ignores_comments_only():
+    # the hash that ties the committed traffic counters to the kernel code
+    # changes with code, not with comments or layout
+    a = "int f(int x) {  // twice\n    return 2 * x; /* doubled */\n}\n"
+    b = "// header\nint f(int x) {\n  return 2 * x;\n}\n"
+    c = "int f(int x) {\n    return 3 * x;\n}\n"
+    assert bench._code_only(a) == bench._code_only(b)
+    assert bench._code_only(a) != bench._code_only(c)
+    # the stripping assumes no string literal holds a comment marker
+    csrc = os.path.join(ROOT, "paper_2409_04202_amd", "csrc")
+    for f in ("kernels.hpp", "resident.hpp", "exec.hip", "exec_state.hpp", "rewrite.cpp",
+              "schedule.cpp"):
+        for line in open(os.path.join(csrc, f)):
+            code = line.split("//")[0]
+            for lit in code.split('"')[1::2]:
+                assert "//" not in lit and "/*" not in lit, (f, line)
