@@ -18,7 +18,8 @@ using namespace arp;
 // Host-side check of the executed phases and the launch tiling (no GPU):
 // every executed phase is free of hazards, and walking every wave tile of
 // every launch with the kernel's own index helpers covers each step exactly
-// once, in bounds, with 16-byte aligned vector parts.  Declared in csrc/ar_debug.h (test hook, not part of the ABI).
+// once, in bounds, with 16-byte aligned vector parts (the padding entries of
+// a tile table excepted, which the kernel skips).
 AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                                           char* msg, int64_t msglen) {
     clear_error();
@@ -51,6 +52,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 if (unit >= L.nunits) continue;  // the kernel returns here
                 int64_t s, t;
                 unit_tile(unit, tiles, L.tiles_per_step, s, t);
+                if (tiles && s == -1 && t == 0) continue;  // padding entry: the kernel skips it
                 if (s < 0 || s >= L.count || t < 0) return bad("unit maps outside the launch");
                 const DevStep& st = ex->hsteps[size_t(L.first + s)];
                 if (st.k < 1 || st.src_off < 0 ||

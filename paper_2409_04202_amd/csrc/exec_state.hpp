@@ -96,6 +96,11 @@ constexpr double kResOverlap = 0.5;
 constexpr int64_t kResWavesPerCU = 16;
 constexpr int64_t kLdsBytesPerCU = int64_t(160) << 10;
 constexpr int64_t kNumCUs = 256;
+constexpr int64_t kNumXCDs = 8;         // compute dies, each with its own L2
+// Copy launches whose steps read a range several times deal their tiles to
+// XCDs by source range (xcd_tiles in schedule.cpp) when a step has at most
+// this many tiles.
+constexpr int64_t kXcdMaxTiles = 64;
 
 struct LaunchDesc {
     int32_t phase;

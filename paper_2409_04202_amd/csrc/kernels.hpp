@@ -433,6 +433,7 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     unit_tile(unit, tiles, tiles_per_step, s, t);
     s = uniform64(s);
     t = uniform64(t);
+    if (s < 0) return;  // a padding entry of a tile table
     const uint64_t* rec = recs + s * stride;
     const StepHead st = *reinterpret_cast<const StepHead*>(rec);
     const int k = K ? K : st.k;

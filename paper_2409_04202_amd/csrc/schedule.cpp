@@ -20,6 +20,55 @@ int kernel_k(int32_t k) {
     }
 }
 
+// Tile table of a copy launch whose steps read some range more than once:
+// the copies reading the same range are grouped, the range is cut into
+// super-tiles of one workgroup's worth of tiles, and each super-tile is dealt
+// to one XCD, where one workgroup per copy runs it, one after the other: the
+// repeated reads of a super-tile hit that XCD's L2 instead of going to
+// memory again, and each workgroup still writes one contiguous stretch.
+// Workgroups are dispatched to the kNumXCDs XCDs round-robin by workgroup
+// id, so workgroup b runs on XCD b % kNumXCDs; the table gives each XCD the
+// same number of workgroups, padding with entries (-1, 0) that the kernel
+// skips.  Used for copies of at most kXcdMaxTiles tiles: the repeated reads
+// of longer copies come far enough apart for the last-level cache, shared by
+// all XCDs, to serve them, and their writes streamed better without the
+// grouping (measured).  Steps are idx[g0..g1) of executed phase xp, in
+// launch order.
+static bool xcd_tiles(const XPhase& xp, const std::vector<size_t>& idx, size_t g0, size_t g1,
+                      int64_t te, int64_t VEC, LaunchDesc& L, ExecState& ex) {
+    std::map<std::tuple<int32_t, int64_t, int64_t>, std::vector<int32_t>> groups;
+    for (size_t g = g0; g < g1; ++g) {
+        const XStep& x = xp.steps[idx[g]];
+        if (x.end > x.begin)
+            groups[std::make_tuple(x.srcs[0], x.begin, x.end)].push_back(int32_t(g - g0));
+    }
+    const int64_t wpb = L.wpb;
+    std::vector<std::vector<int2>> seq(static_cast<size_t>(kNumXCDs));
+    size_t next_xcd = 0;
+    for (const auto& gr : groups) {
+        const XStep& x = xp.steps[idx[g0 + size_t(gr.second[0])]];
+        const int64_t nt = (x.end - (x.begin & ~(VEC - 1)) + te - 1) / te;
+        for (int64_t t0 = 0; t0 < nt; t0 += wpb) {
+            std::vector<int2>& q = seq[next_xcd];
+            next_xcd = (next_xcd + 1) % size_t(kNumXCDs);
+            for (int32_t j : gr.second)
+                for (int64_t t = t0; t < t0 + wpb; ++t)
+                    q.push_back(t < nt ? make_int2(j, int(t)) : make_int2(-1, 0));
+        }
+    }
+    size_t len = 0;
+    for (const auto& q : seq) len = std::max(len, q.size());
+    const int64_t nunits = int64_t(len) * kNumXCDs;
+    if ((nunits + wpb - 1) / wpb > kMaxBlocks) return false;
+    L.tile_off = int64_t(ex.htiles.size());
+    for (size_t q0 = 0; q0 < len; q0 += size_t(wpb))  // block q0 / wpb of each XCD
+        for (size_t x = 0; x < size_t(kNumXCDs); ++x)
+            for (size_t u = q0; u < q0 + size_t(wpb); ++u)
+                ex.htiles.push_back(u < seq[x].size() ? seq[x][u] : make_int2(-1, 0));
+    L.nunits = nunits;
+    return true;
+}
+
 // Group the steps of every executed phase by source count, choose the
 // tiling and the cache mode of each launch.  Host only.
 static void build_launches(const Plan& p, ExecState& ex) {
@@ -119,7 +168,10 @@ static void build_launches(const Plan& p, ExecState& ex) {
             L.tiles_per_step = (maxspan + te - 1) / te;
             int64_t used = 0;
             for (int64_t sp : spans) used += (sp + te - 1) / te;
-            if (used * 5 < L.count * L.tiles_per_step * 4) {
+            if (k == 1 && reuse && L.tiles_per_step <= kXcdMaxTiles &&
+                xcd_tiles(xp, idx, g0, g1, te, VEC, L, ex)) {
+                // copies reading the same range run on one XCD (tile table)
+            } else if (used * 5 < L.count * L.tiles_per_step * 4) {
                 // uneven steps: explicit tile table
                 L.tile_off = int64_t(ex.htiles.size());
                 for (int64_t j = 0; j < L.count; ++j) {
