@@ -41,14 +41,15 @@ constexpr int64_t kKeepBytes = int64_t(256) << 20;
 constexpr int32_t kFuseDst = 2;
 constexpr int64_t kFuseBytes = int64_t(256) << 20;
 // Automatic choice of sliced launches (AR_OPT_SLICE = 2).  A run of
-// consecutive executed phases may become one sliced launch when every phase
-// in it writes at most kKeepBytes (what one phase hands to the next would
-// stay in the last-level cache with phase launches as well) and moves at most
-// kSliceMaxBytes.  The runs are chosen by dynamic programming over the phases
+// consecutive executed phases may become one plain sliced launch when every
+// phase in it writes at most kKeepBytes (what one phase hands to the next
+// would stay in the last-level cache with phase launches as well) and moves
+// at most kSliceMaxBytes; a resident run (below) keeps what its phases hand
+// on in LDS and takes phases of any size.  The runs are chosen by dynamic programming over the phases
 // with a cost model fitted to MI355X measurements (back-to-back launches, no
 // events between them):
-//  * a phase launch costs kLaunchNs plus its bytes at kBytesPerNs, at least
-//    kKernelMinNs (one dependent load and store through memory);
+//  * a phase launch costs kLaunchNs plus its HBM traffic at kBytesPerNs, at
+//    least kKernelMinNs (one dependent load and store through memory);
 //  * a sliced launch costs kLaunchNs plus, per phase, the largest of its
 //    dependent chain, its read time and its write time.  The chain is the
 //    most steps covering one element position, which a wavefront runs one
@@ -116,6 +117,8 @@ struct LaunchDesc {
     int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
     int32_t max_dst;         // most destinations of a step
     int64_t bytes;           // (k + destinations) * len * e over the steps
+    int64_t hbm;             // predicted HBM traffic: bytes, less the repeated
+                             // reads of a range by the launch's copies
     int64_t rec_off;         // first word of its steps' records
     int64_t rec_stride;      // words per record
 };

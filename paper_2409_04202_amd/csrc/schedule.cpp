@@ -4,6 +4,7 @@
 // only.
 #include <algorithm>
 #include <cmath>
+#include <limits>
 #include <map>
 #include <memory>
 #include <tuple>
@@ -168,6 +169,15 @@ static void build_launches(const Plan& p, ExecState& ex) {
             L.tiles_per_step = (maxspan + te - 1) / te;
             int64_t used = 0;
             for (int64_t sp : spans) used += (sp + te - 1) / te;
+            // copies reading the same range run next to each other (or on one
+            // XCD, below): their repeated reads hit the cache
+            L.hbm = bytes;
+            if (k == 1 && reuse) {
+                L.hbm = written;
+                for (size_t r = 0; r < ranges.size(); ++r)
+                    if (r == 0 || ranges[r] != ranges[r - 1])
+                        L.hbm += (std::get<2>(ranges[r]) - std::get<1>(ranges[r])) * p.esize;
+            }
             if (k == 1 && reuse && L.tiles_per_step <= kXcdMaxTiles &&
                 xcd_tiles(xp, idx, g0, g1, te, VEC, L, ex)) {
                 // copies reading the same range run on one XCD (tile table)
@@ -504,7 +514,7 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
         }
     }
     for (const LaunchDesc& L : ex.launches)
-        pc[size_t(L.xphase)].t_launch += kLaunchNs + std::max(kKernelMinNs, double(L.bytes) / kBytesPerNs);
+        pc[size_t(L.xphase)].t_launch += kLaunchNs + std::max(kKernelMinNs, double(L.hbm) / kBytesPerNs);
     return pc;
 }
 
@@ -546,9 +556,15 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
         double body = 0.0, chain = 0.0;
         uint64_t touched = 0;
         bool next_link = false;
+        // a plain sliced run hands data between its phases through the
+        // cache, so its phases must be small; a resident run keeps them in
+        // LDS and takes phases of any size
+        bool plain_ok = true;
         for (int32_t a = b - 1; a >= 0; --a) {
             const PhaseCost& c = pc[size_t(a)];
-            if (!c.aligned || c.written > kKeepBytes || c.bytes > kSliceMaxBytes) break;
+            if (!c.aligned) break;
+            plain_ok = plain_ok && c.written <= kKeepBytes && c.bytes <= kSliceMaxBytes;
+            if (!plain_ok && !res_ok) break;
             body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
                               stretch * double(c.read) / kBytesPerNs,
                               double(c.written) / kBytesPerNs});
@@ -566,7 +582,7 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             next_link = link;
             touched |= c.touched;
             if (b - a == 1 && nl[size_t(a)] < 2) continue;
-            double t = kLaunchNs + body;
+            double t = plain_ok ? kLaunchNs + body : std::numeric_limits<double>::infinity();
             bool res = false;
             if (res_ok) {
                 const double rows = 2.0 * double(__builtin_popcountll(touched));

@@ -302,6 +302,7 @@ def test_executor_rewrites_launch_structure():
     # RHD: each eighth is reduced once and stored to all 8 buffers (its
     # copies read every range once, so the rewrite applies at any size)
     with arplan.Plan(8, 1 << 26, "f32", "rhd") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 0)
         L = p.launches()
         assert [(x[0], x[1], x[2], x[3]) for x in L] == [(0, 2, 1, 8), (1, 2, 1, 8), (2, 2, 8, 8)]
         assert L[2][4] == 8 * (2 + 8) * (1 << 26) // 8 * 4
@@ -473,8 +474,9 @@ def test_gentree_errors():
 def test_sliced_runs_of_workloads(name):
     # AR_OPT_SLICE = 2 partitions the executed phases into sliced runs and
     # phase launches: the same executed steps (same bytes) as the phase
-    # launches, every launch tiled exactly, and no sliced launch on the
-    # 2 GiB RHD plan, whose phases each write more than the 256 MiB cache
+    # launches, every launch tiled exactly; the 2 GiB RHD plan, whose
+    # phases each write more than the 256 MiB cache, runs resident or as
+    # phase launches, never plain sliced
     from paper_2409_04202_amd import workloads
     c = workloads.CONFIGS[name]
     esize = 2 if c["dtype"] == "bf16" else 4
@@ -499,7 +501,11 @@ def test_sliced_runs_of_workloads(name):
             st, msg = _check_tiling(p.handle, vecok)
             assert st == arplan.AR_OK, msg
         if name == "rhd_n8_f32":
-            assert all(x[0] >= 0 for x in L)
+            # each buffer in and out once: 4 GiB against 7.5 GiB of phases
+            assert [(x[0], x[4]) for x in L] == [(-2, 2 * c["n"] * c["N"] * esize)]
+            p.set_option(arplan.AR_OPT_RESIDENT, 0)
+            assert all(x[0] >= 0 for x in p.launches())
+            p.set_option(arplan.AR_OPT_RESIDENT, 1)
         if name == "tree8x8x8_n512_bf16":
             # the last AllGather phase covers each position with 448 copies:
             # a chain far too long for a sliced launch
