@@ -300,15 +300,25 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                 const SliceDesc& sd = ex->slices[size_t(stg.slice)];
                 const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(64 * sd.res_waves);
                 const size_t lds = size_t(plan->n) * 1024;
-#define AR_RESIDENT(DT, W)                                                                    \
-    hipLaunchKernelGGL((resident_kernel<DT, W>), grid, block, lds, stream, pe->dev + ex->rec_words, \
-                       plan->n, d->runits + sd.runit_base, d->prog + sd.prog_base, sd.nunits)
-                const bool four = sd.res_waves == 4;
+#define AR_RESIDENT(DT, W, NT)                                                                \
+    hipLaunchKernelGGL((resident_kernel<DT, W, NT>), grid, block, lds, stream,                \
+                       pe->dev + ex->rec_words, plan->n, d->runits + sd.runit_base,           \
+                       d->prog + sd.prog_base, sd.nunits)
+                // runs moving more than the last-level cache holds stream
+                // their rows past it
+                const bool nt = sd.res_bytes > 2 * kKeepBytes;
+#define AR_RESIDENT_W(DT)                                                                     \
+    if (sd.res_waves == 4) {                                                                  \
+        if (nt) AR_RESIDENT(DT, 4, true); else AR_RESIDENT(DT, 4, false);                     \
+    } else {                                                                                  \
+        if (nt) AR_RESIDENT(DT, 1, true); else AR_RESIDENT(DT, 1, false);                     \
+    }
                 switch (plan->dtype) {
-                    case AR_F32: if (four) AR_RESIDENT(DT_F32, 4); else AR_RESIDENT(DT_F32, 1); break;
-                    case AR_I32: if (four) AR_RESIDENT(DT_I32, 4); else AR_RESIDENT(DT_I32, 1); break;
-                    default: if (four) AR_RESIDENT(DT_BF16, 4); else AR_RESIDENT(DT_BF16, 1); break;
+                    case AR_F32: AR_RESIDENT_W(DT_F32); break;
+                    case AR_I32: AR_RESIDENT_W(DT_I32); break;
+                    default: AR_RESIDENT_W(DT_BF16); break;
                 }
+#undef AR_RESIDENT_W
 #undef AR_RESIDENT
             } else if (stg.slice >= 0) {
                 const SliceDesc& sd = ex->slices[size_t(stg.slice)];

@@ -14,7 +14,9 @@ namespace arp {
 // Its W wavefronts (1 or 4) load the rows the run reads before writing them
 // (global_load_lds_dwordx4: straight into LDS, all in flight at once; wave w
 // takes the rows b with b % W == w), wave 0 runs the steps of every phase of
-// the run on the rows, and all waves store the rows the run wrote.  Four
+// the run on the rows, and all waves store the rows the run wrote.  NT marks
+// the row loads and stores nontemporal (cache policy NT), for runs whose
+// traffic is larger than the last-level cache.  Four
 // waves issue the row loads and stores four times as fast; one wave per
 // workgroup lets a compute unit hold more tiles when LDS does not limit it.
 // A phase costs a few LDS accesses instead of a round trip through the
@@ -71,7 +73,7 @@ constexpr uint32_t kResStore = 0xFA;
 
 __device__ __forceinline__ int res_byte(uint32_t x, int i) { return int((x >> (8 * i)) & 0xFFu); }
 
-template <int DT, int W>
+template <int DT, int W, bool NT>
 __global__ __launch_bounds__(64 * W) void resident_kernel(
     const uint64_t* __restrict__ bufs, int32_t n, const ResUnit* __restrict__ units,
     const uint32_t* __restrict__ prog, int64_t nunits) {
@@ -104,7 +106,7 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
     for (uint64_t m = u.load & mine_rows; m; m &= m - 1) {
         const int b = __builtin_ctzll(m);
         __builtin_amdgcn_global_load_lds((const AR_GLOBAL void*)(at(b)),
-                                         (AR_LDS void*)(rows + b * 64), 16, 0, 0);
+                                         (AR_LDS void*)(rows + b * 64), 16, 0, NT ? 2 : 0);
     }
     if (W == 1) __builtin_amdgcn_s_waitcnt(0);
     else __syncthreads();  // waits for this wave's loads, then for every wave
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
         if (act) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if (b[j] >= 0) *at(b[j]) = x[j];
+                if (b[j] >= 0) vstore<NT>(at(b[j]), x[j]);
         }
     }
 }
