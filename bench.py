@@ -14,16 +14,21 @@ region.
 
 Prints one JSON line:
   value       AllReduce algorithm bandwidth n * N * e / time, GB/s
-  roofline    the reduce launches of the phase kernel: algorithmic bytes per
-              launch ((k + d) * len * e per step folding k sources into d
-              destinations) over their mean duration (HIP events on the
-              launch stream), against MI355X's 8 TB/s HBM peak
+  roofline    the launches that reduce (k >= 2 sources): algorithmic bytes
+              per launch over their mean duration (HIP events on the launch
+              stream), against MI355X's 8 TB/s HBM peak.  A phase or plain
+              sliced launch moves (k + d) * len * e per step folding k
+              sources into d destinations; a resident launch moves each
+              buffer tile its run reads in once and each it writes out once
   cpu_baseline  the CPU oracle executing the same plan on the host
 and, beside the contract's fields: the step time's median and minimum over
 individually timed executions, the whole plan's and the copy launches'
 fractions of the peak, a practical ceiling measured in the same run (a plain
-device copy and a two-source fold through the library, 2 GiB each), and the
-oracle with the steps of each phase spread over a thread pool.
+device copy and a two-source fold through the library, 2 GiB each), the
+oracle with the steps of each phase spread over a thread pool, and, when the
+default executor runs sliced or resident launches, the same plan with one
+launch per executed phase (`phase_launches`: its time, and its reduce
+launches' algorithmic bytes against the peak).
 """
 
 import argparse
@@ -205,6 +210,51 @@ def cpu_baseline(name, budget_s=25.0):
             "seconds": round(spent, 3)}
 
 
+def launch_ms(torch, arplan, plan, ptrs, sh, K, nlaunch):
+    """Mean duration of each launch of the plan over K executions, from HIP
+    events around every launch on the launch stream (ms)."""
+    cap = max(1, K * nlaunch)
+    timer = arplan.ar_timer_create(cap)
+    torch.cuda.synchronize()
+    for _ in range(K):
+        plan.execute_timed(ptrs, sh, timer)
+    torch.cuda.synchronize()
+    recs = arplan.ar_timer_read(timer, cap)
+    arplan.ar_timer_destroy(timer)
+    l_ms = [0.0] * nlaunch
+    for li, ms in recs:
+        l_ms[li] += ms / K
+    return l_ms
+
+
+def phase_form(torch, arplan, plan, ptrs, sh, K, restore, total):
+    """Time the plan with one launch per executed phase (AR_OPT_SLICE = 0):
+    K back-to-back executions, then the reduce launches' algorithmic bytes
+    over their durations against the HBM peak."""
+    launches = plan.launches()
+    restore()
+    plan.execute(ptrs, sh)
+    restore()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        plan.execute(ptrs, sh)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / K
+    restore()
+    l_ms = launch_ms(torch, arplan, plan, ptrs, sh, K, len(launches))
+    red = [i for i, L in enumerate(launches) if L[1] >= 2]
+    red_ms = sum(l_ms[i] for i in red)
+    red_gbs = sum(launches[i][4] for i in red) / (red_ms * 1e-3) / 1e9 if red_ms > 0 else 0.0
+    return {"ms_per_step": round(ms_step, 5),
+            "value": round(total / (ms_step * 1e-3) / 1e9, 2),
+            "reduce_gbs": round(red_gbs, 1),
+            "reduce_frac": round(red_gbs / HBM_PEAK_GBS, 4),
+            "launches": [{"phase": L[0], "k": L[1], "max_dst": L[2], "steps": L[3],
+                          "bytes": L[4], "ms": round(m, 5)}
+                         for L, m in zip(launches, l_ms)]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -279,14 +329,7 @@ def main():
     t1 = time.perf_counter()
     # per-launch durations, outside the timed region
     restore()
-    cap = max(1, K * len(launches))
-    timer = arplan.ar_timer_create(cap)
-    torch.cuda.synchronize()
-    for _ in range(K):
-        plan.execute_timed(ptrs, sh, timer)
-    torch.cuda.synchronize()
-    recs = arplan.ar_timer_read(timer, cap)
-    arplan.ar_timer_destroy(timer)
+    l_ms = launch_ms(torch, arplan, plan, ptrs, sh, K, len(launches))
     # step time distribution: each execution between two events
     restore()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -303,9 +346,6 @@ def main():
     total = n * N * esize
     value = total / (ms_step * 1e-3) / 1e9
 
-    l_ms = [0.0] * len(launches)
-    for li, ms in recs:
-        l_ms[li] += ms / K
     # dominant kernel: the launches that reduce (k >= 2 sources)
     red = [i for i, L in enumerate(launches) if L[1] >= 2]
     red_ms = sum(l_ms[i] for i in red)
@@ -364,6 +404,14 @@ def main():
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    if (args.slice is None and args.resident is None
+            and any(L[0] < 0 for L in launches)):
+        # the same plan with one launch per executed phase, every phase's
+        # output going through HBM
+        print("bench: phase launches", file=sys.stderr, flush=True)
+        plan.set_option(arplan.AR_OPT_SLICE, 0)
+        out["phase_launches"] = phase_form(torch, arplan, plan, ptrs, sh, K,
+                                           restore, total)
     plan.close()
     del bufs, pristine
     if not args.no_ceiling:
