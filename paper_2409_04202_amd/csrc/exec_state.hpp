@@ -59,7 +59,7 @@ constexpr int64_t kFuseBytes = int64_t(256) << 20;
 //    stretched by kMinSliceWaves / waves when the slice has fewer wave tiles
 //    than that (too few loads in flight to reach full bandwidth).
 constexpr double kLaunchNs = 3000.0;
-constexpr double kKernelMinNs = 2000.0;
+constexpr double kKernelMinNs = 3000.0;
 constexpr double kBytesPerNs = 5500.0;
 constexpr double kStepNs = 350.0;
 constexpr double kStepNsPerSrcF32 = 120.0;

@@ -13,12 +13,13 @@ namespace arp {
 // for every buffer, in a 1 KiB LDS row (row b, lane l at rows[b * 64 + l]).
 // Its W wavefronts (1 or 4) load the rows the run reads before writing them
 // (global_load_lds_dwordx4: straight into LDS, all in flight at once; wave w
-// takes the rows b with b % W == w), wave 0 runs the steps of every phase of
-// the run on the rows, and all waves store the rows the run wrote.  NT marks
-// the row loads and stores nontemporal (cache policy NT), for runs whose
-// traffic is larger than the last-level cache.  Four
-// waves issue the row loads and stores four times as fast; one wave per
-// workgroup lets a compute unit hold more tiles when LDS does not limit it.
+// takes the rows b with b % W == w), run the steps of every phase of the run
+// on the rows (with four waves each wave on its own quarter of every row,
+// ResLane), and store the rows the run wrote.  NT marks the row loads and
+// stores nontemporal (cache policy NT), for runs whose traffic is larger
+// than the last-level cache.  Four waves issue the row loads and stores and
+// run the steps four times as fast; one wave per workgroup lets a compute
+// unit hold more tiles when LDS does not limit it.
 // A phase costs a few LDS accesses instead of a round trip through the
 // memory hierarchy, and each buffer position is read and written once per
 // run.
@@ -73,11 +74,55 @@ constexpr uint32_t kResStore = 0xFA;
 
 __device__ __forceinline__ int res_byte(uint32_t x, int i) { return int((x >> (8 * i)) & 0xFFu); }
 
+// One 32-bit word of an element vector: the accumulator of a lane that owns
+// a word (one fp32 or int32 element, or two bf16 elements) of each row.
+template <int DT> struct WAcc;
+template <> struct WAcc<DT_F32> {
+    float v;
+    __device__ __forceinline__ void init(uint32_t x) { v = __uint_as_float(x); }
+    __device__ __forceinline__ void add(uint32_t x) { v += __uint_as_float(x); }
+    __device__ __forceinline__ uint32_t out() const { return __float_as_uint(v); }
+};
+template <> struct WAcc<DT_I32> {
+    uint32_t v;
+    __device__ __forceinline__ void init(uint32_t x) { v = x; }
+    __device__ __forceinline__ void add(uint32_t x) { v += x; }
+    __device__ __forceinline__ uint32_t out() const { return v; }
+};
+template <> struct WAcc<DT_BF16> {
+    float lo, hi;
+    __device__ __forceinline__ void init(uint32_t x) { lo = bf16_lo(x); hi = bf16_hi(x); }
+    __device__ __forceinline__ void add(uint32_t x) { lo += bf16_lo(x); hi += bf16_hi(x); }
+    __device__ __forceinline__ uint32_t out() const { return bf16_pack(lo, hi); }
+};
+
+// What a lane of a W-wave workgroup owns of each row while the records run:
+// with one wave its 16-byte vector (row stride 64 vectors), with four waves
+// one 32-bit word of its wave's quarter of the row (wave w, lane l: word
+// 64 w + l, row stride 256 words).  Every record is element-wise, so the
+// waves run the same records on their own words with no barrier between
+// records; a quarter row is 256 contiguous bytes, so a wave's LDS accesses
+// hit every bank once.
+template <int DT, int W> struct ResLane;
+template <int DT> struct ResLane<DT, 1> {
+    using Word = u32x4;
+    using Acc = VAcc<DT>;
+    static constexpr int kStride = 64;
+};
+template <int DT> struct ResLane<DT, 4> {
+    using Word = uint32_t;
+    using Acc = WAcc<DT>;
+    static constexpr int kStride = 256;
+};
+
 template <int DT, int W, bool NT>
 __global__ __launch_bounds__(64 * W) void resident_kernel(
     const uint64_t* __restrict__ bufs, int32_t n, const ResUnit* __restrict__ units,
     const uint32_t* __restrict__ prog, int64_t nunits) {
     extern __shared__ u32x4 rows[];
+    using Word = typename ResLane<DT, W>::Word;
+    using Acc = typename ResLane<DT, W>::Acc;
+    constexpr int RS = ResLane<DT, W>::kStride;
     constexpr int VEC = Elem<DT>::VEC;
     const int lane = int(threadIdx.x) & 63;
     const int wv = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
@@ -110,20 +155,22 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
     }
     if (W == 1) __builtin_amdgcn_s_waitcnt(0);
     else __syncthreads();  // waits for this wave's loads, then for every wave
-    if (wv == 0) {
-        u32x4 last = {0u, 0u, 0u, 0u};  // result of the previous one-word record
-        int last_row = -1;               // the row it went to (-1: none)
+    // this lane's part of row b is R[b * RS]
+    Word* const R = reinterpret_cast<Word*>(rows) + (W == 1 ? lane : wv * 64 + lane);
+    {
+        Word last{};       // result of the previous one-word record
+        int last_row = -1;  // the row it went to (-1: none)
         for (int c0 = 0; c0 < u.nw; c0 += 64) {
             const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
             const int m = min(64, u.nw - c0);
             int c = 0;
             uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(w), 0));
-            u32x4 pa = last, pb = last;  // LDS reads issued for a one-word record
+            Word pa = last, pb = last;  // LDS reads issued for a one-word record
             auto issue = [&]() {
                 const uint32_t op = h & 0xFFu;
                 if (op == kResAdd2 || op == kResCopy) {
-                    pa = rows[res_byte(h, 1) * 64 + lane];
-                    pb = rows[res_byte(h, 2) * 64 + lane];
+                    pa = R[res_byte(h, 1) * RS];
+                    pb = R[res_byte(h, 2) * RS];
                 }
             };
             issue();
@@ -132,11 +179,11 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
                 if (op == 0) break;
                 if (op == kResAdd2 || op == kResCopy) {
                     const int r0 = res_byte(h, 1), r1 = res_byte(h, 2), d = res_byte(h, 3);
-                    const u32x4 a = r0 == last_row ? last : pa;
-                    u32x4 out = a;
+                    const Word a = r0 == last_row ? last : pa;
+                    Word out = a;
                     if (op == kResAdd2) {
-                        const u32x4 b = r1 == last_row ? last : pb;
-                        VAcc<DT> acc;
+                        const Word b = r1 == last_row ? last : pb;
+                        Acc acc;
                         acc.init(a);
                         acc.add(b);
                         out = acc.out();
@@ -144,24 +191,24 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
                     c += 1;
                     h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
                     issue();  // the next record's reads, before this write
-                    rows[d * 64 + lane] = out;
+                    R[d * RS] = out;
                     last = out;
                     last_row = d;
                 } else if (op == kResChain) {
                     const int mm = res_byte(h, 1), d = res_byte(h, 3);
-                    u32x4 cur = rows[res_byte(h, 2) * 64 + lane];
+                    Word cur = R[res_byte(h, 2) * RS];
                     for (int i0 = 0; i0 < mm; i0 += 8) {
                         const uint32_t wa = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (i0 >> 2)));
                         const uint32_t wb =
                             i0 + 4 < mm ? uint32_t(__builtin_amdgcn_readlane(int(w), c + 2 + (i0 >> 2))) : 0u;
-                        u32x4 y[8];
+                        Word y[8];
 #pragma unroll
                         for (int j = 0; j < 8; ++j)
-                            if (i0 + j < mm) y[j] = rows[res_byte(j < 4 ? wa : wb, j & 3) * 64 + lane];
+                            if (i0 + j < mm) y[j] = R[res_byte(j < 4 ? wa : wb, j & 3) * RS];
 #pragma unroll
                         for (int j = 0; j < 8; ++j)
                             if (i0 + j < mm) {
-                                VAcc<DT> acc;
+                                Acc acc;
                                 acc.init(cur);
                                 acc.add(y[j]);
                                 cur = acc.out();
@@ -170,19 +217,19 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
                     c += 1 + (mm + 3) / 4;
                     h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
                     issue();  // the next record's reads, before this write
-                    rows[d * 64 + lane] = cur;
+                    R[d * RS] = cur;
                     last = cur;
                     last_row = d;
                 } else if (op == kResFold) {
                     const int k = res_byte(h, 1), d = res_byte(h, 2);
-                    VAcc<DT> acc;
+                    Acc acc;
                     const int kg = k >> 2;  // full groups of four sources
                     for (int g = 0; g < kg; ++g) {
                         const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + g));
-                        const u32x4 a0 = rows[res_byte(x, 0) * 64 + lane];
-                        const u32x4 a1 = rows[res_byte(x, 1) * 64 + lane];
-                        const u32x4 a2 = rows[res_byte(x, 2) * 64 + lane];
-                        const u32x4 a3 = rows[res_byte(x, 3) * 64 + lane];
+                        const Word a0 = R[res_byte(x, 0) * RS];
+                        const Word a1 = R[res_byte(x, 1) * RS];
+                        const Word a2 = R[res_byte(x, 2) * RS];
+                        const Word a3 = R[res_byte(x, 3) * RS];
                         if (g == 0) acc.init(a0);
                         else acc.add(a0);
                         acc.add(a1);
@@ -192,29 +239,29 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
                     const int rem = k & 3;
                     if (rem) {
                         const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + kg));
-                        const u32x4 a0 = rows[res_byte(x, 0) * 64 + lane];
-                        const u32x4 a1 = rows[res_byte(x, rem > 1 ? 1 : 0) * 64 + lane];
-                        const u32x4 a2 = rows[res_byte(x, rem > 2 ? 2 : 0) * 64 + lane];
+                        const Word a0 = R[res_byte(x, 0) * RS];
+                        const Word a1 = R[res_byte(x, rem > 1 ? 1 : 0) * RS];
+                        const Word a2 = R[res_byte(x, rem > 2 ? 2 : 0) * RS];
                         if (kg == 0) acc.init(a0);
                         else acc.add(a0);
                         if (rem > 1) acc.add(a1);
                         if (rem > 2) acc.add(a2);
                     }
-                    const u32x4 out = acc.out();
+                    const Word out = acc.out();
                     c += 1 + ((k + 3) >> 2);
                     h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
                     issue();  // the next record's reads, before this write
-                    rows[d * 64 + lane] = out;
+                    R[d * RS] = out;
                     last = out;
                     last_row = d;
                 } else {  // kResStore: the previous result into nd rows
                     const int nq = res_byte(h, 1) >> 2;
                     for (int j = 0; j < nq; ++j) {
                         const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + j));
-                        rows[res_byte(x, 0) * 64 + lane] = last;
-                        rows[res_byte(x, 1) * 64 + lane] = last;
-                        rows[res_byte(x, 2) * 64 + lane] = last;
-                        rows[res_byte(x, 3) * 64 + lane] = last;
+                        R[res_byte(x, 0) * RS] = last;
+                        R[res_byte(x, 1) * RS] = last;
+                        R[res_byte(x, 2) * RS] = last;
+                        R[res_byte(x, 3) * RS] = last;
                     }
                     c += 1 + nq;
                     h = c < m ? uint32_t(__builtin_amdgcn_readlane(int(w), c)) : 0u;
