@@ -240,26 +240,31 @@ ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
  *  0: never; 1: the whole plan as one sliced launch whenever possible;
  *  2: the runs of phases a cost model predicts faster as sliced launches,
  *  among phases that each write at most 256 MiB (what one phase hands to the
- *  next then fits the last-level cache either way).  A run is possible when
+ *  next then fits the last-level cache either way) for a plain sliced launch,
+ *  of any size for a resident one.  A run is possible when
  *  every boundary of its steps is a multiple of 16 bytes; sliced launches
  *  are used only with 16-byte aligned buffers (otherwise every phase runs
  *  as its phase launches, those reported with AR_OPT_SLICE = 0). */
-/*  AR_OPT_RESIDENT (default 1): a sliced launch of a plan with n <= 64
- *  buffers may run resident instead: each wavefront keeps its tile of
- *  element positions of every buffer in on-chip memory (LDS) for the whole
- *  run, loading each buffer's tile before the run's first read of it and
- *  storing each tile the run writes after its last phase, so that the
- *  run's intermediate values stay on chip; every step is still run in
- *  order with the plan's sources in their listed order, so results are the
- *  same bits.  With AR_OPT_SLICE = 2 the cost model picks the plain or the
- *  resident form per run; with AR_OPT_SLICE = 1 the whole plan runs
- *  resident when n <= 64.  0: sliced launches always run plain. */
+/*  AR_OPT_RESIDENT (default 1): a sliced launch may run resident instead:
+ *  each workgroup keeps its tile of element positions in on-chip memory
+ *  (LDS) for the whole run, loading each buffer's tile once, before the
+ *  run's first read of it, and storing each tile the run writes once, with
+ *  its final value, so that the run's intermediate values stay on chip.
+ *  With n <= 64 buffers the tile of every buffer has its own LDS row; with
+ *  more (streamed form) the run's values share up to 64 LDS slots, each
+ *  value held from its load or computation to its last use, the folds
+ *  computed depth first and the loads issued ahead.  Every step still folds
+ *  the same values with the plan's sources in their listed order, so
+ *  results are the same bits.  With AR_OPT_SLICE = 2 the cost model picks
+ *  the plain or the resident form per run; with AR_OPT_SLICE = 1 the whole
+ *  plan runs resident.  0: sliced launches always run plain. */
 typedef enum ar_option { AR_OPT_FUSE = 0, AR_OPT_SLICE = 1, AR_OPT_RESIDENT = 2 } ar_option;
 ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value);
 
 /* The kernel launches one execution on 16-byte aligned buffers issues (host
  * only, no GPU call): their number, and for launch i the plan phase its
- * steps come from (-1 for a sliced launch, -2 for a resident one), their
+ * steps come from (-1 for a sliced launch, -2 for a resident one, -3 for a
+ * streamed resident one), their
  * source count (the
  * largest, for a sliced launch), the most destinations any of its
  * steps stores to, its number of steps and its algorithmic bytes:

@@ -26,13 +26,15 @@ ar_status ar_debug_exec_steps(ar_plan* plan, int64_t step_cap, int32_t* phase,
                               int64_t* count, int64_t* idx_count);
 
 /* The tables of launch `stage` (as in ar_plan_launch_info) when it is a
- * resident sliced launch: info[0..3] = first executed phase, number of
- * phases, number of units (workgroups), words of the program; units[7 i ..
- * 7 i + 6] = first element of unit i's tile, rows to load (bit b = buffer
- * b), rows to store, 16-byte vectors in the tile, first word and number of
- * words of its step records, first word of its alias table (-1: none);
- * prog the program words (the resident kernel's encoding).  Call with NULL arrays to read info first.  AR_ERR_INVALID_ARG
- * when the launch is not resident.  Host only. */
+ * resident or streamed sliced launch: info[0..4] = first executed phase,
+ * number of phases, number of units (workgroups), words of the program, LDS
+ * slots (0: a resident launch, one row per buffer); units[7 i .. 7 i + 6] =
+ * first element of unit i's tile, rows to load (bit b = buffer b), rows to
+ * store, 16-byte vectors in the tile, first word and number of words of its
+ * step records, first word of its alias table (-1: none; masks 0 and no
+ * alias table for a streamed launch); prog the program words (the resident
+ * or streamed kernel's encoding).  Call with NULL arrays to read info
+ * first.  AR_ERR_INVALID_ARG when the launch is neither.  Host only. */
 ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* info,
                             int64_t* units, uint32_t* prog);
 #ifdef __cplusplus

@@ -15,6 +15,163 @@
 
 using namespace arp;
 
+// Symbolic check of a streamed slice (stream_kernel): per segment, running
+// its program on terms (an input row, an unordered 2-operand add, the
+// rounding at the end of a fold) with the buffers' rows in memory and the
+// slots in LDS, and with the wave's loads and stores in flight until a wait
+// covers them (a wait for m leaves at most the last m in flight), gives every
+// buffer the term the executed steps give it phase by phase; no slot is read,
+// or written by a fold, while a load into it may be in flight, no row is
+// loaded while a store to it may be in flight or stored while a load of it
+// may be, no slot beyond the launch's slots is used and no record crosses a
+// 64-word chunk.  Per unit: its tile and its segment's program.  Returns ""
+// or the first problem.
+static std::string check_streamed(const ar_plan& plan, const ExecState& ex, const SliceDesc& sd) {
+    const int64_t VEC = 16 / plan.esize;
+    const size_t n = size_t(plan.n);
+    if (sd.res_waves != 4 || sd.slots < 1 || sd.slots > kStreamMaxSlots) return "streamed launch shape";
+    if (int64_t(sd.runits.size()) != sd.nunits || int64_t(sd.tiles.size()) != sd.nunits ||
+        int64_t(sd.rec_off.size()) != sd.nseg)
+        return "streamed table sizes";
+    std::vector<int32_t> words(size_t(sd.nseg), -1);
+    for (int64_t i = 0; i < sd.nunits; ++i) {
+        const size_t sg = size_t(sd.tiles[size_t(i)].x);
+        if (words[sg] < 0) words[sg] = sd.runits[size_t(i)].nw;
+    }
+    for (int32_t sg = 0; sg < sd.nseg; ++sg) {
+        std::map<std::tuple<int, int64_t, int64_t>, int64_t> terms;
+        auto term = [&](int kind, int64_t x, int64_t y) {
+            if (kind == 1 && x > y) std::swap(x, y);
+            return terms.emplace(std::make_tuple(kind, x, y), int64_t(terms.size())).first->second;
+        };
+        auto fold = [&](const std::vector<int64_t>& v) {
+            if (v.size() == 1) return v[0];
+            int64_t t = v[0];
+            for (size_t j = 1; j < v.size(); ++j) t = term(1, t, v[j]);
+            return term(2, t, 0);
+        };
+        std::vector<int64_t> want(n), hbm(n);
+        for (size_t b = 0; b < n; ++b) want[b] = hbm[b] = term(0, int64_t(b), 0);
+        bool covered = false;
+        for (int32_t q = 0; q < sd.nphases; ++q) {
+            std::vector<std::pair<int32_t, int64_t>> outs;
+            for (const XStep& x : ex.phases[size_t(sd.p0 + q)].steps) {
+                if (!(x.end > x.begin && x.begin <= sd.cuts[size_t(sg)] &&
+                      sd.cuts[size_t(sg) + 1] <= x.end))
+                    continue;
+                covered = true;
+                std::vector<int64_t> v;
+                for (int32_t b : x.srcs) v.push_back(want[size_t(b)]);
+                const int64_t t = fold(v);
+                for (int32_t b : x.dsts) outs.push_back({b, t});
+            }
+            for (const auto& o : outs) want[size_t(o.first)] = o.second;
+        }
+        const int32_t off = sd.rec_off[size_t(sg)];
+        if (!covered) {
+            if (off != -1 || words[size_t(sg)] >= 0) return "streamed program on an idle segment";
+            continue;
+        }
+        const int32_t nw = words[size_t(sg)];
+        if (off < 0 || nw < 0 || int64_t(off) + nw > int64_t(sd.prog.size()))
+            return "streamed program outside the table";
+        const size_t S = size_t(sd.slots);
+        std::vector<int64_t> slot(S, -1), pend(S, -1);   // term; its load's operation
+        std::vector<int64_t> ld_of(n, -1), st_of(n, -1);  // last load / store of a row
+        int64_t seq = 0, done = 0;  // operations issued; those before `done` finished
+        auto read = [&](uint32_t sl, int64_t& t) -> const char* {
+            if (sl >= S) return "streamed slot out of range";
+            if (pend[sl] >= done) return "streamed slot read while its load may be in flight";
+            if (slot[sl] < 0) return "streamed slot read before it holds a value";
+            t = slot[sl];
+            return nullptr;
+        };
+        const uint32_t* sp = sd.prog.data() + off;
+        for (int32_t c0 = 0; c0 < nw; c0 += 64) {
+            const int32_t m = std::min(64, nw - c0);
+            int32_t c = 0;
+            while (c < m) {
+                const uint32_t h = sp[c0 + c], op = h & 0xFF;
+                const uint32_t b1 = (h >> 8) & 0xFF, b2 = (h >> 16) & 0xFF, b3 = h >> 24;
+                if (op == 0) {
+                    for (int32_t j = c; j < m; ++j)
+                        if (sp[c0 + j]) return "streamed chunk padding not zero";
+                    break;
+                }
+                int32_t len = 1;
+                if (op == kResAdd2 || op == kResFold) {
+                    std::vector<uint32_t> src;
+                    uint32_t d;
+                    if (op == kResAdd2) {
+                        src = {b1, b2};
+                        d = b3;
+                    } else {
+                        len = 1 + int32_t(b1 + 3) / 4;
+                        if (b1 < 2 || b3 || c + len > m) return "streamed fold malformed or across a chunk";
+                        for (uint32_t i = 0; i < b1; ++i)
+                            src.push_back((sp[c0 + c + 1 + i / 4] >> (8 * (i % 4))) & 0xFF);
+                        d = b2;
+                    }
+                    std::vector<int64_t> v;
+                    for (uint32_t r : src) {
+                        int64_t t;
+                        if (const char* e = read(r, t)) return e;
+                        v.push_back(t);
+                    }
+                    if (d >= S) return "streamed slot out of range";
+                    if (pend[d] >= done) return "streamed fold into a slot whose load may be in flight";
+                    slot[d] = fold(v);
+                    pend[d] = -1;
+                } else if (op == kResLoad) {
+                    len = 1 + int32_t(b1);
+                    if (b1 < 1 || b2 || b3 || c + len > m) return "streamed load malformed or across a chunk";
+                    for (uint32_t i = 0; i < b1; ++i) {
+                        const uint32_t x = sp[c0 + c + 1 + i], sl = x & 0xFF, b = x >> 8;
+                        if (sl >= S || b >= n) return "streamed load out of range";
+                        if (pend[sl] >= done) return "streamed load into a slot whose load may be in flight";
+                        if (st_of[b] >= done) return "streamed load of a row whose store may be in flight";
+                        slot[sl] = hbm[b];
+                        pend[sl] = ld_of[b] = seq++;
+                    }
+                } else if (op == kResWait) {
+                    if (b2 || b3) return "streamed wait malformed";
+                    done = std::max(done, seq - int64_t(b1));
+                } else if (op == kResPut) {
+                    len = 1 + int32_t(b1 + 1) / 2;
+                    if (b1 < 1 || b3 || c + len > m) return "streamed store malformed or across a chunk";
+                    int64_t t;
+                    if (const char* e = read(b2, t)) return e;
+                    for (uint32_t i = 0; i < b1; ++i) {
+                        const uint32_t x = sp[c0 + c + 1 + i / 2];
+                        const uint32_t b = i % 2 ? x >> 16 : x & 0xFFFF;
+                        if (b >= n) return "streamed store out of range";
+                        if (ld_of[b] >= done) return "streamed store to a row whose load may be in flight";
+                        hbm[b] = t;
+                        st_of[b] = seq++;
+                    }
+                    if (b1 % 2 && (sp[c0 + c + len - 1] >> 16)) return "streamed store padding not zero";
+                } else {
+                    return "streamed record with an unknown opcode";
+                }
+                c += len;
+            }
+        }
+        for (size_t b = 0; b < n; ++b)
+            if (hbm[b] != want[b]) return "streamed result differs from the phases' steps";
+    }
+    for (int64_t i = 0; i < sd.nunits; ++i) {
+        const ResUnit& u = sd.runits[size_t(i)];
+        const int2 e = sd.tiles[size_t(i)];
+        const size_t sg = size_t(e.x);
+        const int64_t lo = sd.cuts[sg] + int64_t(e.y) * sd.tile_elems;
+        const int64_t nv = std::min(sd.tile_elems, sd.cuts[sg + 1] - lo) / VEC;
+        if (u.lo != lo || u.nv != nv || nv < 1 || nv > 64) return "streamed unit tile";
+        if (u.load || u.store || u.alias != -1) return "streamed unit with row masks";
+        if (u.off != sd.rec_off[sg] || u.nw != words[sg]) return "streamed unit program";
+    }
+    return "";
+}
+
 // Host-side check of the executed phases and the launch tiling (no GPU):
 // every executed phase is free of hazards, and walking every wave tile of
 // every launch with the kernel's own index helpers covers each step exactly
@@ -207,7 +364,10 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     if (want != got) return bad("schedule differs from the steps of a phase");
                 }
             }
-            if (sd.resident) {
+            if (sd.streamed) {
+                const std::string e = check_streamed(*plan, *ex, sd);
+                if (!e.empty()) return bad(e);
+            } else if (sd.resident) {
                 // per segment: running its records symbolically (each value a
                 // term: an input row, an unordered 2-operand add, the rounding
                 // at the end of a fold) gives, for every row it stores, the
@@ -461,6 +621,7 @@ AR_EXPORT ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* inf
         info[1] = sd.nphases;
         info[2] = sd.nunits;
         info[3] = int64_t(sd.prog.size());
+        info[4] = sd.streamed ? sd.slots : 0;
         if (units)
             for (size_t i = 0; i < sd.runits.size(); ++i) {
                 const ResUnit& u = sd.runits[i];

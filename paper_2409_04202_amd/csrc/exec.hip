@@ -296,7 +296,25 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             s = mark(0);
             if (s != AR_OK) return s;
             const Stage stg = staged ? ex->stages[size_t(li)] : Stage{-1, int32_t(li)};
-            if (stg.slice >= 0 && ex->slices[size_t(stg.slice)].resident) {
+            if (stg.slice >= 0 && ex->slices[size_t(stg.slice)].streamed) {
+                const SliceDesc& sd = ex->slices[size_t(stg.slice)];
+                const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(256);
+                const size_t lds = size_t(sd.slots) * 1024;
+                const bool nt = sd.res_bytes > 2 * kKeepBytes;
+#define AR_STREAM(DT)                                                                         \
+    if (nt) hipLaunchKernelGGL((stream_kernel<DT, true>), grid, block, lds, stream,             \
+                               pe->dev + ex->rec_words, d->runits + sd.runit_base,              \
+                               d->prog + sd.prog_base, sd.nunits);                              \
+    else hipLaunchKernelGGL((stream_kernel<DT, false>), grid, block, lds, stream,               \
+                            pe->dev + ex->rec_words, d->runits + sd.runit_base,                 \
+                            d->prog + sd.prog_base, sd.nunits)
+                switch (plan->dtype) {
+                    case AR_F32: AR_STREAM(DT_F32); break;
+                    case AR_I32: AR_STREAM(DT_I32); break;
+                    default: AR_STREAM(DT_BF16); break;
+                }
+#undef AR_STREAM
+            } else if (stg.slice >= 0 && ex->slices[size_t(stg.slice)].resident) {
                 const SliceDesc& sd = ex->slices[size_t(stg.slice)];
                 const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(64 * sd.res_waves);
                 const size_t lds = size_t(plan->n) * 1024;
@@ -507,7 +525,7 @@ AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t*
         const Stage stg = ex->stages[size_t(i)];
         if (stg.slice >= 0) {
             const SliceDesc& sd = ex->slices[size_t(stg.slice)];
-            if (phase) *phase = sd.resident ? -2 : -1;
+            if (phase) *phase = sd.streamed ? -3 : sd.resident ? -2 : -1;
             if (nsrc) *nsrc = sd.max_k;
             if (max_dst) *max_dst = sd.max_dst;
             if (num_steps) *num_steps = sd.nsteps;

@@ -184,6 +184,11 @@ struct SliceDesc {
     // resident kernel's tiles (one vector per lane), unit i = tiles[i]
     bool resident = false;
     int32_t res_waves = 1;       // wavefronts per resident workgroup (1 or 4)
+    // streamed form (stream_kernel, plans with more than kResMaxN buffers):
+    // resident with `slots` LDS slots of 1 KiB per workgroup and load, wait
+    // and store records in `prog`; the units' row masks are then zero
+    bool streamed = false;
+    int32_t slots = 0;
     std::vector<ResUnit> runits;
     std::vector<uint32_t> prog;
     std::vector<int32_t> rec_off;

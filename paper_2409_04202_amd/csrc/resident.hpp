@@ -293,4 +293,153 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
     }
 }
 
+// ------------------------------------------------------------------------
+// Streamed resident kernel: the resident form for plans with more buffers
+// than rows fit in LDS.  A workgroup still owns one 1 KiB tile of a segment,
+// but its LDS holds S slots of 1 KiB instead of a row per buffer: the host
+// turns the segment's steps into values (a copy names its source's value, a
+// step with k >= 2 sources a new one), computes each value once its inputs
+// are there, in an order that finishes one subtree of folds before the next
+// (depth first), gives every value a slot from its load or fold to its last
+// use, and stores each buffer's final value as soon as it is computed.  The
+// buffer rows a segment reads before writing are loaded into slots up to
+// kStreamAhead rows ahead of their first use.  Every fold runs on the same
+// values in the same source order as in the plan, so the results are the
+// same bits.
+//
+// Its four waves run independently, each on its own 256-byte quarter of the
+// tile (wave w, lane l: bytes 256 w + 4 l), with no barrier: each loads its
+// quarter of every row straight into LDS (global_load_lds_dword, one 32-bit
+// word per lane), runs every record on its words and stores its quarter.
+// Besides add (kResAdd2) and fold (kResFold) records over slot bytes:
+//  * kResLoad | c << 8, then c words slot | buffer << 8: load the buffers'
+//    quarter rows into the slots (in flight until a wait);
+//  * kResWait | m << 8: wait until at most m of the wave's row loads and
+//    stores are outstanding (the counter decrements in issue order; the
+//    kernel may wait for more);
+//  * kResPut | c << 8 | slot << 16, then (c + 1) / 2 words of two 16-bit
+//    buffer numbers: store the slot's value into the buffers.
+constexpr uint32_t kResLoad = 0xF9;
+constexpr uint32_t kResWait = 0xF8;
+constexpr uint32_t kResPut = 0xF7;
+constexpr int kStreamMaxSlots = 64;
+
+// s_waitcnt vmcnt(V) with the other counters not waited for (gfx9 encoding:
+// vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+template <int V>
+__device__ __forceinline__ void wait_vm() {
+    __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// wait until at most m vector memory operations are outstanding (m rounded
+// down to one of the immediates below)
+__device__ __forceinline__ void wait_vm_at_most(int m) {
+    if (m >= 48) wait_vm<48>();
+    else if (m >= 32) wait_vm<32>();
+    else if (m >= 24) wait_vm<24>();
+    else if (m >= 16) wait_vm<16>();
+    else if (m >= 8) wait_vm<8>();
+    else if (m >= 4) wait_vm<4>();
+    else if (m >= 2) wait_vm<2>();
+    else if (m >= 1) wait_vm<1>();
+    else wait_vm<0>();
+}
+
+template <int DT, bool NT>
+__global__ __launch_bounds__(256) void stream_kernel(
+    const uint64_t* __restrict__ bufs, const ResUnit* __restrict__ units,
+    const uint32_t* __restrict__ prog, int64_t nunits) {
+    extern __shared__ u32x4 rows[];
+    using Acc = WAcc<DT>;
+    constexpr int RS = 256;  // words per slot
+    const int lane = int(threadIdx.x) & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+    const int64_t unit = int64_t(blockIdx.x);
+    if (unit >= nunits) return;  // the same for the whole workgroup
+    const ResUnit u = units[unit];
+    // this lane's word of the tile; lanes past the tile's end read its first
+    // word and store nothing
+    const int wb = wv * 256 + lane * 4;
+    const bool act = wb < u.nv * 16;
+    const int64_t goff = u.lo * int64_t(Elem<DT>::VEC == 8 ? 2 : 4) + (act ? wb : 0);
+    uint32_t* const R = reinterpret_cast<uint32_t*>(rows) + wv * 64 + lane;  // slot s: R[s * RS]
+    const uint32_t* sp = prog + u.off;
+    uint32_t w = lane < u.nw ? sp[lane] : 0u;  // first chunk of records
+    auto gptr = [&](uint32_t b) {  // this lane's word of buffer b's tile
+        return (AR_GLOBAL uint32_t*)(bufs[b] + uint64_t(goff));
+    };
+    for (int c0 = 0; c0 < u.nw; c0 += 64) {
+        const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
+        const int m = min(64, u.nw - c0);
+        int c = 0;
+        while (c < m) {
+            const uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(w), c));
+            const uint32_t op = h & 0xFFu;
+            if (op == 0) break;
+            if (op == kResAdd2) {
+                Acc acc;
+                acc.init(R[res_byte(h, 1) * RS]);
+                acc.add(R[res_byte(h, 2) * RS]);
+                R[res_byte(h, 3) * RS] = acc.out();
+                c += 1;
+            } else if (op == kResFold) {
+                const int k = res_byte(h, 1), d = res_byte(h, 2);
+                Acc acc;
+                const int kg = k >> 2;  // full groups of four sources
+                for (int g = 0; g < kg; ++g) {
+                    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + g));
+                    const uint32_t a0 = R[res_byte(x, 0) * RS];
+                    const uint32_t a1 = R[res_byte(x, 1) * RS];
+                    const uint32_t a2 = R[res_byte(x, 2) * RS];
+                    const uint32_t a3 = R[res_byte(x, 3) * RS];
+                    if (g == 0) acc.init(a0);
+                    else acc.add(a0);
+                    acc.add(a1);
+                    acc.add(a2);
+                    acc.add(a3);
+                }
+                const int rem = k & 3;
+                if (rem) {
+                    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + kg));
+                    const uint32_t a0 = R[res_byte(x, 0) * RS];
+                    const uint32_t a1 = R[res_byte(x, rem > 1 ? 1 : 0) * RS];
+                    const uint32_t a2 = R[res_byte(x, rem > 2 ? 2 : 0) * RS];
+                    if (kg == 0) acc.init(a0);
+                    else acc.add(a0);
+                    if (rem > 1) acc.add(a1);
+                    if (rem > 2) acc.add(a2);
+                }
+                R[d * RS] = acc.out();
+                c += 1 + ((k + 3) >> 2);
+            } else if (op == kResLoad) {
+                const int cnt = res_byte(h, 1);
+                for (int j = 0; j < cnt; ++j) {
+                    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + j));
+                    __builtin_amdgcn_global_load_lds(
+                        (const AR_GLOBAL void*)(gptr(x >> 8)),
+                        (AR_LDS void*)((AR_LDS char*)(rows) + (x & 0xFFu) * 1024u + uint32_t(wv) * 256u),
+                        4, 0, NT ? 2 : 0);
+                }
+                c += 1 + cnt;
+            } else if (op == kResWait) {
+                wait_vm_at_most(res_byte(h, 1));
+                c += 1;
+            } else {  // kResPut
+                const int cnt = res_byte(h, 1);
+                const uint32_t val = R[res_byte(h, 2) * RS];
+                for (int j = 0; j < cnt; ++j) {
+                    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (j >> 1)));
+                    const uint32_t b = j & 1 ? x >> 16 : x & 0xFFFFu;
+                    if (act) {
+                        if constexpr (NT) __builtin_nontemporal_store(val, gptr(b));
+                        else *gptr(b) = val;
+                    }
+                }
+                c += 1 + ((cnt + 1) >> 1);
+            }
+        }
+        w = wn;
+    }
+}
+
 }  // namespace arp

@@ -357,8 +357,9 @@ def test_whole_plan_launch_schedule(kind, n, N, fan, dtype):
         off = oracle.block_bounds(N, n)
         vec = 16 // (4 if dtype == "f32" else 2)
         aligned = all(o % vec == 0 for o in off)
-        # plans of at most 64 buffers run resident (-2) unless that is off
-        marker = -2 if n <= 64 else -1
+        # plans of at most 64 buffers run resident (-2), larger ones streamed
+        # (-3), unless that is off
+        marker = -2 if n <= 64 else -3
         L = p.launches()
         if p.num_phases:
             sliced = len(L) == 1 and L[0][0] == marker
@@ -376,9 +377,10 @@ def test_whole_plan_launch_schedule(kind, n, N, fan, dtype):
             p.set_option(arplan.AR_OPT_RESIDENT, 1)
             (ph, k, d, cnt, b2), = p.launches()
             assert ph == marker
-            # resident: every buffer position loaded once and stored once
+            # resident or streamed: every buffer position loaded once and
+            # stored once
             esize = 4 if dtype == "f32" else 2
-            assert b2 == (2 * n * N * esize if marker == -2 else b)
+            assert b2 == 2 * n * N * esize
             p.set_option(arplan.AR_OPT_SLICE, 0)
             assert b == sum(x[4] for x in p.launches())
 

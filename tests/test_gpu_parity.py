@@ -178,6 +178,59 @@ def test_full_size_configs(name):
         assert err <= 1e-2
 
 
+# ------------------------------------------- streamed runs (n > 64 buffers)
+
+STREAMED = [("tree", 512, 1 << 15, "bf16", (8, 8, 8)), ("tree", 512, 1 << 16, "f32", (8, 8, 8)),
+            ("ring", 70, 70 * 4 * 64, "f32", None), ("ring", 65, 65 * 8 * 3, "bf16", None),
+            ("rhd", 128, 128 * 4 * 40, "f32", None), ("rhd", 96, 96 * 4 * 8, "i32", None),
+            ("tree", 96, 96 * 4 * 30, "i32", (4, 4, 6)),
+            ("gentree", 384, 384 * 256, "f32",
+             tuple(workloads.CONFIGS["cdc384_gentree_f32"]["fanin"])),
+            ("gentree", 384, 384 * 512, "bf16",
+             tuple(workloads.CONFIGS["asy384_gentree_f32"]["fanin"]))]
+
+
+@pytest.mark.parametrize("kind,n,N,dtype,fan", STREAMED)
+@pytest.mark.parametrize("fuse", [1, 0])
+def test_streamed_whole_plan(kind, n, N, dtype, fan, fuse):
+    # the whole plan as one streamed launch (LDS slots shared by values,
+    # loads ahead, stores as soon as a final value is there), bit-exact
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_FUSE, fuse)
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        assert [x[0] for x in p.launches()] == [-3]
+    dist = "int1000" if dtype == "i32" else "uniform"
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=n + fuse, fuse=fuse, slice_=1)
+    if dtype == "bf16":
+        assert _normwise_bf16(got[0], xs0) <= 1e-2
+
+
+@pytest.mark.parametrize("name", ["tree8x8x8_n512_bf16", "asy384_gentree_f32",
+                                  "cdc384_gentree_f32"])
+def test_streamed_full_size(name):
+    # the full-size workloads with more than 64 buffers as one streamed
+    # launch, on sampled positions
+    c = workloads.CONFIGS[name]
+    n, N, dt = c["n"], c["N"], c["dtype"]
+    say("case: full-size streamed %s" % name)
+    xs0 = workloads.inputs(name)
+    ts = to_device(xs0, dt)
+    rng = np.random.default_rng(98)
+    idx = _sample_positions(n, N, rng)
+    with arplan.Plan(n, N, dt, c["kind"], c["fanin"]) as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        assert [x[0] for x in p.launches()] == [-3]
+        run_plan(p, ts)
+    plan = _oracle_plan(c["kind"], n, N, c["fanin"])
+    want = oracle.execute_sampled(plan, [x[idx] for x in xs0], idx, dt)
+    it = torch.from_numpy(idx).to("cuda")
+    for q in range(n):
+        g = ts[q].index_select(0, it).cpu().numpy()
+        g = g.view(np.uint16) if dt == "bf16" else g
+        assert np.array_equal(g, want[q]), (name, q)
+        assert torch.equal(ts[q], ts[0]), (name, q)
+
+
 # --------------------------------------------------------------- edge cases
 
 @pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("rhd", 4, None), ("rhd", 5, None),

@@ -31,11 +31,12 @@ def _resident_tables(handle, stage):
     I64 = ctypes.POINTER(ctypes.c_int64)
     f.argtypes = [ctypes.c_void_p, ctypes.c_int32, I64, I64, ctypes.POINTER(ctypes.c_uint32)]
     f.restype = ctypes.c_int32
-    info = (ctypes.c_int64 * 4)()
+    info = (ctypes.c_int64 * 5)()
     st = f(handle, stage, info, None, None)
     if st != arplan.AR_OK:
         return None
     nunits, nw = info[2], info[3]
+    _resident_tables.slots = info[4]
     units = (ctypes.c_int64 * (7 * nunits))()
     prog = (ctypes.c_uint32 * max(1, nw))()
     assert f(handle, stage, info, units, prog) == arplan.AR_OK
@@ -82,6 +83,73 @@ def _decode(words):
                 c += 1 + b1 // 4
             else:
                 raise AssertionError("unknown opcode %#x" % op)
+    return out
+
+
+def _decode_streamed(words):
+    """Records of one streamed segment: ("add", [s0, s1], d), ("fold", slots,
+    d), ("load", [(slot, buffer), ...], None), ("wait", m, None), ("put",
+    buffers, slot); 64-word chunks, a zero word ends a chunk."""
+    out = []
+    for c0 in range(0, len(words), 64):
+        chunk = [int(w) for w in words[c0:c0 + 64]]
+        c = 0
+        while c < len(chunk):
+            h = chunk[c]
+            op, b1, b2, b3 = h & 0xFF, (h >> 8) & 0xFF, (h >> 16) & 0xFF, h >> 24
+            if op == 0:
+                assert not any(chunk[c:]), "padding must be zero"
+                break
+            if op == 0xFE:
+                out.append(("add", [b1, b2], b3))
+                c += 1
+            elif op == 0xFB:
+                n = 1 + (b1 + 3) // 4
+                assert b1 >= 2 and b3 == 0 and c + n <= len(chunk)
+                out.append(("fold", [(chunk[c + 1 + i // 4] >> (8 * (i % 4))) & 0xFF
+                                     for i in range(b1)], b2))
+                c += n
+            elif op == 0xF9:
+                assert b1 >= 1 and b2 == 0 and b3 == 0 and c + 1 + b1 <= len(chunk)
+                out.append(("load", [(x & 0xFF, x >> 8) for x in chunk[c + 1:c + 1 + b1]], None))
+                c += 1 + b1
+            elif op == 0xF8:
+                out.append(("wait", b1, None))
+                c += 1
+            elif op == 0xF7:
+                n = 1 + (b1 + 1) // 2
+                assert b1 >= 1 and b3 == 0 and c + n <= len(chunk)
+                ids = [(chunk[c + 1 + i // 2] >> (16 * (i % 2))) & 0xFFFF for i in range(b1)]
+                out.append(("put", ids, b2))
+                c += n
+            else:
+                raise AssertionError("unknown opcode %#x" % op)
+    return out
+
+
+def _interpret_streamed(tables, bufs, dtype, slots):
+    """Run every unit of a streamed launch in program order (a load completes
+    at once; the library's symbolic check covers what may be in flight):
+    loads copy a buffer's tile into a slot, folds combine slots, puts store a
+    slot into buffers."""
+    units, prog = tables
+    vec = 8 if dtype == "bf16" else 4
+    out = [b.copy() for b in bufs]
+    for lo, load, store, nv, off, nw, alias in units:
+        assert load == 0 and store == 0 and alias == -1
+        hi = lo + nv * vec
+        slot = {}
+        for kind, a, b in _decode_streamed(prog[off:off + nw]):
+            if kind == "load":
+                for sl, buf in a:
+                    assert sl < slots
+                    slot[sl] = out[buf][lo:hi].copy()
+            elif kind in ("add", "fold"):
+                assert b < slots and all(x in slot for x in a)
+                slot[b] = fold(dtype, [slot[x] for x in a])
+            elif kind == "put":
+                for buf in a:
+                    out[buf][lo:hi] = slot[b]
     return out
 
 
@@ -136,9 +204,12 @@ def _interpret(tables, bufs, dtype):
 def _check_whole_plan(handle, ref_plan, n, N, dtype, seed):
     arplan.ar_plan_set_option(handle, arplan.AR_OPT_SLICE, 1)
     assert arplan.ar_plan_num_launches(handle) == 1
-    assert arplan.ar_plan_launch_info(handle, 0)[0] == -2
+    kind = arplan.ar_plan_launch_info(handle, 0)[0]
+    assert kind == (-2 if n <= 64 else -3)
     tables = _resident_tables(handle, 0)
     assert tables is not None
+    slots = _resident_tables.slots
+    assert (slots == 0) == (kind == -2) and slots <= 64
     # the library's own check: each segment's records, run symbolically, give
     # the executed steps' result terms for every stored row
     st, msg = _check_tiling(handle, 1)
@@ -146,7 +217,10 @@ def _check_whole_plan(handle, ref_plan, n, N, dtype, seed):
     dist = "int1000" if dtype == "i32" else "uniform"
     xs = workloads.draw(n, N, dtype, dist, seed)
     want = oracle.execute(ref_plan, [x.copy() for x in xs], dtype)
-    got = _interpret(tables, [x.copy() for x in xs], dtype)
+    if kind == -2:
+        got = _interpret(tables, [x.copy() for x in xs], dtype)
+    else:
+        got = _interpret_streamed(tables, [x.copy() for x in xs], dtype, slots)
     for q in range(n):
         assert np.array_equal(got[q], want[q]), q
 
@@ -168,15 +242,36 @@ def test_whole_plan_resident_program(kind, n, fan, dtype, fuse):
         _check_whole_plan(p.handle, oracle.make_plan(kind, n, N, fan), n, N, dtype, seed=n)
 
 
-def test_resident_needs_at_most_64_buffers():
+def test_more_than_64_buffers_run_streamed():
+    # a row per buffer up to 64 buffers; beyond, LDS slots shared by values
     with arplan.Plan(128, 128 * 4, "f32", "ring") as p:
         p.set_option(arplan.AR_OPT_SLICE, 1)
         L = p.launches()
-        assert len(L) == 1 and L[0][0] == -1
-        assert _resident_tables(p.handle, 0) is None
+        assert len(L) == 1 and L[0][0] == -3
+        assert _resident_tables(p.handle, 0) is not None and 0 < _resident_tables.slots <= 64
     with arplan.Plan(64, 64 * 4, "f32", "ring") as p:
         p.set_option(arplan.AR_OPT_SLICE, 1)
         assert p.launches()[0][0] == -2
+        assert _resident_tables(p.handle, 0) is not None and _resident_tables.slots == 0
+    # a 100-source fold needs more than 64 slots at once: plain sliced
+    with arplan.Plan(100, 100 * 4, "f32", "cps") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        assert p.launches()[0][0] == -1 and _resident_tables(p.handle, 0) is None
+
+
+STREAMED = [("ring", 65, None), ("ring", 70, None), ("rhd", 128, None), ("rhd", 96, None),
+            ("tree", 96, (4, 4, 6)), ("tree", 512, (8, 8, 8)), ("tree", 384, (16, 24))]
+
+
+@pytest.mark.parametrize("kind,n,fan", STREAMED)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("fuse", [1, 0])
+def test_whole_plan_streamed_program(kind, n, fan, dtype, fuse):
+    vec = 8 if dtype == "bf16" else 4
+    N = n * vec * (2 if n > 128 else 8)  # every block boundary 16-byte aligned
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_FUSE, fuse)
+        _check_whole_plan(p.handle, oracle.make_plan(kind, n, N, fan), n, N, dtype, seed=n + 1)
 
 
 @pytest.mark.parametrize("seed", range(60))
