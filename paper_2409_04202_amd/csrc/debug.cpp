@@ -29,7 +29,9 @@ using namespace arp;
 static std::string check_streamed(const ar_plan& plan, const ExecState& ex, const SliceDesc& sd) {
     const int64_t VEC = 16 / plan.esize;
     const size_t n = size_t(plan.n);
-    if (sd.res_waves != 4 || sd.slots < 1 || sd.slots > kStreamMaxSlots) return "streamed launch shape";
+    if ((sd.res_waves != 1 && sd.res_waves != 4) || sd.slots < 1 || sd.slots > kStreamMaxSlots || plan.n > kStreamMaxN ||
+        int64_t(sd.slots) * 1024 + int64_t(plan.n) * 8 + int64_t(sd.max_nw) * 4 > kLdsBytesPerCU / 2)
+        return "streamed launch shape";
     if (int64_t(sd.runits.size()) != sd.nunits || int64_t(sd.tiles.size()) != sd.nunits ||
         int64_t(sd.rec_off.size()) != sd.nseg)
         return "streamed table sizes";
@@ -167,7 +169,8 @@ static std::string check_streamed(const ar_plan& plan, const ExecState& ex, cons
         const int64_t nv = std::min(sd.tile_elems, sd.cuts[sg + 1] - lo) / VEC;
         if (u.lo != lo || u.nv != nv || nv < 1 || nv > 64) return "streamed unit tile";
         if (u.load || u.store || u.alias != -1) return "streamed unit with row masks";
-        if (u.off != sd.rec_off[sg] || u.nw != words[sg]) return "streamed unit program";
+        if (u.off != sd.rec_off[sg] || u.nw != words[sg] || u.nw > sd.max_nw)
+            return "streamed unit program";
     }
     return "";
 }

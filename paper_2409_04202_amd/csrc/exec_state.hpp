@@ -189,6 +189,7 @@ struct SliceDesc {
     // and store records in `prog`; the units' row masks are then zero
     bool streamed = false;
     int32_t slots = 0;
+    int32_t max_nw = 0;          // words of the longest unit program (in LDS)
     std::vector<ResUnit> runits;
     std::vector<uint32_t> prog;
     std::vector<int32_t> rec_off;

@@ -307,10 +307,13 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
 // values in the same source order as in the plan, so the results are the
 // same bits.
 //
-// Its four waves run independently, each on its own 256-byte quarter of the
-// tile (wave w, lane l: bytes 256 w + 4 l), with no barrier: each loads its
-// quarter of every row straight into LDS (global_load_lds_dword, one 32-bit
-// word per lane), runs every record on its words and stores its quarter.
+// Its W waves (1 or 4) run independently, with no barrier after the
+// workgroup has copied the n buffer pointers and the unit's records into LDS
+// behind the slots: one wave owns the whole tile (16 bytes a lane), four
+// waves a 256-byte quarter each (wave w, lane l: bytes 256 w + 4 l); each
+// loads its part of every row straight into LDS (global_load_lds), runs every
+// record on it and stores it.  A load or store record's lanes look up its
+// entries' pointers in LDS at once.
 // Besides add (kResAdd2) and fold (kResFold) records over slot bytes:
 //  * kResLoad | c << 8, then c words slot | buffer << 8: load the buffers'
 //    quarter rows into the slots (in flight until a wait);
@@ -323,6 +326,7 @@ constexpr uint32_t kResLoad = 0xF9;
 constexpr uint32_t kResWait = 0xF8;
 constexpr uint32_t kResPut = 0xF7;
 constexpr int kStreamMaxSlots = 64;
+constexpr int kStreamMaxN = 4096;  // buffers: their pointers take 8 n bytes of LDS
 
 // s_waitcnt vmcnt(V) with the other counters not waited for (gfx9 encoding:
 // vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
@@ -332,44 +336,72 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // wait until at most m vector memory operations are outstanding (m rounded
-// down to one of the immediates below)
+// down to a multiple of four below 64, or to 0, 1 or 2)
 __device__ __forceinline__ void wait_vm_at_most(int m) {
-    if (m >= 48) wait_vm<48>();
-    else if (m >= 32) wait_vm<32>();
-    else if (m >= 24) wait_vm<24>();
-    else if (m >= 16) wait_vm<16>();
-    else if (m >= 8) wait_vm<8>();
-    else if (m >= 4) wait_vm<4>();
-    else if (m >= 2) wait_vm<2>();
-    else if (m >= 1) wait_vm<1>();
-    else wait_vm<0>();
+    switch (m >= 60 ? 15 : m >> 2) {
+        case 15: wait_vm<60>(); break;
+        case 14: wait_vm<56>(); break;
+        case 13: wait_vm<52>(); break;
+        case 12: wait_vm<48>(); break;
+        case 11: wait_vm<44>(); break;
+        case 10: wait_vm<40>(); break;
+        case 9: wait_vm<36>(); break;
+        case 8: wait_vm<32>(); break;
+        case 7: wait_vm<28>(); break;
+        case 6: wait_vm<24>(); break;
+        case 5: wait_vm<20>(); break;
+        case 4: wait_vm<16>(); break;
+        case 3: wait_vm<12>(); break;
+        case 2: wait_vm<8>(); break;
+        case 1: wait_vm<4>(); break;
+        default:
+            if (m >= 2) wait_vm<2>();
+            else if (m == 1) wait_vm<1>();
+            else wait_vm<0>();
+    }
 }
 
-template <int DT, bool NT>
-__global__ __launch_bounds__(256) void stream_kernel(
-    const uint64_t* __restrict__ bufs, const ResUnit* __restrict__ units,
-    const uint32_t* __restrict__ prog, int64_t nunits) {
+template <int DT, int W, bool NT>
+__global__ __launch_bounds__(64 * W) void stream_kernel(
+    const uint64_t* __restrict__ bufs, int32_t n, int32_t slots,
+    const ResUnit* __restrict__ units, const uint32_t* __restrict__ prog, int64_t nunits) {
     extern __shared__ u32x4 rows[];
-    using Acc = WAcc<DT>;
-    constexpr int RS = 256;  // words per slot
+    using Word = typename ResLane<DT, W>::Word;
+    using Acc = typename ResLane<DT, W>::Acc;
+    constexpr int RS = ResLane<DT, W>::kStride;  // words per slot
+    constexpr int BYTES = W == 1 ? 16 : 4;       // bytes a lane owns of the tile
     const int lane = int(threadIdx.x) & 63;
     const int wv = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
     const int64_t unit = int64_t(blockIdx.x);
     if (unit >= nunits) return;  // the same for the whole workgroup
     const ResUnit u = units[unit];
-    // this lane's word of the tile; lanes past the tile's end read its first
-    // word and store nothing
-    const int wb = wv * 256 + lane * 4;
+    // behind the slots: the buffer pointers (a record's lanes look up the
+    // pointers of its entries at once) and the unit's records, copied once
+    // before any row load: reading the records from memory as they run
+    // would make every 64-word chunk wait for all row loads in flight
+    uint64_t* const ptab = reinterpret_cast<uint64_t*>(rows + slots * 64);
+    uint32_t* const lprog = reinterpret_cast<uint32_t*>(ptab + n);
+    for (int i = int(threadIdx.x); i < n; i += 64 * W) ptab[i] = bufs[i];
+    for (int i = int(threadIdx.x); i < u.nw; i += 64 * W) lprog[i] = prog[u.off + i];
+    __syncthreads();
+    // this lane's part of the tile; lanes past the tile's end read its first
+    // bytes and store nothing
+    const int wb = wv * 256 + lane * BYTES;
     const bool act = wb < u.nv * 16;
     const int64_t goff = u.lo * int64_t(Elem<DT>::VEC == 8 ? 2 : 4) + (act ? wb : 0);
-    uint32_t* const R = reinterpret_cast<uint32_t*>(rows) + wv * 64 + lane;  // slot s: R[s * RS]
-    const uint32_t* sp = prog + u.off;
-    uint32_t w = lane < u.nw ? sp[lane] : 0u;  // first chunk of records
-    auto gptr = [&](uint32_t b) {  // this lane's word of buffer b's tile
-        return (AR_GLOBAL uint32_t*)(bufs[b] + uint64_t(goff));
+    Word* const R = reinterpret_cast<Word*>(rows) + (W == 1 ? lane : wv * 64 + lane);  // slot s: R[s * RS]
+    uint32_t w = lane < u.nw ? lprog[lane] : 0u;  // first chunk of records
+    auto gptr = [&](uint64_t base) {  // this lane's part of a buffer's tile
+        return (AR_GLOBAL Word*)(base + uint64_t(goff));
+    };
+    // the pointer of entry j of the record at word c (entry j in lane
+    // c + 1 + j), held by lane c + 1 + j
+    auto entry_ptr = [&](const uint64_t p, int j, int c) {
+        return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(p >> 32)), c + 1 + j))) << 32) |
+               uint32_t(__builtin_amdgcn_readlane(int(uint32_t(p)), c + 1 + j));
     };
     for (int c0 = 0; c0 < u.nw; c0 += 64) {
-        const uint32_t wn = c0 + 64 + lane < u.nw ? sp[c0 + 64 + lane] : 0u;
+        const uint32_t wn = c0 + 64 + lane < u.nw ? lprog[c0 + 64 + lane] : 0u;
         const int m = min(64, u.nw - c0);
         int c = 0;
         while (c < m) {
@@ -388,10 +420,10 @@ __global__ __launch_bounds__(256) void stream_kernel(
                 const int kg = k >> 2;  // full groups of four sources
                 for (int g = 0; g < kg; ++g) {
                     const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + g));
-                    const uint32_t a0 = R[res_byte(x, 0) * RS];
-                    const uint32_t a1 = R[res_byte(x, 1) * RS];
-                    const uint32_t a2 = R[res_byte(x, 2) * RS];
-                    const uint32_t a3 = R[res_byte(x, 3) * RS];
+                    const Word a0 = R[res_byte(x, 0) * RS];
+                    const Word a1 = R[res_byte(x, 1) * RS];
+                    const Word a2 = R[res_byte(x, 2) * RS];
+                    const Word a3 = R[res_byte(x, 3) * RS];
                     if (g == 0) acc.init(a0);
                     else acc.add(a0);
                     acc.add(a1);
@@ -401,9 +433,9 @@ __global__ __launch_bounds__(256) void stream_kernel(
                 const int rem = k & 3;
                 if (rem) {
                     const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + kg));
-                    const uint32_t a0 = R[res_byte(x, 0) * RS];
-                    const uint32_t a1 = R[res_byte(x, rem > 1 ? 1 : 0) * RS];
-                    const uint32_t a2 = R[res_byte(x, rem > 2 ? 2 : 0) * RS];
+                    const Word a0 = R[res_byte(x, 0) * RS];
+                    const Word a1 = R[res_byte(x, rem > 1 ? 1 : 0) * RS];
+                    const Word a2 = R[res_byte(x, rem > 2 ? 2 : 0) * RS];
                     if (kg == 0) acc.init(a0);
                     else acc.add(a0);
                     if (rem > 1) acc.add(a1);
@@ -413,12 +445,15 @@ __global__ __launch_bounds__(256) void stream_kernel(
                 c += 1 + ((k + 3) >> 2);
             } else if (op == kResLoad) {
                 const int cnt = res_byte(h, 1);
+                const bool mine = lane > c && lane <= c + cnt;  // this lane's word is an entry
+                const uint64_t p = ptab[mine ? w >> 8 : 0u];
                 for (int j = 0; j < cnt; ++j) {
                     const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + j));
-                    __builtin_amdgcn_global_load_lds(
-                        (const AR_GLOBAL void*)(gptr(x >> 8)),
-                        (AR_LDS void*)((AR_LDS char*)(rows) + (x & 0xFFu) * 1024u + uint32_t(wv) * 256u),
-                        4, 0, NT ? 2 : 0);
+                    const AR_GLOBAL void* src = (const AR_GLOBAL void*)(gptr(entry_ptr(p, j, c)));
+                    AR_LDS void* dst =
+                        (AR_LDS void*)((AR_LDS char*)(rows) + (x & 0xFFu) * 1024u + uint32_t(wv) * 256u);
+                    if constexpr (W == 1) __builtin_amdgcn_global_load_lds(src, dst, 16, 0, NT ? 2 : 0);
+                    else __builtin_amdgcn_global_load_lds(src, dst, 4, 0, NT ? 2 : 0);
                 }
                 c += 1 + cnt;
             } else if (op == kResWait) {
@@ -426,13 +461,15 @@ __global__ __launch_bounds__(256) void stream_kernel(
                 c += 1;
             } else {  // kResPut
                 const int cnt = res_byte(h, 1);
-                const uint32_t val = R[res_byte(h, 2) * RS];
+                const Word val = R[res_byte(h, 2) * RS];
+                const bool mine = lane > c && lane <= c + ((cnt + 1) >> 1);
+                const uint64_t p0 = ptab[mine ? w & 0xFFFFu : 0u];
+                const uint64_t p1 = ptab[mine ? w >> 16 : 0u];
                 for (int j = 0; j < cnt; ++j) {
-                    const uint32_t x = uint32_t(__builtin_amdgcn_readlane(int(w), c + 1 + (j >> 1)));
-                    const uint32_t b = j & 1 ? x >> 16 : x & 0xFFFFu;
+                    const uint64_t base = entry_ptr(j & 1 ? p1 : p0, j >> 1, c);
                     if (act) {
-                        if constexpr (NT) __builtin_nontemporal_store(val, gptr(b));
-                        else *gptr(b) = val;
+                        if constexpr (NT) __builtin_nontemporal_store(val, gptr(base));
+                        else *gptr(base) = val;
                     }
                 }
                 c += 1 + ((cnt + 1) >> 1);

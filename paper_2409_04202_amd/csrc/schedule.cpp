@@ -403,7 +403,10 @@ static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint
 // into a buffer whose row the segment still has to load waits until the end.
 // Fills w (64-word chunks) and the slots, loads and stores it uses; false when
 // a fold has more than 252 sources or the slots run out.
-constexpr int32_t kStreamAhead = 32;
+constexpr int32_t kStreamAhead = 48;
+// waves of a streamed workgroup (the kernel takes 1 or 4; one wave owning
+// the whole tile measured the same as four owning a quarter each)
+constexpr int32_t kStreamWaves = 4;
 constexpr size_t kStreamReserve = 2;  // slots kept for fold results
 
 static bool encode_stream(const std::vector<const XStep*>& st, int32_t n,
@@ -540,10 +543,13 @@ static bool encode_stream(const std::vector<const XStep*>& st, int32_t n,
                 while (seq_of[size_t(i)] < 0)
                     if (!load_next()) return false;
             }
+        // one wait, for the input loaded last
+        int32_t last = -1;
         for (int32_t i : in) {
             if (vals[size_t(i)].leaf >= 0 && qused < q.size() && q[qused] == i) ++qused;
-            ready(i);
+            if (vals[size_t(i)].leaf >= 0 && (last < 0 || seq_of[size_t(i)] > seq_of[size_t(last)])) last = i;
         }
+        if (last >= 0) ready(last);
         if (e >= 0) {  // the fold; its slot: an input's that dies here, else a free one
             const std::vector<int32_t>& x = vals[size_t(v)].in;
             for (int32_t i : x) release(i);
@@ -608,7 +614,7 @@ static bool encode_stream(const std::vector<const XStep*>& st, int32_t n,
 // Leaves `sd` in its plain form when a program cannot be built or a table
 // would overflow.
 static void build_streamed(const Plan& p, const ExecState& ex, SliceDesc& sd) {
-    if (p.n > 65535 || sd.nseg < 1) return;  // 16-bit buffer numbers in stores
+    if (p.n > kStreamMaxN || sd.nseg < 1) return;
     const int64_t VEC = 16 / p.esize;
     const size_t nseg = size_t(sd.nseg);
     auto seg_of = [&](int64_t x) {
@@ -654,11 +660,18 @@ static void build_streamed(const Plan& p, const ExecState& ex, SliceDesc& sd) {
             units.push_back(u);
         }
     }
-    if (units.empty() || int64_t(units.size()) > kMaxBlocks) return;
+    int32_t max_nw = 0;
+    for (const int32_t l : rec_len) max_nw = std::max(max_nw, l);
+    // LDS of a workgroup: slots, pointers and program, two workgroups a
+    // compute unit at most
+    if (units.empty() || int64_t(units.size()) > kMaxBlocks ||
+        int64_t(slots) * 1024 + int64_t(p.n) * 8 + int64_t(max_nw) * 4 > kLdsBytesPerCU / 2)
+        return;
     sd.resident = true;
     sd.streamed = true;
     sd.slots = slots;
-    sd.res_waves = 4;
+    sd.max_nw = max_nw;
+    sd.res_waves = kStreamWaves;
     sd.runits = std::move(units);
     sd.prog = std::move(prog);
     sd.rec_off = std::move(rec_off);
