@@ -178,6 +178,20 @@ def test_full_size_configs(name):
         assert err <= 1e-2
 
 
+@pytest.mark.parametrize("N", [(1 << 24) + 160, (1 << 21) + 160])
+def test_large_resident_with_partial_tiles(N):
+    # RHD n = 8 as one resident launch whose segments end in a partial tile
+    # (N / 8 is not a multiple of 256 elements); at 2^24 + 160 the run moves
+    # more than the last-level cache and streams its rows nontemporally
+    with arplan.Plan(8, N, "f32", "rhd") as p:
+        if N > 1 << 24:  # the default choice at this size
+            assert [x[0] for x in p.launches()] == [-2]
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        L = p.launches()
+        assert [x[0] for x in L] == [-2] and L[0][4] == 2 * 8 * N * 4
+    _full_compare("rhd", 8, N, "f32", None, "uniform", seed=N % 97, slice_=1)
+
+
 # ------------------------------------------- streamed runs (n > 64 buffers)
 
 STREAMED = [("tree", 512, 1 << 15, "bf16", (8, 8, 8)), ("tree", 512, 1 << 16, "f32", (8, 8, 8)),
