@@ -219,6 +219,70 @@ def test_streamed_whole_plan(kind, n, N, dtype, fan, fuse):
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_streamed_random_custom_plans(seed):
+    # random hazard-free plans over 65-200 buffers (folds of 3-16 sources,
+    # copies into up to 40 buffers; the host-side program test's generator)
+    # as one streamed launch, and with the default executor, bit-exact
+    from test_resident_host import _wide_random_plan
+    from oracle.plans import Plan as OPlan, Step as OStep
+    rng = np.random.default_rng(9500 + seed)
+    n = int(rng.choice([65, 80, 130, 200]))
+    M = int(rng.integers(3, 90))
+    phases = _wide_random_plan(rng, n, M)
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    vec = 8 if dtype == "bf16" else 4
+    N = M * vec
+    flat = [(q, op, d, s_, b * vec, e * vec)
+            for q, ph in enumerate(phases) for (op, d, s_, b, e) in ph]
+    ref_plan = OPlan("custom", n, N, [[OStep(op, d, s_, b * vec, e * vec)
+                                       for (op, d, s_, b, e) in ph] for ph in phases])
+    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", seed)
+    ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
+    say("case: streamed random custom plan seed=%d n=%d N=%d %s" % (seed, n, N, dtype))
+    for sl in (1, 2):
+        ts = to_device(xs0, dtype)
+        h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+        try:
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, sl)
+            if sl == 1:
+                assert arplan.ar_plan_launch_info(h, 0)[0] == -3
+            arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+        finally:
+            arplan.ar_plan_destroy(h)
+        got = to_host(ts, dtype)
+        for q in range(n):
+            assert np.array_equal(got[q], ref[q]), (seed, sl, q)
+
+
+def test_streamed_held_back_store():
+    # a store into a buffer whose initial row a later fold still needs
+    # (held back to the end of the program), bit-exact on the GPU
+    from oracle.plans import Plan as OPlan, Step as OStep
+    n = 70
+    for dtype in ("f32", "bf16"):
+        vec = 8 if dtype == "bf16" else 4
+        N = 64 * vec * 3
+        flat = [(0, "reduce", 4, list(range(10, 64)) + [1], 0, N),
+                (1, "reduce", 1, [2, 3], 0, N), (2, "reduce", 4, [4, 7], 0, N)]
+        ref_plan = OPlan("custom", n, N, [[OStep(op, d, s_, b, e)] for (_, op, d, s_, b, e) in flat])
+        xs0 = workloads.draw(n, N, dtype, "uniform", 3)
+        ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
+        ts = to_device(xs0, dtype)
+        h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+        try:
+            arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 1)
+            assert arplan.ar_plan_launch_info(h, 0)[0] == -3
+            arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+        finally:
+            arplan.ar_plan_destroy(h)
+        got = to_host(ts, dtype)
+        for q in range(n):
+            assert np.array_equal(got[q], ref[q]), (dtype, q)
+
+
 @pytest.mark.parametrize("name", ["tree8x8x8_n512_bf16", "asy384_gentree_f32",
                                   "cdc384_gentree_f32"])
 def test_streamed_full_size(name):

@@ -374,6 +374,60 @@ def test_wide_random_plans_resident_program(seed):
         arplan.ar_plan_destroy(h)
 
 
+@pytest.mark.parametrize("seed", range(40))
+def test_wide_random_plans_streamed_program(seed):
+    # more than 64 buffers: streamed programs (slots shared by values, loads
+    # ahead, stores held back while a buffer's own row is still to load)
+    rng = np.random.default_rng(9500 + seed)
+    n = int(rng.choice([65, 80, 130, 200]))
+    M = int(rng.integers(3, 90))
+    phases = _wide_random_plan(rng, n, M)
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    vec = 8 if dtype == "bf16" else 4
+    N = M * vec
+    flat = [(q, op, d, s, b * vec, e * vec)
+            for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref = OPlan("custom", n, N, [[OStep(op, d, s, b * vec, e * vec)
+                                  for (op, d, s, b, e) in ph] for ph in phases])
+    h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+    try:
+        _check_whole_plan(h, ref, n, N, dtype, seed=seed)
+    finally:
+        arplan.ar_plan_destroy(h)
+
+
+def test_streamed_encoder_holds_back_stores():
+    # phase 0: x4 <- x10 + ... + x63 + x1; phase 1: x1 <- x2 + x3; phase 2:
+    # x4 <- x4 + x7.  Depth first from the final values, x1's new value is
+    # computed first, but x1's initial row is only needed by the 55-source
+    # fold, more than the loads run ahead later: the store into x1 is held
+    # back to the end, after that row has been loaded; bit-exact, and the
+    # library's symbolic check accepts the order
+    n, vec = 70, 4
+    N = 64 * vec * 3
+    flat = [(0, "reduce", 4, list(range(10, 64)) + [1], 0, N), (1, "reduce", 1, [2, 3], 0, N),
+            (2, "reduce", 4, [4, 7], 0, N)]
+    ref = OPlan("custom", n, N, [[OStep(op, d, s_, b, e)] for (_, op, d, s_, b, e) in flat])
+    for dtype in ("f32", "bf16", "i32"):
+        h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+        try:
+            _check_whole_plan(h, ref, n, N, dtype, seed=1)
+            units, prog = _resident_tables(h, 0)
+            lo, load, store, nv, off, nw, alias = units[0]
+            order = []
+            for kind, a, b in _decode_streamed(prog[off:off + nw]):
+                if kind == "load":
+                    order += [("load", buf) for _, buf in a]
+                elif kind == "put":
+                    order += [("put", buf) for buf in a]
+                elif kind in ("add", "fold"):
+                    order.append((kind, len(a)))
+            assert order[:3] == [("load", 2), ("load", 3), ("add", 2)]
+            assert order[-1] == ("put", 1) and order.index(("load", 1)) < len(order) - 1
+        finally:
+            arplan.ar_plan_destroy(h)
+
+
 def test_wide_random_plans_use_every_record_kind():
     kinds = set()
     for seed in range(40):
