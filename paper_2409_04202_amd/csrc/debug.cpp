@@ -19,7 +19,9 @@ using namespace arp;
 // its program on terms (an input row, an unordered 2-operand add, the
 // rounding at the end of a fold) with the buffers' rows in memory and the
 // slots in LDS, and with the wave's loads and stores in flight until a wait
-// covers them (a wait for m leaves at most the last m in flight), gives every
+// covers them (loads finish in issue order, stores in any order: a wait for
+// m finishes every load but the last m issued, and the stores only when m is
+// 0), gives every
 // buffer the term the executed steps give it phase by phase; no slot is read,
 // or written by a fold, while a load into it may be in flight, no row is
 // loaded while a store to it may be in flight or stored while a load of it
@@ -78,9 +80,10 @@ static std::string check_streamed(const ar_plan& plan, const ExecState& ex, cons
         if (off < 0 || nw < 0 || int64_t(off) + nw > int64_t(sd.prog.size()))
             return "streamed program outside the table";
         const size_t S = size_t(sd.slots);
-        std::vector<int64_t> slot(S, -1), pend(S, -1);   // term; its load's operation
-        std::vector<int64_t> ld_of(n, -1), st_of(n, -1);  // last load / store of a row
-        int64_t seq = 0, done = 0;  // operations issued; those before `done` finished
+        std::vector<int64_t> slot(S, -1), pend(S, -1);   // term; its load (number)
+        std::vector<int64_t> ld_of(n, -1);               // last load of a row
+        std::vector<char> st_pend(n, 0);                 // a store to a row in flight
+        int64_t seq = 0, done = 0;  // loads issued; those before `done` finished
         auto read = [&](uint32_t sl, int64_t& t) -> const char* {
             if (sl >= S) return "streamed slot out of range";
             if (pend[sl] >= done) return "streamed slot read while its load may be in flight";
@@ -131,13 +134,14 @@ static std::string check_streamed(const ar_plan& plan, const ExecState& ex, cons
                         const uint32_t x = sp[c0 + c + 1 + i], sl = x & 0xFF, b = x >> 8;
                         if (sl >= S || b >= n) return "streamed load out of range";
                         if (pend[sl] >= done) return "streamed load into a slot whose load may be in flight";
-                        if (st_of[b] >= done) return "streamed load of a row whose store may be in flight";
+                        if (st_pend[b]) return "streamed load of a row whose store may be in flight";
                         slot[sl] = hbm[b];
                         pend[sl] = ld_of[b] = seq++;
                     }
                 } else if (op == kResWait) {
                     if (b2 || b3) return "streamed wait malformed";
                     done = std::max(done, seq - int64_t(b1));
+                    if (b1 == 0) std::fill(st_pend.begin(), st_pend.end(), char(0));
                 } else if (op == kResPut) {
                     len = 1 + int32_t(b1 + 1) / 2;
                     if (b1 < 1 || b3 || c + len > m) return "streamed store malformed or across a chunk";
@@ -149,7 +153,7 @@ static std::string check_streamed(const ar_plan& plan, const ExecState& ex, cons
                         if (b >= n) return "streamed store out of range";
                         if (ld_of[b] >= done) return "streamed store to a row whose load may be in flight";
                         hbm[b] = t;
-                        st_of[b] = seq++;
+                        st_pend[b] = 1;
                     }
                     if (b1 % 2 && (sp[c0 + c + len - 1] >> 16)) return "streamed store padding not zero";
                 } else {

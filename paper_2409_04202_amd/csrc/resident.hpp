@@ -318,8 +318,9 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(
 //  * kResLoad | c << 8, then c words slot | buffer << 8: load the buffers'
 //    quarter rows into the slots (in flight until a wait);
 //  * kResWait | m << 8: wait until at most m of the wave's row loads and
-//    stores are outstanding (the counter decrements in issue order; the
-//    kernel may wait for more);
+//    stores are outstanding (the kernel may wait for more).  Loads finish in
+//    the order they were issued, stores in any order relative to them, so
+//    a load followed by m loads is done once at most m operations remain;
 //  * kResPut | c << 8 | slot << 16, then (c + 1) / 2 words of two 16-bit
 //    buffer numbers: store the slot's value into the buffers.
 constexpr uint32_t kResLoad = 0xF9;

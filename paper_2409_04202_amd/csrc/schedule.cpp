@@ -399,7 +399,8 @@ static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint
 // computed depth first (each fold after its inputs, in source order) and
 // stored into those buffers at once, each value holds a slot from its load or
 // fold to its last use, and the rows are loaded kStreamAhead rows ahead of
-// their first use, with a wait for a load before its value is read.  A store
+// their first use, with a wait for a load before its value is read (until at
+// most as many memory operations are outstanding as loads followed it).  A store
 // into a buffer whose row the segment still has to load waits until the end.
 // Fills w (64-word chunks) and the slots, loads and stores it uses; false when
 // a fold has more than 252 sources or the slots run out.
@@ -477,11 +478,14 @@ static bool encode_stream(const std::vector<const XStep*>& st, int32_t n,
                 q.push_back(i);
             }
     }
-    // slots, loads ahead, waits
+    // slots, loads ahead, waits.  Row loads complete in the order they were
+    // issued, stores in any order relative to them: to know a load finished,
+    // wait until at most as many operations are outstanding as loads were
+    // issued after it (whatever the stores do, the load is then done)
     std::vector<int32_t> slot_of(V, -1), seq_of(V, -1);
     std::vector<int32_t> free_slots;
     for (int32_t sl = kStreamMaxSlots; sl-- > 0;) free_slots.push_back(sl);
-    int32_t seq = 0, done = 0, top = 0;  // memory operations issued, completed; slots used
+    int32_t seq = 0, done = 0, top = 0;  // loads issued, loads finished; slots used
     size_t qi = 0, qused = 0;
     std::vector<uint32_t> loads;  // entries of the load record being built
     auto put = [&](const std::vector<uint32_t>& rec) {
@@ -530,7 +534,6 @@ static bool encode_stream(const std::vector<const XStep*>& st, int32_t n,
             for (size_t j = 0; j < c; ++j) rec[1 + j / 2] |= uint32_t(to[i0 + j]) << (16 * (j % 2));
             flush();
             put(rec);
-            seq += int32_t(c);
         }
     };
     std::vector<std::pair<int32_t, int32_t>> later;  // stores held back
