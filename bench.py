@@ -44,7 +44,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 # kernel of a launch by its phase field in ar_plan_launch_info
-KERNEL_OF = {-1: "sliced_kernel", -2: "resident_kernel"}
+KERNEL_OF = {-1: "sliced_kernel", -2: "resident_kernel", -3: "stream_kernel"}
 DEFAULT = "rhd_n8_f32"
 
 

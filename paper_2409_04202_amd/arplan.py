@@ -350,7 +350,9 @@ class Plan:
         ar_plan_set_option(self.handle, option, value)
 
     def launches(self):
-        """[(phase, nsrc, max_dst, num_steps, bytes)] per kernel launch."""
+        """[(phase, nsrc, max_dst, num_steps, bytes)] per kernel launch; phase
+        is the plan phase of a phase launch, -1 for a sliced launch, -2 for a
+        resident one and -3 for a streamed resident one."""
         return [ar_plan_launch_info(self.handle, i)
                 for i in range(ar_plan_num_launches(self.handle))]
 
