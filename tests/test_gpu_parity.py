@@ -192,6 +192,30 @@ def test_large_resident_with_partial_tiles(N):
     _full_compare("rhd", 8, N, "f32", None, "uniform", seed=N % 97, slice_=1)
 
 
+@pytest.mark.parametrize("dtype,N", [("bf16", 1 << 25), ("i32", (1 << 24) + 160)])
+def test_large_resident_nontemporal_dtypes(dtype, N):
+    # RHD n = 8 as one resident launch moving more than the last-level cache
+    # (nontemporal rows) in bf16 and int32, on sampled positions
+    n = 8
+    with arplan.Plan(n, N, dtype, "rhd") as p:
+        L = p.launches()
+        assert [x[0] for x in L] == [-2] and L[0][4] > 512 << 20
+    say("case: large resident rhd n=8 N=%d %s" % (N, dtype))
+    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", 21)
+    ts = to_device(xs0, dtype)
+    with arplan.Plan(n, N, dtype, "rhd") as p:
+        run_plan(p, ts)
+    rng = np.random.default_rng(5)
+    idx = _sample_positions(n, N, rng)
+    want = oracle.execute_sampled(oracle.rhd(n, N), [x[idx] for x in xs0], idx, dtype)
+    it = torch.from_numpy(idx).to("cuda")
+    for q in range(n):
+        g = ts[q].index_select(0, it).cpu().numpy()
+        g = g.view(np.uint16) if dtype == "bf16" else g
+        assert np.array_equal(g, want[q]), (dtype, q)
+        assert torch.equal(ts[q], ts[0]), (dtype, q)
+
+
 # ------------------------------------------- streamed runs (n > 64 buffers)
 
 STREAMED = [("tree", 512, 1 << 15, "bf16", (8, 8, 8)), ("tree", 512, 1 << 16, "f32", (8, 8, 8)),
