@@ -61,7 +61,7 @@ def kernel_source_hash():
     their launches (comments and layout excluded)."""
     h = hashlib.sha256()
     for f in ("kernels.hpp", "resident.hpp", "exec.hip", "exec_state.hpp", "rewrite.cpp",
-              "schedule.cpp"):
+              "schedule.cpp", "programs.cpp"):
         with open(os.path.join(ROOT, "paper_2409_04202_amd", "csrc", f)) as fh:
             h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]

@@ -3,7 +3,7 @@
 Run ``python -m paper_2409_04202_amd.build`` (or ``__graft_entry__.build()``).
 The plan library and the C ABI (plan.cpp, capi.cpp) are compiled with the
 host compiler; the executor (exec.hip, and its host-side planning in
-rewrite.cpp and schedule.cpp, which share its HIP types) with
+rewrite.cpp, schedule.cpp and programs.cpp, which share its HIP types) with
 ``hipcc --offload-arch=gfx950``; hipcc links the shared library.  Always
 recompiles.
 """
@@ -21,7 +21,7 @@ LIB = os.path.join(LIBDIR, "libarplan.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HOST_SRCS = ["plan.cpp", "capi.cpp"]
-HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp", "debug.cpp"]
+HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp", "programs.cpp", "debug.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
           "-Wextra", "-Wno-unused-parameter"]

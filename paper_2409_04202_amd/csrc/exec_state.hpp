@@ -1,7 +1,7 @@
 // Host-side state of the executor, shared by its translation units: the
 // executed phases after the rewrites (rewrite.cpp), their launches and
-// sliced runs (schedule.cpp), and the per-device state and launching
-// (exec.hip).
+// sliced runs (schedule.cpp), the resident and streamed programs
+// (programs.cpp), and the per-device state and launching (exec.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -68,7 +68,7 @@ constexpr double kStepNsPerDst = 15.0;
 constexpr double kMinSliceWaves = 256.0;
 constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 // A sliced run may instead run resident (resident_kernel, AR_OPT_RESIDENT):
-// a workgroup of W waves (res_waves in schedule.cpp) per 64 vectors of a
+// a workgroup of W waves (res_waves in programs.cpp) per 64 vectors of a
 // segment, the plan's n <= kResMaxN buffers in LDS rows of 1 KiB.  Its
 // predicted time is kLaunchNs plus the larger of its HBM traffic (each row
 // read and written once) at kBytesPerNs and its workgroups' time, plus
@@ -266,5 +266,11 @@ bool exec_phases_hazard_free(const std::vector<XPhase>& ph, int32_t n, std::stri
 // The plan's executor state under its current options, built on first use
 // (schedule.cpp).  Host only.
 ExecState* exec_state(Plan& p);
+// Wavefronts per resident workgroup for a plan of n buffers and `units` tiles
+// (programs.cpp).
+int32_t res_waves(int32_t n, int64_t units);
+// The resident (n <= kResMaxN) or streamed form of sliced run `sd`, in place;
+// `sd` stays plain when its program cannot be built (programs.cpp).
+void build_resident(const Plan& p, const ExecState& ex, SliceDesc& sd);
 
 }  // namespace arp

@@ -54,7 +54,7 @@ def test_kernel_source_hash_ignores_comments_only():
     # the stripping assumes no string literal holds a comment marker
     csrc = os.path.join(ROOT, "paper_2409_04202_amd", "csrc")
     for f in ("kernels.hpp", "resident.hpp", "exec.hip", "exec_state.hpp", "rewrite.cpp",
-              "schedule.cpp"):
+              "schedule.cpp", "programs.cpp"):
         for line in open(os.path.join(csrc, f)):
             code = line.split("//")[0]
             for lit in code.split('"')[1::2]:
