@@ -31,7 +31,7 @@ using namespace arp;
 static std::string check_streamed(const ar_plan& plan, const ExecState& ex, const SliceDesc& sd) {
     const int64_t VEC = 16 / plan.esize;
     const size_t n = size_t(plan.n);
-    if ((sd.res_waves != 1 && sd.res_waves != 4) || sd.slots < 1 || sd.slots > kStreamMaxSlots || plan.n > kStreamMaxN ||
+    if (sd.res_waves != 4 || sd.slots < 1 || sd.slots > kStreamMaxSlots || plan.n > kStreamMaxN ||
         int64_t(sd.slots) * 1024 + int64_t(plan.n) * 8 + int64_t(sd.max_nw) * 4 > kLdsBytesPerCU / 2)
         return "streamed launch shape";
     if (int64_t(sd.runits.size()) != sd.nunits || int64_t(sd.tiles.size()) != sd.nunits ||

@@ -298,7 +298,8 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             const Stage stg = staged ? ex->stages[size_t(li)] : Stage{-1, int32_t(li)};
             if (stg.slice >= 0 && ex->slices[size_t(stg.slice)].streamed) {
                 const SliceDesc& sd = ex->slices[size_t(stg.slice)];
-                const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(64 * sd.res_waves);
+                if (sd.res_waves != 4) return fail(AR_ERR_INTERNAL, "streamed launch shape");
+                const dim3 grid(static_cast<uint32_t>(sd.nunits)), block(256);
                 // the slots, the n buffer pointers, the longest unit program
                 const size_t lds = size_t(sd.slots) * 1024 + size_t(plan->n) * 8 + size_t(sd.max_nw) * 4;
                 const bool nt = sd.res_bytes > 2 * kKeepBytes;
@@ -307,11 +308,8 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                        pe->dev + ex->rec_words, plan->n, sd.slots,                              \
                        d->runits + sd.runit_base, d->prog + sd.prog_base, sd.nunits)
 #define AR_STREAM(DT)                                                                         \
-    if (sd.res_waves == 1) {                                                                  \
-        if (nt) AR_STREAM_K(DT, 1, true); else AR_STREAM_K(DT, 1, false);                     \
-    } else {                                                                                  \
-        if (nt) AR_STREAM_K(DT, 4, true); else AR_STREAM_K(DT, 4, false);                     \
-    }
+    if (nt) AR_STREAM_K(DT, 4, true);                                                         \
+    else AR_STREAM_K(DT, 4, false)
                 switch (plan->dtype) {
                     case AR_F32: AR_STREAM(DT_F32); break;
                     case AR_I32: AR_STREAM(DT_I32); break;

@@ -128,8 +128,9 @@ static void encode_segment(const std::vector<const XStep*>& st, std::vector<uint
 // Fills w (64-word chunks) and the slots, loads and stores it uses; false when
 // a fold has more than 252 sources or the slots run out.
 constexpr int32_t kStreamAhead = 48;
-// waves of a streamed workgroup (the kernel takes 1 or 4; one wave owning
-// the whole tile measured the same as four owning a quarter each)
+// waves of a streamed workgroup (the kernel is written for 1 or 4; one wave
+// owning the whole tile measured the same as four owning a quarter each, and
+// the executor launches four)
 constexpr int32_t kStreamWaves = 4;
 constexpr size_t kStreamReserve = 2;  // slots kept for fold results
 
