@@ -24,7 +24,8 @@ Prints one JSON line:
 and, beside the contract's fields: the step time's median and minimum over
 individually timed executions, the whole plan's and the copy launches'
 fractions of the peak, a practical ceiling measured in the same run (a plain
-device copy and a two-source fold through the library, 2 GiB each), the
+device copy with torch and with the library, and a two-source fold through
+the library, 2 GiB each), the
 oracle with the steps of each phase spread over a thread pool, and, when the
 default executor runs sliced or resident launches, the same plan with one
 launch per executed phase (`phase_launches`: its time, and its reduce
@@ -140,10 +141,10 @@ def cpu_parallel(name, budget_s=10.0):
 
 
 def ceiling(torch, arplan):
-    """Practical HBM ceiling in this run: a plain device copy (torch's copy
-    kernel) and a two-source fold through the library, 2 GiB of traffic per
-    repetition each (copy: 1 GiB read + 1 GiB written; fold: 2 x 683 MiB
-    read + 683 MiB written)."""
+    """Practical HBM ceiling in this run, 2 GiB of traffic per repetition
+    each: a plain device copy with torch's copy kernel and with the library
+    (one copy step, 1 GiB read + 1 GiB written), and a two-source fold
+    through the library (2 x 683 MiB read + 683 MiB written)."""
     reps = 10
     out = {}
     a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")    # 1 GiB
@@ -159,24 +160,30 @@ def ceiling(torch, arplan):
     e1.synchronize()
     ms = e0.elapsed_time(e1) / reps
     out["copy_gbs"] = round(2 * a.numel() * 4 / (ms * 1e-3) / 1e9, 1)
+
+    def lib_ms(bufs, steps):
+        h = arplan.ar_plan_create_custom(len(bufs), bufs[0].numel(), "f32", steps)
+        try:
+            ptrs = arplan.pointers(bufs)
+            sh = torch.cuda.current_stream().cuda_stream
+            for _ in range(2):
+                arplan.ar_plan_execute(h, ptrs, sh)
+            e0.record()
+            for _ in range(reps):
+                arplan.ar_plan_execute(h, ptrs, sh)
+            e1.record()
+            e1.synchronize()
+        finally:
+            arplan.ar_plan_destroy(h)
+        return e0.elapsed_time(e1) / reps
+
+    ms = lib_ms([a, b], [(0, "copy", 1, (0,), 0, a.numel())])
+    out["copy_lib_gbs"] = round(2 * a.numel() * 4 / (ms * 1e-3) / 1e9, 1)
     del a, b
     N = (2 << 30) // 12                     # 3 x N x 4 bytes = 2 GiB
     N -= N % 64
     xs = [torch.ones(N, dtype=torch.float32, device="cuda") for _ in range(3)]
-    h = arplan.ar_plan_create_custom(3, N, "f32", [(0, "reduce", 2, (0, 1), 0, N)])
-    try:
-        ptrs = arplan.pointers(xs)
-        sh = torch.cuda.current_stream().cuda_stream
-        for _ in range(2):
-            arplan.ar_plan_execute(h, ptrs, sh)
-        e0.record()
-        for _ in range(reps):
-            arplan.ar_plan_execute(h, ptrs, sh)
-        e1.record()
-        e1.synchronize()
-    finally:
-        arplan.ar_plan_destroy(h)
-    ms = e0.elapsed_time(e1) / reps
+    ms = lib_ms(xs, [(0, "reduce", 2, (0, 1), 0, N)])
     out["fold2_gbs"] = round(3 * N * 4 / (ms * 1e-3) / 1e9, 1)
     del xs
     return out
