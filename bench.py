@@ -279,7 +279,7 @@ def main():
                     help="AR_OPT_RESIDENT (default: the library's, 1)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build executes every emulated processor on one "
+        print("bench.py: the library executes every emulated processor on one "
               "GPU; runs on more than one GPU are not supported (--gpus 1).",
               file=sys.stderr)
         sys.exit(2)
