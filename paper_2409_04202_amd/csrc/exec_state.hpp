@@ -67,6 +67,12 @@ constexpr double kStepNsPerSrcBF16 = 190.0;
 constexpr double kStepNsPerDst = 15.0;
 constexpr double kMinSliceWaves = 256.0;
 constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
+// A sliced run of one phase replacing that phase's only launch is taken only
+// when predicted to cost at most this fraction of the launch: for one phase
+// the estimate above is optimistic (measured: co-located PS n = 16 at 2^18
+// fp32, predicted 0.66 of its launch, ran 1.4 times slower; at 2^20,
+// predicted 0.56, ran 0.82 of it).
+constexpr double kSingleRunGain = 0.6;
 // A sliced run may instead run resident (resident_kernel, AR_OPT_RESIDENT):
 // a workgroup of W waves (res_waves in programs.cpp) per 64 vectors of a
 // segment, the plan's n <= kResMaxN buffers in LDS rows of 1 KiB.  Its

@@ -330,11 +330,12 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
     return pc;
 }
 
-// Sliced runs for AR_OPT_SLICE = 2: phases [a, b), each aligned, writing at
-// most kKeepBytes and moving at most kSliceMaxBytes, chosen to minimise the
-// predicted time, each in its plain or (AR_OPT_RESIDENT, n <= kResMaxN) its
-// resident form, whichever is predicted faster.  A run of one phase only
-// pays off when it replaces several launches.
+// Sliced runs for AR_OPT_SLICE = 2: phases [a, b), each aligned, chosen to
+// minimise the predicted time, each in its plain form (phases writing at most
+// kKeepBytes and moving at most kSliceMaxBytes) or (AR_OPT_RESIDENT,
+// n <= kResMaxN) its resident form, whichever is predicted faster.  A run of
+// one phase that replaces a single launch must be predicted kSingleRunGain
+// of that launch's time or less.
 struct Run {
     int32_t a, b;
     bool resident;
@@ -393,7 +394,9 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
                                 : kResStepNs + kResStepNsPerSrc * c.kmax + kResStepNsPerDst * d);
             next_link = link;
             touched |= c.touched;
-            if (b - a == 1 && nl[size_t(a)] < 2) continue;
+            // a run of one phase that replaces a single launch: only when
+            // predicted far cheaper (the estimate for one phase is optimistic)
+            const bool single = b - a == 1 && nl[size_t(a)] < 2;
             double t = plain_ok ? kLaunchNs + body : std::numeric_limits<double>::infinity();
             bool res = false;
             if (res_ok) {
@@ -407,6 +410,7 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
                     res = true;
                 }
             }
+            if (single && !(t < kSingleRunGain * pc[size_t(a)].t_launch)) continue;
             if (best[size_t(a)] + t < best[size_t(b)]) {
                 best[size_t(b)] = best[size_t(a)] + t;
                 from[size_t(b)] = a;
