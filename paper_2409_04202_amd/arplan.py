@@ -26,8 +26,11 @@ try:
 except ImportError:
     torch = None
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib",
-                        "libarplan.so")
+# The test suite loads this file a second time under another module name,
+# bound to the test build of the library (the same code plus its checking
+# hooks), by placing _LIB_PATH in the module's namespace before running it.
+LIB_PATH = globals().get("_LIB_PATH") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "lib", "libarplan.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(
         "libarplan.so is not built (%s); run "

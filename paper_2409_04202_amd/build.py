@@ -4,8 +4,17 @@ Run ``python -m paper_2409_04202_amd.build`` (or ``__graft_entry__.build()``).
 The plan library and the C ABI (plan.cpp, capi.cpp) are compiled with the
 host compiler; the executor (exec.hip, and its host-side planning in
 rewrite.cpp, schedule.cpp and programs.cpp, which share its HIP types) with
-``hipcc --offload-arch=gfx950``; hipcc links the shared library.  Always
-recompiles.
+``hipcc --offload-arch=gfx950``; hipcc links the shared library.  The
+objects are compiled in parallel and always from scratch.
+
+Two libraries are linked from the same objects:
+
+* ``lib/libarplan.so`` -- the product: exactly the functions
+  ``include/ar_plan.h`` declares;
+* ``lib/libarplan_check.so`` -- for the tests only: the same code plus the
+  checking hooks of ``csrc/debug.cpp`` (``csrc/ar_debug.h``), which read a
+  plan's executor tables back on the host.  Nothing outside ``tests/``
+  loads it.
 """
 
 import os
@@ -13,15 +22,18 @@ import shutil
 import subprocess
 import sys
 import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libarplan.so")
+CHECK_LIB = os.path.join(LIBDIR, "libarplan_check.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HOST_SRCS = ["plan.cpp", "capi.cpp"]
-HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp", "programs.cpp", "debug.cpp"]
+HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp", "programs.cpp"]
+CHECK_SRCS = ["debug.cpp"]          # compiled as HIP, linked into the check library only
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
           "-Wextra", "-Wno-unused-parameter"]
@@ -45,26 +57,32 @@ def _run(cmd, verbose):
         print(out)
 
 
-def build(verbose=False):
+def build(verbose=False, jobs=None):
     hipcc = os.environ.get("HIPCC", os.path.join(ROCM, "bin", "hipcc"))
     cxx = os.environ.get("CXX", "g++")
     os.makedirs(LIBDIR, exist_ok=True)
     tmp = tempfile.mkdtemp(prefix="arplan_build_")
     try:
-        objs = []
+        cmds, objs = [], {}
         for s in HOST_SRCS:
             o = os.path.join(tmp, s + ".o")
-            _run([cxx, "-c", os.path.join(CSRC, s), "-o", o] + COMMON, verbose)
-            objs.append(o)
-        for s in HIP_SRCS:
+            cmds.append([cxx, "-c", os.path.join(CSRC, s), "-o", o] + COMMON)
+            objs[s] = o
+        for s in HIP_SRCS + CHECK_SRCS:
             o = os.path.join(tmp, s + ".o")
-            _run([hipcc, "-c", "-x", "hip", os.path.join(CSRC, s), "-o", o]
-                 + COMMON + HIP_FLAGS, verbose)
-            objs.append(o)
-        tmp_lib = os.path.join(tmp, "libarplan.so")
-        _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o",
-              tmp_lib] + objs, verbose)
-        shutil.move(tmp_lib, LIB)   # atomic replace of the loaded file
+            cmds.append([hipcc, "-c", "-x", "hip", os.path.join(CSRC, s), "-o", o]
+                        + COMMON + HIP_FLAGS)
+            objs[s] = o
+        jobs = jobs or min(8, os.cpu_count() or 1)
+        with ThreadPoolExecutor(max_workers=jobs) as pool:
+            for f in [pool.submit(_run, c, verbose) for c in cmds]:
+                f.result()
+        product = [objs[s] for s in HOST_SRCS + HIP_SRCS]
+        for lib, srcs in ((LIB, product), (CHECK_LIB, product + [objs[s] for s in CHECK_SRCS])):
+            tmp_lib = os.path.join(tmp, os.path.basename(lib))
+            _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp_lib]
+                 + srcs, verbose)
+            shutil.move(tmp_lib, lib)   # atomic replace of the loaded file
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
     return LIB

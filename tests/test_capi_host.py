@@ -16,9 +16,12 @@ import pytest
 import oracle
 from oracle import model
 
-arplan = pytest.importorskip(
+product = pytest.importorskip(
     "paper_2409_04202_amd.arplan",
     reason="HIP library not built (run python -m paper_2409_04202_amd.build)")
+# everything below the export test runs on the test build (same code, plus
+# the checking hooks)
+from checklib import arplan  # noqa: E402
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "ar_plan.h")
@@ -28,10 +31,25 @@ def test_library_exports_every_declared_function():
     text = open(HEADER).read()
     declared = set(re.findall(r"\b(ar_[a-z_]+)\s*\(", text))
     assert declared, "no declarations found"
-    lib = ctypes.CDLL(arplan.LIB_PATH)
     for name in sorted(declared):
-        assert hasattr(lib, name), name
-    assert declared == set(arplan.EXPORTED)
+        assert hasattr(product._lib, name), name
+    assert declared == set(product.EXPORTED)
+    # the product exports exactly the declared functions: no test hook
+    exported = _exported_functions(product.LIB_PATH)
+    assert {f for f in exported if f.startswith("ar_")} == declared
+    # the test build adds the hooks and nothing else
+    extra = {f for f in _exported_functions(arplan.LIB_PATH) if f.startswith("ar_")} - declared
+    assert extra == {"ar_debug_check_tiling", "ar_debug_exec_steps", "ar_debug_resident"}
+
+
+def _exported_functions(path):
+    """Names of the functions a shared library exports (its dynamic symbol
+    table, read with the ELF tools of the host)."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", path], check=True,
+                         stdout=subprocess.PIPE, text=True).stdout
+    return {l.split()[-1] for l in out.splitlines() if len(l.split()) == 3
+            and l.split()[1] == "T"}
 
 
 def _norm(phases):
@@ -212,8 +230,7 @@ def test_timer_host_side():
 
 
 def _check_tiling(handle, vecok):
-    lib = ctypes.CDLL(arplan.LIB_PATH)
-    f = lib.ar_debug_check_tiling
+    f = arplan._lib.ar_debug_check_tiling
     f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_char_p, ctypes.c_int64]
     f.restype = ctypes.c_int32
     buf = ctypes.create_string_buffer(512)

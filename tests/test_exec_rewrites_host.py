@@ -18,7 +18,8 @@ import pytest
 import oracle
 from oracle.plans import Plan as OPlan, Step as OStep
 
-from paper_2409_04202_amd import arplan, workloads
+from paper_2409_04202_amd import workloads
+from checklib import arplan
 
 
 def _exec_steps(handle):

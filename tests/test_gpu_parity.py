@@ -248,7 +248,7 @@ def test_streamed_random_custom_plans(seed):
     # random hazard-free plans over 65-200 buffers (folds of 3-16 sources,
     # copies into up to 40 buffers; the host-side program test's generator)
     # as one streamed launch, and with the default executor, bit-exact
-    from test_resident_host import _wide_random_plan
+    from plan_gen import wide_random_plan as _wide_random_plan
     from oracle.plans import Plan as OPlan, Step as OStep
     rng = np.random.default_rng(9500 + seed)
     n = int(rng.choice([65, 80, 130, 200]))
@@ -538,7 +538,7 @@ def test_wide_random_plans_resident(seed):
     # 8-64 buffers, folds of up to 16 sources, copies into up to 40 buffers
     # (fold and store records); whole plan resident, plain sliced and the
     # default choice, against the oracle
-    from test_resident_host import _wide_random_plan
+    from plan_gen import wide_random_plan as _wide_random_plan
     from oracle.plans import Plan as OPlan, Step as OStep
     rng = np.random.default_rng(9600 + seed)
     n = int(rng.choice([8, 17, 33, 64]))

@@ -20,10 +20,12 @@ import oracle
 from oracle.execute import fold
 from oracle.plans import Plan as OPlan, Step as OStep
 
-from paper_2409_04202_amd import arplan, workloads
+from paper_2409_04202_amd import workloads
+from checklib import arplan
 
 from test_capi_host import _check_tiling
 from test_exec_rewrites_host import _random_plan
+from plan_gen import wide_random_plan as _wide_random_plan
 
 
 def _resident_tables(handle, stage):
@@ -324,32 +326,6 @@ def test_ring_program_is_one_chain_and_a_broadcast():
             recs = _decode(prog[off:off + nw])
             assert [r[0] for r in recs] == ["chain", "add"] and alias >= 0
             assert len(recs[0][1]) == 63
-
-
-def _wide_random_plan(rng, n, M):
-    """Random hazard-free phases over n buffers on M positions: per phase the
-    positions are cut into blocks and each block gets one reduce of 3..16
-    distinct sources (its destination may be one of them) or copies of one
-    source into several destinations (the executor merges them into one step
-    with many destinations)."""
-    phases = []
-    for q in range(int(rng.integers(2, 6))):
-        cuts = np.unique(np.concatenate([[0, M], rng.integers(1, M, size=rng.integers(1, 6))]))
-        steps = []
-        for b, e in zip(cuts[:-1], cuts[1:]):
-            if rng.random() < 0.5:
-                k = int(rng.integers(3, min(n, 16) + 1))
-                srcs = [int(x) for x in rng.choice(n, size=k, replace=False)]
-                dst = int(rng.choice(srcs)) if rng.random() < 0.5 else int(rng.integers(n))
-                steps.append(("reduce", dst, srcs, int(b), int(e)))
-            else:
-                src = int(rng.integers(n))
-                others = [x for x in range(n) if x != src]
-                m = int(rng.integers(1, min(n - 1, 40) + 1))
-                for d in rng.choice(others, size=m, replace=False):
-                    steps.append(("copy", int(d), [src], int(b), int(e)))
-        phases.append(steps)
-    return phases
 
 
 @pytest.mark.parametrize("seed", range(40))
