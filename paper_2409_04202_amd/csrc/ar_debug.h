@@ -1,4 +1,5 @@
-/* Test hooks of libarplan.so; not part of the public ABI (include/ar_plan.h). */
+/* Test hooks, exported only by the test build of the library
+ * (lib/libarplan_check.so); not part of the public ABI (include/ar_plan.h). */
 #ifndef AR_DEBUG_H
 #define AR_DEBUG_H
 #include "../../include/ar_plan.h"
@@ -37,6 +38,14 @@ ar_status ar_debug_exec_steps(ar_plan* plan, int64_t step_cap, int32_t* phase,
  * first.  AR_ERR_INVALID_ARG when the launch is neither.  Host only. */
 ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* info,
                             int64_t* units, uint32_t* prog);
+
+/* How phase launch `stage` (as in ar_plan_launch_info) runs: out[0] = its
+ * kernel's template source count (0: read at run time), out[1] = cache mode
+ * (bit 0: nontemporal loads, bit 1: nontemporal stores), out[2] = wave tile
+ * in elements, out[3] = wave tiles, out[4] = wavefronts per block, out[5] =
+ * 1 when the tiles come from a table.  AR_ERR_INVALID_ARG for a sliced
+ * launch.  Host only. */
+ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* out);
 #ifdef __cplusplus
 }
 #endif

@@ -649,3 +649,25 @@ AR_EXPORT ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* inf
         return fail(AR_ERR_INTERNAL, e.what());
     }
 }
+
+AR_EXPORT ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* out) {
+    clear_error();
+    if (!plan || !out) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    try {
+        const ExecState* ex = exec_state(*plan);
+        if (stage < 0 || stage >= int32_t(ex->stages.size()))
+            return fail(AR_ERR_INVALID_ARG, "launch index out of range");
+        const Stage stg = ex->stages[size_t(stage)];
+        if (stg.slice >= 0) return fail(AR_ERR_INVALID_ARG, "a sliced launch");
+        const LaunchDesc& L = ex->launches[size_t(stg.launch)];
+        out[0] = L.kern_k;
+        out[1] = L.cm;
+        out[2] = L.tile_elems;
+        out[3] = L.nunits;
+        out[4] = L.wpb;
+        out[5] = L.tile_off >= 0 ? 1 : 0;
+        return AR_OK;
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}

@@ -39,7 +39,8 @@ def test_library_exports_every_declared_function():
     assert {f for f in exported if f.startswith("ar_")} == declared
     # the test build adds the hooks and nothing else
     extra = {f for f in _exported_functions(arplan.LIB_PATH) if f.startswith("ar_")} - declared
-    assert extra == {"ar_debug_check_tiling", "ar_debug_exec_steps", "ar_debug_resident"}
+    assert extra == {"ar_debug_check_tiling", "ar_debug_exec_steps", "ar_debug_resident",
+                     "ar_debug_launch_desc"}
 
 
 def _exported_functions(path):
@@ -532,3 +533,46 @@ def test_sliced_runs_of_workloads(name):
         if name.startswith("sweep_ring"):
             # 126 phases of short steps: one sliced launch
             assert len(L) == 1 and L[0][0] in (-1, -2)
+
+
+def _launch_desc(handle, stage):
+    f = arplan._lib.ar_debug_launch_desc
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)]
+    f.restype = ctypes.c_int32
+    out = (ctypes.c_int64 * 6)()
+    assert f(handle, stage, out) == arplan.AR_OK, arplan.ar_last_error()
+    return {"k": out[0], "cm": out[1], "tile": out[2], "tiles": out[3], "wpb": out[4],
+            "table": out[5]}
+
+
+def test_full_size_forms_use_the_nontemporal_kernels():
+    # The benchmark's as-written RHD plan at full size (n = 8, 2^26 fp32):
+    # the first two halving launches write more than the last-level cache
+    # holds (nontemporal loads and stores), the third writes 256 MiB that
+    # the first doubling phase reads (nontemporal loads, cached stores).
+    # The full-size GPU parity test runs this same plan, so these kernel
+    # instances are covered there.
+    with arplan.Plan(8, 1 << 26, "f32", "rhd") as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        L = p.launches()
+        assert [(x[0], x[1]) for x in L] == [(0, 2), (1, 2), (2, 2), (3, 1), (4, 1), (5, 1)]
+        d = [_launch_desc(p.handle, i) for i in range(3)]
+        assert [x["k"] for x in d] == [2, 2, 2]
+        assert [x["cm"] for x in d] == [3, 3, 1]
+        # with the rewrites, the last halving launch stores to all 8 buffers
+        p.set_option(arplan.AR_OPT_FUSE, 1)
+        d = [_launch_desc(p.handle, i) for i in range(len(p.launches()))]
+        assert [x["cm"] for x in d] == [3, 3, 3]
+    # co-located PS (16-source fold, 1088 MiB) and the tree (8, 8) level-0
+    # reduce (8 sources, 1152 MiB) as written: nontemporal loads
+    with arplan.Plan(16, 1 << 24, "f32", "cps") as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        d = _launch_desc(p.handle, 0)
+        assert d["k"] == 16 and d["cm"] & 1
+    with arplan.Plan(64, 1 << 22, "f32", "tree", (8, 8)) as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        d = _launch_desc(p.handle, 0)
+        assert d["k"] == 8 and d["cm"] & 1

@@ -3,10 +3,8 @@
 fp32 and int32 must match bit for bit (the plan fixes the association
 order); bf16 must match the oracle's per-step rounding bit for bit and lie
 within 1e-2 normwise of the fp64 sum.  Small and scaled-down workloads are
-compared element by element over every buffer; the full-size workloads are
-compared at sampled positions (every block edge, tile edges and random
-positions, for every processor) plus the property that all n outputs are
-identical over the whole buffer.
+compared element by element over every buffer, and so are the full-size
+workloads, in every executor form the benchmark times.
 """
 
 import numpy as np
@@ -136,17 +134,49 @@ def test_sliced_runs_between_phase_launches():
             assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
-# ------------------------------------------------- full-size, sampled check
+# ------------------------------------------- full size, every element
 
-def _sample_positions(n, N, rng):
-    off = np.array(oracle.block_bounds(N, n))
-    edges = np.concatenate([off, off - 1, off + 1])
-    if len(edges) > 4096:
-        edges = rng.choice(edges, 4096, replace=False)
-    tiles = np.arange(0, N, 1 << 15)
-    idx = np.concatenate([edges, tiles, tiles - 1, rng.integers(0, N, 4096),
-                          [0, N - 1]])
-    return np.unique(idx[(idx >= 0) & (idx < N)])
+# The executor forms the benchmark times: the default choice, phase launches
+# with the rewrites, and the plan as written (every step as listed, one
+# launch per phase).  (AR_OPT_FUSE, AR_OPT_SLICE, AR_OPT_RESIDENT)
+BENCH_FORMS = [("default", 1, 2, 1), ("phase launches", 1, 0, 1), ("as written", 0, 0, 1)]
+
+
+def _full_size_every_element(name, forms):
+    """Run the full-size workload once per form from the same inputs and
+    compare every element of every buffer with the oracle's run of the
+    plan (computed once)."""
+    c = workloads.CONFIGS[name]
+    n, N, dt = c["n"], c["N"], c["dtype"]
+    say("case: full-size %s: drawing inputs and running the oracle" % name)
+    xs0 = workloads.inputs(name)
+    ref = oracle.execute(_oracle_plan(c["kind"], n, N, c["fanin"]),
+                         [x.copy() for x in xs0], dt)
+    pristine = to_device(xs0, dt)
+    for label, fuse, slice_, resident in forms:
+        say("case: full-size %s, %s (fuse=%d slice=%d resident=%d)" % (
+            name, label, fuse, slice_, resident))
+        ts = [t.clone() for t in pristine]
+        with arplan.Plan(n, N, dt, c["kind"], c["fanin"]) as p:
+            p.set_option(arplan.AR_OPT_FUSE, fuse)
+            p.set_option(arplan.AR_OPT_SLICE, slice_)
+            p.set_option(arplan.AR_OPT_RESIDENT, resident)
+            kinds = sorted({x[0] for x in p.launches()})
+            run_plan(p, ts)
+        say("  launch kinds %s" % kinds)
+        for q in range(n):
+            g = ts[q].cpu().numpy()
+            g = g.view(np.uint16) if dt == "bf16" else g
+            if not np.array_equal(g, ref[q]):
+                bad = np.nonzero(g != ref[q])[0]
+                raise AssertionError("%s %s: processor %d differs at %d positions, "
+                                     "first %s" % (name, label, q, len(bad), bad[:8]))
+        del ts
+    if dt == "bf16":
+        err = _normwise_bf16(ref[0], xs0)
+        say("bf16 normwise error %.3e" % err)
+        assert err <= 1e-2
+    return kinds
 
 
 @pytest.mark.parametrize("name", ["rhd_n8_f32", "cps_n16_f32",
@@ -154,28 +184,7 @@ def _sample_positions(n, N, rng):
                                   "tree8x8x8_n512_bf16", "asy384_gentree_f32",
                                   "cdc384_gentree_f32"])
 def test_full_size_configs(name):
-    c = workloads.CONFIGS[name]
-    n, N, dt = c["n"], c["N"], c["dtype"]
-    say("case: full-size %s" % name)
-    xs0 = workloads.inputs(name)
-    ts = to_device(xs0, dt)
-    rng = np.random.default_rng(99)
-    idx = _sample_positions(n, N, rng)
-    with arplan.Plan(n, N, dt, c["kind"], c["fanin"]) as p:
-        run_plan(p, ts)
-    plan = _oracle_plan(c["kind"], n, N, c["fanin"])
-    want = oracle.execute_sampled(plan, [x[idx] for x in xs0], idx, dt)
-    it = torch.from_numpy(idx).to("cuda")
-    for q in range(n):
-        g = ts[q].index_select(0, it).cpu().numpy()
-        g = g.view(np.uint16) if dt == "bf16" else g
-        assert np.array_equal(g, want[q]), (name, q)
-        assert torch.equal(ts[q], ts[0]), (name, q)
-    if dt == "bf16":
-        y = ts[0].cpu().numpy().view(np.uint16)
-        err = _normwise_bf16(y, xs0)
-        say("bf16 normwise error %.3e" % err)
-        assert err <= 1e-2
+    _full_size_every_element(name, BENCH_FORMS)
 
 
 @pytest.mark.parametrize("N", [(1 << 24) + 160, (1 << 21) + 160])
@@ -195,25 +204,13 @@ def test_large_resident_with_partial_tiles(N):
 @pytest.mark.parametrize("dtype,N", [("bf16", 1 << 25), ("i32", (1 << 24) + 160)])
 def test_large_resident_nontemporal_dtypes(dtype, N):
     # RHD n = 8 as one resident launch moving more than the last-level cache
-    # (nontemporal rows) in bf16 and int32, on sampled positions
+    # (nontemporal rows) in bf16 and int32, every element
     n = 8
     with arplan.Plan(n, N, dtype, "rhd") as p:
         L = p.launches()
         assert [x[0] for x in L] == [-2] and L[0][4] > 512 << 20
-    say("case: large resident rhd n=8 N=%d %s" % (N, dtype))
-    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", 21)
-    ts = to_device(xs0, dtype)
-    with arplan.Plan(n, N, dtype, "rhd") as p:
-        run_plan(p, ts)
-    rng = np.random.default_rng(5)
-    idx = _sample_positions(n, N, rng)
-    want = oracle.execute_sampled(oracle.rhd(n, N), [x[idx] for x in xs0], idx, dtype)
-    it = torch.from_numpy(idx).to("cuda")
-    for q in range(n):
-        g = ts[q].index_select(0, it).cpu().numpy()
-        g = g.view(np.uint16) if dtype == "bf16" else g
-        assert np.array_equal(g, want[q]), (dtype, q)
-        assert torch.equal(ts[q], ts[0]), (dtype, q)
+    _full_compare("rhd", n, N, dtype, None, "int1000" if dtype == "i32" else "uniform",
+                  seed=21)
 
 
 # ------------------------------------------- streamed runs (n > 64 buffers)
@@ -311,26 +308,12 @@ def test_streamed_held_back_store():
                                   "cdc384_gentree_f32"])
 def test_streamed_full_size(name):
     # the full-size workloads with more than 64 buffers as one streamed
-    # launch, on sampled positions
+    # launch, every element
     c = workloads.CONFIGS[name]
-    n, N, dt = c["n"], c["N"], c["dtype"]
-    say("case: full-size streamed %s" % name)
-    xs0 = workloads.inputs(name)
-    ts = to_device(xs0, dt)
-    rng = np.random.default_rng(98)
-    idx = _sample_positions(n, N, rng)
-    with arplan.Plan(n, N, dt, c["kind"], c["fanin"]) as p:
+    with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
         p.set_option(arplan.AR_OPT_SLICE, 1)
         assert [x[0] for x in p.launches()] == [-3]
-        run_plan(p, ts)
-    plan = _oracle_plan(c["kind"], n, N, c["fanin"])
-    want = oracle.execute_sampled(plan, [x[idx] for x in xs0], idx, dt)
-    it = torch.from_numpy(idx).to("cuda")
-    for q in range(n):
-        g = ts[q].index_select(0, it).cpu().numpy()
-        g = g.view(np.uint16) if dt == "bf16" else g
-        assert np.array_equal(g, want[q]), (name, q)
-        assert torch.equal(ts[q], ts[0]), (name, q)
+    _full_size_every_element(name, [("whole plan streamed", 1, 1, 1)])
 
 
 # --------------------------------------------------------------- edge cases
