@@ -359,7 +359,7 @@ def bench_workload(torch, arplan, name, K, W, forms, stream, cpu_s, headline=Fal
     for form in forms:
         print("bench: %s %s form, %d steps" % (name, form, K), file=sys.stderr, flush=True)
         res[form] = time_form(torch, arplan, c, bufs, restore, K, W, FORMS[form], stream)
-    if headline:
+    if headline and "default" in forms:
         res["step_ms"] = step_distribution(torch, arplan, c, bufs, restore, K, stream)
     del bufs, pristine
     torch.cuda.empty_cache()
@@ -377,7 +377,8 @@ def public(form_res):
 
 def headline_line(h, K, W, name):
     """The contract's JSON line from the headline workload's results."""
-    d, w = h["default"], h.get("as_written")
+    w = h.get("as_written")
+    d = h.get("default") or w
     red_b, cpy_b = d["_plan_bytes"]
     out = {
         "metric": "AllReduce algbw GB/s and % HBM roofline per plan at 1 MI355X",
@@ -393,7 +394,8 @@ def headline_line(h, K, W, name):
         "dtype": h["dtype"],
         "data": "synthetic (seeded inputs, %s)" % name,
         "config": {"workload": name, "plan": h["plan"], "n": h["n"], "N": h["N"],
-                   "fanin": h["fanin"], "form": "default executor",
+                   "fanin": h["fanin"],
+                   "form": "default executor" if "default" in h else "plan as written",
                    "parallelism": "emulated %d processors on 1 GPU" % h["n"]},
         "plan_bytes_per_step": red_b + cpy_b,
     }
@@ -427,7 +429,8 @@ def headline_line(h, K, W, name):
     out["plan_frac_as_written"] = (round(_gbs(red_b + cpy_b, w["ms_per_step"]) / HBM_PEAK_GBS, 4)
                                    if w is not None else None)
     out["step_ms"] = h.get("step_ms")
-    out["default"] = public(d)
+    if "default" in h:
+        out["default"] = public(d)
     if w is not None:
         out["as_written"] = public(w)
     out["cpu_baseline"] = h.get("cpu_baseline")
@@ -444,7 +447,12 @@ def config_entry(r):
             e[form] = {k: f[k] for k in ("ms_per_step", "algbw_gbs", "plan_gbs",
                                          "reduce_launches", "reduce_gbs", "reduce_frac",
                                          "copy_gbs", "kernels")}
-            e[form]["launches"] = len(f["launches"])
+            L = f["launches"]
+            if len(L) <= 16:   # (plan phase, k, destinations, steps, bytes, ms)
+                e[form]["launches"] = [[x["phase"], x["k"], x["max_dst"], x["steps"],
+                                        x["bytes"], x["ms"]] for x in L]
+            else:
+                e[form]["launches"] = "%d launches" % len(L)
     e["cpu_baseline"] = r.get("cpu_baseline")
     return e
 
