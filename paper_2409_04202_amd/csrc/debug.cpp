@@ -238,13 +238,9 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     const int32_t dst = ex->hidx[size_t(st.dst_off + q)];
                     if (dst < 0 || dst >= plan->n) return bad("destination index out of range");
                 }
-                DstPart part = dst_part(unit, L.dsplit, st.ndst);
+                const DstPart part = dst_part(unit, L.dsplit, st.ndst);
                 if (part.tile != tile || part.d0 < 0 || part.nd < 0 || part.d0 + part.nd > st.ndst)
                     return bad("destination part out of range");
-                if (L.dsplit > 1 && !vecok) {  // the first wave of the tile does it all
-                    part.d0 = 0;
-                    part.nd = unit == tile * L.dsplit ? st.ndst : 0;
-                }
                 const TileSpan sp = tile_span(st.begin, st.end, t, L.tile_elems, VEC, vecok != 0);
                 if (sp.lo >= sp.hi || part.nd == 0) continue;
                 if (sp.lo < st.begin || sp.hi > st.end || st.begin < 0 || st.end > plan->N)

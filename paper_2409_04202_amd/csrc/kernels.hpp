@@ -267,25 +267,17 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
 
 // Fold elements [lo, hi) of the k sources sp[] into the destinations dp[],
 // one element per lane per pass (used for unaligned heads/tails and for
-// unaligned buffers).  SYNC: the waves of the workgroup share this range
-// (a split launch, see dst_part); every pass waits at a workgroup barrier
-// between its loads and its stores, so no wave stores into a source before
-// every wave has loaded it.  The pass count depends on lo and hi only, so
-// all waves of the workgroup reach the same barriers.
-template <int DT, int K, bool SYNC = false>
+// unaligned buffers).
+template <int DT, int K>
 __device__ __forceinline__ void fold_scalar(void* const* __restrict__ sp, int k,
                                             void* const* __restrict__ dp, int ndst,
                                             int64_t lo, int64_t hi, int lane) {
     using T = typename Elem<DT>::T;
     if (K == 1 || (K == 0 && k == 1)) {  // copy: move the bits unchanged
         const AR_GLOBAL T* s = as_global<T>(sp[0]);
-        for (int64_t e0 = lo; e0 < hi; e0 += 64) {
-            const int64_t e = e0 + lane;
-            T v{};
-            if (e < hi) v = s[e];
-            if constexpr (SYNC) __syncthreads();
-            if (e < hi)
-                for (int j = 0; j < ndst; ++j) as_global<T>(dp[j])[e] = v;
+        for (int64_t e = lo + lane; e < hi; e += 64) {
+            const T v = s[e];
+            for (int j = 0; j < ndst; ++j) as_global<T>(dp[j])[e] = v;
         }
         return;
     }
@@ -308,7 +300,6 @@ __device__ __forceinline__ void fold_scalar(void* const* __restrict__ sp, int k,
             for (int u = 0; u < SU; ++u)
                 if (ok[u]) acc[u].add(s[e0 + u * 64 + lane]);
         }
-        if constexpr (SYNC) __syncthreads();
         for (int j = 0; j < ndst; ++j) {
             AR_GLOBAL T* d = as_global<T>(dp[j]);
 #pragma unroll
@@ -381,9 +372,8 @@ __device__ __forceinline__ void store_all(const DstMem& dst, int64_t v0, const u
 // folded in source order and stored to every destination.  FULL: all U
 // vectors are in range, so the loads are issued back to back with no
 // per-vector branch.  Cache mode CM of a launch: bit 0 = nontemporal loads,
-// bit 1 = nontemporal stores.  SYNC: a workgroup barrier between the fold
-// and the stores (split launches, see fold_scalar).
-template <int DT, int K, int U, int CM, bool FULL, class D, bool SYNC = false>
+// bit 1 = nontemporal stores.
+template <int DT, int K, int U, int CM, bool FULL, class D>
 __device__ __forceinline__ void fold_vectors(const gvec* const* sp, const D& dst,
                                              int64_t v0, int64_t at, int64_t nv, int lane) {
     bool ok[U];
@@ -409,12 +399,11 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, const D& dst
             out[u] = acc.out();
         }
     }
-    if constexpr (SYNC) __syncthreads();
     store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
 }
 
 // Runtime source count: one source at a time, U vectors in flight.
-template <int DT, int U, int CM, bool FULL, class D, bool SYNC = false>
+template <int DT, int U, int CM, bool FULL, class D>
 __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, int k,
                                                 const D& dst, int64_t v0, int64_t at,
                                                 int64_t nv, int lane) {
@@ -450,58 +439,20 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, 
 #pragma unroll
         for (int u = 0; u < U; ++u) out[u] = acc[u].out();
     }
-    if constexpr (SYNC) __syncthreads();
     store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
 }
 
-// The vector and element-wise parts of one wave tile (see tile_span); SYNC:
-// the waves of the workgroup share the tile (split launch).
-template <int DT, int K, bool VECOK, int CM, bool SYNC>
-__device__ __forceinline__ void run_tile(void* const* __restrict__ sp, int k,
-                                         void* const* __restrict__ dp, int ndst,
-                                         const TileSpan& ts, int lane) {
-    constexpr int VEC = Elem<DT>::VEC;
-    constexpr int U = kcfg(K).U;
-    if (ts.vlo > ts.lo) fold_scalar<DT, K, SYNC>(sp, k, dp, ndst, ts.lo, ts.vlo, lane);
-    if (ts.hi > ts.vhi) fold_scalar<DT, K, SYNC>(sp, k, dp, ndst, ts.vhi, ts.hi, lane);
-    if (!VECOK || ts.vhi <= ts.vlo) return;
-
-    const int64_t v0 = ts.vlo / VEC;
-    const int64_t nv = (ts.vhi - ts.vlo) / VEC;
-    const Dsts dst = load_dsts(dp, ndst);
-    int64_t at = 0;
-    if constexpr (K > 0) {
-        const gvec* sv[K];
-#pragma unroll
-        for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(sp[j]) + v0;
-        for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors<DT, K, U, CM, true, Dsts, SYNC>(sv, dst, v0, at, nv, lane);
-        if (at < nv) fold_vectors<DT, K, U, CM, false, Dsts, SYNC>(sv, dst, v0, at, nv, lane);
-    } else {
-        for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors_rt<DT, U, CM, true, Dsts, SYNC>(sp, k, dst, v0, at, nv, lane);
-        if (at < nv)
-            fold_vectors_rt<DT, U, CM, false, Dsts, SYNC>(sp, k, dst, v0, at, nv, lane);
-    }
-}
-
 // One launch: `nunits` wave units over the steps whose records start at
-// `recs`, `stride` words apart.  K = 0 means the source count is read from
-// each step (any k >= 1).  VECOK: every buffer is 16-byte aligned.  CM:
-// cache mode of the vector loads and stores.
-//
-// dsplit > 1 (a split launch; dsplit equals the wavefronts per block, so a
-// workgroup is one tile): every wave of the workgroup folds the tile and
-// stores to its part of the destinations (dst_part), waiting at a
-// workgroup barrier between each pass's loads and stores, because a step's
-// destinations may be among its sources.  All waves of the workgroup take
-// the same branches (same step and tile).  With unaligned buffers the first
-// wave does the whole tile alone.
+// `recs`, `stride` words apart; `dsplit` units per wave tile, each storing
+// to its part of the destinations (see dst_part).  K = 0 means the source
+// count is read from each step (any k >= 1).  VECOK: every buffer is 16-byte
+// aligned.  CM: cache mode of the vector loads and stores.
 template <int DT, int K, bool VECOK, int CM>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
     int64_t nunits, int64_t tiles_per_step, int64_t tile_elems, int dsplit) {
     constexpr int VEC = Elem<DT>::VEC;
+    constexpr int U = kcfg(K).U;
     constexpr int WPB = kcfg(K).WPB;
     const int lane = int(threadIdx.x) & 63;
     const int64_t unit = int64_t(blockIdx.x) * WPB +
@@ -517,18 +468,34 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const StepHead st = *reinterpret_cast<const StepHead*>(rec);
     const int k = K ? K : st.k;
     void* const* sp = reinterpret_cast<void* const*>(rec + kRecHead);
+    const DstPart part = dst_part(unit, dsplit, st.ndst);
+    if (part.nd <= 0) return;
+    void* const* dp = sp + k + part.d0;
+    const int ndst = part.nd;
+
     const TileSpan ts = tile_span(st.begin, st.end, t, tile_elems, VEC, VECOK);
     if (ts.lo >= ts.hi) return;
-    if (dsplit > 1) {
-        if constexpr (VECOK) {
-            const DstPart part = dst_part(unit, dsplit, st.ndst);
-            run_tile<DT, K, VECOK, CM, true>(sp, k, sp + k + part.d0, part.nd, ts, lane);
-            return;
-        } else {
-            if (unit != tile * dsplit) return;
-        }
+    if (ts.vlo > ts.lo) fold_scalar<DT, K>(sp, k, dp, ndst, ts.lo, ts.vlo, lane);
+    if (ts.hi > ts.vhi) fold_scalar<DT, K>(sp, k, dp, ndst, ts.vhi, ts.hi, lane);
+    if (!VECOK || ts.vhi <= ts.vlo) return;
+
+    const int64_t v0 = ts.vlo / VEC;
+    const int64_t nv = (ts.vhi - ts.vlo) / VEC;
+    const Dsts dst = load_dsts(dp, ndst);
+    int64_t at = 0;
+    if constexpr (K > 0) {
+        const gvec* sv[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(sp[j]) + v0;
+        for (; at + 64 * U <= nv; at += 64 * U)
+            fold_vectors<DT, K, U, CM, true>(sv, dst, v0, at, nv, lane);
+        if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, dst, v0, at, nv, lane);
+    } else {
+        for (; at + 64 * U <= nv; at += 64 * U)
+            fold_vectors_rt<DT, U, CM, true>(sp, k, dst, v0, at, nv, lane);
+        if (at < nv)
+            fold_vectors_rt<DT, U, CM, false>(sp, k, dst, v0, at, nv, lane);
     }
-    run_tile<DT, K, VECOK, CM, false>(sp, k, sp + k, st.ndst, ts, lane);
 }
 
 // ------------------------------------------------------------------------

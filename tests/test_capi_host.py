@@ -576,27 +576,3 @@ def test_full_size_forms_use_the_nontemporal_kernels():
         p.set_option(arplan.AR_OPT_SLICE, 0)
         d = _launch_desc(p.handle, 0)
         assert d["k"] == 8 and d["cm"] & 1
-
-
-def test_many_destination_launches_are_split():
-    # the tree (8, 8, 8)'s last reduce phase stores each 1 KiB step to 64
-    # buffers: one workgroup of 4 waves per tile, each storing to 16
-    with arplan.Plan(512, 1 << 18, "bf16", "tree", (8, 8, 8)) as p:
-        p.set_option(arplan.AR_OPT_SLICE, 0)
-        L = p.launches()
-        assert [(x[1], x[2]) for x in L][2] == (8, 64)
-        d = _launch_desc(p.handle, 2)
-        assert d["wpb"] == 4 and d["tiles"] == 512 * 4
-        # one 16-byte vector of each of 64 lanes per tile
-        assert d["tile"] == 1024 and not d["table"]
-    # co-located PS at a small size: every step stores to all 16 buffers,
-    # each also a source
-    with arplan.Plan(16, (1 << 14) + 3, "f32", "cps") as p:
-        p.set_option(arplan.AR_OPT_SLICE, 0)
-        (ph, k, dmax, cnt, b), = p.launches()
-        assert (k, dmax) == (16, 16)
-        d = _launch_desc(p.handle, 0)
-        assert d["tiles"] % 4 == 0 and d["wpb"] == 4
-        for vecok in (1, 0):
-            st, msg = _check_tiling(p.handle, vecok)
-            assert st == arplan.AR_OK, msg
