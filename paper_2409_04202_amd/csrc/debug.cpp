@@ -200,8 +200,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
         std::string why;
         if (!exec_phases_hazard_free(ex->phases, plan->n, why)) return bad(why);
         const int64_t VEC = 16 / plan->esize;
-        // per step: (destination slot, lo, hi) of every tile storing to it
-        std::vector<std::vector<std::tuple<int32_t, int64_t, int64_t>>> cover(ex->hsteps.size());
+        std::vector<std::vector<std::pair<int64_t, int64_t>>> cover(ex->hsteps.size());
         std::vector<char> launched(ex->hsteps.size(), 0);
         for (const LaunchDesc& L : ex->launches) {
             if (L.nunits <= 0) return bad("launch without work units");
@@ -210,16 +209,13 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             if (L.wpb != kcfg(L.kern_k).WPB) return bad("block size differs from the kernel's");
             if (L.tile_elems % (64 * VEC) != 0) return bad("tile not a multiple of a wave vector");
             const int2* tiles = L.tile_off >= 0 ? ex->htiles.data() + L.tile_off : nullptr;
-            if (L.dsplit < 1 || L.nunits % L.dsplit) return bad("destination split does not divide the units");
-            if (tiles && L.tile_off + L.nunits / L.dsplit > int64_t(ex->htiles.size()))
+            if (tiles && L.tile_off + L.nunits > int64_t(ex->htiles.size()))
                 return bad("tile table overrun");
             for (int64_t j = 0; j < L.count; ++j) launched[size_t(L.first + j)] = 1;
-            if (L.dsplit > 1 && L.dsplit != L.wpb) return bad("destination split is not one block");
             for (int64_t unit = 0; unit < blocks * L.wpb; ++unit) {
                 if (unit >= L.nunits) continue;  // the kernel returns here
-                const int64_t tile = L.dsplit > 1 ? unit / L.dsplit : unit;
                 int64_t s, t;
-                unit_tile(tile, tiles, L.tiles_per_step, s, t);
+                unit_tile(unit, tiles, L.tiles_per_step, s, t);
                 if (tiles && s == -1 && t == 0) continue;  // padding entry: the kernel skips it
                 if (s < 0 || s >= L.count || t < 0) return bad("unit maps outside the launch");
                 const DevStep& st = ex->hsteps[size_t(L.first + s)];
@@ -238,11 +234,8 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     const int32_t dst = ex->hidx[size_t(st.dst_off + q)];
                     if (dst < 0 || dst >= plan->n) return bad("destination index out of range");
                 }
-                const DstPart part = dst_part(unit, L.dsplit, st.ndst);
-                if (part.tile != tile || part.d0 < 0 || part.nd < 0 || part.d0 + part.nd > st.ndst)
-                    return bad("destination part out of range");
                 const TileSpan sp = tile_span(st.begin, st.end, t, L.tile_elems, VEC, vecok != 0);
-                if (sp.lo >= sp.hi || part.nd == 0) continue;
+                if (sp.lo >= sp.hi) continue;
                 if (sp.lo < st.begin || sp.hi > st.end || st.begin < 0 || st.end > plan->N)
                     return bad("tile outside its step");
                 if (!(sp.lo <= sp.vlo && sp.vlo <= sp.vhi && sp.vhi <= sp.hi))
@@ -251,8 +244,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     return bad("misaligned vector part");
                 if (sp.vlo - sp.lo >= VEC || (sp.vhi > sp.vlo && sp.hi - sp.vhi >= VEC))
                     if (sp.vhi > sp.vlo) return bad("head or tail longer than a vector");
-                for (int32_t j = part.d0; j < part.d0 + part.nd; ++j)
-                    cover[size_t(L.first + s)].emplace_back(j, sp.lo, sp.hi);
+                cover[size_t(L.first + s)].push_back({sp.lo, sp.hi});
             }
         }
         // step records: inside the record area, disjoint, long enough for
@@ -284,21 +276,13 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             auto& c = cover[i];
             if (st.end > st.begin && !launched[i]) return bad("step never launched");
             std::sort(c.begin(), c.end());
-            // every destination slot: its tiles cover [begin, end) exactly once
-            size_t at_i = 0;
-            for (int32_t j = 0; j < st.ndst; ++j) {
-                int64_t at = st.begin;
-                for (; at_i < c.size() && std::get<0>(c[at_i]) == j; ++at_i) {
-                    if (std::get<1>(c[at_i]) != at)
-                        return bad("gap or overlap in step " + std::to_string(i) + " destination " +
-                                   std::to_string(j));
-                    at = std::get<2>(c[at_i]);
-                }
-                if (st.end > st.begin && at != st.end)
-                    return bad("step " + std::to_string(i) + " destination " + std::to_string(j) +
-                               " not covered to its end");
+            int64_t at = st.begin;
+            for (auto& iv : c) {
+                if (iv.first != at) return bad("gap or overlap in step " + std::to_string(i));
+                at = iv.second;
             }
-            if (at_i != c.size()) return bad("tile stores to a destination the step lacks");
+            if (st.end > st.begin && at != st.end)
+                return bad("step " + std::to_string(i) + " not covered to its end");
         }
         // sliced launches: the runs are disjoint and in order, every stage
         // names a launch or a slice, every launch of a phase outside the

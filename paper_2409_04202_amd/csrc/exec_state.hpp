@@ -109,14 +109,6 @@ constexpr int64_t kNumXCDs = 8;         // compute dies, each with its own L2
 // this many tiles.
 constexpr int64_t kXcdMaxTiles = 64;
 
-// A launch whose steps store to at least kSplitMinDst destinations and
-// that has fewer than kMinUnits wave tiles gives each tile one wave per
-// slot of its block (dsplit = wavefronts per block): each folds the tile
-// and stores to its share of the destinations, so the stores of one tile
-// are issued by a whole workgroup, whose re-reads of the tile's sources
-// hit its compute unit's caches.  0 disables the split.
-constexpr int32_t kSplitMinDst = 16;
-
 struct LaunchDesc {
     int32_t phase;
     int32_t xphase;          // executed phase
@@ -130,7 +122,6 @@ struct LaunchDesc {
     int32_t wpb;             // wavefronts per block
     int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
     int32_t max_dst;         // most destinations of a step
-    int32_t dsplit;          // wave units per tile (dst_part), 1: one
     int64_t bytes;           // (k + destinations) * len * e over the steps
     int64_t hbm;             // predicted HBM traffic: bytes, less the repeated
                              // reads of a range by the launch's copies

@@ -231,34 +231,6 @@ __host__ __device__ __forceinline__ void unit_tile(int64_t unit, const int2* til
     }
 }
 
-// A launch whose steps store to many destinations may give each wave tile
-// `dsplit` waves: wave unit = tile * dsplit + part folds the tile's sources
-// and stores to part `part` of the destination list, ceil(ndst / dsplit)
-// destinations each (the last parts may get fewer or none).  dsplit = 1:
-// one wave per tile, every destination.  Shared by the kernel and the
-// host-side tiling check.
-struct DstPart {
-    int64_t tile;  // wave tile of the launch
-    int d0, nd;    // destinations [d0, d0 + nd) of the step
-};
-__host__ __device__ __forceinline__ DstPart dst_part(int64_t unit, int dsplit, int ndst) {
-    DstPart r;
-    if (dsplit <= 1) {
-        r.tile = unit;
-        r.d0 = 0;
-        r.nd = ndst;
-        return r;
-    }
-    r.tile = unit / dsplit;
-    const int part = int(unit - r.tile * dsplit);
-    const int per = (ndst + dsplit - 1) / dsplit;
-    const int a = part * per < ndst ? part * per : ndst;
-    const int b = a + per < ndst ? a + per : ndst;
-    r.d0 = a;
-    r.nd = b - a;
-    return r;
-}
-
 __device__ __forceinline__ int64_t uniform64(int64_t x) {
     const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(x)));
     const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(x) >> 32));
@@ -442,15 +414,14 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, 
     store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
 }
 
-// One launch: `nunits` wave units over the steps whose records start at
-// `recs`, `stride` words apart; `dsplit` units per wave tile, each storing
-// to its part of the destinations (see dst_part).  K = 0 means the source
-// count is read from each step (any k >= 1).  VECOK: every buffer is 16-byte
-// aligned.  CM: cache mode of the vector loads and stores.
+// One launch: `nunits` wave tiles over the steps whose records start at
+// `recs`, `stride` words apart.  K = 0 means the source count is read from
+// each step (any k >= 1).  VECOK: every buffer is 16-byte aligned.  CM:
+// cache mode of the vector loads and stores.
 template <int DT, int K, bool VECOK, int CM>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
-    int64_t nunits, int64_t tiles_per_step, int64_t tile_elems, int dsplit) {
+    int64_t nunits, int64_t tiles_per_step, int64_t tile_elems) {
     constexpr int VEC = Elem<DT>::VEC;
     constexpr int U = kcfg(K).U;
     constexpr int WPB = kcfg(K).WPB;
@@ -458,9 +429,8 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const int64_t unit = int64_t(blockIdx.x) * WPB +
                          int64_t(__builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
     if (unit >= nunits) return;
-    const int64_t tile = dsplit > 1 ? unit / dsplit : unit;
     int64_t s, t;
-    unit_tile(tile, tiles, tiles_per_step, s, t);
+    unit_tile(unit, tiles, tiles_per_step, s, t);
     s = uniform64(s);
     t = uniform64(t);
     if (s < 0) return;  // a padding entry of a tile table
@@ -468,10 +438,8 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const StepHead st = *reinterpret_cast<const StepHead*>(rec);
     const int k = K ? K : st.k;
     void* const* sp = reinterpret_cast<void* const*>(rec + kRecHead);
-    const DstPart part = dst_part(unit, dsplit, st.ndst);
-    if (part.nd <= 0) return;
-    void* const* dp = sp + k + part.d0;
-    const int ndst = part.nd;
+    void* const* dp = sp + k;
+    const int ndst = st.ndst;
 
     const TileSpan ts = tile_span(st.begin, st.end, t, tile_elems, VEC, VECOK);
     if (ts.lo >= ts.hi) return;

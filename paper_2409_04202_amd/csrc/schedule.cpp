@@ -194,11 +194,6 @@ static void build_launches(const Plan& p, ExecState& ex) {
                 L.tile_off = -1;
                 L.nunits = L.count * L.tiles_per_step;
             }
-            L.dsplit = 1;
-            if (kSplitMinDst > 0 && maxdst >= kSplitMinDst && L.nunits < kMinUnits) {
-                L.dsplit = L.wpb;
-                L.nunits *= L.dsplit;
-            }
             ex.launches.push_back(L);
             g0 = g1;
         }
