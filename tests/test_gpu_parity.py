@@ -347,6 +347,8 @@ def test_unaligned_buffers(dtype, pad):
         _full_compare("ring", 3, 4099, dtype, None, dist, seed=4, **kw)
         _full_compare("cps", 5, 3001, dtype, None, dist, seed=6, **kw)
         _full_compare("ring", 4, 4096, dtype, None, dist, seed=7, **kw)
+        # 16 destinations per step, each also a source
+        _full_compare("cps", 16, 20011, dtype, None, dist, seed=8, **kw)
 
 
 @pytest.mark.parametrize("n", [3, 5, 16, 32])
@@ -769,3 +771,16 @@ def test_paper_asymmetric_topologies_scaled(name):
     for fuse, sl, res in MODES:
         _full_compare("gentree", c["n"], 384 * 64 + 17, "f32", c["fanin"], seed=3,
                       fuse=fuse, slice_=sl, resident=res)
+
+
+@pytest.mark.parametrize("kind,n,N,fan,dtype", [
+    ("cps", 16, (1 << 14) + 3, None, "f32"), ("cps", 32, 32 * 1000 + 17, None, "bf16"),
+    ("cps", 16, 4096, None, "i32"), ("tree", 512, 1 << 15, (8, 8, 8), "bf16"),
+    ("tree", 64, 4096 + 64 * 5, (8, 8), "f32"), ("ring", 64, 64 * 1000, None, "f32")])
+def test_many_destination_phase_launches(kind, n, N, fan, dtype):
+    # phase launches whose steps store to 16 or more buffers, some of them
+    # the step's own sources (the reduce-then-broadcast rewrite)
+    dist = "int1000" if dtype == "i32" else "uniform"
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=N % 101, slice_=0)
+    if dtype == "bf16":
+        assert _normwise_bf16(got[0], xs0) <= 1e-2
