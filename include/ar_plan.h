@@ -217,6 +217,33 @@ ar_status ar_plan_execute_strided(ar_plan* plan, void* base,
 ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
                                 void* stream, ar_timer* timer);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * ar_plan_execute without any device allocation.  Same arguments, same
+ * launches and the same result bits as ar_plan_execute; no call makes a
+ * device allocation or calls hipMalloc, hipFree or any other allocating HIP
+ * routine.  The plan's device-side tables and the step records of the buffer
+ * set (the staging ar_plan_execute allocates per plan) live instead in one
+ * array of AR_NOALLOC_MAX_BYTES bytes that the library holds on every device
+ * it runs on, from that device's first such call until the process ends.
+ *   - Every call on a device shares that device's array, which keeps the last
+ *     call's contents: the call copies the plan's tables and records into it
+ *     (hipMemcpyAsync from host memory the plan owns, on `stream`) unless the
+ *     last call on the device used the same plan, options and buffer set.
+ *     Calls that may overlap on one device (other streams, other host
+ *     threads without ordering) race on the array and must be ordered by
+ *     the caller.
+ *   - The first call with a plan (and after each option change) builds the
+ *     plan's host-side image of the tables (host memory, freed with the
+ *     plan).
+ *   - AR_ERR_UNSUPPORTED, with the size in ar_last_error(), when the plan's
+ *     tables and records exceed AR_NOALLOC_MAX_BYTES (their size grows with
+ *     the number of steps and, for a resident launch, with N: 40 bytes per
+ *     256-element tile; RHD n = 8 at 2^26 fp32 takes about 10 MiB).
+ *   Errors otherwise as ar_plan_execute. */
+#define AR_NOALLOC_MAX_BYTES (32u << 20)
+ar_status ar_plan_execute_noalloc(ar_plan* plan, void* const* bufs, void* stream);
+
 /* Executor options (ar_plan_set_option).
  *  AR_OPT_FUSE (default 1): let the executor merge steps where that removes
  *  memory traffic without changing any result bit:

@@ -72,6 +72,7 @@ _sig = {
     "ar_plan_destroy": [_P],
     "ar_plan_execute": [_P, POINTER(c_void_p), c_void_p],
     "ar_plan_execute_strided": [_P, c_void_p, c_int64, c_void_p],
+    "ar_plan_execute_noalloc": [_P, POINTER(c_void_p), c_void_p],
     "ar_plan_execute_timed": [_P, POINTER(c_void_p), c_void_p, _P],
     "ar_plan_info": [_P, POINTER(c_int32), POINTER(c_int64), POINTER(c_int32),
                      POINTER(c_int32), POINTER(c_int64)],
@@ -208,6 +209,13 @@ def ar_plan_execute(plan, bufs, stream=None):
     _check(_lib.ar_plan_execute(plan, _ptr_array(bufs), _stream(stream)))
 
 
+def ar_plan_execute_noalloc(plan, bufs, stream=None):
+    _check(_lib.ar_plan_execute_noalloc(plan, _ptr_array(bufs), _stream(stream)))
+
+
+AR_NOALLOC_MAX_BYTES = 32 << 20
+
+
 def ar_plan_execute_strided(plan, base, stride_bytes, stream=None):
     _check(_lib.ar_plan_execute_strided(plan, _ptr(base), int(stride_bytes),
                                         _stream(stream)))
@@ -322,6 +330,9 @@ class Plan:
 
     def execute(self, bufs, stream=None):
         ar_plan_execute(self.handle, self._bufs(bufs), stream)
+
+    def execute_noalloc(self, bufs, stream=None):
+        ar_plan_execute_noalloc(self.handle, self._bufs(bufs), stream)
 
     def execute_strided(self, base, stride_bytes, stream=None):
         ar_plan_execute_strided(self.handle, base, stride_bytes, stream)

@@ -18,6 +18,7 @@
 #include <cstring>
 #include <map>
 #include <memory>
+#include <mutex>
 #include <tuple>
 #include <new>
 #include <string>
@@ -83,6 +84,29 @@ static ar_status upload(T** dst, const std::vector<T>& src, const char* what) {
     return AR_OK;
 }
 
+// The sliced launches' tables of all slices, concatenated (each slice
+// indexes them from its *_base offsets).
+struct SliceTables {
+    std::vector<int64_t> cuts;
+    std::vector<int32_t> soff, sched;
+    std::vector<int2> tiles;
+    std::vector<ResUnit> runits;
+    std::vector<uint32_t> prog;
+};
+
+static SliceTables slice_tables(const ExecState& ex) {
+    SliceTables t;
+    for (const SliceDesc& sd : ex.slices) {
+        t.cuts.insert(t.cuts.end(), sd.cuts.begin(), sd.cuts.end());
+        t.soff.insert(t.soff.end(), sd.sched_off.begin(), sd.sched_off.end());
+        t.sched.insert(t.sched.end(), sd.sched.begin(), sd.sched.end());
+        t.tiles.insert(t.tiles.end(), sd.tiles.begin(), sd.tiles.end());
+        t.runits.insert(t.runits.end(), sd.runits.begin(), sd.runits.end());
+        t.prog.insert(t.prog.end(), sd.prog.begin(), sd.prog.end());
+    }
+    return t;
+}
+
 static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
@@ -94,25 +118,13 @@ static ar_status device_state(Plan& p, ExecState& ex, DevState** out) {
         d->device = dev;
         ar_status s = upload(&d->tiles, ex.htiles, "tile table");
         if (s == AR_OK && !ex.slices.empty()) {
-            std::vector<int64_t> cuts;
-            std::vector<int32_t> soff, sched;
-            std::vector<int2> tiles;
-            std::vector<ResUnit> runits;
-            std::vector<uint32_t> prog;
-            for (const SliceDesc& sd : ex.slices) {
-                cuts.insert(cuts.end(), sd.cuts.begin(), sd.cuts.end());
-                soff.insert(soff.end(), sd.sched_off.begin(), sd.sched_off.end());
-                sched.insert(sched.end(), sd.sched.begin(), sd.sched.end());
-                tiles.insert(tiles.end(), sd.tiles.begin(), sd.tiles.end());
-                runits.insert(runits.end(), sd.runits.begin(), sd.runits.end());
-                prog.insert(prog.end(), sd.prog.begin(), sd.prog.end());
-            }
-            s = upload(&d->cuts, cuts, "segment table");
-            if (s == AR_OK) s = upload(&d->sched_off, soff, "schedule offsets");
-            if (s == AR_OK) s = upload(&d->sched, sched, "schedule");
-            if (s == AR_OK) s = upload(&d->stiles, tiles, "slice tiles");
-            if (s == AR_OK) s = upload(&d->runits, runits, "resident units");
-            if (s == AR_OK) s = upload(&d->prog, prog, "resident programs");
+            const SliceTables t = slice_tables(ex);
+            s = upload(&d->cuts, t.cuts, "segment table");
+            if (s == AR_OK) s = upload(&d->sched_off, t.soff, "schedule offsets");
+            if (s == AR_OK) s = upload(&d->sched, t.sched, "schedule");
+            if (s == AR_OK) s = upload(&d->stiles, t.tiles, "slice tiles");
+            if (s == AR_OK) s = upload(&d->runits, t.runits, "resident units");
+            if (s == AR_OK) s = upload(&d->prog, t.prog, "resident programs");
         }
         if (s != AR_OK) {
             free_dev(d);
@@ -142,6 +154,30 @@ static ar_status check_buffers(const Plan& p, const std::vector<void*>& bufs) {
                         "buffers " + std::to_string(a[i - 1].second) + " and " +
                             std::to_string(a[i].second) + " overlap");
     return AR_OK;
+}
+
+static bool buffers_aligned(void* const* bufs, int32_t n) {
+    for (int32_t i = 0; i < n; ++i)
+        if (reinterpret_cast<uint64_t>(bufs[i]) & 15) return false;
+    return true;
+}
+
+// The step records of buffer set bufs[0..n) (see StepHead) followed by the n
+// buffer pointers, written to w[0 .. rec_words + n).
+static void fill_records(const ExecState& ex, void* const* bufs, int32_t n, uint64_t* w) {
+    std::memset(w, 0, size_t(ex.rec_words + n) * sizeof(uint64_t));
+    for (size_t i = 0; i < ex.hsteps.size(); ++i) {
+        const DevStep& st = ex.hsteps[i];
+        uint64_t* r = w + ex.rec_of[i];
+        StepHead h{st.begin, st.end, st.k, st.ndst, 0};
+        std::memcpy(r, &h, sizeof(h));
+        for (int32_t j = 0; j < st.k; ++j)
+            r[kRecHead + j] = reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.src_off + j)])]);
+        for (int32_t j = 0; j < st.ndst; ++j)
+            r[kRecHead + st.k + j] =
+                reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.dst_off + j)])]);
+    }
+    for (int32_t i = 0; i < n; ++i) w[ex.rec_words + i] = reinterpret_cast<uint64_t>(bufs[i]);
 }
 
 // The step records for buffer set `bufs` on this device (see StepHead),
@@ -190,20 +226,7 @@ static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
         if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipEventSynchronize", e));
     }
     v->valid = false;
-    uint64_t* w = v->pinned;
-    std::memset(w, 0, nb);
-    for (size_t i = 0; i < ex.hsteps.size(); ++i) {
-        const DevStep& st = ex.hsteps[i];
-        uint64_t* r = w + ex.rec_of[i];
-        StepHead h{st.begin, st.end, st.k, st.ndst, 0};
-        std::memcpy(r, &h, sizeof(h));
-        for (int32_t j = 0; j < st.k; ++j)
-            r[kRecHead + j] = reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.src_off + j)])]);
-        for (int32_t j = 0; j < st.ndst; ++j)
-            r[kRecHead + st.k + j] =
-                reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.dst_off + j)])]);
-    }
-    for (size_t i = 0; i < bufs.size(); ++i) w[ex.rec_words + int64_t(i)] = reinterpret_cast<uint64_t>(bufs[i]);
+    fill_records(ex, bufs.data(), p.n, v->pinned);
     e = hipMemcpyAsync(v->dev, v->pinned, nb, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("step record upload", e));
     e = hipEventRecord(v->done, stream);
@@ -211,9 +234,7 @@ static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
     v->key = bufs;
     v->valid = true;
     v->stamp = d.clock;
-    v->aligned = true;
-    for (void* b : bufs)
-        if (reinterpret_cast<uint64_t>(b) & 15) v->aligned = false;
+    v->aligned = buffers_aligned(bufs.data(), p.n);
     *out = v;
     return AR_OK;
 }
@@ -260,21 +281,29 @@ struct ar_timer {
 
 using namespace arp;
 
-static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
-                     hipStream_t stream, ar_timer* timer) {
-    try {
-        if (plan->N == 0 || plan->num_phases() == 0) return AR_OK;
-        ExecState* ex = exec_state(*plan);
-        if (ex->launches.empty()) return AR_OK;
-        DevState* d = nullptr;
-        ar_status s = device_state(*plan, *ex, &d);
-        if (s != AR_OK) return s;
-        PtrEntry* pe = nullptr;
-        s = step_records(*plan, *ex, *d, bufs, stream, &pe);
-        if (s != AR_OK) return s;
+// Where one execution's device-side tables and step records are: the
+// plan's own device state, or the no-allocation entry point's scratch.
+struct DevView {
+    const int2* tiles;
+    const int64_t* cuts;
+    const int32_t* sched_off;
+    const int32_t* sched;
+    const int2* stiles;
+    const ResUnit* runits;
+    const uint32_t* prog;
+    const uint64_t* recs;  // step records, then the n buffer pointers
+    bool aligned;          // every buffer 16-byte aligned
+};
+
+// Enqueue the launches of one execution on `stream`.
+static ar_status launch_all(ar_plan* plan, const ExecState* ex, const DevView& v,
+                            hipStream_t stream, ar_timer* timer) {
+    const DevView* d = &v;
+    ar_status s = AR_OK;
+    {
         // sliced launches need 16-byte aligned buffers; otherwise every
         // phase runs as its phase launches
-        const bool staged = pe->aligned;
+        const bool staged = v.aligned;
         const int64_t nlaunch = staged ? int64_t(ex->stages.size()) : int64_t(ex->launches.size());
         if (timer && timer->count + nlaunch > timer->cap)
             return fail(AR_ERR_INVALID_ARG, "timer is full");
@@ -305,7 +334,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                 const bool nt = sd.res_bytes > 2 * kKeepBytes;
 #define AR_STREAM_K(DT, W, NT)                                                                \
     hipLaunchKernelGGL((stream_kernel<DT, W, NT>), grid, block, lds, stream,                    \
-                       pe->dev + ex->rec_words, plan->n, sd.slots,                              \
+                       v.recs + ex->rec_words, plan->n, sd.slots,                              \
                        d->runits + sd.runit_base, d->prog + sd.prog_base, sd.nunits)
 #define AR_STREAM(DT)                                                                         \
     if (nt) AR_STREAM_K(DT, 4, true);                                                         \
@@ -323,7 +352,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                 const size_t lds = size_t(plan->n) * 1024;
 #define AR_RESIDENT(DT, W, NT)                                                                \
     hipLaunchKernelGGL((resident_kernel<DT, W, NT>), grid, block, lds, stream,                \
-                       pe->dev + ex->rec_words, plan->n, d->runits + sd.runit_base,           \
+                       v.recs + ex->rec_words, plan->n, d->runits + sd.runit_base,           \
                        d->prog + sd.prog_base, sd.nunits)
                 // runs moving more than the last-level cache holds stream
                 // their rows past it
@@ -346,7 +375,7 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
                 const dim3 grid(static_cast<uint32_t>((sd.nunits + kSliceWPB - 1) / kSliceWPB));
                 const dim3 block(64 * kSliceWPB);
 #define AR_SLICED(DT)                                                                   \
-    hipLaunchKernelGGL((sliced_kernel<DT>), grid, block, 0, stream, pe->dev,             \
+    hipLaunchKernelGGL((sliced_kernel<DT>), grid, block, 0, stream, v.recs,             \
                        d->sched_off + sd.soff_base, d->sched + sd.sched_base,           \
                        d->cuts + sd.cuts_base, d->stiles + sd.tiles_base, sd.nunits,    \
                        sd.nphases, sd.nseg, sd.tile_elems)
@@ -359,21 +388,21 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             } else {
                 const LaunchDesc& L = ex->launches[size_t(stg.launch)];
                 const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
-                const uint64_t* recs = pe->dev + L.rec_off;
+                const uint64_t* recs = v.recs + L.rec_off;
                 const int2* tiles = L.tile_off >= 0 ? d->tiles + L.tile_off : nullptr;
                 switch (plan->dtype) {
                     case AR_F32:
-                        launch_d<DT_F32>(L.kern_k, pe->aligned, L.cm, blocks, stream, recs,
+                        launch_d<DT_F32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
                                          L.tile_elems);
                         break;
                     case AR_I32:
-                        launch_d<DT_I32>(L.kern_k, pe->aligned, L.cm, blocks, stream, recs,
+                        launch_d<DT_I32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
                                          L.tile_elems);
                         break;
                     default:
-                        launch_d<DT_BF16>(L.kern_k, pe->aligned, L.cm, blocks, stream, recs,
+                        launch_d<DT_BF16>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                           L.rec_stride, tiles, L.nunits, L.tiles_per_step,
                                           L.tile_elems);
                         break;
@@ -385,7 +414,145 @@ static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
             if (s != AR_OK) return s;
             if (timer) timer->launch[size_t(timer->count++)] = int32_t(li);
         }
-        return AR_OK;
+    }
+    return AR_OK;
+}
+
+static ar_status run(ar_plan* plan, const std::vector<void*>& bufs,
+                     hipStream_t stream, ar_timer* timer) {
+    try {
+        if (plan->N == 0 || plan->num_phases() == 0) return AR_OK;
+        ExecState* ex = exec_state(*plan);
+        if (ex->launches.empty()) return AR_OK;
+        DevState* d = nullptr;
+        ar_status s = device_state(*plan, *ex, &d);
+        if (s != AR_OK) return s;
+        PtrEntry* pe = nullptr;
+        s = step_records(*plan, *ex, *d, bufs, stream, &pe);
+        if (s != AR_OK) return s;
+        const DevView v{d->tiles, d->cuts, d->sched_off, d->sched, d->stiles,
+                        d->runits, d->prog, pe->dev, pe->aligned};
+        return launch_all(plan, ex, v, stream, timer);
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}
+
+// ------------------------------------------- execution without allocation
+//
+// ar_plan_execute_noalloc keeps an execution's device-side tables and step
+// records in `scratch`, a fixed array of this library on every device (no
+// device allocation at any call).  Host code never uses the array's name
+// as an address: on a device's first call the device address comes from
+// hipGetSymbolAddress with that device current, and is kept per device.
+// Calls on one device share the array; the host remembers which executor
+// state and buffer set the last call on each device wrote into it and
+// copies the tables and records again only when they differ.
+
+static __device__ __align__(256) uint8_t scratch[AR_NOALLOC_MAX_BYTES];
+
+namespace {
+
+struct ScratchDev {
+    uint8_t* ptr = nullptr;       // device address of `scratch` on this device
+    uint64_t serial = 0;          // executor state whose tables it holds
+    std::vector<void*> bufs;      // buffer set whose records it holds
+};
+std::mutex g_scratch_mu;
+std::vector<ScratchDev> g_scratch;  // by device ordinal
+
+constexpr int64_t kImgAlign = 256;
+
+int64_t img_align(int64_t b) { return (b + kImgAlign - 1) / kImgAlign * kImgAlign; }
+
+}  // namespace
+
+// Lay out the tables of `ex` and room for the records of one buffer set in
+// ex->img; returns the image's size in bytes.
+static int64_t build_image(const Plan& p, ExecState& ex) {
+    const SliceTables t = slice_tables(ex);
+    const int64_t sizes[8] = {
+        int64_t(ex.htiles.size() * sizeof(int2)), int64_t(t.cuts.size() * sizeof(int64_t)),
+        int64_t(t.soff.size() * sizeof(int32_t)), int64_t(t.sched.size() * sizeof(int32_t)),
+        int64_t(t.tiles.size() * sizeof(int2)),   int64_t(t.runits.size() * sizeof(ResUnit)),
+        int64_t(t.prog.size() * sizeof(uint32_t)),
+        (ex.rec_words + p.n) * int64_t(sizeof(uint64_t))};
+    int64_t at = 0;
+    for (int i = 0; i < 8; ++i) {
+        ex.img_off[i] = at;
+        at = img_align(at + sizes[i]);
+    }
+    if (at > int64_t(AR_NOALLOC_MAX_BYTES)) return at;
+    ex.img.assign(size_t(at / 8), 0);
+    char* b = reinterpret_cast<char*>(ex.img.data());
+    const void* src[7] = {ex.htiles.data(), t.cuts.data(), t.soff.data(), t.sched.data(),
+                          t.tiles.data(), t.runits.data(), t.prog.data()};
+    for (int i = 0; i < 7; ++i)
+        if (sizes[i]) std::memcpy(b + ex.img_off[i], src[i], size_t(sizes[i]));
+    return at;
+}
+
+AR_EXPORT ar_status ar_plan_execute_noalloc(ar_plan* plan, void* const* bufs, void* stream) {
+    clear_error();
+    if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+    if (!bufs) return fail(AR_ERR_INVALID_ARG, "bufs is NULL");
+    try {
+        if (plan->N == 0 || plan->num_phases() == 0) return AR_OK;
+        ExecState* ex = exec_state(*plan);
+        if (ex->launches.empty()) return AR_OK;
+        const std::vector<void*> set(bufs, bufs + plan->n);
+        ar_status s = check_buffers(*plan, set);
+        if (s != AR_OK) return s;
+        if (ex->img.empty()) {
+            const int64_t need = build_image(*plan, *ex);
+            if (ex->img.empty())
+                return fail(AR_ERR_UNSUPPORTED,
+                            "the plan's tables and step records take " + std::to_string(need) +
+                                " bytes; ar_plan_execute_noalloc holds at most " +
+                                std::to_string(int64_t(AR_NOALLOC_MAX_BYTES)));
+        }
+        int dev = -1;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("hipGetDevice", e));
+        if (dev < 0) return fail(AR_ERR_HIP, "no current device");
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        uint8_t* base = nullptr;
+        {
+            std::lock_guard<std::mutex> lock(g_scratch_mu);
+            if (size_t(dev) >= g_scratch.size()) g_scratch.resize(size_t(dev) + 1);
+            ScratchDev& sd = g_scratch[size_t(dev)];
+            if (!sd.ptr) {
+                void* ptr = nullptr;
+                e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+                if (e != hipSuccess || !ptr)
+                    return fail(AR_ERR_HIP, hip_msg("hipGetSymbolAddress(scratch)", e));
+                sd.ptr = static_cast<uint8_t*>(ptr);
+            }
+            base = sd.ptr;
+            const bool tables = sd.serial != ex->serial;
+            if (tables || sd.bufs != set) {
+                const int64_t rec = ex->img_off[7];
+                const int64_t end = int64_t(ex->img.size()) * 8;
+                fill_records(*ex, bufs, plan->n,
+                             ex->img.data() + rec / int64_t(sizeof(uint64_t)));
+                const int64_t from = tables ? 0 : rec;
+                sd.serial = 0;  // unknown until the copy is enqueued
+                e = hipMemcpyAsync(base + from, reinterpret_cast<const char*>(ex->img.data()) + from,
+                                   size_t(end - from), hipMemcpyHostToDevice, st);
+                if (e != hipSuccess) return fail(AR_ERR_HIP, hip_msg("scratch upload", e));
+                sd.serial = ex->serial;
+                sd.bufs = set;
+            }
+        }
+        auto at = [&](int i) { return base + ex->img_off[i]; };
+        const DevView v{reinterpret_cast<const int2*>(at(0)), reinterpret_cast<const int64_t*>(at(1)),
+                        reinterpret_cast<const int32_t*>(at(2)), reinterpret_cast<const int32_t*>(at(3)),
+                        reinterpret_cast<const int2*>(at(4)), reinterpret_cast<const ResUnit*>(at(5)),
+                        reinterpret_cast<const uint32_t*>(at(6)), reinterpret_cast<const uint64_t*>(at(7)),
+                        buffers_aligned(bufs, plan->n)};
+        return launch_all(plan, ex, v, st, nullptr);
     } catch (const std::bad_alloc&) {
         return fail(AR_ERR_OOM, "host allocation failed");
     } catch (const std::exception& e) {

@@ -223,6 +223,12 @@ struct ExecState {
     std::vector<SliceDesc> slices;
     std::vector<Stage> stages;   // the launches for 16-byte aligned buffers
     std::vector<DevState*> dev;  // indexed by device ordinal
+    uint64_t serial = 0;         // unique per executor state ever built
+    // ar_plan_execute_noalloc: the tables and step records laid out as in
+    // the scratch array (built on its first call with this state)
+    std::vector<uint64_t> img;
+    int64_t img_off[8] = {};     // byte offsets: tiles, cuts, sched_off,
+                                 // sched, stiles, runits, prog, records
 };
 
 // Every (buffer, range) a phase touches, with the step touching it; answers

@@ -3,6 +3,7 @@
 // (their tables; the resident programs are built in programs.cpp), chosen by
 // a cost model.  Host only.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <limits>
 #include <map>
@@ -431,9 +432,12 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
     return runs;
 }
 
+static std::atomic<uint64_t> g_exec_serial{0};
+
 ExecState* exec_state(Plan& p) {
     if (!p.exec) {
         ExecState* ex = new ExecState();
+        ex->serial = ++g_exec_serial;
         try {
             ex->phases = exec_phases(p, p.fuse != 0);
             build_launches(p, *ex);
