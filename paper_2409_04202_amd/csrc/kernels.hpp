@@ -58,7 +58,10 @@ constexpr int kRecHead = 4;  // header words
 //   TE  largest wave tile, in 16-byte vectors per source.
 // Chosen by measurement on MI355X: a 2-input fold and a copy stream best
 // with 16 KiB per source per wave and 8-wave blocks; wide folds want fewer
-// vectors per source in flight and smaller tiles.
+// vectors per source in flight and smaller tiles.  The 16-source fold runs
+// best with one 1 KiB vector slot per source and tile (6.06 TB/s on 1 GiB,
+// against 5.86 with 4 KiB tiles; 2 slots per lane, 512-vector tiles or
+// 8-wave blocks were slower still).
 struct KCfg {
     int U, WPB, TE;
 };
@@ -67,7 +70,7 @@ __host__ __device__ constexpr KCfg kcfg(int K) {
          : K == 2 ? KCfg{8, 8, 1024}
          : K <= 4 && K > 0 ? KCfg{4, 4, 512}
          : K == 8 ? KCfg{2, 4, 256}
-         : K == 16 ? KCfg{1, 4, 256}
+         : K == 16 ? KCfg{1, 4, 64}
          : KCfg{4, 4, 256};
 }
 

@@ -156,7 +156,8 @@ static void build_launches(const Plan& p, ExecState& ex) {
             auto units_for = [&](int64_t t) {
                 return L.count * ((maxspan + t - 1) / t);
             };
-            while (te > tmin && units_for(te) < kMinUnits) te /= 2;
+            const int64_t min_units = k >= 2 ? kMinUnitsReduce : kMinUnits;
+            while (te > tmin && units_for(te) < min_units) te /= 2;
             while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
             L.wpb = cfg.WPB;
             std::sort(ranges.begin(), ranges.end());
