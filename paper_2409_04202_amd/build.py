@@ -88,5 +88,60 @@ def build(verbose=False, jobs=None):
     return LIB
 
 
+# The sanitized test build (``build_sanitized``): the test library with its
+# host code under AddressSanitizer and UndefinedBehaviorSanitizer (device
+# code is compiled as usual and left uninstrumented); any undefined
+# behaviour aborts.  Loaded only by ``tests/sanitized_host_suite.py``, with
+# the sanitizer runtime of the ROCm compiler preloaded.
+SAN_LIB = os.path.join(LIBDIR, "libarplan_check_san.so")
+SAN = ["-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=undefined"]
+SAN_COMMON = ["-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "-fPIC",
+              "-fvisibility=hidden"]
+
+
+def sanitizer_runtime():
+    """The ROCm compiler's shared AddressSanitizer runtime (UBSan included)."""
+    clang = os.path.join(ROCM, "llvm", "bin", "clang++")
+    r = subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"],
+                       stdout=subprocess.PIPE, text=True, check=True)
+    path = r.stdout.strip()
+    if not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError("sanitizer runtime not found (%s)" % path)
+    return path
+
+
+def build_sanitized(verbose=False, jobs=None):
+    hipcc = os.environ.get("HIPCC", os.path.join(ROCM, "bin", "hipcc"))
+    clang = os.path.join(ROCM, "llvm", "bin", "clang++")
+    os.makedirs(LIBDIR, exist_ok=True)
+    tmp = tempfile.mkdtemp(prefix="arplan_san_")
+    host_san = [x for f in SAN for x in ("-Xarch_host", f)]
+    try:
+        cmds, objs = [], []
+        for s in HOST_SRCS:
+            o = os.path.join(tmp, s + ".o")
+            cmds.append([clang, "-c", os.path.join(CSRC, s), "-o", o] + SAN_COMMON + SAN)
+            objs.append(o)
+        for s in HIP_SRCS + CHECK_SRCS:
+            o = os.path.join(tmp, s + ".o")
+            cmds.append([hipcc, "-c", "-x", "hip", os.path.join(CSRC, s), "-o", o]
+                        + SAN_COMMON + HIP_FLAGS + host_san)
+            objs.append(o)
+        jobs = jobs or min(8, os.cpu_count() or 1)
+        with ThreadPoolExecutor(max_workers=jobs) as pool:
+            for f in [pool.submit(_run, c, verbose) for c in cmds]:
+                f.result()
+        tmp_lib = os.path.join(tmp, os.path.basename(SAN_LIB))
+        _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp_lib]
+             + host_san + ["-Xarch_host", "-shared-libasan"] + objs, verbose)
+        shutil.move(tmp_lib, SAN_LIB)
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitized" in sys.argv:
+        print(build_sanitized(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))
