@@ -76,58 +76,57 @@ def symmetric_tree(fanin):
 
 
 def basic_placement(root, n_total=None, complete=False):
-    """Run the bottom-up placement.
+    """Block placement of GenTree's basic sub-plans (Algorithm 1), switch by
+    switch from the bottom of the tree up.
 
     Returns ``{id(node): {server_id: [blocks...]}}`` for every node; for a
     server the map is ``{server_id: [0, ..., n_total - 1]}``.
 
-    On some asymmetric trees the rule leaves a block that no server below a
-    switch takes (every server holding it reached its quota first).  With
-    ``complete``, such a block goes to the server holding it in the first
-    child, in block order (a completion added here; where the rule places
-    every block, nothing changes).
+    The rule at a switch: list the servers below it in child order (those of
+    its first child first, each child's in that child's own order).  With s
+    of them, the j-th (from 0) may hold floor(n / s) blocks, plus one when
+    j < n mod s.  Each server's candidates are the blocks it held below the
+    child it belongs to (a server child: every block), in that order; the
+    servers claim in list order, each the first still-unclaimed candidates
+    up to its quota.
+
+    On some asymmetric trees this leaves a block that no server claims (all
+    its holders reached their quotas first).  With ``complete``, every such
+    block, in block order, is added to the server that holds it in the
+    first child holding it (a completion added here; where every block is
+    claimed, nothing changes).
     """
     if n_total is None:
         n_total = number_servers(root)
     place = {}
-
-    def visit(node):
+    def init(node):
         if node.is_server:
             place[id(node)] = {node.server_id: list(range(n_total))}
-            return
         for c in node.children:
-            visit(c)
-        servers = len(servers_below(node))
-        quota, extra = divmod(n_total, servers)
-        taken = [False] * n_total
-        mine = {}
-        for c in node.children:
-            for sid, blocks in place[id(c)].items():
-                want = quota + (1 if extra > 0 else 0)
-                if extra > 0:
-                    extra -= 1
-                got = []
-                for b in blocks:
-                    if want == 0:
-                        break
-                    if not taken[b]:
-                        taken[b] = True
-                        got.append(b)
-                        want -= 1
-                mine[sid] = got
-        if complete:
-            for b in range(n_total):
-                if taken[b]:
-                    continue
-                for c in node.children:
-                    owner = [sid for sid, bl in place[id(c)].items() if b in bl]
-                    if owner:
-                        mine[owner[0]].append(b)
-                        taken[b] = True
-                        break
-        place[id(node)] = mine
+            init(c)
+    init(root)
 
-    visit(root)
+    for level in switch_levels(root):        # children are placed first
+        for sw in level:
+            members = [(sid, cands) for c in sw.children
+                       for sid, cands in place[id(c)].items()]
+            s = len(members)
+            quotas = [n_total // s + (1 if j < n_total % s else 0) for j in range(s)]
+            claimed = set()
+            mine = {}
+            for (sid, cands), q in zip(members, quotas):
+                pick = [b for b in cands if b not in claimed][:q]
+                mine[sid] = pick
+                claimed.update(pick)
+            if complete:
+                for b in range(n_total):
+                    if b in claimed:
+                        continue
+                    holder = next(sid for c in sw.children
+                                  for sid, cands in place[id(c)].items() if b in cands)
+                    mine[holder].append(b)
+                    claimed.add(b)
+            place[id(sw)] = mine
     return place
 
 

@@ -331,12 +331,13 @@ struct TNode {
 
 }  // namespace
 
-// Bottom-up block placement of Algorithm 1 (floor share per server, one
-// more for the first `remain` servers in child order; each server takes the
-// first blocks of its own list that no earlier server below the switch took),
-// completed where the rule leaves a block: the block goes to its holder in
-// the first child.  Each switch reduces every block over one holder per
-// child; switches of one height share a phase; the AllGather reverses it.
+// GenTree's basic plan on a tree given by preorder child counts.  Block
+// placement (Algorithm 1), bottom-up: at a switch the servers below it, in
+// child order, get quotas of floor(n / s) blocks, one more for the first
+// n mod s, and claim in that order the first unclaimed blocks of what they
+// held below their child; a block left unclaimed goes to its holder in the
+// first child.  Each switch reduces every block over one holder per child;
+// switches of one height share a phase; the AllGather reverses it.
 void expand_gentree(Plan& p, const std::vector<int32_t>& nchild) {
     const int32_t n = p.n;
     const int64_t N = p.N;
@@ -382,21 +383,10 @@ void expand_gentree(Plan& p, const std::vector<int32_t>& nchild) {
     }
     std::vector<std::vector<Step>> rs(static_cast<size_t>(H)), ag(static_cast<size_t>(H));
     std::vector<std::vector<int32_t>> rs_srcs(static_cast<size_t>(H)), ag_srcs(static_cast<size_t>(H));
-    auto servers_below = [&](int32_t v) {
-        int64_t c = 0;
-        std::vector<int32_t> st{v};
-        while (!st.empty()) {
-            const int32_t x = st.back();
-            st.pop_back();
-            if (t[size_t(x)].server >= 0) ++c;
-            for (int32_t k : t[size_t(x)].kids) st.push_back(k);
-        }
-        return c;
-    };
-    // next_free[b]: smallest untaken block >= b (path-halving union-find),
-    // so that a server child (whose list is every block) takes its share in
+    // next_free[b]: smallest unclaimed block >= b (path-halving union-find),
+    // so that a member whose candidates are every block claims its share in
     // amortised constant time per block
-    std::vector<int32_t> taken(static_cast<size_t>(n)), next_free(static_cast<size_t>(n) + 1);
+    std::vector<int32_t> claimed(static_cast<size_t>(n)), next_free(static_cast<size_t>(n) + 1);
     auto find_free = [&](int32_t b) {
         while (next_free[size_t(b)] != b) {
             next_free[size_t(b)] = next_free[size_t(next_free[size_t(b)])];
@@ -404,24 +394,40 @@ void expand_gentree(Plan& p, const std::vector<int32_t>& nchild) {
         }
         return b;
     };
-    auto take = [&](int32_t b) {
-        taken[size_t(b)] = 1;
+    auto claim = [&](int32_t b) {
+        claimed[size_t(b)] = 1;
         next_free[size_t(b)] = b + 1;
     };
+    std::vector<int32_t> slot_of(static_cast<size_t>(n), -1);  // server -> index in place
     for (int32_t v : order) {
         TNode& a = t[size_t(v)];
         if (a.server >= 0) {
             a.place.push_back({a.server, {}});  // implicit: every block
             continue;
         }
-        const int64_t s = servers_below(v);
-        const int64_t quota = n / s;
-        int64_t remain = n % s;
-        std::fill(taken.begin(), taken.end(), 0);
-        for (int32_t b = 0; b <= n; ++b) next_free[size_t(b)] = b;
-        // holder of block b after child i's ReduceScatter: a server child
-        // holds every block; a switch child's placement gives the server
+        // The members of this switch: the servers below it in child order,
+        // each with its candidate blocks (what it held below its child; a
+        // server child: every block, in order), and their quotas, fixed up
+        // front: floor(n / s) each, one more for the first n mod s.
+        struct Member {
+            int32_t sid;
+            const std::vector<int32_t>* cands;  // nullptr: every block
+        };
         const size_t nk = a.kids.size();
+        std::vector<Member> members;
+        for (size_t i = 0; i < nk; ++i) {
+            const TNode& c = t[size_t(a.kids[i])];
+            if (c.server >= 0) {
+                members.push_back({c.server, nullptr});
+            } else {
+                for (const auto& pr : c.place) members.push_back({pr.first, &pr.second});
+            }
+        }
+        const int64_t s = int64_t(members.size());
+        std::vector<int64_t> quota(members.size(), n / s);
+        for (int64_t j = 0; j < n % s; ++j) ++quota[size_t(j)];
+        // holder of block b below child i: a server child holds every
+        // block; a switch child's placement names the server
         std::vector<int32_t> const_holder(nk, -1);
         std::vector<std::vector<int32_t>> holders(nk);
         for (size_t i = 0; i < nk; ++i) {
@@ -437,45 +443,37 @@ void expand_gentree(Plan& p, const std::vector<int32_t>& nchild) {
         auto holder = [&](size_t i, int32_t b) {
             return const_holder[i] >= 0 ? const_holder[i] : holders[i][size_t(b)];
         };
-        for (size_t i = 0; i < nk; ++i) {
-            const TNode& c = t[size_t(a.kids[i])];
-            for (const auto& pr : c.place) {
-                int64_t want = quota + (remain > 0 ? 1 : 0);
-                if (remain > 0) --remain;
-                std::vector<int32_t> got;
-                if (c.server >= 0) {  // its list is every block, in order
-                    for (int32_t b = find_free(0); want > 0 && b < n; b = find_free(b)) {
-                        take(b);
-                        got.push_back(b);
-                        --want;
-                    }
-                } else {
-                    for (int32_t b : pr.second) {
-                        if (want == 0) break;
-                        if (!taken[size_t(b)]) {
-                            take(b);
-                            got.push_back(b);
-                            --want;
-                        }
-                    }
+        // one claiming pass over the members in order
+        std::fill(claimed.begin(), claimed.end(), 0);
+        for (int32_t b = 0; b <= n; ++b) next_free[size_t(b)] = b;
+        a.place.reserve(members.size());
+        for (size_t j = 0; j < members.size(); ++j) {
+            std::vector<int32_t> got;
+            const size_t q = size_t(quota[j]);
+            if (!members[j].cands) {
+                for (int32_t b = find_free(0); got.size() < q && b < n; b = find_free(b)) {
+                    claim(b);
+                    got.push_back(b);
                 }
-                a.place.push_back({pr.first, std::move(got)});
-            }
-        }
-        for (int32_t b = 0; b < n; ++b) {  // completion
-            if (taken[size_t(b)]) continue;
-            for (size_t i = 0; i < nk; ++i) {
-                const int32_t h = holder(i, b);
-                if (h < 0) continue;
-                for (auto& pr : a.place)
-                    if (pr.first == h) {
-                        pr.second.push_back(b);
-                        break;
+            } else {
+                for (auto it = members[j].cands->begin();
+                     got.size() < q && it != members[j].cands->end(); ++it)
+                    if (!claimed[size_t(*it)]) {
+                        claim(*it);
+                        got.push_back(*it);
                     }
-                take(b);
-                break;
             }
-            if (!taken[size_t(b)]) throw std::logic_error("block without holder");
+            slot_of[size_t(members[j].sid)] = int32_t(a.place.size());
+            a.place.push_back({members[j].sid, std::move(got)});
+        }
+        // completion: an unclaimed block, in block order, joins the list of
+        // its holder in the first child that holds it
+        for (int32_t b = find_free(0); b < n; b = find_free(b)) {
+            int32_t h = -1;
+            for (size_t i = 0; i < nk && h < 0; ++i) h = holder(i, b);
+            if (h < 0 || slot_of[size_t(h)] < 0) throw std::logic_error("block without holder");
+            a.place[size_t(slot_of[size_t(h)])].second.push_back(b);
+            claim(b);
         }
         // steps: runs of consecutive blocks of one server with equal holders
         const size_t lvl = size_t(a.height - 1);
