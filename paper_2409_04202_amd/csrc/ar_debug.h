@@ -43,8 +43,9 @@ ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* info,
  * kernel's template source count (0: read at run time), out[1] = cache mode
  * (bit 0: nontemporal loads, bit 1: nontemporal stores), out[2] = wave tile
  * in elements, out[3] = wave tiles, out[4] = wavefronts per block, out[5] =
- * 1 when the tiles come from a table.  AR_ERR_INVALID_ARG for a sliced
- * launch.  Host only. */
+ * 1 when the tiles come from a table, out[6] = sources whose loads the
+ * runtime-source-count kernel keeps in flight together.  AR_ERR_INVALID_ARG
+ * for a sliced launch.  Host only. */
 ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* out);
 #ifdef __cplusplus
 }

@@ -207,6 +207,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
             if (blocks > kMaxBlocks) return bad("grid too large");
             if (L.wpb != kcfg(L.kern_k).WPB) return bad("block size differs from the kernel's");
+            if (L.rt_group < 1 || L.rt_group > kRtGroup) return bad("source group out of range");
             if (L.tile_elems % (64 * VEC) != 0) return bad("tile not a multiple of a wave vector");
             const int2* tiles = L.tile_off >= 0 ? ex->htiles.data() + L.tile_off : nullptr;
             if (tiles && L.tile_off + L.nunits > int64_t(ex->htiles.size()))
@@ -666,6 +667,7 @@ AR_EXPORT ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* 
         out[3] = L.nunits;
         out[4] = L.wpb;
         out[5] = L.tile_off >= 0 ? 1 : 0;
+        out[6] = L.rt_group;
         return AR_OK;
     } catch (const std::exception& e) {
         return fail(AR_ERR_INTERNAL, e.what());

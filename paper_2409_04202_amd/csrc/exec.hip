@@ -242,11 +242,11 @@ static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
 template <int DT, int K>
 static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
                       const uint64_t* recs, int64_t stride, const int2* tiles,
-                      int64_t nunits, int64_t tps, int64_t te) {
+                      int64_t nunits, int64_t tps, int64_t te, int rtg) {
     const dim3 grid(static_cast<uint32_t>(blocks)), block(64 * kcfg(K).WPB);
 #define AR_LAUNCH(V, C)                                                                \
     hipLaunchKernelGGL((phase_kernel<DT, K, V, C>), grid, block, 0, st, recs, stride, \
-                       tiles, nunits, tps, te)
+                       tiles, nunits, tps, te, rtg)
     if (!vecok) AR_LAUNCH(false, 0);
     else if (cm == 0) AR_LAUNCH(true, 0);
     else if (cm == 1) AR_LAUNCH(true, 1);
@@ -258,15 +258,15 @@ static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
 template <int DT>
 static void launch_d(int K, bool vecok, int cm, int64_t blocks, hipStream_t st,
                      const uint64_t* recs, int64_t stride, const int2* tiles,
-                     int64_t nunits, int64_t tps, int64_t te) {
+                     int64_t nunits, int64_t tps, int64_t te, int rtg) {
     switch (K) {
-        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
-        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
-        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
-        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
-        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
-        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
-        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te); break;
+        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
     }
 }
 
@@ -394,17 +394,17 @@ static ar_status launch_all(ar_plan* plan, const ExecState* ex, const DevView& v
                     case AR_F32:
                         launch_d<DT_F32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                         L.tile_elems);
+                                         L.tile_elems, L.rt_group);
                         break;
                     case AR_I32:
                         launch_d<DT_I32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                         L.tile_elems);
+                                         L.tile_elems, L.rt_group);
                         break;
                     default:
                         launch_d<DT_BF16>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                           L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                          L.tile_elems);
+                                          L.tile_elems, L.rt_group);
                         break;
                 }
             }

@@ -377,11 +377,18 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, const D& dst
     store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
 }
 
-// Runtime source count: one source at a time, U vectors in flight.
+// Runtime source count: the sources in groups of `group` (1..kRtGroup),
+// every load of a group in flight at once (U vectors per lane and source),
+// then added in source order, so the fold is the same left fold as the
+// unrolled kernels'.  Short launches want the loads of several sources in
+// flight; long ones stream best one source at a time (more loads per wave
+// cost occupancy where there is work enough to hide the latency).
+constexpr int kRtGroup = 4;
+
 template <int DT, int U, int CM, bool FULL, class D>
 __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, int k,
                                                 const D& dst, int64_t v0, int64_t at,
-                                                int64_t nv, int lane) {
+                                                int64_t nv, int lane, int group) {
     bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
@@ -393,23 +400,27 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, 
             if (ok[u]) out[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
     } else {
         VAcc<DT> acc[U];
-        {
-            const gvec* s0 = as_global<u32x4>(srcp[0]) + v0;
-            u32x4 x[U];
+        for (int j0 = 0; j0 < k; j0 += group) {
+            u32x4 x[kRtGroup][U];
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (ok[u]) x[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
+            for (int g = 0; g < kRtGroup; ++g) {
+                if (g < group && j0 + g < k) {  // wave-uniform
+                    const gvec* sj = as_global<u32x4>(srcp[j0 + g]) + v0;
 #pragma unroll
-            for (int u = 0; u < U; ++u) acc[u].init(x[u]);
-        }
-        for (int j = 1; j < k; ++j) {
-            const gvec* sj = as_global<u32x4>(srcp[j]) + v0;
-            u32x4 x[U];
+                    for (int u = 0; u < U; ++u)
+                        if (ok[u]) x[g][u] = vload<(CM & 1) != 0>(sj + at + u * 64 + lane);
+                }
+            }
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (ok[u]) x[u] = vload<(CM & 1) != 0>(sj + at + u * 64 + lane);
+            for (int g = 0; g < kRtGroup; ++g) {
+                if (g < group && j0 + g < k) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) acc[u].add(x[u]);
+                    for (int u = 0; u < U; ++u) {
+                        if (j0 + g == 0) acc[u].init(x[g][u]);
+                        else acc[u].add(x[g][u]);
+                    }
+                }
+            }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) out[u] = acc[u].out();
@@ -419,12 +430,12 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, 
 
 // One launch: `nunits` wave tiles over the steps whose records start at
 // `recs`, `stride` words apart.  K = 0 means the source count is read from
-// each step (any k >= 1).  VECOK: every buffer is 16-byte aligned.  CM:
-// cache mode of the vector loads and stores.
+// each step (any k >= 1), folded `rt_group` sources at a time.  VECOK: every
+// buffer is 16-byte aligned.  CM: cache mode of the vector loads and stores.
 template <int DT, int K, bool VECOK, int CM>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
-    int64_t nunits, int64_t tiles_per_step, int64_t tile_elems) {
+    int64_t nunits, int64_t tiles_per_step, int64_t tile_elems, int rt_group) {
     constexpr int VEC = Elem<DT>::VEC;
     constexpr int U = kcfg(K).U;
     constexpr int WPB = kcfg(K).WPB;
@@ -463,9 +474,9 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
         if (at < nv) fold_vectors<DT, K, U, CM, false>(sv, dst, v0, at, nv, lane);
     } else {
         for (; at + 64 * U <= nv; at += 64 * U)
-            fold_vectors_rt<DT, U, CM, true>(sp, k, dst, v0, at, nv, lane);
+            fold_vectors_rt<DT, U, CM, true>(sp, k, dst, v0, at, nv, lane, rt_group);
         if (at < nv)
-            fold_vectors_rt<DT, U, CM, false>(sp, k, dst, v0, at, nv, lane);
+            fold_vectors_rt<DT, U, CM, false>(sp, k, dst, v0, at, nv, lane, rt_group);
     }
 }
 
@@ -536,9 +547,11 @@ __global__ __launch_bounds__(64 * kSliceWPB) void sliced_kernel(
                 default: {
                     const DstMem dst{dp, st.ndst};
                     if (nv == 64 * kSliceU)
-                        fold_vectors_rt<DT, kSliceU, 0, true>(sp, st.k, dst, v0, 0, nv, lane);
+                        fold_vectors_rt<DT, kSliceU, 0, true>(sp, st.k, dst, v0, 0, nv, lane,
+                                                              kRtGroup);
                     else
-                        fold_vectors_rt<DT, kSliceU, 0, false>(sp, st.k, dst, v0, 0, nv, lane);
+                        fold_vectors_rt<DT, kSliceU, 0, false>(sp, st.k, dst, v0, 0, nv, lane,
+                                                               kRtGroup);
                 }
             }
         }

@@ -138,6 +138,7 @@ static void build_launches(const Plan& p, ExecState& ex) {
             }
             L.bytes = bytes;
             L.max_dst = maxdst;
+            L.rt_group = L.kern_k == 0 && bytes < kRtGroupMaxBytes ? kRtGroup : 1;
             L.rec_stride = (kRecHead + k + maxdst + 1) & ~int64_t(1);
             L.rec_off = ex.rec_words;
             ex.rec_of.resize(ex.hsteps.size(), -1);

@@ -539,10 +539,10 @@ def _launch_desc(handle, stage):
     f = arplan._lib.ar_debug_launch_desc
     f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)]
     f.restype = ctypes.c_int32
-    out = (ctypes.c_int64 * 6)()
+    out = (ctypes.c_int64 * 7)()
     assert f(handle, stage, out) == arplan.AR_OK, arplan.ar_last_error()
     return {"k": out[0], "cm": out[1], "tile": out[2], "tiles": out[3], "wpb": out[4],
-            "table": out[5]}
+            "table": out[5], "group": out[6]}
 
 
 def test_full_size_forms_use_the_nontemporal_kernels():
@@ -576,3 +576,18 @@ def test_full_size_forms_use_the_nontemporal_kernels():
         p.set_option(arplan.AR_OPT_SLICE, 0)
         d = _launch_desc(p.handle, 0)
         assert d["k"] == 8 and d["cm"] & 1
+
+
+def test_runtime_source_count_groups():
+    # fan-ins without an unrolled kernel: short launches keep four sources'
+    # loads in flight, launches of 512 MiB or more one source at a time;
+    # unrolled kernels report 1
+    for n, N, group in ((24, 1 << 16, 4), (32, (1 << 22) + 17, 1), (12, 1 << 20, 4)):
+        with arplan.Plan(n, N, "f32", "cps") as p:
+            p.set_option(arplan.AR_OPT_FUSE, 0)
+            p.set_option(arplan.AR_OPT_SLICE, 0)
+            d = _launch_desc(p.handle, 0)
+            assert (d["k"], d["group"]) == (0, group), (n, N, d)
+    with arplan.Plan(16, 1 << 20, "f32", "cps") as p:
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        assert _launch_desc(p.handle, 0)["group"] == 1

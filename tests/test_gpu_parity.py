@@ -361,6 +361,12 @@ def test_source_counts(n):
             _full_compare("cps", n, 512 * n, dtype, None, "uniform", seed=n, **kw)
 
 
+def test_runtime_source_count_long_launch():
+    # a 32-source fold of more than 512 MiB: the runtime-source-count kernel
+    # one source at a time (shorter launches group four sources)
+    got, xs0 = _full_compare("cps", 32, (1 << 22) + 17, "f32", seed=3, fuse=0, slice_=0)
+
+
 def test_fp32_denormals_are_kept():
     n, N = 4, 8192
     rng = np.random.default_rng(7)
