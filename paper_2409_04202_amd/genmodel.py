@@ -15,9 +15,27 @@ per-round cost (a kernel launch and its drain), delta and beta are seconds
 per byte.  Plans are timed as written: one launch per phase, no executor
 rewrites (AR_OPT_FUSE = 0, AR_OPT_SLICE = 0).
 
-``python -m paper_2409_04202_amd.genmodel`` measures, fits, predicts Ring,
-RHD and hierarchical-tree plans, reports the errors and the plan the model
-picks per (n, N), and prints one JSON document.
+An extended single-GPU form adds what the paper's cluster terms leave out
+on one GPU:
+
+    T = A * alpha + K * lam + Dh * delta_h + Dc * delta_c
+                            + Bh * beta_h  + Bc * beta_c
+
+K sums, over the phases, the largest source count of a step of the phase
+(a k-way step's first store waits for k dependent loads per element: a
+per-phase latency that grows with k), and the byte terms are split by
+where each access is served: an access is "cached" (Dc, Bc) when the
+plan's whole footprint n * N * e fits the last-level cache, when it reads a
+range read earlier in the same phase, or when it reads a range the previous
+phase wrote and that phase wrote at most the cache's capacity; otherwise
+it goes to HBM (Dh, Bh).  Fitted by non-negative least squares in relative
+error.
+
+``python -m paper_2409_04202_amd.genmodel`` measures, fits both forms (from
+co-located PS runs as the paper does, and the extended form also from
+co-located PS plus two-level tree runs), predicts Ring, RHD and
+hierarchical-tree plans, reports the errors and the plan each model picks
+per (n, N), and prints one JSON document.
 """
 
 import argparse
@@ -44,19 +62,65 @@ def features(plan):
     return A, D, B
 
 
+LLC_BYTES = 256 << 20   # MI355X last-level (Infinity) cache
+
+
+def ext_features(plan, cache_bytes=LLC_BYTES):
+    """(A, K, Dh, Dc, Bh, Bc) of a plan for the extended form (see the
+    module docstring), from the library's own step list."""
+    e = plan.esize
+    footprint = plan.n * plan.N * e
+    phases = plan.phases()
+    K = Dh = Dc = Bh = Bc = 0
+    prev_written, prev_bytes = set(), 0
+    for ph in phases:
+        if not ph:
+            continue
+        K += max(len(srcs) for _, _, srcs, _, _ in ph)
+        red = any(op == "reduce" for op, _, _, _, _ in ph)
+        seen, written, wbytes, h, c = set(), set(), 0, 0, 0
+        for op, dst, srcs, b, end in ph:
+            L = (end - b) * e
+            for q in srcs:
+                key = (q, b, end)
+                if footprint <= cache_bytes or key in seen or \
+                        (key in prev_written and prev_bytes <= cache_bytes):
+                    c += L
+                else:
+                    h += L
+                seen.add(key)
+            if footprint <= cache_bytes:
+                c += L
+            else:
+                h += L
+            written.add((dst, b, end))
+            wbytes += L
+        if red:
+            Dh, Dc = Dh + h, Dc + c
+        else:
+            Bh, Bc = Bh + h, Bc + c
+        prev_written, prev_bytes = written, wbytes
+    return len(phases), K, Dh, Dc, Bh, Bc
+
+
 def predict(params, feats):
-    alpha, delta, beta = params
-    A, D, B = feats
-    return A * alpha + D * delta + B * beta
+    """Predicted seconds: the dot product of parameters and features (either
+    form)."""
+    return float(sum(p * f for p, f in zip(params, feats)))
 
 
-def fit(samples):
+def fit(samples, nonneg=False):
     """Least squares on (features, seconds) samples, relative error
-    weighting (each equation divided by its measured time)."""
-    X = np.array([[A, D, B] for (A, D, B), _ in samples], dtype=np.float64)
+    weighting (each equation divided by its measured time); `nonneg`
+    constrains every parameter to be >= 0."""
+    X = np.array([list(f) for f, _ in samples], dtype=np.float64)
     y = np.array([t for _, t in samples], dtype=np.float64)
     w = 1.0 / y
-    sol, *_ = np.linalg.lstsq(X * w[:, None], y * w, rcond=None)
+    if nonneg:
+        from scipy.optimize import nnls
+        sol, _ = nnls(X * w[:, None], y * w)
+    else:
+        sol, *_ = np.linalg.lstsq(X * w[:, None], y * w, rcond=None)
     return tuple(float(v) for v in sol)
 
 
@@ -84,12 +148,14 @@ def candidates(n):
     return cands
 
 
-def select(params, n, N, dtype="f32"):
-    """The plan with the smallest predicted time."""
+def select(params, n, N, dtype="f32", feature_fn=None):
+    """The plan with the smallest predicted time (`feature_fn`: features or
+    ext_features, matching `params`)."""
+    feature_fn = feature_fn or features
     best = None
     for kind, fan in candidates(n):
         with arplan.Plan(n, N, dtype, kind, fan) as p:
-            t = predict(params, features(p))
+            t = predict(params, feature_fn(p))
         if best is None or t < best[0]:
             best = (t, kind, fan)
     return best
@@ -121,7 +187,7 @@ class Timer:
                 p.execute(ptrs, s)
             e1.record(s)
             e1.synchronize()
-            feats = features(p)
+            feats = (features(p), ext_features(p))
         del bufs
         return feats, e0.elapsed_time(e1) * 1e-3 / self.reps
 
@@ -149,7 +215,6 @@ def main():
         train.append(((n, N, "cps", None), feats, t))
         print("genmodel: cps n=%d S=%d MiB %.4f ms" % (n, S // MiB, t * 1e3),
               file=sys.stderr, flush=True)
-    params = fit([(f, t) for _, f, t in train])
     tests = []
     test_ns = [4, 8, 16, 32] if not args.quick else [8]
     for n, S in itertools.product(test_ns, sizes):
@@ -160,38 +225,50 @@ def main():
             tests.append(((n, N, kind, fan), feats, t))
             print("genmodel: %s %s n=%d S=%d MiB %.4f ms" % (kind, fan, n, S // MiB, t * 1e3),
                   file=sys.stderr, flush=True)
-    rows = []
-    for (n, N, kind, fan), feats, t in train + tests:
-        pr = predict(params, feats)
-        rows.append({"n": n, "N": N, "plan": kind, "fanin": list(fan) if fan else None,
-                     "A": feats[0], "D": feats[1], "B": feats[2],
-                     "measured_ms": t * 1e3, "predicted_ms": pr * 1e3,
-                     "error": (pr - t) / t, "fit": kind == "cps"})
-    # selection: the model's pick per (n, N) against the measured best
-    sel = []
+    runs = train + tests
+    # the paper's form and the extended form from co-located PS runs; the
+    # extended form also from co-located PS and two-level tree runs
+    two_level = [r for r in tests if r[0][2] == "tree" and len(r[0][3]) == 2]
+    models = {
+        "paper_cps": (0, False, train),
+        "extended_cps": (1, True, train),
+        "extended_cps_tree2": (1, True, train + two_level),
+    }
+    out = {"runs": [{"n": n, "N": N, "plan": kind, "fanin": list(fan) if fan else None,
+                     "features": list(f[0]), "ext_features": list(f[1]),
+                     "measured_ms": t * 1e3}
+                    for (n, N, kind, fan), f, t in runs],
+           "models": {}}
     meas = {}
-    for (n, N, kind, fan), feats, t in train + tests:
-        meas.setdefault((n, N), []).append((t, kind, fan))
-    for (n, N), lst in sorted(meas.items()):
-        if n not in test_ns:
-            continue
-        best_t, best_kind, best_fan = min(lst, key=lambda x: x[0])
-        pick = min(lst, key=lambda x: predict(params, timer_features(n, N, x[1], x[2])))
-        sel.append({"n": n, "N": N, "measured_best": [best_kind, best_fan],
-                    "model_pick": [pick[1], pick[2]],
-                    "pick_ms": pick[0] * 1e3, "best_ms": best_t * 1e3,
-                    "loss": pick[0] / best_t - 1})
-    test_err = [abs(r["error"]) for r in rows if not r["fit"]]
-    fit_err = [abs(r["error"]) for r in rows if r["fit"]]
-    out = {"params": {"alpha_us": params[0] * 1e6,
-                      "delta_ns_per_byte": params[1] * 1e9,
-                      "beta_ns_per_byte": params[2] * 1e9,
-                      "delta_GBps": 1e-9 / params[1] if params[1] > 0 else None,
-                      "beta_GBps": 1e-9 / params[2] if params[2] > 0 else None},
-           "fit_max_error": max(fit_err), "fit_mean_error": float(np.mean(fit_err)),
-           "test_max_error": max(test_err) if test_err else None,
-           "test_mean_error": float(np.mean(test_err)) if test_err else None,
-           "rows": rows, "selection": sel, "seconds": time.time() - t0}
+    for (n, N, kind, fan), f, t in runs:
+        meas.setdefault((n, N), []).append((t, kind, fan, f))
+    for name, (fi, nonneg, tr) in models.items():
+        params = fit([(f[fi], t) for _, f, t in tr], nonneg=nonneg)
+        in_train = {id(r) for r in tr}
+        errs = [((predict(params, r[1][fi]) - r[2]) / r[2], id(r) in in_train) for r in runs]
+        fit_err = [abs(e) for e, it in errs if it]
+        test_err = [abs(e) for e, it in errs if not it]
+        sel = []
+        for (n, N), lst in sorted(meas.items()):
+            if n not in test_ns:
+                continue
+            best = min(lst, key=lambda x: x[0])
+            pick = min(lst, key=lambda x: predict(params, x[3][fi]))
+            sel.append({"n": n, "N": N, "measured_best": [best[1], best[2]],
+                        "model_pick": [pick[1], pick[2]], "pick_ms": pick[0] * 1e3,
+                        "best_ms": best[0] * 1e3, "loss": pick[0] / best[0] - 1})
+        out["models"][name] = {
+            "params": list(params),
+            "param_names": (["alpha_s", "delta_s_per_B", "beta_s_per_B"] if fi == 0 else
+                            ["alpha_s", "lambda_s_per_source", "delta_hbm_s_per_B",
+                             "delta_cached_s_per_B", "beta_hbm_s_per_B", "beta_cached_s_per_B"]),
+            "train_runs": len(tr),
+            "fit_max_error": max(fit_err), "fit_mean_error": float(np.mean(fit_err)),
+            "test_max_error": max(test_err) if test_err else None,
+            "test_mean_error": float(np.mean(test_err)) if test_err else None,
+            "errors": [e for e, _ in errs],
+            "selection": sel}
+    out["seconds"] = time.time() - t0
     print(json.dumps(out))
 
 

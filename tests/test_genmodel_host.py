@@ -99,3 +99,52 @@ def test_select_is_argmin_of_prediction(params, n, N):
             with arplan.Plan(n, N, "f32", k, f) as p:
                 _, d2, b2 = genmodel.features(p)
             assert d + b <= d2 + b2
+
+
+@pytest.mark.parametrize("kind,n,fan", [("ring", 8, None), ("rhd", 8, None), ("cps", 16, None),
+                                        ("tree", 64, (8, 8)), ("tree", 24, (2, 3, 4))])
+@pytest.mark.parametrize("N", [1 << 12, 1 << 22, 1 << 24])
+def test_extended_features_split_the_paper_terms(kind, n, fan, N):
+    # the extended form's byte terms add up to the paper form's, and K is
+    # the sum over phases of the widest step's source count
+    with arplan.Plan(n, N, "f32", kind, fan) as p:
+        A, D, B = genmodel.features(p)
+        A2, K, Dh, Dc, Bh, Bc = genmodel.ext_features(p)
+        phases = p.phases()
+    assert A2 == A and Dh + Dc == D and Bh + Bc == B
+    assert K == sum(max(len(s) for _, _, s, _, _ in ph) for ph in phases)
+    if n * N * 4 <= genmodel.LLC_BYTES:
+        assert Dh == 0 and Bh == 0          # everything stays in the cache
+
+
+def test_extended_features_cache_rule():
+    # co-located PS at 1 GiB: the fold reads 16 inputs from HBM and writes
+    # to HBM; the broadcast reads what the fold just wrote (64 MiB, and each
+    # range 15 times) from the cache and writes 960 MiB to HBM
+    with arplan.Plan(16, 1 << 24, "f32", "cps") as p:
+        A, K, Dh, Dc, Bh, Bc = genmodel.ext_features(p)
+    S = (1 << 24) * 4
+    assert (A, K) == (2, 17)
+    assert (Dh, Dc) == (17 * S, 0)
+    assert Bc == 15 * S and Bh == 15 * S
+    # RHD at 2 GiB: the halvings write 1 GiB, 512 MiB and 256 MiB, so the
+    # second and third read from HBM; the first doubling reads the 256 MiB
+    # the last halving wrote from the cache
+    with arplan.Plan(8, 1 << 26, "f32", "rhd") as p:
+        _, K, Dh, Dc, Bh, Bc = genmodel.ext_features(p)
+    assert K == 3 * 2 + 3 * 1
+    assert Dc == 0 and Bc == 256 << 20
+
+
+def test_nonnegative_fit_recovers_extended_parameters():
+    true = (4e-6, 3e-7, 1.6e-13, 0.7e-13, 1.3e-13, 0.6e-13)
+    plans = [("cps", n, None, N) for n in (2, 3, 4, 8, 16, 24)
+             for N in (1 << 10, 1 << 18, 1 << 22, 1 << 24)] + \
+            [("tree", 16, (4, 4), N) for N in (1 << 18, 1 << 24)]
+    s = []
+    for kind, n, fan, N in plans:
+        with arplan.Plan(n, N, "f32", kind, fan) as p:
+            f = genmodel.ext_features(p)
+        s.append((f, genmodel.predict(true, f)))
+    got = genmodel.fit(s, nonneg=True)
+    assert np.allclose(got, true, rtol=1e-6, atol=0)
