@@ -34,7 +34,9 @@ Prints one JSON line.  The headline (RHD, n = 8, N = 2^26 fp32):
   cpu_baseline  the CPU oracle executing the same plan on the host
   configs     every workload (each config of the scope, the GenTree
               topologies and the n = 64 sweep) in both forms, each with a
-              bounded CPU oracle baseline
+              bounded CPU oracle baseline; a form whose K executions take
+              less than 5 ms is timed over enough executions for about 5 ms
+              (`timed_steps`)
 and, beside those: the step time's median and minimum over individually
 timed executions, a practical ceiling measured in the same run (a device
 copy with torch and with the library, a two-source fold through the
@@ -203,11 +205,13 @@ def _gbs(nbytes, ms):
     return nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
 
 
-def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream):
+def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream, min_ms=0.0):
     """One form of one workload: W warm-up executions, then K back-to-back
     executions timed with the host clock between two device
-    synchronisations, then K executions with HIP events around every launch
-    (after a restore) for the per-launch durations."""
+    synchronisations (with `min_ms`, a plan whose K executions take less is
+    timed again over enough executions for about min_ms), then K executions
+    with HIP events around every launch (after a restore) for the per-launch
+    durations."""
     plan = arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"])
     try:
         if "fuse" in opts:
@@ -230,6 +234,17 @@ def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream):
             plan.execute(ptrs, sh)
         torch.cuda.synchronize()
         ms_step = (time.perf_counter() - t0) * 1e3 / K
+        reps = K
+        if min_ms and ms_step * K < min_ms:
+            # a short plan: time enough executions for about min_ms of work
+            reps = min(4000, int(min_ms / max(ms_step, 1e-4)) + 1)
+            restore()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                plan.execute(ptrs, sh)
+            torch.cuda.synchronize()
+            ms_step = (time.perf_counter() - t0) * 1e3 / reps
         restore()
         l_ms = launch_ms(torch, arplan, plan, ptrs, sh, K, len(launches))
     finally:
@@ -244,6 +259,7 @@ def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream):
     cpy_bytes = sum(launches[i][4] for i in cpy)
     return {
         "ms_per_step": round(ms_step, 5),
+        "timed_steps": reps,
         "algbw_gbs": round(_gbs(total, ms_step), 2),
         "plan_gbs": round(_gbs(red_b + cpy_b, ms_step), 1),
         "kernel_ms_per_step": round(sum(l_ms), 5),
@@ -335,7 +351,8 @@ def ceiling(torch, arplan):
     return out
 
 
-def bench_workload(torch, arplan, name, K, W, forms, stream, cpu_s, headline=False):
+def bench_workload(torch, arplan, name, K, W, forms, stream, cpu_s, headline=False,
+                   min_ms=0.0):
     """Both forms of one workload (and, for the headline, the per-step time
     distribution), plus the oracle on the host."""
     import numpy as np
@@ -358,7 +375,8 @@ def bench_workload(torch, arplan, name, K, W, forms, stream, cpu_s, headline=Fal
                      else "%d-node tree" % len(c["fanin"])) if c["fanin"] else None}
     for form in forms:
         print("bench: %s %s form, %d steps" % (name, form, K), file=sys.stderr, flush=True)
-        res[form] = time_form(torch, arplan, c, bufs, restore, K, W, FORMS[form], stream)
+        res[form] = time_form(torch, arplan, c, bufs, restore, K, W, FORMS[form], stream,
+                              min_ms)
     if headline and "default" in forms:
         res["step_ms"] = step_distribution(torch, arplan, c, bufs, restore, K, stream)
     del bufs, pristine
@@ -444,7 +462,7 @@ def config_entry(r):
     for form in FORMS:
         if form in r:
             f = r[form]
-            e[form] = {k: f[k] for k in ("ms_per_step", "algbw_gbs", "plan_gbs",
+            e[form] = {k: f[k] for k in ("ms_per_step", "timed_steps", "algbw_gbs", "plan_gbs",
                                          "reduce_launches", "reduce_gbs", "reduce_frac",
                                          "copy_gbs", "kernels")}
             L = f["launches"]
@@ -498,7 +516,7 @@ def main():
             if name == args.config:
                 continue
             r = bench_workload(torch, arplan, name, K, W, forms, stream,
-                               1.5 if cpu else 0.0)
+                               1.5 if cpu else 0.0, min_ms=5.0)
             out["configs"].append(config_entry(r))
     if not args.no_ceiling:
         print("bench: practical ceiling", file=sys.stderr, flush=True)
