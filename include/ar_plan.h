@@ -335,6 +335,47 @@ ar_status ar_plan_owner(const ar_plan* plan, int32_t p, int64_t* begin,
 ar_status ar_plan_bytes(const ar_plan* plan, int64_t* reduce_bytes,
                         int64_t* copy_bytes);
 
+/* ------------------------------------------------------------- GenModel */
+
+/* GenModel (Section 3) with the terms one GPU has, for predicting a plan's
+ * time and choosing a plan (Section 3.4 fits the model from co-located PS
+ * runs; Algorithm 2 picks the plan of smallest predicted time).  The
+ * predicted time of a plan is the dot product of AR_GENMODEL_TERMS
+ * parameters with its terms:
+ *   terms[0] A   rounds: the plan's phases (the alpha term of Tables 1-2);
+ *   terms[1] K   the sum over phases of the largest source count of a step
+ *                of the phase (a k-way step waits for k dependent loads per
+ *                element: a per-phase latency growing with k);
+ *   terms[2] Dh, terms[3] Dc   the reduce steps' memory traffic, (k + 1) *
+ *                len * e per k-way step (the delta term, Section 3.1), split
+ *                by where each access is served;
+ *   terms[4] Bh, terms[5] Bc   the copy steps' traffic, 2 * len * e each,
+ *                split the same way.
+ * An access is counted as served from the last-level cache of cache_bytes
+ * (the "c" terms) when the plan's whole footprint n * N * e fits it, when it
+ * reads a range an earlier step of the same phase read, or when it reads a
+ * range the previous phase wrote and that phase wrote at most cache_bytes;
+ * otherwise from HBM (the "h" terms).  Host only, no GPU call.  Errors:
+ * AR_ERR_INVALID_ARG (NULL argument, cache_bytes < 0). */
+#define AR_GENMODEL_TERMS 6
+ar_status ar_genmodel_terms(const ar_plan* plan, int64_t cache_bytes, double* terms);
+
+/* The plan of smallest predicted time (params . terms, with the terms of
+ * ar_genmodel_terms for cache_bytes) for n processors of N elements of
+ * dtype, among: Ring, co-located PS, RHD, and AR_TREE for every ordered
+ * factorisation of n into 2..max_levels fan-ins >= 2 (innermost first; the
+ * factorisations in increasing order of their first fan-in, depth first).
+ * Ties go to the earlier candidate.  Candidates too large to expand are
+ * skipped.  Out: *kind (ar_kind), *num_levels and fanin[0..*num_levels)
+ * (fanin has room for max_levels entries; 0 levels for the non-tree
+ * kinds), *seconds the predicted time.  Host only.  Errors:
+ * AR_ERR_INVALID_ARG (NULL argument, n < 1, N < 0, cache_bytes < 0,
+ * max_levels outside [2, 32], unknown dtype), AR_ERR_UNSUPPORTED (no
+ * candidate could be expanded), AR_ERR_OOM. */
+ar_status ar_genmodel_select(int32_t n, int64_t N, int32_t dtype, const double* params,
+                             int64_t cache_bytes, int32_t max_levels, int32_t* kind,
+                             int32_t* num_levels, int32_t* fanin, double* seconds);
+
 /* --------------------------------------------------------------- timing */
 
 /* A timer holds up to `capacity` launch records (capacity >= 1).  Its HIP

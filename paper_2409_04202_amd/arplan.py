@@ -15,7 +15,7 @@ objects with a ``cuda_stream`` attribute.
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_int64, c_void_p
 
 # One HIP runtime per process: buffers and streams come from torch, so the
 # library must bind to the HIP runtime torch loads.  Both runtimes carry the
@@ -85,6 +85,10 @@ _sig = {
     "ar_plan_num_launches": [_P, POINTER(c_int32)],
     "ar_plan_launch_info": [_P, c_int32, POINTER(c_int32), POINTER(c_int32),
                             POINTER(c_int32), POINTER(c_int64), POINTER(c_int64)],
+    "ar_genmodel_terms": [_P, c_int64, POINTER(c_double)],
+    "ar_genmodel_select": [c_int32, c_int64, c_int32, POINTER(c_double), c_int64, c_int32,
+                           POINTER(c_int32), POINTER(c_int32), POINTER(c_int32),
+                           POINTER(c_double)],
     "ar_timer_create": [c_int64, POINTER(_P)],
     "ar_timer_reset": [_P],
     "ar_timer_read": [_P, c_int64, POINTER(c_int64), POINTER(c_int32),
@@ -281,6 +285,33 @@ def ar_plan_launch_info(plan, i):
                                     ctypes.byref(k), ctypes.byref(d),
                                     ctypes.byref(n), ctypes.byref(b)))
     return ph.value, k.value, d.value, n.value, b.value
+
+
+# -------------------------------------------------------------- GenModel
+
+AR_GENMODEL_TERMS = 6
+
+
+def ar_genmodel_terms(plan, cache_bytes):
+    """(A, K, Dh, Dc, Bh, Bc) of a plan, as numbers."""
+    t = (c_double * AR_GENMODEL_TERMS)()
+    _check(_lib.ar_genmodel_terms(plan, int(cache_bytes), t))
+    return tuple(t)
+
+
+def ar_genmodel_select(n, N, dtype, params, cache_bytes, max_levels=3):
+    """(kind name, fan-in tuple or None, predicted seconds)."""
+    if len(params) != AR_GENMODEL_TERMS:
+        raise ValueError("%d parameters expected" % AR_GENMODEL_TERMS)
+    pa = (c_double * AR_GENMODEL_TERMS)(*[float(x) for x in params])
+    kind, lv = c_int32(), c_int32()
+    fan = (c_int32 * max(1, int(max_levels)))()
+    sec = c_double()
+    _check(_lib.ar_genmodel_select(int(n), int(N), _dtype(dtype), pa, int(cache_bytes),
+                                   int(max_levels), ctypes.byref(kind), ctypes.byref(lv),
+                                   fan, ctypes.byref(sec)))
+    name = {v: k for k, v in KINDS.items()}[kind.value]
+    return name, (tuple(fan[i] for i in range(lv.value)) if lv.value else None), sec.value
 
 
 # ---------------------------------------------------------------- timing

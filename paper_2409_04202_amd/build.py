@@ -31,7 +31,7 @@ LIB = os.path.join(LIBDIR, "libarplan.so")
 CHECK_LIB = os.path.join(LIBDIR, "libarplan_check.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
-HOST_SRCS = ["plan.cpp", "capi.cpp"]
+HOST_SRCS = ["plan.cpp", "capi.cpp", "genmodel.cpp"]
 HIP_SRCS = ["exec.hip", "rewrite.cpp", "schedule.cpp", "programs.cpp"]
 CHECK_SRCS = ["debug.cpp"]          # compiled as HIP, linked into the check library only
 

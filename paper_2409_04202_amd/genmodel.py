@@ -67,40 +67,8 @@ LLC_BYTES = 256 << 20   # MI355X last-level (Infinity) cache
 
 def ext_features(plan, cache_bytes=LLC_BYTES):
     """(A, K, Dh, Dc, Bh, Bc) of a plan for the extended form (see the
-    module docstring), from the library's own step list."""
-    e = plan.esize
-    footprint = plan.n * plan.N * e
-    phases = plan.phases()
-    K = Dh = Dc = Bh = Bc = 0
-    prev_written, prev_bytes = set(), 0
-    for ph in phases:
-        if not ph:
-            continue
-        K += max(len(srcs) for _, _, srcs, _, _ in ph)
-        red = any(op == "reduce" for op, _, _, _, _ in ph)
-        seen, written, wbytes, h, c = set(), set(), 0, 0, 0
-        for op, dst, srcs, b, end in ph:
-            L = (end - b) * e
-            for q in srcs:
-                key = (q, b, end)
-                if footprint <= cache_bytes or key in seen or \
-                        (key in prev_written and prev_bytes <= cache_bytes):
-                    c += L
-                else:
-                    h += L
-                seen.add(key)
-            if footprint <= cache_bytes:
-                c += L
-            else:
-                h += L
-            written.add((dst, b, end))
-            wbytes += L
-        if red:
-            Dh, Dc = Dh + h, Dc + c
-        else:
-            Bh, Bc = Bh + h, Bc + c
-        prev_written, prev_bytes = written, wbytes
-    return len(phases), K, Dh, Dc, Bh, Bc
+    module docstring), computed by the library (ar_genmodel_terms)."""
+    return tuple(int(x) for x in arplan.ar_genmodel_terms(plan.handle, cache_bytes))
 
 
 def predict(params, feats):
@@ -150,8 +118,12 @@ def candidates(n):
 
 def select(params, n, N, dtype="f32", feature_fn=None):
     """The plan with the smallest predicted time (`feature_fn`: features or
-    ext_features, matching `params`)."""
+    ext_features, matching `params`).  The extended form's choice is made by
+    the library (ar_genmodel_select) over the same candidates."""
     feature_fn = feature_fn or features
+    if feature_fn is ext_features:
+        kind, fan, t = arplan.ar_genmodel_select(n, N, dtype, params, LLC_BYTES, 3)
+        return t, kind, fan
     best = None
     for kind, fan in candidates(n):
         with arplan.Plan(n, N, dtype, kind, fan) as p:

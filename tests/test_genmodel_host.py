@@ -148,3 +148,65 @@ def test_nonnegative_fit_recovers_extended_parameters():
         s.append((f, genmodel.predict(true, f)))
     got = genmodel.fit(s, nonneg=True)
     assert np.allclose(got, true, rtol=1e-6, atol=0)
+
+
+def _reference_terms(plan, cache_bytes=genmodel.LLC_BYTES):
+    """The extended form's terms computed here from the step list, to check
+    the library's: per phase, the widest step's source count, and each read
+    and write counted as served from the cache (whole footprint fits, or a
+    range read earlier in the phase, or written by a previous phase that
+    wrote at most cache_bytes) or from HBM."""
+    e = plan.esize
+    fits = plan.n * plan.N * e <= cache_bytes
+    K = Dh = Dc = Bh = Bc = 0
+    prev_written, prev_bytes = set(), 0
+    phases = plan.phases()
+    for ph in phases:
+        K += max(len(srcs) for _, _, srcs, _, _ in ph)
+        seen, written, wbytes, h, c = set(), set(), 0, 0, 0
+        for op, dst, srcs, b, end in ph:
+            L = (end - b) * e
+            for q in srcs:
+                if fits or (q, b, end) in seen or \
+                        ((q, b, end) in prev_written and prev_bytes <= cache_bytes):
+                    c += L
+                else:
+                    h += L
+                seen.add((q, b, end))
+            if fits:
+                c += L
+            else:
+                h += L
+            written.add((dst, b, end))
+            wbytes += L
+        if any(op == "reduce" for op, *_ in ph):
+            Dh, Dc = Dh + h, Dc + c
+        else:
+            Bh, Bc = Bh + h, Bc + c
+        prev_written, prev_bytes = written, wbytes
+    return len(phases), K, Dh, Dc, Bh, Bc
+
+
+@pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("rhd", 6, None), ("rb", 4, None),
+                                        ("cps", 9, None), ("tree", 24, (2, 3, 4))])
+@pytest.mark.parametrize("N,cache", [(1000, 0), (1 << 20, 1 << 22), (1 << 22, 256 << 20)])
+def test_library_terms_match_reference(kind, n, fan, N, cache):
+    with arplan.Plan(n, N, "f32", kind, fan) as p:
+        got = arplan.ar_genmodel_terms(p.handle, cache)
+        assert tuple(int(x) for x in got) == _reference_terms(p, cache)
+
+
+def test_library_select_is_argmin():
+    params = (3.85e-6, 2.92e-7, 2.44e-13, 1.79e-13, 0.0, 7.68e-14)
+    for n, N in ((8, 1 << 12), (12, 1 << 20), (32, 1 << 22), (7, 1000), (1, 10)):
+        t, kind, fan = genmodel.select(params, n, N, feature_fn=genmodel.ext_features)
+        preds = []
+        for k, f in genmodel.candidates(n):
+            with arplan.Plan(n, N, "f32", k, f) as p:
+                preds.append((genmodel.predict(params, genmodel.ext_features(p)), k, f))
+        best = min(preds, key=lambda x: x[0])     # first of equal minima
+        assert (t, kind, fan) == best, (n, N)
+    with pytest.raises(arplan.ArError):
+        arplan.ar_genmodel_select(0, 10, "f32", params, 0)
+    with pytest.raises(arplan.ArError):
+        arplan.ar_genmodel_select(8, 10, "f32", params, 0, max_levels=1)
