@@ -28,8 +28,10 @@ except ImportError:
 
 # The test suite loads this file a second time under another module name,
 # bound to the test build of the library (the same code plus its checking
-# hooks), by placing _LIB_PATH in the module's namespace before running it.
-LIB_PATH = globals().get("_LIB_PATH") or os.path.join(
+# hooks), by placing _LIB_PATH in the module's namespace before running it;
+# ARPLAN_LIB names another build of the same library (the sanitized
+# host-test build) to load instead.
+LIB_PATH = globals().get("_LIB_PATH") or os.environ.get("ARPLAN_LIB") or os.path.join(
     os.path.dirname(os.path.abspath(__file__)), "lib", "libarplan.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(
