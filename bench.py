@@ -58,7 +58,6 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 # kernel of a launch by its phase field in ar_plan_launch_info
 KERNEL_OF = {-1: "sliced_kernel", -2: "resident_kernel", -3: "stream_kernel"}
-DTYPE_NAME = {"f32": "f32", "i32": "i32", "bf16": "bf16"}
 HEADLINE = "rhd_n8_f32"
 FORMS = {"default": {}, "as_written": {"fuse": 0, "slice": 0}}
 

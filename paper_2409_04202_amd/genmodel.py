@@ -244,10 +244,5 @@ def main():
     print(json.dumps(out))
 
 
-def timer_features(n, N, kind, fan, dtype="f32"):
-    with arplan.Plan(n, N, dtype, kind, fan) as p:
-        return features(p)
-
-
 if __name__ == "__main__":
     main()
