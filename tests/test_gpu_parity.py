@@ -790,3 +790,34 @@ def test_many_destination_phase_launches(kind, n, N, fan, dtype):
     got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=N % 101, slice_=0)
     if dtype == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
+
+
+@pytest.mark.parametrize("N,forms", [
+    ((1 << 30) + 4099, [(1, 2, 1), (0, 0, 1)]),     # unaligned steps: phase launches
+    ((1 << 30) + 8192, [(1, 1, 1), (0, 0, 1)])])    # aligned: one resident launch
+def test_buffers_larger_than_4_GiB(N, forms):
+    # every byte offset past 2^32: 64-bit addressing in the phase kernel (with
+    # element-wise heads and tails) and the resident kernel, every element
+    # compared with the oracle
+    n = 2
+    say("case: rhd n=2 N=%d (4 GiB + per buffer)" % N)
+    xs0 = workloads.draw(n, N, "f32", "uniform", 77)
+    ref = oracle.execute(oracle.rhd(n, N), [x.copy() for x in xs0], "f32")
+    del xs0[1:]
+    for fuse, slice_, resident in forms:
+        with arplan.Plan(n, N, "f32", "rhd") as p:
+            p.set_option(arplan.AR_OPT_FUSE, fuse)
+            p.set_option(arplan.AR_OPT_SLICE, slice_)
+            kinds = [x[0] for x in p.launches()]
+            if slice_ == 1:
+                assert kinds == [-2]
+            ts = [torch.from_numpy(x).to("cuda") for x in
+                  workloads.draw(n, N, "f32", "uniform", 77)]
+            say("  fuse=%d slice=%d launches %s" % (fuse, slice_, kinds))
+            run_plan(p, ts)
+        for q in range(n):
+            g = ts[q].cpu().numpy()
+            assert np.array_equal(g, ref[q]), (N, fuse, slice_, q)
+            del g
+        del ts
+        torch.cuda.empty_cache()
