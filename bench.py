@@ -282,6 +282,13 @@ def step_distribution(torch, arplan, c, bufs, restore, K, stream):
     """The default form's step time, each execution between two events."""
     plan = arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"])
     try:
+        opts = FORMS["default"]
+        if "fuse" in opts:
+            plan.set_option(arplan.AR_OPT_FUSE, opts["fuse"])
+        if "slice" in opts:
+            plan.set_option(arplan.AR_OPT_SLICE, opts["slice"])
+        if "resident" in opts:
+            plan.set_option(arplan.AR_OPT_RESIDENT, opts["resident"])
         ptrs = arplan.pointers(bufs)
         sh = stream.cuda_stream
         restore()
@@ -412,7 +419,9 @@ def headline_line(h, K, W, name):
         "data": "synthetic (seeded inputs, %s)" % name,
         "config": {"workload": name, "plan": h["plan"], "n": h["n"], "N": h["N"],
                    "fanin": h["fanin"],
-                   "form": "default executor" if "default" in h else "plan as written",
+                   "form": ("default executor" if not FORMS["default"] else
+                            "executor with %s" % FORMS["default"]) if "default" in h
+                           else "plan as written",
                    "parallelism": "emulated %d processors on 1 GPU" % h["n"]},
         "plan_bytes_per_step": red_b + cpy_b,
     }
@@ -485,6 +494,12 @@ def main():
                     help="time only one form (for profiler runs)")
     ap.add_argument("--no-configs", action="store_true",
                     help="time the headline workload only, not every workload")
+    ap.add_argument("--slice", type=int, choices=(0, 1, 2), default=None,
+                    help="AR_OPT_SLICE for the default form (the library's default: 2)")
+    ap.add_argument("--resident", type=int, choices=(0, 1), default=None,
+                    help="AR_OPT_RESIDENT for the default form (the library's default: 1)")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="AR_OPT_FUSE = 0 for the default form")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the copy / two-source fold ceiling measurement")
@@ -504,6 +519,14 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     forms = tuple(FORMS) if args.form == "both" else (args.form,)
+    # executor overrides of the default form (for exploring and profiling
+    # other executions of the same plan; the configs entries use them too)
+    if args.slice is not None:
+        FORMS["default"]["slice"] = args.slice
+    if args.resident is not None:
+        FORMS["default"]["resident"] = args.resident
+    if args.no_fuse:
+        FORMS["default"]["fuse"] = 0
     K, W = args.steps, args.warmup
     cpu = not args.no_cpu_baseline
     h = bench_workload(torch, arplan, args.config, K, W, forms, stream,
