@@ -236,6 +236,11 @@ ar_status ar_plan_execute_timed(ar_plan* plan, void* const* bufs,
  *   - The first call with a plan (and after each option change) builds the
  *     plan's host-side image of the tables (host memory, freed with the
  *     plan).
+ *   - A call whose plan and buffer set are those of the last call on the
+ *     device enqueues kernel launches only; so a caller capturing the call
+ *     into a HIP graph makes one uncaptured call with the same plan and
+ *     buffers first, and does not interleave calls with other plans or
+ *     buffer sets on the device between the replays.
  *   - AR_ERR_UNSUPPORTED, with the size in ar_last_error(), when the plan's
  *     tables and records exceed AR_NOALLOC_MAX_BYTES (their size grows with
  *     the number of steps and, for a resident launch, with N: 40 bytes per
