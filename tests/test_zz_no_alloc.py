@@ -140,3 +140,37 @@ def test_too_large_is_refused_before_any_launch():
         del bufs
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def test_graph_capture_after_an_uncaptured_call():
+    # after one uncaptured call with the same plan and buffers, a captured
+    # call records kernel launches only; replays match the oracle applied once
+    # more each; after a call with another plan, one uncaptured call with
+    # this plan puts its tables back and the graph replays correctly again
+    kind, n, N, fan = "tree", 64, (1 << 16) + 64, (8, 8)
+    xs0 = workloads.draw(n, N, "i32", "int1000", 31)
+    plan_o = oracle.make_plan(kind, n, N, fan)
+    want = oracle.execute(plan_o, [x.copy() for x in xs0], "i32")
+    ts = to_device(xs0, "i32")
+    with arplan.Plan(n, N, "i32", kind, fan) as p, arplan.Plan(16, 4096, "f32", "cps") as other:
+        p.execute_noalloc(ts, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert all(np.array_equal(g, w) for g, w in zip(to_host(ts, "i32"), want))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            p.execute_noalloc(ts, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert all(np.array_equal(g_, w) for g_, w in zip(to_host(ts, "i32"), want))
+        ob = to_device(workloads.draw(16, 4096, "f32", "uniform", 2), "f32")
+        for r in range(3):
+            g.replay()
+            torch.cuda.synchronize()
+            want = oracle.execute(plan_o, want, "i32")
+            assert all(np.array_equal(g_, w) for g_, w in zip(to_host(ts, "i32"), want)), r
+            if r == 1:
+                # another plan on the device, then this plan uncaptured once
+                other.execute_noalloc(ob, torch.cuda.current_stream())
+                p.execute_noalloc(ts, torch.cuda.current_stream())
+                torch.cuda.synchronize()
+                want = oracle.execute(plan_o, want, "i32")
+                assert all(np.array_equal(g_, w) for g_, w in zip(to_host(ts, "i32"), want))
