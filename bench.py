@@ -266,7 +266,11 @@ def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream, min_ms=0.0):
         "reduce_bytes": red_bytes,
         "reduce_ms": round(red_ms, 5),
         "reduce_gbs": round(_gbs(red_bytes, red_ms), 1),
-        "reduce_frac": round(_gbs(red_bytes, red_ms) / HBM_PEAK_GBS, 4),
+        # a plain sliced launch's steps hand their results to the next phase
+        # through the cache: its bytes are not HBM traffic, so no fraction of
+        # the HBM peak is given for it
+        "reduce_frac": (None if any(launches[i][0] == -1 for i in red)
+                        else round(_gbs(red_bytes, red_ms) / HBM_PEAK_GBS, 4)),
         "copy_gbs": round(_gbs(cpy_bytes, cpy_ms), 1) if cpy_ms > 0 else None,
         "kernels": sorted({KERNEL_OF.get(L[0], "phase_kernel") for L in launches}),
         "launches": [{"phase": L[0], "k": L[1], "max_dst": L[2], "steps": L[3],
