@@ -44,8 +44,10 @@ ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* info,
  * (bit 0: nontemporal loads, bit 1: nontemporal stores), out[2] = wave tile
  * in elements, out[3] = wave tiles, out[4] = wavefronts per block, out[5] =
  * 1 when the tiles come from a table, out[6] = sources whose loads the
- * runtime-source-count kernel keeps in flight together.  AR_ERR_INVALID_ARG
- * for a sliced launch.  Host only. */
+ * runtime-source-count kernel keeps in flight together, out[7] = waves per
+ * tile (1, or the wavefronts per block in a split launch), out[8] = 1 when
+ * the tile table places tiles on XCDs by position.
+ * AR_ERR_INVALID_ARG for a sliced launch.  Host only. */
 ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* out);
 #ifdef __cplusplus
 }

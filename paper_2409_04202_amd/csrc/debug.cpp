@@ -183,7 +183,11 @@ static std::string check_streamed(const ar_plan& plan, const ExecState& ex, cons
 // every executed phase is free of hazards, and walking every wave tile of
 // every launch with the kernel's own index helpers covers each step exactly
 // once, in bounds, with 16-byte aligned vector parts (the padding entries of
-// a tile table excepted, which the kernel skips).
+// a tile table excepted, which the kernel skips).  In a split launch the
+// waves of a workgroup share one tile, and their shares of a step's
+// destinations cover each destination once, the ones among the step's
+// sources (stored after the barrier) last.  An affinity table puts every
+// tile on the XCD (workgroup id modulo kNumXCDs) that xcd_of names.
 AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                                           char* msg, int64_t msglen) {
     clear_error();
@@ -209,17 +213,26 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             if (L.wpb != kcfg(L.kern_k).WPB) return bad("block size differs from the kernel's");
             if (L.rt_group < 1 || L.rt_group > kRtGroup) return bad("source group out of range");
             if (L.tile_elems % (64 * VEC) != 0) return bad("tile not a multiple of a wave vector");
+            if (L.dsplit < 1 || (L.dsplit > 1 && (L.dsplit != L.wpb || L.nunits % L.dsplit)))
+                return bad("split launch not one tile per workgroup");
             const int2* tiles = L.tile_off >= 0 ? ex->htiles.data() + L.tile_off : nullptr;
-            if (tiles && L.tile_off + L.nunits > int64_t(ex->htiles.size()))
+            if (tiles && L.tile_off + L.nunits / L.dsplit > int64_t(ex->htiles.size()))
                 return bad("tile table overrun");
             for (int64_t j = 0; j < L.count; ++j) launched[size_t(L.first + j)] = 1;
             for (int64_t unit = 0; unit < blocks * L.wpb; ++unit) {
                 if (unit >= L.nunits) continue;  // the kernel returns here
+                const int64_t tile = L.dsplit > 1 ? unit / L.dsplit : unit;
+                const int part = int(unit - tile * L.dsplit);
                 int64_t s, t;
-                unit_tile(unit, tiles, L.tiles_per_step, s, t);
+                unit_tile(tile, tiles, L.tiles_per_step, s, t);
                 if (tiles && s == -1 && t == 0) continue;  // padding entry: the kernel skips it
                 if (s < 0 || s >= L.count || t < 0) return bad("unit maps outside the launch");
                 const DevStep& st = ex->hsteps[size_t(L.first + s)];
+                if (L.affinity && !tiles) return bad("affinity launch without a tile table");
+                if (L.affinity &&
+                    xcd_of(std::max((st.begin & ~(VEC - 1)) + t * L.tile_elems, st.begin),
+                           plan->N) != (unit / L.wpb) % kNumXCDs)
+                    return bad("tile not on the XCD of its position");
                 if (st.k < 1 || st.src_off < 0 ||
                     int64_t(st.src_off) + st.k > int64_t(ex->hidx.size()))
                     return bad("source list out of range");
@@ -234,6 +247,26 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                 for (int32_t q = 0; q < st.ndst; ++q) {
                     const int32_t dst = ex->hidx[size_t(st.dst_off + q)];
                     if (dst < 0 || dst >= plan->n) return bad("destination index out of range");
+                    bool is_src = false;
+                    for (int32_t j = 0; j < st.k; ++j)
+                        is_src = is_src || ex->hidx[size_t(st.src_off + j)] == dst;
+                    if (is_src != (q >= st.nfree))
+                        return bad("destinations among the sources not last");
+                }
+                if (L.dsplit > 1 && part == L.dsplit - 1) {
+                    // the parts' shares tile [0, nfree) and [nfree, ndst)
+                    int fa = 0, ga = 0;
+                    for (int pp = 0; pp < L.dsplit; ++pp) {
+                        int a, b;
+                        split_share(st.nfree, pp, L.dsplit, a, b);
+                        if (a != fa || b < a) return bad("destination shares not contiguous");
+                        fa = b;
+                        split_share(st.ndst - st.nfree, pp, L.dsplit, a, b);
+                        if (a != ga || b < a) return bad("destination shares not contiguous");
+                        ga = b;
+                    }
+                    if (fa != st.nfree || ga != st.ndst - st.nfree)
+                        return bad("destination shares do not cover the step");
                 }
                 const TileSpan sp = tile_span(st.begin, st.end, t, L.tile_elems, VEC, vecok != 0);
                 if (sp.lo >= sp.hi) continue;
@@ -245,7 +278,7 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
                     return bad("misaligned vector part");
                 if (sp.vlo - sp.lo >= VEC || (sp.vhi > sp.vlo && sp.hi - sp.vhi >= VEC))
                     if (sp.vhi > sp.vlo) return bad("head or tail longer than a vector");
-                cover[size_t(L.first + s)].push_back({sp.lo, sp.hi});
+                if (part == 0) cover[size_t(L.first + s)].push_back({sp.lo, sp.hi});
             }
         }
         // step records: inside the record area, disjoint, long enough for
@@ -668,6 +701,8 @@ AR_EXPORT ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* 
         out[4] = L.wpb;
         out[5] = L.tile_off >= 0 ? 1 : 0;
         out[6] = L.rt_group;
+        out[7] = L.dsplit;
+        out[8] = L.affinity;
         return AR_OK;
     } catch (const std::exception& e) {
         return fail(AR_ERR_INTERNAL, e.what());

@@ -169,7 +169,7 @@ static void fill_records(const ExecState& ex, void* const* bufs, int32_t n, uint
     for (size_t i = 0; i < ex.hsteps.size(); ++i) {
         const DevStep& st = ex.hsteps[i];
         uint64_t* r = w + ex.rec_of[i];
-        StepHead h{st.begin, st.end, st.k, st.ndst, 0};
+        StepHead h{st.begin, st.end, st.k, st.ndst, st.nfree, 0};
         std::memcpy(r, &h, sizeof(h));
         for (int32_t j = 0; j < st.k; ++j)
             r[kRecHead + j] = reinterpret_cast<uint64_t>(bufs[size_t(ex.hidx[size_t(st.src_off + j)])]);
@@ -242,8 +242,27 @@ static ar_status step_records(const Plan& p, const ExecState& ex, DevState& d,
 template <int DT, int K>
 static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
                       const uint64_t* recs, int64_t stride, const int2* tiles,
-                      int64_t nunits, int64_t tps, int64_t te, int rtg) {
-    const dim3 grid(static_cast<uint32_t>(blocks)), block(64 * kcfg(K).WPB);
+                      int64_t nunits, int64_t tps, int64_t te, int rtg,
+                      int dsplit) {
+    const dim3 block(64 * kcfg(K).WPB);
+    if (dsplit > 1 && vecok) {  // a workgroup per table entry
+        const int64_t ntiles = nunits / dsplit;
+        const dim3 grid(static_cast<uint32_t>(ntiles));
+#define AR_SPLIT(C)                                                                      \
+    hipLaunchKernelGGL((split_kernel<DT, K, C>), grid, block, 0, st, recs, stride, tiles, \
+                       ntiles, te, rtg)
+        if (cm == 0) AR_SPLIT(0);
+        else if (cm == 1) AR_SPLIT(1);
+        else if (cm == 2) AR_SPLIT(2);
+        else AR_SPLIT(3);
+#undef AR_SPLIT
+        return;
+    }
+    if (dsplit > 1) {  // unaligned buffers: one wave per table entry
+        nunits /= dsplit;
+        blocks = (nunits + kcfg(K).WPB - 1) / kcfg(K).WPB;
+    }
+    const dim3 grid(static_cast<uint32_t>(blocks));
 #define AR_LAUNCH(V, C)                                                                \
     hipLaunchKernelGGL((phase_kernel<DT, K, V, C>), grid, block, 0, st, recs, stride, \
                        tiles, nunits, tps, te, rtg)
@@ -258,15 +277,16 @@ static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
 template <int DT>
 static void launch_d(int K, bool vecok, int cm, int64_t blocks, hipStream_t st,
                      const uint64_t* recs, int64_t stride, const int2* tiles,
-                     int64_t nunits, int64_t tps, int64_t te, int rtg) {
+                     int64_t nunits, int64_t tps, int64_t te, int rtg,
+                     int dsplit) {
     switch (K) {
-        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
-        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
-        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
-        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
-        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
-        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
-        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg); break;
+        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
     }
 }
 
@@ -394,17 +414,17 @@ static ar_status launch_all(ar_plan* plan, const ExecState* ex, const DevView& v
                     case AR_F32:
                         launch_d<DT_F32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                         L.tile_elems, L.rt_group);
+                                         L.tile_elems, L.rt_group, L.dsplit);
                         break;
                     case AR_I32:
                         launch_d<DT_I32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                         L.tile_elems, L.rt_group);
+                                         L.tile_elems, L.rt_group, L.dsplit);
                         break;
                     default:
                         launch_d<DT_BF16>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                           L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                          L.tile_elems, L.rt_group);
+                                          L.tile_elems, L.rt_group, L.dsplit);
                         break;
                 }
             }

@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -123,6 +124,32 @@ constexpr int64_t kNumXCDs = 8;         // compute dies, each with its own L2
 // this many tiles.
 constexpr int64_t kXcdMaxTiles = 64;
 
+// A launch of fewer than kMinUnits wave tiles whose steps store to at least
+// kSplitMinDst destinations is split (dsplit = wavefronts per block, see
+// split_tile).
+constexpr int32_t kSplitMinDst = 16;
+// Launches moving at most kAffinityMaxBytes, and split launches, place their
+// tiles on XCDs by element position (affinity_tiles in schedule.cpp), so
+// that what one such launch writes is read by the next on the XCD whose L2
+// holds it.  Measured on MI355X: the bf16 tree (8, 8, 8)'s split level-2
+// reduce (sources written by the 36 MiB level-1 reduce) 19.8 -> 12.5 us;
+// phase launches of the tree (8, 8) at 2^16 fp32 and Ring n = 4 at 2^16,
+// 14-32 % less per AllReduce; but with a limit of 512 MiB the tree (8, 8)'s
+// 144 MiB level-1 reduce ran 27 -> 31 us.
+constexpr int64_t kAffinityMaxBytes = int64_t(64) << 20;
+
+// XCD of a tile starting at element e of N: each XCD owns a contiguous
+// 1/kNumXCDs of every buffer's element range.  Launches with an affinity
+// table place their tiles this way, so a launch reading (or overwriting)
+// what the launch before it wrote finds it in its own XCD's L2 rather than
+// in another's (the XCDs' L2s are kept coherent with each other, and a line
+// another XCD holds is slow to read or overwrite), and each XCD gets an
+// equal share of a phase that covers the whole vector.  Shared with the
+// host-side check.
+inline int64_t xcd_of(int64_t e, int64_t N) {
+    return N > 0 ? std::min<int64_t>(e * kNumXCDs / N, kNumXCDs - 1) : 0;
+}
+
 struct LaunchDesc {
     int32_t phase;
     int32_t xphase;          // executed phase
@@ -137,6 +164,8 @@ struct LaunchDesc {
     int32_t cm;              // cache mode: bit 0 NT loads, bit 1 NT stores
     int32_t max_dst;         // most destinations of a step
     int32_t rt_group;        // runtime-k kernel: sources with loads in flight together
+    int32_t dsplit;          // waves per tile (split_tile), 1: one
+    int32_t affinity;        // 1: the tile table places tiles by xcd_of
     int64_t bytes;           // (k + destinations) * len * e over the steps
     int64_t hbm;             // predicted HBM traffic: bytes, less the repeated
                              // reads of a range by the launch's copies

@@ -28,8 +28,9 @@ namespace arp {
 enum DType : int32_t { DT_F32 = 0, DT_I32 = 1, DT_BF16 = 2 };
 
 // One executed step: fold the k sources over [begin, end) and store the
-// result into each of the ndst destinations.  Host form, 32 bytes; the
-// indices point into the plan's index pool.
+// result into each of the ndst destinations.  Host form; the indices point
+// into the plan's index pool, where a step's destinations that are not
+// among its sources come first.
 struct DevStep {
     int64_t begin;
     int64_t end;
@@ -37,18 +38,21 @@ struct DevStep {
     int32_t k;        // number of sources
     int32_t dst_off;  // first destination index in the same pool
     int32_t ndst;     // number of destinations
+    int32_t nfree;    // the first nfree destinations are not sources of the step
 };
 
 // The record a kernel reads for a step, built per buffer set: this header
 // (4 words) followed by k source and ndst destination buffer pointers, one
-// 8-byte word each.  Records of one launch have a common stride, so a wave
-// finds its step's pointers with one dependent load.
+// 8-byte word each, the nfree destinations that are not sources first.
+// Records of one launch have a common stride, so a wave finds its step's
+// pointers with one dependent load.
 struct StepHead {
     int64_t begin;
     int64_t end;
     int32_t k;
     int32_t ndst;
-    int64_t pad;
+    int32_t nfree;
+    int32_t pad;
 };
 constexpr int kRecHead = 4;  // header words
 
@@ -343,6 +347,36 @@ __device__ __forceinline__ void store_all(const DstMem& dst, int64_t v0, const u
     }
 }
 
+// The loads and adds of fold_vectors (below) without its stores, for split
+// tiles, which store in two parts around a barrier (split_pass): out[u] is
+// the folded vector u, ok[u] whether it is in range.  fold_vectors keeps its
+// own copy of these lines: built on this function, its loop compiled to a
+// different schedule and the 3 GiB two-source fold ran 3 % slower.
+template <int DT, int K, int U, int CM, bool FULL>
+__device__ __forceinline__ void fold_load(const gvec* const* sp, int64_t at, int64_t nv,
+                                          int lane, u32x4 (&out)[U], bool (&ok)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
+    u32x4 x[K][U];
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) x[j][u] = vload<(CM & 1) != 0>(sp[j] + at + u * 64 + lane);
+    if constexpr (K == 1) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) out[u] = x[0][u];
+    } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            VAcc<DT> acc;
+            acc.init(x[0][u]);
+#pragma unroll
+            for (int j = 1; j < K; ++j) acc.add(x[j][u]);
+            out[u] = acc.out();
+        }
+    }
+}
 // U vectors per lane of K sources at vector offset `at` (+ u * 64 + lane),
 // folded in source order and stored to every destination.  FULL: all U
 // vectors are in range, so the loads are issued back to back with no
@@ -385,6 +419,47 @@ __device__ __forceinline__ void fold_vectors(const gvec* const* sp, const D& dst
 // cost occupancy where there is work enough to hide the latency).
 constexpr int kRtGroup = 4;
 
+// fold_load for a runtime source count (as fold_vectors_rt, below, without
+// its stores).
+template <int DT, int U, int CM, bool FULL>
+__device__ __forceinline__ void fold_load_rt(void* const* __restrict__ srcp, int k, int64_t v0,
+                                             int64_t at, int64_t nv, int lane, int group,
+                                             u32x4 (&out)[U], bool (&ok)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = FULL || at + u * 64 + lane < nv;
+    if (k == 1) {
+        const gvec* s0 = as_global<u32x4>(srcp[0]) + v0;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) out[u] = vload<(CM & 1) != 0>(s0 + at + u * 64 + lane);
+    } else {
+        VAcc<DT> acc[U];
+        for (int j0 = 0; j0 < k; j0 += group) {
+            u32x4 x[kRtGroup][U];
+#pragma unroll
+            for (int g = 0; g < kRtGroup; ++g) {
+                if (g < group && j0 + g < k) {  // wave-uniform
+                    const gvec* sj = as_global<u32x4>(srcp[j0 + g]) + v0;
+#pragma unroll
+                    for (int u = 0; u < U; ++u)
+                        if (ok[u]) x[g][u] = vload<(CM & 1) != 0>(sj + at + u * 64 + lane);
+                }
+            }
+#pragma unroll
+            for (int g = 0; g < kRtGroup; ++g) {
+                if (g < group && j0 + g < k) {
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        if (j0 + g == 0) acc[u].init(x[g][u]);
+                        else acc[u].add(x[g][u]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) out[u] = acc[u].out();
+    }
+}
 template <int DT, int U, int CM, bool FULL, class D>
 __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, int k,
                                                 const D& dst, int64_t v0, int64_t at,
@@ -426,6 +501,84 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, 
         for (int u = 0; u < U; ++u) out[u] = acc[u].out();
     }
     store_all<U, CM, FULL>(dst, v0, out, ok, at, lane);
+}
+
+// Split launches.  A wave storing one small tile to many destinations
+// spends its time issuing the stores (measured on MI355X: 512 waves each
+// storing 1 KiB to 64 buffers take 13.5 us, 2048 waves storing 16 each
+// 7.4 us).  A launch of few tiles whose steps have many destinations
+// therefore gives each tile a whole workgroup (dsplit = wavefronts per
+// block): every wave folds the tile and stores to its share of the
+// destinations.  The destinations that are sources of the step as well
+// (they come last in the record) are stored only after a workgroup barrier,
+// when every wave has loaded the sources; the others are stored at once.
+// This pays only where each tile runs on the XCD that wrote its sources in
+// the launch before (the host places tiles so): the bf16 tree (8, 8, 8)'s
+// level-2 reduce into 64 buffers takes 12.5 us so, 26 us split with tiles on
+// other XCDs, 20 us unsplit.
+// split_share: part `part` of `parts` gets items [a, b) of n, contiguous,
+// the shares differing by at most one.  Shared with the host-side check.
+__host__ __device__ __forceinline__ void split_share(int n, int part, int parts, int& a, int& b) {
+    const int q = n / parts, r = n % parts;
+    a = part * q + (part < r ? part : r);
+    b = a + q + (part < r ? 1 : 0);
+}
+
+// One pass of a split tile: fold U vectors per lane at `at`, store them to
+// this wave's share of the destinations that are not sources (fd), and,
+// when the step has destinations among its sources, wait for the
+// workgroup and store to this wave's share of those (sd).
+template <int DT, int K, int U, int CM, bool FULL>
+__device__ __forceinline__ void split_pass(const gvec* const* sv, void* const* __restrict__ sp,
+                                           int k, int rt_group, const Dsts& fd, const DstMem& sd,
+                                           bool sync, int64_t v0, int64_t at, int64_t nv,
+                                           int lane) {
+    u32x4 out[U];
+    bool ok[U];
+    if constexpr (K > 0) fold_load<DT, K, U, CM, FULL>(sv, at, nv, lane, out, ok);
+    else fold_load_rt<DT, U, CM, FULL>(sp, k, v0, at, nv, lane, rt_group, out, ok);
+    store_all<U, CM, FULL>(fd, v0, out, ok, at, lane);
+    if (sync) {
+        __syncthreads();
+        store_all<U, CM, FULL>(sd, v0, out, ok, at, lane);
+    }
+}
+
+// A tile run by the `parts` waves of a workgroup, this one being `part`
+// (buffers 16-byte aligned).  Every wave takes the same branches and passes
+// (same step and tile), so all reach the same barriers.  Element-wise heads
+// and tails are done by the first wave alone, with every destination: no
+// other wave touches those positions.
+template <int DT, int K, int CM>
+__device__ __forceinline__ void split_tile(void* const* __restrict__ sp, int k,
+                                           void* const* __restrict__ dp, int ndst, int nfree,
+                                           const TileSpan& ts, int part, int parts, int lane,
+                                           int rt_group) {
+    constexpr int VEC = Elem<DT>::VEC;
+    constexpr int U = kcfg(K).U;
+    if (part == 0) {
+        if (ts.vlo > ts.lo) fold_scalar<DT, K>(sp, k, dp, ndst, ts.lo, ts.vlo, lane);
+        if (ts.hi > ts.vhi) fold_scalar<DT, K>(sp, k, dp, ndst, ts.vhi, ts.hi, lane);
+    }
+    if (ts.vhi <= ts.vlo) return;
+    const int64_t v0 = ts.vlo / VEC;
+    const int64_t nv = (ts.vhi - ts.vlo) / VEC;
+    int f0, f1, g0, g1;
+    split_share(nfree, part, parts, f0, f1);
+    split_share(ndst - nfree, part, parts, g0, g1);
+    const Dsts fd = load_dsts(dp + f0, f1 - f0);
+    const DstMem sd{dp + nfree + g0, g1 - g0};
+    const bool sync = ndst > nfree;
+    const gvec* sv[K > 0 ? K : 1];
+    if constexpr (K > 0) {
+#pragma unroll
+        for (int j = 0; j < K; ++j) sv[j] = as_global<u32x4>(sp[j]) + v0;
+    }
+    int64_t at = 0;
+    for (; at + 64 * U <= nv; at += 64 * U)
+        split_pass<DT, K, U, CM, true>(sv, sp, k, rt_group, fd, sd, sync, v0, at, nv, lane);
+    if (at < nv)
+        split_pass<DT, K, U, CM, false>(sv, sp, k, rt_group, fd, sd, sync, v0, at, nv, lane);
 }
 
 // One launch: `nunits` wave tiles over the steps whose records start at
@@ -478,6 +631,37 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
         if (at < nv)
             fold_vectors_rt<DT, U, CM, false>(sp, k, dst, v0, at, nv, lane, rt_group);
     }
+}
+
+// Split launch (see split_tile): workgroup b runs wave tile b of the
+// launch's tile table (tiles[b] = (step, tile in step), or (-1, 0) padding),
+// its WPB waves each storing to a share of the destinations.  Buffers are
+// 16-byte aligned (a split launch on unaligned buffers runs phase_kernel over
+// the same table instead).  CM: cache mode of the vector loads and stores.
+// A kernel of its own, so that phase_kernel's code stays as it was: with
+// the split path inside it, the compiler scheduled the fold loop's loads
+// and stores differently and the 3 GiB two-source fold ran 3 % slower.
+template <int DT, int K, int CM>
+__global__ __launch_bounds__(64 * kcfg(K).WPB) void split_kernel(
+    const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
+    int64_t ntiles, int64_t tile_elems, int rt_group) {
+    constexpr int VEC = Elem<DT>::VEC;
+    constexpr int WPB = kcfg(K).WPB;
+    const int lane = int(threadIdx.x) & 63;
+    const int part = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+    const int64_t tile = blockIdx.x;
+    if (tile >= ntiles) return;
+    const int2 e = tiles[tile];
+    const int64_t s = __builtin_amdgcn_readfirstlane(e.x);
+    const int64_t t = __builtin_amdgcn_readfirstlane(e.y);
+    if (s < 0) return;  // a padding entry of the table
+    const uint64_t* rec = recs + s * stride;
+    const StepHead st = *reinterpret_cast<const StepHead*>(rec);
+    const int k = K ? K : st.k;
+    void* const* sp = reinterpret_cast<void* const*>(rec + kRecHead);
+    const TileSpan ts = tile_span(st.begin, st.end, t, tile_elems, VEC, true);
+    if (ts.lo >= ts.hi) return;
+    split_tile<DT, K, CM>(sp, k, sp + k, st.ndst, st.nfree, ts, part, WPB, lane, rt_group);
 }
 
 // ------------------------------------------------------------------------

@@ -24,14 +24,15 @@ int kernel_k(int32_t k) {
 
 // Tile table of a copy launch whose steps read some range more than once:
 // the copies reading the same range are grouped, the range is cut into
-// super-tiles of one workgroup's worth of tiles, and each super-tile is dealt
-// to one XCD, where one workgroup per copy runs it, one after the other: the
-// repeated reads of a super-tile hit that XCD's L2 instead of going to
-// memory again, and each workgroup still writes one contiguous stretch.
-// Workgroups are dispatched to the kNumXCDs XCDs round-robin by workgroup
-// id, so workgroup b runs on XCD b % kNumXCDs; the table gives each XCD the
-// same number of workgroups, padding with entries (-1, 0) that the kernel
-// skips.  Used for copies of at most kXcdMaxTiles tiles: the repeated reads
+// super-tiles of one workgroup's worth of tiles, and the super-tiles are
+// dealt to the XCDs in turn, where one workgroup per copy runs each, one
+// after the other: the repeated reads of a super-tile hit that XCD's L2
+// instead of going to memory again, and each workgroup still writes one
+// contiguous stretch (dealing them by position instead, as xcd_of does,
+// measured slower: the tree (8, 8)'s last AllGather 152 -> 179 us).  Workgroups are dispatched to the kNumXCDs XCDs
+// round-robin by workgroup id, so workgroup b runs on XCD b % kNumXCDs; the
+// table gives each XCD the same number of workgroups, padding with entries
+// (-1, 0) that the kernel skips.  Used for copies of at most kXcdMaxTiles tiles: the repeated reads
 // of longer copies come far enough apart for the last-level cache, shared by
 // all XCDs, to serve them, and their writes streamed better without the
 // grouping (measured).  Steps are idx[g0..g1) of executed phase xp, in
@@ -69,6 +70,37 @@ static bool xcd_tiles(const XPhase& xp, const std::vector<size_t>& idx, size_t g
                 ex.htiles.push_back(u < seq[x].size() ? seq[x][u] : make_int2(-1, 0));
     L.nunits = nunits;
     return true;
+}
+
+// Affinity table: each tile goes to the XCD xcd_of its first element.
+// Workgroups are dispatched to the XCDs round-robin by workgroup id, so
+// workgroup b runs on XCD b % kNumXCDs: the table gives each XCD's
+// workgroups its tiles in launch order, padding with entries (-1, 0) that
+// the kernel skips.  A split launch (dsplit > 1) has one tile per
+// workgroup, others wpb.  Steps are idx[g0..g1) of executed phase xp, in
+// launch order, spans[j] the element span of step g0 + j.
+static void affinity_tiles(const XPhase& xp, const std::vector<size_t>& idx, size_t g0,
+                           size_t g1, const std::vector<int64_t>& spans, int64_t te,
+                           int64_t VEC, int64_t N, LaunchDesc& L, ExecState& ex) {
+    std::vector<std::vector<int2>> seq(static_cast<size_t>(kNumXCDs));
+    for (size_t j = 0; j < g1 - g0; ++j) {
+        const XStep& x = xp.steps[idx[g0 + j]];
+        const int64_t abase = x.begin & ~(VEC - 1);
+        for (int64_t t = 0; t * te < spans[j]; ++t) {
+            const int64_t lo = std::max(abase + t * te, x.begin);
+            seq[size_t(xcd_of(lo, N))].push_back(make_int2(int(j), int(t)));
+        }
+    }
+    const size_t per_wg = L.dsplit > 1 ? 1 : size_t(L.wpb);
+    size_t len = 0;
+    for (const auto& q : seq) len = std::max(len, (q.size() + per_wg - 1) / per_wg * per_wg);
+    L.tile_off = int64_t(ex.htiles.size());
+    for (size_t q0 = 0; q0 < len; q0 += per_wg)
+        for (size_t x = 0; x < size_t(kNumXCDs); ++x)
+            for (size_t u = q0; u < q0 + per_wg; ++u)
+                ex.htiles.push_back(u < seq[x].size() ? seq[x][u] : make_int2(-1, 0));
+    L.nunits = int64_t(len * size_t(kNumXCDs)) * L.dsplit;
+    L.affinity = 1;
 }
 
 // Group the steps of every executed phase by source count, choose the
@@ -117,9 +149,18 @@ static void build_launches(const Plan& p, ExecState& ex) {
                 d.k = k;
                 d.src_off = int32_t(ex.hidx.size());
                 ex.hidx.insert(ex.hidx.end(), x.srcs.begin(), x.srcs.end());
+                // destinations that are not sources of the step first
                 d.ndst = int32_t(x.dsts.size());
                 d.dst_off = int32_t(ex.hidx.size());
-                ex.hidx.insert(ex.hidx.end(), x.dsts.begin(), x.dsts.end());
+                for (int pass = 0; pass < 2; ++pass)
+                    for (int32_t dd : x.dsts) {
+                        const bool src =
+                            std::find(x.srcs.begin(), x.srcs.end(), dd) != x.srcs.end();
+                        if (src == (pass == 1)) ex.hidx.push_back(dd);
+                    }
+                d.nfree = d.ndst;
+                for (int32_t dd : x.dsts)
+                    if (std::find(x.srcs.begin(), x.srcs.end(), dd) != x.srcs.end()) --d.nfree;
                 ex.dev_of[q][idx[g]] = int32_t(ex.hsteps.size());
                 ex.hsteps.push_back(d);
                 const int64_t len = x.end - x.begin;
@@ -172,6 +213,8 @@ static void build_launches(const Plan& p, ExecState& ex) {
             L.tiles_per_step = (maxspan + te - 1) / te;
             int64_t used = 0;
             for (int64_t sp : spans) used += (sp + te - 1) / te;
+            // few tiles storing to many destinations: a workgroup per tile
+            L.dsplit = maxdst >= kSplitMinDst && used < kMinUnits ? L.wpb : 1;
             // copies reading the same range run next to each other (or on one
             // XCD, below): their repeated reads hit the cache
             L.hbm = bytes;
@@ -181,7 +224,10 @@ static void build_launches(const Plan& p, ExecState& ex) {
                     if (r == 0 || ranges[r] != ranges[r - 1])
                         L.hbm += (std::get<2>(ranges[r]) - std::get<1>(ranges[r])) * p.esize;
             }
-            if (k == 1 && reuse && L.tiles_per_step <= kXcdMaxTiles &&
+            const bool xcd_copy = k == 1 && reuse && L.tiles_per_step <= kXcdMaxTiles;
+            if (L.dsplit > 1 || (!xcd_copy && bytes <= kAffinityMaxBytes)) {
+                affinity_tiles(xp, idx, g0, g1, spans, te, VEC, p.N, L, ex);
+            } else if (xcd_copy &&
                 xcd_tiles(xp, idx, g0, g1, te, VEC, L, ex)) {
                 // copies reading the same range run on one XCD (tile table)
             } else if (used * 5 < L.count * L.tiles_per_step * 4) {

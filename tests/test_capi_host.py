@@ -539,10 +539,10 @@ def _launch_desc(handle, stage):
     f = arplan._lib.ar_debug_launch_desc
     f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)]
     f.restype = ctypes.c_int32
-    out = (ctypes.c_int64 * 7)()
+    out = (ctypes.c_int64 * 9)()
     assert f(handle, stage, out) == arplan.AR_OK, arplan.ar_last_error()
     return {"k": out[0], "cm": out[1], "tile": out[2], "tiles": out[3], "wpb": out[4],
-            "table": out[5], "group": out[6]}
+            "table": out[5], "group": out[6], "split": out[7], "affinity": out[8]}
 
 
 def test_full_size_forms_use_the_nontemporal_kernels():
@@ -591,3 +591,38 @@ def test_runtime_source_count_groups():
     with arplan.Plan(16, 1 << 20, "f32", "cps") as p:
         p.set_option(arplan.AR_OPT_SLICE, 0)
         assert _launch_desc(p.handle, 0)["group"] == 1
+
+
+# Split launches (a workgroup per tile, each wave storing to a share of the
+# destinations) in the shapes the GPU parity tests run: the 16-source fold
+# whose destinations are all its sources, the runtime-source-count fold, the
+# 8- and 2-source folds storing to 64 or 512 buffers, and one with
+# nontemporal loads.  (fuse, slice) = (1, 0): phase launches.
+SPLIT_CASES = [
+    ("cps", 16, (1 << 14) + 3, None, "f32", 16, 0), ("cps", 32, 32 * 1000 + 17, None, "bf16", 0, 0),
+    ("tree", 512, 1 << 15, (8, 8, 8), "bf16", 8, 0), ("tree", 512, 1 << 18, (8, 8, 8), "bf16", 8, 0),
+    ("tree", 512, 1 << 20, (8, 8, 8), "bf16", 8, 1), ("tree", 64, 4096 + 64 * 5, (8, 8), "f32", 8, 0),
+    ("ring", 64, 64 * 1000, None, "f32", 2, 0), ("ring", 64, 1 << 20, None, "f32", 2, 3)]
+
+
+@pytest.mark.parametrize("kind,n,N,fan,dtype,k,cm", SPLIT_CASES)
+def test_split_launches(kind, n, N, fan, dtype, k, cm):
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        L = p.launches()
+        split = []
+        for i in range(len(L)):
+            d = _launch_desc(p.handle, i)
+            if d["split"] > 1:
+                assert d["split"] == d["wpb"] and d["table"] and d["affinity"], d
+                split.append((d["k"], d["cm"]))
+            # every launch of at most 64 MiB places its tiles by position
+            # (copies reading a range several times keep their own table)
+            if L[i][4] <= 64 << 20 and not (L[i][1] == 1 and d["table"] and not d["affinity"]):
+                assert d["affinity"], (i, L[i], d)
+            if L[i][4] > 64 << 20 and d["split"] == 1:
+                assert not d["affinity"], (i, L[i], d)
+        assert (k, cm) in split, split
+        for vecok in (1, 0):
+            st, msg = _check_tiling(p.handle, vecok)
+            assert st == arplan.AR_OK, msg
