@@ -57,7 +57,6 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 # kernel of a launch by its phase field in ar_plan_launch_info
-KERNEL_OF = {-1: "sliced_kernel", -2: "resident_kernel", -3: "stream_kernel"}
 HEADLINE = "rhd_n8_f32"
 FORMS = {"default": {}, "as_written": {"fuse": 0, "slice": 0}}
 
@@ -220,6 +219,7 @@ def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream, min_ms=0.0):
         if "resident" in opts:
             plan.set_option(arplan.AR_OPT_RESIDENT, opts["resident"])
         launches = plan.launches()          # (phase, nsrc, max_dst, steps, bytes)
+        kernels = plan.launch_kernels()
         red_b, cpy_b = plan.bytes()
         ptrs = arplan.pointers(bufs)        # marshalled once for the buffer set
         sh = stream.cuda_stream
@@ -272,7 +272,7 @@ def time_form(torch, arplan, c, bufs, restore, K, W, opts, stream, min_ms=0.0):
         "reduce_frac": (None if any(launches[i][0] == -1 for i in red)
                         else round(_gbs(red_bytes, red_ms) / HBM_PEAK_GBS, 4)),
         "copy_gbs": round(_gbs(cpy_bytes, cpy_ms), 1) if cpy_ms > 0 else None,
-        "kernels": sorted({KERNEL_OF.get(L[0], "phase_kernel") for L in launches}),
+        "kernels": sorted(set(kernels)),
         "launches": [{"phase": L[0], "k": L[1], "max_dst": L[2], "steps": L[3],
                       "bytes": L[4], "ms": round(m, 5),
                       "gbs": round(_gbs(L[4], m), 1) if m > 0 else None}

@@ -309,6 +309,21 @@ ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t* phase,
                               int32_t* nsrc, int32_t* max_dst,
                               int64_t* num_steps, int64_t* bytes);
 
+/* The kernel launch i (as in ar_plan_launch_info) runs on 16-byte aligned
+ * buffers: AR_KERNEL_PHASE, one wavefront per wave tile of its steps;
+ * AR_KERNEL_SPLIT, a workgroup per wave tile, each wavefront storing the
+ * folded tile to a share of the step's destinations (a launch of few tiles
+ * whose steps store to many buffers; on unaligned buffers it runs as
+ * AR_KERNEL_PHASE); AR_KERNEL_SLICED, AR_KERNEL_RESIDENT and AR_KERNEL_STREAM
+ * for the sliced, resident and streamed resident launches (phase -1, -2 and
+ * -3 above).  Host only, no GPU call.  AR_ERR_INVALID_ARG for a NULL plan or
+ * kernel, or i out of range. */
+typedef enum ar_kernel {
+    AR_KERNEL_PHASE = 0, AR_KERNEL_SPLIT = 1, AR_KERNEL_SLICED = 2,
+    AR_KERNEL_RESIDENT = 3, AR_KERNEL_STREAM = 4
+} ar_kernel;
+ar_status ar_plan_launch_kernel(const ar_plan* plan, int32_t i, int32_t* kernel);
+
 /* -------------------------------------------------------- introspection */
 
 /* Shape of the plan: any out-pointer may be NULL. */

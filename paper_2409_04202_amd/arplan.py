@@ -87,6 +87,7 @@ _sig = {
     "ar_plan_num_launches": [_P, POINTER(c_int32)],
     "ar_plan_launch_info": [_P, c_int32, POINTER(c_int32), POINTER(c_int32),
                             POINTER(c_int32), POINTER(c_int64), POINTER(c_int64)],
+    "ar_plan_launch_kernel": [_P, c_int32, POINTER(c_int32)],
     "ar_genmodel_terms": [_P, c_int64, POINTER(c_double)],
     "ar_genmodel_select": [c_int32, c_int64, c_int32, POINTER(c_double), c_int64, c_int32,
                            POINTER(c_int32), POINTER(c_int32), POINTER(c_int32),
@@ -289,6 +290,17 @@ def ar_plan_launch_info(plan, i):
     return ph.value, k.value, d.value, n.value, b.value
 
 
+KERNEL_NAMES = {0: "phase_kernel", 1: "split_kernel", 2: "sliced_kernel",
+                3: "resident_kernel", 4: "stream_kernel"}
+
+
+def ar_plan_launch_kernel(plan, i):
+    """Name of the kernel launch i runs on 16-byte aligned buffers."""
+    k = c_int32()
+    _check(_lib.ar_plan_launch_kernel(plan, int(i), ctypes.byref(k)))
+    return KERNEL_NAMES[k.value]
+
+
 # -------------------------------------------------------------- GenModel
 
 AR_GENMODEL_TERMS = 6
@@ -401,6 +413,11 @@ class Plan:
         is the plan phase of a phase launch, -1 for a sliced launch, -2 for a
         resident one and -3 for a streamed resident one."""
         return [ar_plan_launch_info(self.handle, i)
+                for i in range(ar_plan_num_launches(self.handle))]
+
+    def launch_kernels(self):
+        """Name of the kernel of each launch (on 16-byte aligned buffers)."""
+        return [ar_plan_launch_kernel(self.handle, i)
                 for i in range(ar_plan_num_launches(self.handle))]
 
     def close(self):

@@ -703,6 +703,30 @@ AR_EXPORT ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* count) {
     }
 }
 
+AR_EXPORT ar_status ar_plan_launch_kernel(const ar_plan* plan, int32_t i, int32_t* kernel) {
+    clear_error();
+    if (!plan || !kernel) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    try {
+        const ExecState* ex = exec_state(const_cast<ar_plan&>(*plan));
+        if (i < 0 || i >= int32_t(ex->stages.size()))
+            return fail(AR_ERR_INVALID_ARG, "launch index out of range");
+        const Stage stg = ex->stages[size_t(i)];
+        if (stg.slice >= 0) {
+            const SliceDesc& sd = ex->slices[size_t(stg.slice)];
+            *kernel = sd.streamed ? AR_KERNEL_STREAM : sd.resident ? AR_KERNEL_RESIDENT
+                                                                   : AR_KERNEL_SLICED;
+        } else {
+            *kernel = ex->launches[size_t(stg.launch)].dsplit > 1 ? AR_KERNEL_SPLIT
+                                                                   : AR_KERNEL_PHASE;
+        }
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}
+
 AR_EXPORT ar_status ar_plan_launch_info(const ar_plan* plan, int32_t i, int32_t* phase,
                                         int32_t* nsrc, int32_t* max_dst, int64_t* num_steps,
                                         int64_t* bytes) {

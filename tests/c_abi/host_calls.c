@@ -44,6 +44,12 @@ int main(void) {
     CHECK(ar_plan_owner(plan, 9, &b, &e) == AR_OK && e - b == (1 << 16) / 64, "owner of processor 9");
     int32_t launches = 0;
     CHECK(ar_plan_num_launches(plan, &launches) == AR_OK && launches >= 1, "launches");
+    int32_t kernel = -1;
+    CHECK(ar_plan_launch_kernel(plan, 0, &kernel) == AR_OK && kernel >= AR_KERNEL_PHASE &&
+              kernel <= AR_KERNEL_STREAM,
+          "kernel of launch 0");
+    CHECK(ar_plan_launch_kernel(plan, launches, &kernel) == AR_ERR_INVALID_ARG,
+          "launch index out of range refused");
     double terms[AR_GENMODEL_TERMS];
     CHECK(ar_genmodel_terms(plan, (int64_t)256 << 20, terms) == AR_OK && terms[0] == 4.0 &&
               terms[1] == 8 + 8 + 1 + 1 && terms[2] + terms[3] == (double)red,

@@ -623,6 +623,25 @@ def test_split_launches(kind, n, N, fan, dtype, k, cm):
             if L[i][4] > 64 << 20 and d["split"] == 1:
                 assert not d["affinity"], (i, L[i], d)
         assert (k, cm) in split, split
+        names = p.launch_kernels()
+        assert names == ["split_kernel" if _launch_desc(p.handle, i)["split"] > 1
+                         else "phase_kernel" for i in range(len(L))], names
         for vecok in (1, 0):
             st, msg = _check_tiling(p.handle, vecok)
             assert st == arplan.AR_OK, msg
+
+
+def test_launch_kernels_by_form():
+    # the kernel each launch of the benchmark's workloads runs, default form
+    from paper_2409_04202_amd import workloads
+    expect = {"rhd_n8_f32": ["resident_kernel"],
+              "tree8x8x8_n512_bf16": ["phase_kernel", "phase_kernel", "split_kernel",
+                                      "phase_kernel"],
+              "tree8x8_n64_f32": ["phase_kernel", "sliced_kernel", "phase_kernel"]}
+    for name, kernels in expect.items():
+        c = workloads.CONFIGS[name]
+        with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
+            assert p.launch_kernels() == kernels, (name, p.launch_kernels())
+    with arplan.Plan(8, 1 << 12, "f32", "rhd") as p:
+        with pytest.raises(arplan.ArError):
+            arplan.ar_plan_launch_kernel(p.handle, len(p.launches()))
