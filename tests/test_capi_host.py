@@ -602,7 +602,9 @@ SPLIT_CASES = [
     ("cps", 16, (1 << 14) + 3, None, "f32", 16, 0), ("cps", 32, 32 * 1000 + 17, None, "bf16", 0, 0),
     ("tree", 512, 1 << 15, (8, 8, 8), "bf16", 8, 0), ("tree", 512, 1 << 18, (8, 8, 8), "bf16", 8, 0),
     ("tree", 512, 1 << 20, (8, 8, 8), "bf16", 8, 1), ("tree", 64, 4096 + 64 * 5, (8, 8), "f32", 8, 0),
-    ("ring", 64, 64 * 1000, None, "f32", 2, 0), ("ring", 64, 1 << 20, None, "f32", 2, 3)]
+    ("ring", 64, 64 * 1000, None, "f32", 2, 0), ("ring", 64, 1 << 20, None, "f32", 2, 3),
+    ("tree", 64, 65553, (16, 4), "f32", 4, 0), ("tree", 256, 65553, (16, 16), "f32", 16, 3),
+    ("cps", 17, 1 << 20, None, "f32", 0, 3), ("tree", 96, 1 << 20, (3, 32), "f32", 0, 1)]
 
 
 @pytest.mark.parametrize("kind,n,N,fan,dtype,k,cm", SPLIT_CASES)

@@ -783,12 +783,15 @@ def test_paper_asymmetric_topologies_scaled(name):
     ("cps", 16, (1 << 14) + 3, None, "f32"), ("cps", 32, 32 * 1000 + 17, None, "bf16"),
     ("cps", 16, 4096, None, "i32"), ("tree", 512, 1 << 15, (8, 8, 8), "bf16"),
     ("tree", 64, 4096 + 64 * 5, (8, 8), "f32"), ("ring", 64, 64 * 1000, None, "f32"),
-    ("tree", 512, 1 << 20, (8, 8, 8), "bf16")])
+    ("tree", 512, 1 << 20, (8, 8, 8), "bf16"), ("tree", 64, 65553, (16, 4), "f32"),
+    ("tree", 256, 65553, (16, 16), "f32"), ("cps", 17, 1 << 20, None, "f32"),
+    ("tree", 96, 1 << 20, (3, 32), "f32")])
 def test_many_destination_phase_launches(kind, n, N, fan, dtype):
     # phase launches whose steps store to 16 or more buffers, some of them
     # the step's own sources (the reduce-then-broadcast rewrite): split
     # launches, a workgroup per tile (the shapes tests/test_capi_host.py
-    # checks for them), the last with nontemporal loads
+    # checks for them): 2, 4, 8, 16 sources and a runtime source count, with
+    # cached and nontemporal loads and stores
     dist = "int1000" if dtype == "i32" else "uniform"
     got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=N % 101, slice_=0)
     if dtype == "bf16":
