@@ -129,14 +129,20 @@ constexpr int64_t kXcdMaxTiles = 64;
 // split_tile).
 constexpr int32_t kSplitMinDst = 16;
 // Launches moving at most kAffinityMaxBytes, and split launches, place their
-// tiles on XCDs by element position (affinity_tiles in schedule.cpp), so
-// that what one such launch writes is read by the next on the XCD whose L2
-// holds it.  Measured on MI355X: the bf16 tree (8, 8, 8)'s split level-2
+// tiles on XCDs by element position (affinity_tiles in schedule.cpp, xcd_of
+// below), so that what one such launch writes is read by the next on the
+// XCD whose L2 holds it.  Measured on MI355X: the bf16 tree (8, 8, 8)'s split level-2
 // reduce (sources written by the 36 MiB level-1 reduce) 19.8 -> 12.5 us;
 // phase launches of the tree (8, 8) at 2^16 fp32 and Ring n = 4 at 2^16,
 // 14-32 % less per AllReduce; but with a limit of 512 MiB the tree (8, 8)'s
-// 144 MiB level-1 reduce ran 27 -> 31 us.
+// 144 MiB level-1 reduce ran 27 -> 31 us.  Launches of one or two sources
+// moving at least kAffinityBigBytes and reading every range once are placed
+// so too: RHD as written (n = 8, 2^26 fp32) 1.531 -> 1.503 ms, each of its
+// halving folds and doubling copies 1-4 % faster; the 16-source fold placed
+// so left its own time unchanged and slowed the AllGather copies after it
+// (182 -> 189 us), which read its output from other XCDs.
 constexpr int64_t kAffinityMaxBytes = int64_t(64) << 20;
+constexpr int64_t kAffinityBigBytes = int64_t(512) << 20;
 
 // XCD of a tile starting at element e of N: each XCD owns a contiguous
 // 1/kNumXCDs of every buffer's element range.  Launches with an affinity

@@ -225,7 +225,11 @@ static void build_launches(const Plan& p, ExecState& ex) {
                         L.hbm += (std::get<2>(ranges[r]) - std::get<1>(ranges[r])) * p.esize;
             }
             const bool xcd_copy = k == 1 && reuse && L.tiles_per_step <= kXcdMaxTiles;
-            if (L.dsplit > 1 || (!xcd_copy && bytes <= kAffinityMaxBytes)) {
+            const bool affinity =
+                L.dsplit > 1 ||
+                (!xcd_copy && (bytes <= kAffinityMaxBytes ||
+                               (bytes >= kAffinityBigBytes && !reuse && k <= 2)));
+            if (affinity) {
                 affinity_tiles(xp, idx, g0, g1, spans, te, VEC, p.N, L, ex);
             } else if (xcd_copy &&
                 xcd_tiles(xp, idx, g0, g1, te, VEC, L, ex)) {

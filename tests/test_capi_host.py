@@ -622,7 +622,7 @@ def test_split_launches(kind, n, N, fan, dtype, k, cm):
             # (copies reading a range several times keep their own table)
             if L[i][4] <= 64 << 20 and not (L[i][1] == 1 and d["table"] and not d["affinity"]):
                 assert d["affinity"], (i, L[i], d)
-            if L[i][4] > 64 << 20 and d["split"] == 1:
+            if 64 << 20 < L[i][4] < 512 << 20 and d["split"] == 1:
                 assert not d["affinity"], (i, L[i], d)
         assert (k, cm) in split, split
         names = p.launch_kernels()
@@ -647,3 +647,23 @@ def test_launch_kernels_by_form():
     with arplan.Plan(8, 1 << 12, "f32", "rhd") as p:
         with pytest.raises(arplan.ArError):
             arplan.ar_plan_launch_kernel(p.handle, len(p.launches()))
+
+
+def test_large_launches_placed_by_position():
+    # RHD as written at full size: its halving folds (2 sources) and doubling
+    # copies (each range read once) move 512 MiB or more and are placed by
+    # position; the 16-source fold of co-located PS and the copies after it,
+    # which read each range 15 times, are not
+    with arplan.Plan(8, 1 << 26, "f32", "rhd") as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        d = [_launch_desc(p.handle, i) for i in range(len(p.launches()))]
+        assert [x["affinity"] for x in d] == [1] * 6, d
+        for vecok in (1, 0):
+            st, msg = _check_tiling(p.handle, vecok)
+            assert st == arplan.AR_OK, msg
+    with arplan.Plan(16, 1 << 24, "f32", "cps") as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        d = [_launch_desc(p.handle, i) for i in range(len(p.launches()))]
+        assert [x["affinity"] for x in d] == [0, 0], d
