@@ -210,7 +210,8 @@ AR_EXPORT ar_status ar_debug_check_tiling(ar_plan* plan, int32_t vecok,
             if (L.nunits <= 0) return bad("launch without work units");
             const int64_t blocks = (L.nunits + L.wpb - 1) / L.wpb;
             if (blocks > kMaxBlocks) return bad("grid too large");
-            if (L.wpb != kcfg(L.kern_k).WPB) return bad("block size differs from the kernel's");
+            if (L.wpb != (L.dsplit > 1 ? kSplitWaves : kcfg(L.kern_k).WPB))
+                return bad("block size differs from the kernel's");
             if (L.rt_group < 1 || L.rt_group > kRtGroup) return bad("source group out of range");
             if (L.tile_elems % (64 * VEC) != 0) return bad("tile not a multiple of a wave vector");
             if (L.dsplit < 1 || (L.dsplit > 1 && (L.dsplit != L.wpb || L.nunits % L.dsplit)))

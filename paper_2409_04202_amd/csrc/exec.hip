@@ -246,16 +246,16 @@ static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
                       int dsplit) {
     const dim3 block(64 * kcfg(K).WPB);
     if (dsplit > 1 && vecok) {  // a workgroup per table entry
+        // the waves of a workgroup all read the tile's sources: cached loads
+        // (with nontemporal ones each wave fetched them from memory again)
         const int64_t ntiles = nunits / dsplit;
-        const dim3 grid(static_cast<uint32_t>(ntiles));
-#define AR_SPLIT(C)                                                                      \
-    hipLaunchKernelGGL((split_kernel<DT, K, C>), grid, block, 0, st, recs, stride, tiles, \
-                       ntiles, te, rtg)
-        if (cm == 0) AR_SPLIT(0);
-        else if (cm == 1) AR_SPLIT(1);
-        else if (cm == 2) AR_SPLIT(2);
-        else AR_SPLIT(3);
-#undef AR_SPLIT
+        const dim3 grid(static_cast<uint32_t>(ntiles)), sblock(64 * kSplitWaves);
+        if (cm & 2)
+            hipLaunchKernelGGL((split_kernel<DT, K, 2>), grid, sblock, 0, st, recs, stride, tiles,
+                               ntiles, te, rtg);
+        else
+            hipLaunchKernelGGL((split_kernel<DT, K, 0>), grid, sblock, 0, st, recs, stride, tiles,
+                               ntiles, te, rtg);
         return;
     }
     if (dsplit > 1) {  // unaligned buffers: one wave per table entry

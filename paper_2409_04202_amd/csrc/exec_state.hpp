@@ -125,9 +125,17 @@ constexpr int64_t kNumXCDs = 8;         // compute dies, each with its own L2
 constexpr int64_t kXcdMaxTiles = 64;
 
 // A launch of fewer than kMinUnits wave tiles whose steps store to at least
-// kSplitMinDst destinations is split (dsplit = wavefronts per block, see
-// split_tile).
+// kSplitMinDst destinations is split (a workgroup of kSplitWaves per tile,
+// see split_tile) when it moves less than kNtBytes or stores to at least
+// kSplitWideDst destinations per source.  Measured on MI355X against the
+// same launches unsplit (both placed by position): under 64 MiB every
+// split launch was faster (the bf16 tree (8, 8, 8)'s level-2 reduce 13.8 ->
+// 12.2 us, Ring n = 64's last halving step at 2^16 fp32 22.1 -> 9.3 us,
+// 16-source folds 12.0 -> 10.5 us); above, Ring n = 64 at 2^20 (32
+// destinations per source) 59.6 -> 49.6 us, but the 8-source folds into 64
+// buffers of the bf16 trees at 2^20 ran 28-30 us unsplit against 32-34.
 constexpr int32_t kSplitMinDst = 16;
+constexpr int32_t kSplitWideDst = 16;
 // Launches moving at most kAffinityMaxBytes, and split launches, place their
 // tiles on XCDs by element position (affinity_tiles in schedule.cpp, xcd_of
 // below), so that what one such launch writes is read by the next on the

@@ -516,8 +516,10 @@ __device__ __forceinline__ void fold_vectors_rt(void* const* __restrict__ srcp, 
 // the launch before (the host places tiles so): the bf16 tree (8, 8, 8)'s
 // level-2 reduce into 64 buffers takes 12.5 us so, 26 us split with tiles on
 // other XCDs, 20 us unsplit.
+// kSplitWaves: wavefronts per workgroup (and tile) of a split launch.
 // split_share: part `part` of `parts` gets items [a, b) of n, contiguous,
 // the shares differing by at most one.  Shared with the host-side check.
+constexpr int kSplitWaves = 4;
 __host__ __device__ __forceinline__ void split_share(int n, int part, int parts, int& a, int& b) {
     const int q = n / parts, r = n % parts;
     a = part * q + (part < r ? part : r);
@@ -635,18 +637,19 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
 
 // Split launch (see split_tile): workgroup b runs wave tile b of the
 // launch's tile table (tiles[b] = (step, tile in step), or (-1, 0) padding),
-// its WPB waves each storing to a share of the destinations.  Buffers are
-// 16-byte aligned (a split launch on unaligned buffers runs phase_kernel over
-// the same table instead).  CM: cache mode of the vector loads and stores.
+// its kSplitWaves waves each storing to a share of the destinations.
+// Buffers are 16-byte aligned (a split launch on unaligned buffers runs
+// phase_kernel over the same table instead).  CM: cache mode of the vector
+// stores (bit 1); the loads are cached, since every wave of the workgroup
+// reads the sources.
 // A kernel of its own, so that phase_kernel's code stays as it was: with
 // the split path inside it, the compiler scheduled the fold loop's loads
 // and stores differently and the 3 GiB two-source fold ran 3 % slower.
 template <int DT, int K, int CM>
-__global__ __launch_bounds__(64 * kcfg(K).WPB) void split_kernel(
+__global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(
     const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
     int64_t ntiles, int64_t tile_elems, int rt_group) {
     constexpr int VEC = Elem<DT>::VEC;
-    constexpr int WPB = kcfg(K).WPB;
     const int lane = int(threadIdx.x) & 63;
     const int part = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
     const int64_t tile = blockIdx.x;
@@ -661,7 +664,8 @@ __global__ __launch_bounds__(64 * kcfg(K).WPB) void split_kernel(
     void* const* sp = reinterpret_cast<void* const*>(rec + kRecHead);
     const TileSpan ts = tile_span(st.begin, st.end, t, tile_elems, VEC, true);
     if (ts.lo >= ts.hi) return;
-    split_tile<DT, K, CM>(sp, k, sp + k, st.ndst, st.nfree, ts, part, WPB, lane, rt_group);
+    split_tile<DT, K, CM>(sp, k, sp + k, st.ndst, st.nfree, ts, part, kSplitWaves, lane,
+                          rt_group);
 }
 
 // ------------------------------------------------------------------------

@@ -214,7 +214,10 @@ static void build_launches(const Plan& p, ExecState& ex) {
             int64_t used = 0;
             for (int64_t sp : spans) used += (sp + te - 1) / te;
             // few tiles storing to many destinations: a workgroup per tile
-            L.dsplit = maxdst >= kSplitMinDst && used < kMinUnits ? L.wpb : 1;
+            L.dsplit = 1;
+            if (maxdst >= kSplitMinDst && used < kMinUnits &&
+                (bytes < kNtBytes || maxdst >= kSplitWideDst * k))
+                L.dsplit = L.wpb = kSplitWaves;
             // copies reading the same range run next to each other (or on one
             // XCD, below): their repeated reads hit the cache
             L.hbm = bytes;

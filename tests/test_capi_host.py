@@ -596,15 +596,27 @@ def test_runtime_source_count_groups():
 # Split launches (a workgroup per tile, each wave storing to a share of the
 # destinations) in the shapes the GPU parity tests run: the 16-source fold
 # whose destinations are all its sources, the runtime-source-count fold, the
-# 8- and 2-source folds storing to 64 or 512 buffers, and one with
-# nontemporal loads.  (fuse, slice) = (1, 0): phase launches.
+# 8-, 4- and 2-source folds storing to 64 or 512 buffers, and large ones
+# with nontemporal stores.  (fuse, slice) = (1, 0): phase launches.
 SPLIT_CASES = [
     ("cps", 16, (1 << 14) + 3, None, "f32", 16, 0), ("cps", 32, 32 * 1000 + 17, None, "bf16", 0, 0),
     ("tree", 512, 1 << 15, (8, 8, 8), "bf16", 8, 0), ("tree", 512, 1 << 18, (8, 8, 8), "bf16", 8, 0),
-    ("tree", 512, 1 << 20, (8, 8, 8), "bf16", 8, 1), ("tree", 64, 4096 + 64 * 5, (8, 8), "f32", 8, 0),
+    ("tree", 64, 4096 + 64 * 5, (8, 8), "f32", 8, 0),
     ("ring", 64, 64 * 1000, None, "f32", 2, 0), ("ring", 64, 1 << 20, None, "f32", 2, 3),
-    ("tree", 64, 65553, (16, 4), "f32", 4, 0), ("tree", 256, 65553, (16, 16), "f32", 16, 3),
-    ("cps", 17, 1 << 20, None, "f32", 0, 3), ("tree", 96, 1 << 20, (3, 32), "f32", 0, 1)]
+    ("tree", 64, 65553, (16, 4), "f32", 4, 0), ("tree", 256, 65553, (16, 16), "f32", 16, 3)]
+# Launches of 64 MiB or more storing to fewer than 16 destinations per
+# source stay one wave per tile (split, they were slower).
+UNSPLIT_CASES = [("tree", 512, 1 << 20, (8, 8, 8), "bf16"), ("cps", 17, 1 << 20, None, "f32"),
+                 ("tree", 96, 1 << 20, (3, 32), "f32"), ("tree", 64, 1 << 20, (8, 8), "bf16")]
+
+
+@pytest.mark.parametrize("kind,n,N,fan,dtype", UNSPLIT_CASES)
+def test_large_narrow_launches_not_split(kind, n, N, fan, dtype):
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        L = p.launches()
+        assert any(x[2] >= 16 for x in L), L
+        assert all(_launch_desc(p.handle, i)["split"] == 1 for i in range(len(L)))
 
 
 @pytest.mark.parametrize("kind,n,N,fan,dtype,k,cm", SPLIT_CASES)

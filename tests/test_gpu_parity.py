@@ -789,9 +789,10 @@ def test_paper_asymmetric_topologies_scaled(name):
 def test_many_destination_phase_launches(kind, n, N, fan, dtype):
     # phase launches whose steps store to 16 or more buffers, some of them
     # the step's own sources (the reduce-then-broadcast rewrite): split
-    # launches, a workgroup per tile (the shapes tests/test_capi_host.py
-    # checks for them): 2, 4, 8, 16 sources and a runtime source count, with
-    # cached and nontemporal loads and stores
+    # launches, a workgroup per tile, with 2, 4, 8, 16 sources and a runtime
+    # source count, cached and nontemporal stores, and at 2^20 elements
+    # large launches that stay one wave per tile (tests/test_capi_host.py
+    # checks which is which)
     dist = "int1000" if dtype == "i32" else "uniform"
     got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=N % 101, slice_=0)
     if dtype == "bf16":
