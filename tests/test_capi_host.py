@@ -679,3 +679,28 @@ def test_large_launches_placed_by_position():
         p.set_option(arplan.AR_OPT_SLICE, 0)
         d = [_launch_desc(p.handle, i) for i in range(len(p.launches()))]
         assert [x["affinity"] for x in d] == [0, 0], d
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_many_destination_plans_split(seed):
+    # ragged blocks each reduced and copied to 16+ buffers (some of them the
+    # reduce's sources): the executor's steps store to 17+ buffers, the
+    # launch runs split, and the tiling check accepts it with aligned and
+    # unaligned buffers
+    from plan_gen import many_destination_plan
+    rng = np.random.default_rng(7100 + seed)
+    n = int(rng.integers(17, 41))
+    N = int(rng.integers(1000, 200000))
+    phases = many_destination_plan(rng, n, N)
+    flat = [(q, op, d, s_, b, e) for q, ph in enumerate(phases) for (op, d, s_, b, e) in ph]
+    h = arplan.ar_plan_create_custom(n, N, ("f32", "bf16", "i32")[seed % 3], flat)
+    try:
+        arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, 0)
+        L = [arplan.ar_plan_launch_info(h, i) for i in range(arplan.ar_plan_num_launches(h))]
+        kernels = [arplan.ar_plan_launch_kernel(h, i) for i in range(len(L))]
+        assert "split_kernel" in kernels, (L, kernels)
+        for vecok in (1, 0):
+            st, msg = _check_tiling(h, vecok)
+            assert st == arplan.AR_OK, msg
+    finally:
+        arplan.ar_plan_destroy(h)

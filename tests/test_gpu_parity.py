@@ -487,6 +487,39 @@ def test_random_custom_plans(seed):
                 assert np.array_equal(got[q], ref[q]), (seed, fuse, sl, pad, q)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_many_destination_plans(seed):
+    # random plans whose executed steps store to 17+ buffers, some of them
+    # their own sources, over ragged blocks: split launches (phase launches
+    # and the default form, aligned and unaligned buffers), bit-exact vs the
+    # oracle run on the plan as written
+    from plan_gen import many_destination_plan
+    from oracle.plans import Plan as OPlan, Step as OStep
+    rng = np.random.default_rng(7100 + seed)
+    n = int(rng.integers(17, 41))
+    N = int(rng.integers(1000, 200000))
+    phases = many_destination_plan(rng, n, N)
+    flat = [(q, op, d, s, b, e) for q, ph in enumerate(phases) for (op, d, s, b, e) in ph]
+    ref_plan = OPlan("custom", n, N, [[OStep(*st) for st in ph] for ph in phases])
+    dtype = ("f32", "bf16", "i32")[seed % 3]
+    xs0 = workloads.draw(n, N, dtype, "int1000" if dtype == "i32" else "uniform", seed)
+    ref = oracle.execute(ref_plan, [x.copy() for x in xs0], dtype)
+    say("case: random many-destination plan seed=%d n=%d N=%d %s" % (seed, n, N, dtype))
+    for sl in (0, 2):
+        for pad in (0, 1):
+            ts = to_device(xs0, dtype, pad)
+            h = arplan.ar_plan_create_custom(n, N, dtype, flat)
+            try:
+                arplan.ar_plan_set_option(h, arplan.AR_OPT_SLICE, sl)
+                arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+                torch.cuda.synchronize()
+            finally:
+                arplan.ar_plan_destroy(h)
+            got = to_host(ts, dtype)
+            for q in range(n):
+                assert np.array_equal(got[q], ref[q]), (seed, sl, pad, q)
+
+
 @pytest.mark.parametrize("seed", range(16))
 def test_random_aligned_custom_plans_resident(seed):
     # random hazard-free plans whose boundaries are whole 16-byte vectors, so
