@@ -656,6 +656,10 @@ def test_launch_kernels_by_form():
         c = workloads.CONFIGS[name]
         with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
             assert p.launch_kernels() == kernels, (name, p.launch_kernels())
+    # n > 64 with AR_OPT_SLICE = 1: one streamed resident launch
+    with arplan.Plan(512, 1 << 14, "bf16", "tree", (8, 8, 8)) as p:
+        p.set_option(arplan.AR_OPT_SLICE, 1)
+        assert p.launch_kernels() == ["stream_kernel"], p.launch_kernels()
     with arplan.Plan(8, 1 << 12, "f32", "rhd") as p:
         with pytest.raises(arplan.ArError):
             arplan.ar_plan_launch_kernel(p.handle, len(p.launches()))
