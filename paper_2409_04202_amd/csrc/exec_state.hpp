@@ -44,6 +44,12 @@ constexpr int64_t kMaxBlocks = int64_t(1) << 24;
 // 256 MiB last-level cache until then.
 constexpr int64_t kNtBytes = int64_t(64) << 20;
 constexpr int64_t kKeepBytes = int64_t(256) << 20;
+// A fold launch keeps its stores cached up to kKeepBytesFold: RHD's second
+// halving launch (512 MiB written, read by the third) ran 271 -> 254 us with
+// cached stores, and the third 126 -> 124 us, part of its reads hitting the
+// cache; copy launches of that size ran slower with cached stores (the
+// 1 GiB doubling copy 164 -> 167 us).
+constexpr int64_t kKeepBytesFold = int64_t(512) << 20;
 // The step rewrites (multicast, reduce-then-broadcast) pay off where they
 // remove a launch from a short phase, add at most one extra destination, or
 // take over copies that read every range once (their reads are saved; a

@@ -207,7 +207,8 @@ static void build_launches(const Plan& p, ExecState& ex) {
             L.cm = 0;
             if (bytes >= kNtBytes) {
                 if (!reuse) L.cm |= 1;
-                if (written > kKeepBytes || !next_reads_output) L.cm |= 2;
+                const int64_t keep = k >= 2 ? kKeepBytesFold : kKeepBytes;
+                if (written > keep || !next_reads_output) L.cm |= 2;
             }
             L.tile_elems = te;
             L.tiles_per_step = (maxspan + te - 1) / te;

@@ -547,11 +547,11 @@ def _launch_desc(handle, stage):
 
 def test_full_size_forms_use_the_nontemporal_kernels():
     # The benchmark's as-written RHD plan at full size (n = 8, 2^26 fp32):
-    # the first two halving launches write more than the last-level cache
-    # holds (nontemporal loads and stores), the third writes 256 MiB that
-    # the first doubling phase reads (nontemporal loads, cached stores).
-    # The full-size GPU parity test runs this same plan, so these kernel
-    # instances are covered there.
+    # the first halving launch writes 1 GiB (nontemporal loads and stores),
+    # the second 512 MiB that the third reads and the third 256 MiB that the
+    # first doubling phase reads (fold launches keep up to 512 MiB cached:
+    # nontemporal loads, cached stores).  The full-size GPU parity test runs
+    # this same plan, so these kernel instances are covered there.
     with arplan.Plan(8, 1 << 26, "f32", "rhd") as p:
         p.set_option(arplan.AR_OPT_FUSE, 0)
         p.set_option(arplan.AR_OPT_SLICE, 0)
@@ -559,11 +559,12 @@ def test_full_size_forms_use_the_nontemporal_kernels():
         assert [(x[0], x[1]) for x in L] == [(0, 2), (1, 2), (2, 2), (3, 1), (4, 1), (5, 1)]
         d = [_launch_desc(p.handle, i) for i in range(3)]
         assert [x["k"] for x in d] == [2, 2, 2]
-        assert [x["cm"] for x in d] == [3, 3, 1]
+        assert [x["cm"] for x in d] == [3, 1, 1]
         # with the rewrites, the last halving launch stores to all 8 buffers
+        # (2 GiB, nontemporal)
         p.set_option(arplan.AR_OPT_FUSE, 1)
         d = [_launch_desc(p.handle, i) for i in range(len(p.launches()))]
-        assert [x["cm"] for x in d] == [3, 3, 3]
+        assert [x["cm"] for x in d] == [3, 1, 3]
     # co-located PS (16-source fold, 1088 MiB) and the tree (8, 8) level-0
     # reduce (8 sources, 1152 MiB) as written: nontemporal loads
     with arplan.Plan(16, 1 << 24, "f32", "cps") as p:
