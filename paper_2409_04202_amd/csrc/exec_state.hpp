@@ -50,6 +50,12 @@ constexpr int64_t kKeepBytes = int64_t(256) << 20;
 // cache; copy launches of that size ran slower with cached stores (the
 // 1 GiB doubling copy 164 -> 167 us).
 constexpr int64_t kKeepBytesFold = int64_t(512) << 20;
+// A fold launch whose previous phase kept all its stores cached and wrote
+// at most kWarmBytes loads through the cache even when large: the two-level
+// tree's level-1 fold (8 sources, 4 MiB f32 each, reading the 128 MiB that
+// level 0 wrote) took the whole as-written plan 0.403 -> 0.395 ms; copies
+// under the same rule ran slower (RHD's first doubling copy).
+constexpr int64_t kWarmBytes = int64_t(256) << 20;
 // The step rewrites (multicast, reduce-then-broadcast) pay off where they
 // remove a launch from a short phase, add at most one extra destination, or
 // take over copies that read every range once (their reads are saved; a

@@ -108,9 +108,15 @@ static void affinity_tiles(const XPhase& xp, const std::vector<size_t>& idx, siz
 static void build_launches(const Plan& p, ExecState& ex) {
     const int64_t VEC = 16 / p.esize;
     ex.dev_of.assign(ex.phases.size(), {});
+    // the previous executed phase: every launch kept its stores cached, and
+    // the bytes it wrote
+    bool prev_kept = false;
+    int64_t prev_written = 0;
     for (size_t q = 0; q < ex.phases.size(); ++q) {
         const XPhase& xp = ex.phases[q];
         ex.dev_of[q].assign(xp.steps.size(), -1);
+        bool all_kept = true;
+        int64_t phase_written = 0;
         std::unique_ptr<Touches> next_reads;
         if (q + 1 < ex.phases.size())
             next_reads.reset(new Touches(ex.phases[q + 1], p.n, true, false));
@@ -206,10 +212,15 @@ static void build_launches(const Plan& p, ExecState& ex) {
             const bool reuse = std::adjacent_find(ranges.begin(), ranges.end()) != ranges.end();
             L.cm = 0;
             if (bytes >= kNtBytes) {
-                if (!reuse) L.cm |= 1;
+                // a fold reading what the previous phase left in the cache
+                // loads through it
+                const bool warm = k >= 2 && prev_kept && prev_written <= kWarmBytes;
+                if (!reuse && !warm) L.cm |= 1;
                 const int64_t keep = k >= 2 ? kKeepBytesFold : kKeepBytes;
                 if (written > keep || !next_reads_output) L.cm |= 2;
             }
+            all_kept = all_kept && !(L.cm & 2);
+            phase_written += written;
             L.tile_elems = te;
             L.tiles_per_step = (maxspan + te - 1) / te;
             int64_t used = 0;
@@ -254,6 +265,8 @@ static void build_launches(const Plan& p, ExecState& ex) {
             ex.launches.push_back(L);
             g0 = g1;
         }
+        prev_kept = all_kept;
+        prev_written = phase_written;
     }
 }
 
