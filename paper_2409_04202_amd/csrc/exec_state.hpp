@@ -29,6 +29,15 @@ constexpr int kCache = 4;               // buffer sets whose step records are ke
 // are unchanged).
 constexpr int64_t kMinUnits = 2048;
 constexpr int64_t kMinUnitsReduce = 16384;
+// A launch of at least kFineTileMinBytes with fewer than kMinUnits tiles at
+// the smallest full-pass tile (64 lanes x U vectors per source) halves its
+// tile further, down to one vector per lane, until it has kMinUnits (not
+// for copies reading a range several times: their XCD tables lost with
+// smaller tiles, the tree (8, 4) at 1 MiB per processor +50 %).  Measured
+// as written: Ring n = 64 at 1M elements 0.77 -> 0.55 ms (f32) and
+// 0.60 -> 0.44 ms (bf16), Ring n = 8 and RHD n = 8 at 1 MiB per processor
+// -29 % and -27 %.
+constexpr int64_t kFineTileMinBytes = int64_t(2) << 20;
 // A runtime-source-count launch (a fan-in without an unrolled kernel)
 // moving less than kRtGroupMaxBytes keeps the loads of kRtGroup sources in
 // flight together; larger ones load one source at a time (measured: k = 24

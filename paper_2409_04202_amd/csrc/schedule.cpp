@@ -205,11 +205,16 @@ static void build_launches(const Plan& p, ExecState& ex) {
                 return L.count * ((maxspan + t - 1) / t);
             };
             const int64_t min_units = k >= 2 ? kMinUnitsReduce : kMinUnits;
-            while (te > tmin && units_for(te) < min_units) te /= 2;
-            while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
-            L.wpb = cfg.WPB;
             std::sort(ranges.begin(), ranges.end());
             const bool reuse = std::adjacent_find(ranges.begin(), ranges.end()) != ranges.end();
+            while (te > tmin && units_for(te) < min_units) te /= 2;
+            // still too few tiles: below the kernel's full pass, down to one
+            // vector per lane (copies reading a range several times keep
+            // their XCD tables' tile size; many-destination steps split)
+            if (bytes >= kFineTileMinBytes && !(k == 1 && reuse) && maxdst < kSplitMinDst)
+                while (te > 64 * VEC && units_for(te) < kMinUnits) te /= 2;
+            while ((units_for(te) + cfg.WPB - 1) / cfg.WPB > kMaxBlocks) te *= 2;
+            L.wpb = cfg.WPB;
             L.cm = 0;
             if (bytes >= kNtBytes) {
                 // a fold reading what the previous phase left in the cache

@@ -669,6 +669,41 @@ def test_launch_kernels_by_form():
             arplan.ar_plan_launch_kernel(p.handle, len(p.launches()))
 
 
+# 16-byte vectors per lane and source in one pass of each kernel (kcfg)
+_PASS_U = {1: 16, 2: 8, 3: 4, 4: 4, 8: 2, 16: 1, 0: 4}
+
+
+@pytest.mark.parametrize("kind,n,N,fan,dtype", [
+    ("ring", 64, 1 << 20, None, "f32"), ("ring", 64, 1 << 20, None, "bf16"),
+    ("ring", 8, 1 << 18, None, "f32"), ("rhd", 8, 1 << 18, None, "f32"),
+    ("rhd", 5, (1 << 18) + 3, None, "i32"), ("cps", 6, 1 << 20, None, "f32"),
+    ("tree", 32, 1 << 18, (8, 4), "f32")])
+def test_fine_tiles_for_launches_with_few_tiles(kind, n, N, fan, dtype):
+    # As written, launches of 2 MiB or more with fewer than 2048 tiles of a
+    # full kernel pass take smaller tiles, down to one vector per lane,
+    # until they have 2048; copies that read a range several times keep
+    # full-pass tiles (their XCD tables)
+    vec = 16 // (2 if dtype == "bf16" else 4)
+    with arplan.Plan(n, N, dtype, kind, fan) as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        fine = 0
+        for i, x in enumerate(p.launches()):
+            d = _launch_desc(p.handle, i)
+            full = 64 * _PASS_U[d["k"]] * vec
+            if d["k"] == 1 and kind in ("cps", "tree"):
+                assert d["tile"] >= full, (i, x, d)  # AllGather copies re-read ranges
+            elif x[4] >= 2 << 20:
+                assert d["tile"] == full or (d["tile"] < full and d["tile"] >= 64 * vec), (i, x, d)
+                if d["tile"] < full:
+                    fine += 1
+                    assert d["tiles"] >= 2048 or d["tile"] == 64 * vec, (i, x, d)
+        assert fine >= 1
+        for vecok in (1, 0):
+            st, msg = _check_tiling(p.handle, vecok)
+            assert st == arplan.AR_OK, msg
+
+
 def test_large_launches_placed_by_position():
     # RHD as written at full size: its halving folds (2 sources) and doubling
     # copies (each range read once) move 512 MiB or more and are placed by
