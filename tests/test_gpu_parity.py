@@ -837,12 +837,15 @@ def test_many_destination_phase_launches(kind, n, N, fan, dtype):
     ("ring", 8, 1 << 18, None, "f32"), ("rhd", 8, 1 << 18, None, "f32"),
     ("rhd", 5, (1 << 18) + 3, None, "i32"), ("cps", 6, 1 << 20, None, "f32"),
     ("tree", 32, 1 << 18, (8, 4), "f32"), ("ring", 16, (1 << 18) + 5, None, "bf16")])
-def test_fine_tile_launches(kind, n, N, fan, dtype):
+@pytest.mark.parametrize("pad", [0, 1])
+def test_fine_tile_launches(kind, n, N, fan, dtype, pad):
     # the plan as written, its launches of few tiles cut below a full kernel
     # pass (down to one vector per lane; tests/test_capi_host.py checks the
-    # tiles), every element against the oracle
+    # tiles), every element against the oracle; with buffers off 16-byte
+    # alignment (pad) the same tiles run element by element
     dist = "int1000" if dtype == "i32" else "uniform"
-    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=N % 97, fuse=0, slice_=0)
+    got, xs0 = _full_compare(kind, n, N, dtype, fan, dist, seed=N % 97, pad=pad,
+                             fuse=0, slice_=0)
     if dtype == "bf16":
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
