@@ -87,14 +87,18 @@ def test_repeats_new_buffers_and_alternating_plans():
         _same(ref, got, "f32", "option change")
 
 
-@pytest.mark.parametrize("kind,n,N,dtype,fan,slice_", [
-    ("tree", 512, 1 << 14, "bf16", (8, 8, 8), 1),     # one streamed launch
-    ("ring", 64, 64 * 1000, "f32", None, 1),          # one resident launch
-    ("tree", 64, 1 << 16, "f32", (8, 8), 0)])         # phase launches only
-def test_every_launch_kind(kind, n, N, dtype, fan, slice_):
+@pytest.mark.parametrize("kind,n,N,dtype,fan,slice_,kernel", [
+    ("tree", 512, 1 << 14, "bf16", (8, 8, 8), 1, "stream_kernel"),
+    ("ring", 64, 64 * 1000, "f32", None, 1, "resident_kernel"),
+    ("tree", 64, 1 << 16, "f32", (8, 8), 0, "phase_kernel"),
+    ("tree", 512, 1 << 15, "bf16", (8, 8, 8), 0, "split_kernel"),
+    ("tree", 64, 1 << 16, "f32", (8, 8), 1, "sliced_kernel")])
+def test_every_launch_kind(kind, n, N, dtype, fan, slice_, kernel):
     xs0, ref, got = _case(kind, n, N, dtype, fan, seed=n)
     with arplan.Plan(n, N, dtype, kind, fan) as p:
         p.set_option(arplan.AR_OPT_SLICE, slice_)
+        p.set_option(arplan.AR_OPT_RESIDENT, 0 if kernel == "sliced_kernel" else 1)
+        assert kernel in p.launch_kernels(), p.launch_kernels()
         _run_both(p, ref, got)
     _same(ref, got, dtype, (kind, "slice", slice_))
 
