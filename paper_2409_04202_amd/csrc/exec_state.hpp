@@ -84,36 +84,54 @@ constexpr int64_t kFuseBytes = int64_t(256) << 20;
 // on in LDS and takes phases of any size.  The runs are chosen by dynamic programming over the phases
 // with a cost model fitted to MI355X measurements (back-to-back launches, no
 // events between them):
-//  * a phase launch costs kLaunchNs plus its HBM traffic at kBytesPerNs, at
-//    least kKernelMinNs (one dependent load and store through memory);
+//  * bytes move at kBytesPerNs, or at kCachedBytesPerNs when the plan's whole
+//    footprint n * N * e fits the kCacheBytes last-level cache;
+//  * a phase launch costs kPhaseLaunchNs plus its HBM traffic, at least
+//    kKernelMinNs per dependent round of loads (one dependent load and store
+//    through memory; a runtime-source-count fold loads its k sources in
+//    ceil(k / rt_group) rounds);
 //  * a sliced launch costs kLaunchNs plus, per phase, the largest of its
 //    dependent chain, its read time and its write time.  The chain is the
 //    most steps covering one element position, which a wavefront runs one
 //    after the other, at kStepNs + k * kStepNsPerSrc{F32,BF16} +
 //    d * kStepNsPerDst each (k, d = the phase's largest source and
-//    destination counts); reads and writes go at kBytesPerNs, the reads
-//    stretched by kMinSliceWaves / waves when the slice has fewer wave tiles
-//    than that (too few loads in flight to reach full bandwidth).
-constexpr double kLaunchNs = 3000.0;
-constexpr double kKernelMinNs = 3000.0;
+//    destination counts); the reads are stretched by kMinSliceWaves / waves
+//    when the slice has fewer wave tiles than that (too few loads in flight
+//    to reach full bandwidth).
+// The constants of these forms and of the resident form (below) were fitted
+// together, in log error, to 151 plans (Ring, RHD, co-located PS, 2- and
+// 3-level trees, n = 8 to 512, 4K to 1M elements, fp32 and bf16) each timed
+// as phase launches, as one plain sliced launch and (n <= 64) as one
+// resident launch: the prediction error of the phase launches 59 -> 11 %
+// mean, the form the model ranks first within 5 % of the fastest in 141 of
+// the 151 plans (from 114).  kBytesPerNs comes from the HBM-bound
+// workloads, whose footprints exceed the cache.  Terms the fit put at zero
+// (per-destination step costs, the resident per-row cost, sharing between
+// workgroups) are kept, at 0.
+constexpr double kLaunchNs = 2200.0;
+constexpr double kPhaseLaunchNs = 1550.0;
+constexpr double kKernelMinNs = 1750.0;
 constexpr double kBytesPerNs = 5500.0;
-constexpr double kStepNs = 350.0;
-constexpr double kStepNsPerSrcF32 = 120.0;
-constexpr double kStepNsPerSrcBF16 = 190.0;
-constexpr double kStepNsPerDst = 15.0;
-constexpr double kMinSliceWaves = 256.0;
+constexpr double kCachedBytesPerNs = 6450.0;
+constexpr int64_t kCacheBytes = int64_t(256) << 20;
+constexpr double kStepNs = 265.0;
+constexpr double kStepNsPerSrcF32 = 205.0;
+constexpr double kStepNsPerSrcBF16 = 300.0;
+constexpr double kStepNsPerDst = 0.0;
+constexpr double kMinSliceWaves = 400.0;
 constexpr int64_t kSliceMaxBytes = int64_t(512) << 20;
 // A sliced run of one phase replacing that phase's only launch is taken only
 // when predicted to cost at most this fraction of the launch: for one phase
-// the estimate above is optimistic (measured: co-located PS n = 16 at 2^18
-// fp32, predicted 0.66 of its launch, ran 1.4 times slower; at 2^20,
-// predicted 0.56, ran 0.82 of it).
-constexpr double kSingleRunGain = 0.6;
+// the estimate above is optimistic (co-located PS n = 16 at 2^18 fp32 and at
+// 2^20 bf16 run slower sliced than predicted); 0.75 picked best over the
+// co-located PS plans of the fit (n = 16 to 64, sliced where a 32- or
+// 64-source fold into as many buffers runs as one launch at 2^18).
+constexpr double kSingleRunGain = 0.75;
 // A sliced run may instead run resident (resident_kernel, AR_OPT_RESIDENT):
 // a workgroup of W waves (res_waves in programs.cpp) per 64 vectors of a
 // segment, the plan's n <= kResMaxN buffers in LDS rows of 1 KiB.  Its
 // predicted time is kLaunchNs plus the larger of its HBM traffic (each row
-// read and written once) at kBytesPerNs and its workgroups' time, plus
+// read and written once) and its workgroups' time, plus
 // kResOverlap times the smaller (with few workgroups per compute unit the
 // two overlap only in part).  A workgroup takes kResRowNs / W per row
 // loaded or stored, and per step of its chain kResChainNs for a 2-source,
@@ -126,16 +144,22 @@ constexpr double kSingleRunGain = 0.6;
 // wave) or 8 (four waves) per compute unit at a time, or fewer when their
 // LDS rows do not fit (kLdsBytesPerCU), and those sharing a unit (when there
 // are more tiles than units) slow each other by kResShare per extra one.
-// Fitted to MI355X measurements of chains of one-step phases, Ring and tree
-// plans.
-constexpr double kResRowNs = 60.0;
-constexpr double kResFastNs = 210.0;
-constexpr double kResChainNs = 45.0;
-constexpr double kResStepNs = 150.0;
-constexpr double kResStepNsPerSrc = 40.0;
-constexpr double kResStepNsPerDst = 27.0;
-constexpr double kResShare = 0.1;
-constexpr double kResOverlap = 0.5;
+constexpr double kResRowNs = 0.0;
+constexpr double kResFastNs = 275.0;
+constexpr double kResChainNs = 77.0;
+constexpr double kResStepNs = 240.0;
+constexpr double kResStepNsPerSrc = 50.0;
+constexpr double kResStepNsPerDst = 0.0;
+constexpr double kResShare = 0.0;
+constexpr double kResOverlap = 0.45;
+// A resident run that does not start at the first executed phase costs
+// kResAfterLaunchNs more: measured, its time hardly shrinks with the phases
+// left to the launches before it (RHD n = 32 at 2^16 fp32: the first phase
+// as a launch, then the rest resident, 15.2 us; all of it resident 11.1 us),
+// while the model's chain terms would have it shrink; with fan-in 4 trees
+// over 64 buffers at 4K-16K elements the split still pays (9.9 against
+// 11.4 us).
+constexpr double kResAfterLaunchNs = 2000.0;
 constexpr int64_t kResWavesPerCU = 16;
 constexpr int64_t kLdsBytesPerCU = int64_t(160) << 10;
 constexpr int64_t kNumCUs = 256;

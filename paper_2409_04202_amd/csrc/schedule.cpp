@@ -372,6 +372,12 @@ struct PhaseCost {
     double t_launch = 0.0;
 };
 
+// Bytes per ns of the cost model: the cached rate when the plan's whole
+// footprint fits the last-level cache.
+static double byte_rate(const Plan& p) {
+    return int64_t(p.n) * p.N * p.esize <= kCacheBytes ? kCachedBytesPerNs : kBytesPerNs;
+}
+
 static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
     const int64_t VEC = 16 / p.esize;
     std::vector<PhaseCost> pc(ex.phases.size());
@@ -400,8 +406,15 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
             pc[q].cover = std::max(pc[q].cover, c);
         }
     }
-    for (const LaunchDesc& L : ex.launches)
-        pc[size_t(L.xphase)].t_launch += kLaunchNs + std::max(kKernelMinNs, double(L.hbm) / kBytesPerNs);
+    const double bpn = byte_rate(p);
+    for (const LaunchDesc& L : ex.launches) {
+        // dependent rounds of loads: a runtime-source-count fold loads its
+        // sources rt_group at a time
+        const int64_t k = ex.hsteps[size_t(L.first)].k;
+        const double rounds = L.kern_k == 0 ? double((k + L.rt_group - 1) / L.rt_group) : 1.0;
+        pc[size_t(L.xphase)].t_launch +=
+            kPhaseLaunchNs + std::max(kKernelMinNs * rounds, double(L.hbm) / bpn);
+    }
     return pc;
 }
 
@@ -419,6 +432,7 @@ struct Run {
 static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
                                     const std::vector<PhaseCost>& pc) {
     const double per_src = p.dtype == AR_BF16 ? kStepNsPerSrcBF16 : kStepNsPerSrcF32;
+    const double bpn = byte_rate(p);
     const double waves = std::max(1.0, double(p.N) * p.esize / (64.0 * kSliceU * 16.0));
     const double stretch = std::max(1.0, kMinSliceWaves / waves);
     const bool res_ok = p.resident != 0 && p.n <= kResMaxN;
@@ -454,8 +468,8 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             plain_ok = plain_ok && c.written <= kKeepBytes && c.bytes <= kSliceMaxBytes;
             if (!plain_ok && !res_ok) break;
             body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
-                              stretch * double(c.read) / kBytesPerNs,
-                              double(c.written) / kBytesPerNs});
+                              stretch * double(c.read) / bpn,
+                              double(c.written) / bpn});
             // a run is priced from its last phase down: phase a chains into
             // phase a + 1 when both have one 2-source step per position
             const bool link = c.cover == 1 && c.kmax == 2 && c.dmax == 1;
@@ -477,8 +491,9 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             if (res_ok) {
                 const double rows = 2.0 * double(__builtin_popcountll(touched));
                 const double t_waves = rounds * (kResRowNs / W * rows + chain);
-                const double t_bytes = rows * double(p.N) * p.esize / kBytesPerNs;
-                const double t_res = kLaunchNs + std::max(t_waves, t_bytes) +
+                const double t_bytes = rows * double(p.N) * p.esize / bpn;
+                const double t_res = kLaunchNs + (a > 0 ? kResAfterLaunchNs : 0.0) +
+                                     std::max(t_waves, t_bytes) +
                                      kResOverlap * std::min(t_waves, t_bytes);
                 if (t_res < t) {
                     t = t_res;

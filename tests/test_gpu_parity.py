@@ -108,6 +108,9 @@ def test_sweep_configs_bit_exact(name, slice_, resident):
 
 
 _MIXED_CANDIDATES = [
+    ("rhd", 128, 1 << 14, "f32", None), ("tree", 64, 1 << 12, "f32", (4, 4, 4)),
+    ("tree", 256, 1 << 19, "f32", (4, 8, 8)), ("tree", 64, 1 << 12, "bf16", (4, 4, 4)),
+    ("tree", 64, 1 << 14, "f32", (4, 4, 4)), ("tree", 32, 1 << 16, "bf16", (2, 4, 4)),
     ("rhd", 16, 1 << 14, "f32", None), ("rhd", 16, 1 << 16, "bf16", None),
     ("tree", 64, 1 << 18, "bf16", (4, 4, 4)), ("tree", 128, 1 << 18, "f32", (2, 8, 8)),
     ("tree", 512, 1 << 18, "f32", (8, 8, 8)), ("tree", 32, 1 << 18, "bf16", (2, 4, 4)),
