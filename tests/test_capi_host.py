@@ -747,3 +747,40 @@ def test_random_many_destination_plans_split(seed):
             assert st == arplan.AR_OK, msg
     finally:
         arplan.ar_plan_destroy(h)
+
+
+# The automatic choice (AR_OPT_SLICE = 2) on every benchmark workload: the
+# kernel of each launch.  Each is the fastest form measured on MI355X (or
+# within a few % of it); a change to the cost model that moves one of them
+# shows here first.
+BENCH_CHOICE = {
+    "ring_n4_f32": ["resident_kernel"],
+    "ring_n4_i32": ["resident_kernel"],
+    "rhd_n8_f32": ["resident_kernel"],
+    "cps_n16_f32": ["phase_kernel", "phase_kernel"],
+    "tree8x8_n64_f32": ["phase_kernel", "sliced_kernel", "phase_kernel"],
+    "tree8x8_n64_i32": ["phase_kernel", "sliced_kernel", "phase_kernel"],
+    "tree8x8x8_n512_bf16": ["phase_kernel", "phase_kernel", "split_kernel", "phase_kernel"],
+    "asy384_gentree_f32": ["phase_kernel", "sliced_kernel", "phase_kernel"],
+    "cdc384_gentree_f32": ["phase_kernel", "sliced_kernel", "phase_kernel"],
+    "sweep_ring_n64_f32_N4096": ["resident_kernel"],
+    "sweep_tree8x8_n64_f32_N4096": ["phase_kernel", "split_kernel"],
+    "sweep_ring_n64_bf16_N4096": ["resident_kernel"],
+    "sweep_tree8x8_n64_bf16_N4096": ["phase_kernel", "split_kernel"],
+    "sweep_ring_n64_f32_N65536": ["resident_kernel"],
+    "sweep_tree8x8_n64_f32_N65536": ["phase_kernel", "split_kernel"],
+    "sweep_ring_n64_bf16_N65536": ["resident_kernel"],
+    "sweep_tree8x8_n64_bf16_N65536": ["phase_kernel", "split_kernel"],
+    "sweep_ring_n64_f32_N1048576": ["resident_kernel"],
+    "sweep_tree8x8_n64_f32_N1048576": ["sliced_kernel"],
+    "sweep_ring_n64_bf16_N1048576": ["resident_kernel"],
+    "sweep_tree8x8_n64_bf16_N1048576": ["sliced_kernel"],
+}
+
+
+@pytest.mark.parametrize("name", sorted(BENCH_CHOICE))
+def test_automatic_choice_of_bench_workloads(name):
+    from paper_2409_04202_amd import workloads
+    c = workloads.CONFIGS[name]
+    with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
+        assert p.launch_kernels() == BENCH_CHOICE[name]
