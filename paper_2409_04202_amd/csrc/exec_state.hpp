@@ -155,11 +155,11 @@ constexpr double kResOverlap = 0.45;
 // A resident run that does not start at the first executed phase costs
 // kResAfterLaunchNs more: measured, its time hardly shrinks with the phases
 // left to the launches before it (RHD n = 32 at 2^16 fp32: the first phase
-// as a launch, then the rest resident, 15.2 us; all of it resident 11.1 us),
-// while the model's chain terms would have it shrink; with fan-in 4 trees
-// over 64 buffers at 4K-16K elements the split still pays (9.9 against
-// 11.4 us).
-constexpr double kResAfterLaunchNs = 2000.0;
+// as a launch, then the rest resident, 15.2 us; all of it resident 11.1 us;
+// RHD n = 48 at 2^13, two phases as launches, 16.1 against 14.0 us), while
+// the model's chain terms would have it shrink; with fan-in 4 trees over 64
+// buffers at 4K-16K elements the split still pays (9.9 against 11.4 us).
+constexpr double kResAfterLaunchNs = 3000.0;
 constexpr int64_t kResWavesPerCU = 16;
 constexpr int64_t kLdsBytesPerCU = int64_t(160) << 10;
 constexpr int64_t kNumCUs = 256;
