@@ -396,6 +396,28 @@ ar_status ar_genmodel_select(int32_t n, int64_t N, int32_t dtype, const double* 
                              int64_t cache_bytes, int32_t max_levels, int32_t* kind,
                              int32_t* num_levels, int32_t* fanin, double* seconds);
 
+/* The same terms with several cache tiers: cache_bytes[0..tiers) the tiers'
+ * sizes, strictly decreasing (say the last-level cache, then the L2 caches
+ * together), 1 <= tiers <= AR_GENMODEL_MAX_TIERS.  An access is served from
+ * the smallest tier under whose size the rule of ar_genmodel_terms classes
+ * it as cached, else from HBM.  terms has 4 + 2 * tiers entries: A, K, the
+ * reduce bytes from HBM, from tier 0, ..., from tier tiers-1, then the copy
+ * bytes the same way.  With one tier the terms are ar_genmodel_terms'.  Host
+ * only.  Errors: AR_ERR_INVALID_ARG (NULL plan or terms, a bad tier count or
+ * list), AR_ERR_OOM. */
+#define AR_GENMODEL_MAX_TIERS 4
+ar_status ar_genmodel_terms_tiered(const ar_plan* plan, int32_t tiers, const int64_t* cache_bytes,
+                                   double* terms);
+
+/* ar_genmodel_select with the tiered terms: params has 4 + 2 * tiers
+ * entries, one per term of ar_genmodel_terms_tiered.  ar_genmodel_select is
+ * this with one tier.  Errors as ar_genmodel_select's, and a bad tier count
+ * or list is AR_ERR_INVALID_ARG. */
+ar_status ar_genmodel_select_tiered(int32_t n, int64_t N, int32_t dtype, const double* params,
+                                    int32_t tiers, const int64_t* cache_bytes, int32_t max_levels,
+                                    int32_t* kind, int32_t* num_levels, int32_t* fanin,
+                                    double* seconds);
+
 /* --------------------------------------------------------------- timing */
 
 /* A timer holds up to `capacity` launch records (capacity >= 1).  Its HIP

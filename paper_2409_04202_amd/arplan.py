@@ -89,6 +89,10 @@ _sig = {
                             POINTER(c_int32), POINTER(c_int64), POINTER(c_int64)],
     "ar_plan_launch_kernel": [_P, c_int32, POINTER(c_int32)],
     "ar_genmodel_terms": [_P, c_int64, POINTER(c_double)],
+    "ar_genmodel_terms_tiered": [_P, c_int32, POINTER(c_int64), POINTER(c_double)],
+    "ar_genmodel_select_tiered": [c_int32, c_int64, c_int32, POINTER(c_double), c_int32,
+                                  POINTER(c_int64), c_int32, POINTER(c_int32), POINTER(c_int32),
+                                  POINTER(c_int32), POINTER(c_double)],
     "ar_genmodel_select": [c_int32, c_int64, c_int32, POINTER(c_double), c_int64, c_int32,
                            POINTER(c_int32), POINTER(c_int32), POINTER(c_int32),
                            POINTER(c_double)],
@@ -311,6 +315,34 @@ def ar_genmodel_terms(plan, cache_bytes):
     t = (c_double * AR_GENMODEL_TERMS)()
     _check(_lib.ar_genmodel_terms(plan, int(cache_bytes), t))
     return tuple(t)
+
+
+def ar_genmodel_terms_tiered(plan, cache_bytes):
+    """The tiered terms of a plan (cache_bytes: the tiers' sizes, largest
+    first): A, K, reduce bytes from HBM and each tier, copy bytes likewise."""
+    tiers = len(cache_bytes)
+    sizes = (c_int64 * max(1, tiers))(*[int(x) for x in cache_bytes])
+    t = (c_double * (4 + 2 * max(1, tiers)))()
+    _check(_lib.ar_genmodel_terms_tiered(plan, tiers, sizes, t))
+    return tuple(t)
+
+
+def ar_genmodel_select_tiered(n, N, dtype, params, cache_bytes, max_levels=3):
+    """(kind name, fan-in tuple or None, predicted seconds) under the tiered
+    terms (params: one per term)."""
+    tiers = len(cache_bytes)
+    if len(params) != 4 + 2 * tiers:
+        raise ValueError("%d parameters expected" % (4 + 2 * tiers))
+    sizes = (c_int64 * max(1, tiers))(*[int(x) for x in cache_bytes])
+    pa = (c_double * len(params))(*[float(x) for x in params])
+    kind, lv = c_int32(), c_int32()
+    fan = (c_int32 * max(1, int(max_levels)))()
+    sec = c_double()
+    _check(_lib.ar_genmodel_select_tiered(int(n), int(N), _dtype(dtype), pa, tiers, sizes,
+                                          int(max_levels), ctypes.byref(kind), ctypes.byref(lv),
+                                          fan, ctypes.byref(sec)))
+    name = {v: k for k, v in KINDS.items()}[kind.value]
+    return name, (tuple(fan[i] for i in range(lv.value)) if lv.value else None), sec.value
 
 
 def ar_genmodel_select(n, N, dtype, params, cache_bytes, max_levels=3):

@@ -1,8 +1,9 @@
-// GenModel on one GPU: the terms of a plan's predicted time and the plan
-// kind of smallest predicted time among the candidates (the model's use in
-// plan selection, Section 3.4 and Algorithm 2, with the terms a single GPU
-// has).  Host only; no HIP call.
+// GenModel on one GPU: the terms of a plan's predicted time, with one cache
+// or a list of cache tiers, and the plan kind of smallest predicted time
+// among the candidates (the model's use in plan selection, Section 3.4 and
+// Algorithm 2, with the terms a single GPU has).  Host only; no HIP call.
 #include <algorithm>
+#include <array>
 #include <cstring>
 #include <new>
 #include <set>
@@ -73,6 +74,27 @@ void plan_terms(const Plan& p, int64_t cache_bytes, double* t) {
     t[5] = Bc;
 }
 
+// terms[0..4 + 2 * tiers) of plan p with the cache tiers cache_bytes[0..tiers)
+// (strictly decreasing): A, K, then the reduce bytes served from HBM and
+// from each tier, then the copy bytes the same way (see
+// ar_genmodel_terms_tiered).  An access is served from the smallest tier
+// under whose size the one-cache rule classes it as cached: that rule is
+// monotone in the size, so tier i's bytes are what size i classes as cached
+// less what size i + 1 does.
+void tiered_terms(const Plan& p, int32_t tiers, const int64_t* cache_bytes, double* t) {
+    std::vector<std::array<double, AR_GENMODEL_TERMS>> per(size_t(tiers) + 1);
+    for (int32_t i = 0; i < tiers; ++i) plan_terms(p, cache_bytes[i], per[size_t(i)].data());
+    per[size_t(tiers)].fill(0.0);  // a size-0 "tier" below the last: nothing cached
+    t[0] = per[0][0];
+    t[1] = per[0][1];
+    t[2] = per[0][2];                          // reduce bytes from HBM
+    t[3 + tiers] = per[0][4];                  // copy bytes from HBM
+    for (int32_t i = 0; i < tiers; ++i) {
+        t[3 + i] = per[size_t(i)][3] - per[size_t(i) + 1][3];
+        t[4 + tiers + i] = per[size_t(i)][5] - per[size_t(i) + 1][5];
+    }
+}
+
 // Ordered factorisations of n into 2..max_levels factors >= 2, each list
 // built from the smallest first factor up (depth first).
 void factorizations(int32_t rest, int32_t max_levels, std::vector<int32_t>& cur,
@@ -110,14 +132,51 @@ AR_EXPORT ar_status ar_genmodel_terms(const ar_plan* plan, int64_t cache_bytes, 
     }
 }
 
+// Whether cache_bytes[0..tiers) is a valid tier list: 1..AR_GENMODEL_MAX_TIERS
+// sizes, each >= 0, strictly decreasing.
+static bool valid_tiers(int32_t tiers, const int64_t* cache_bytes) {
+    if (tiers < 1 || tiers > AR_GENMODEL_MAX_TIERS || !cache_bytes) return false;
+    for (int32_t i = 0; i < tiers; ++i)
+        if (cache_bytes[i] < 0 || (i > 0 && cache_bytes[i] >= cache_bytes[i - 1])) return false;
+    return true;
+}
+
+AR_EXPORT ar_status ar_genmodel_terms_tiered(const ar_plan* plan, int32_t tiers,
+                                             const int64_t* cache_bytes, double* terms) {
+    clear_error();
+    if (!plan || !terms) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+    if (!valid_tiers(tiers, cache_bytes))
+        return fail(AR_ERR_INVALID_ARG, "bad tier count or sizes (decreasing, >= 0)");
+    try {
+        tiered_terms(*plan, tiers, cache_bytes, terms);
+        return AR_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(AR_ERR_OOM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(AR_ERR_INTERNAL, e.what());
+    }
+}
+
 AR_EXPORT ar_status ar_genmodel_select(int32_t n, int64_t N, int32_t dtype, const double* params,
                                        int64_t cache_bytes, int32_t max_levels, int32_t* kind,
                                        int32_t* num_levels, int32_t* fanin, double* seconds) {
     clear_error();
+    if (cache_bytes < 0) return fail(AR_ERR_INVALID_ARG, "bad n, N, cache_bytes or max_levels");
+    return ar_genmodel_select_tiered(n, N, dtype, params, 1, &cache_bytes, max_levels, kind,
+                                     num_levels, fanin, seconds);
+}
+
+AR_EXPORT ar_status ar_genmodel_select_tiered(int32_t n, int64_t N, int32_t dtype,
+                                              const double* params, int32_t tiers,
+                                              const int64_t* cache_bytes, int32_t max_levels,
+                                              int32_t* kind, int32_t* num_levels,
+                                              int32_t* fanin, double* seconds) {
+    clear_error();
     if (!params || !kind || !num_levels || !fanin || !seconds)
         return fail(AR_ERR_INVALID_ARG, "NULL argument");
-    if (n < 1 || N < 0 || cache_bytes < 0 || max_levels < 2 || max_levels > 32)
+    if (n < 1 || N < 0 || !valid_tiers(tiers, cache_bytes) || max_levels < 2 || max_levels > 32)
         return fail(AR_ERR_INVALID_ARG, "bad n, N, cache_bytes or max_levels");
+    const int32_t nterms = 4 + 2 * tiers;
     try {
         struct Cand {
             int32_t kind;
@@ -138,16 +197,16 @@ AR_EXPORT ar_status ar_genmodel_select(int32_t n, int64_t N, int32_t dtype, cons
             const ar_status s = ar_plan_create(n, N, dtype, &topo, &p);
             if (s == AR_ERR_UNSUPPORTED || s == AR_ERR_OOM) continue;  // too large a plan
             if (s != AR_OK) return s;  // bad arguments: ar_last_error says which
-            double t[AR_GENMODEL_TERMS];
+            double t[4 + 2 * AR_GENMODEL_MAX_TIERS];
             try {
-                plan_terms(*p, cache_bytes, t);
+                tiered_terms(*p, tiers, cache_bytes, t);
             } catch (...) {
                 ar_plan_destroy(p);
                 throw;
             }
             ar_plan_destroy(p);
             double pred = 0;
-            for (int j = 0; j < AR_GENMODEL_TERMS; ++j) pred += params[j] * t[j];
+            for (int j = 0; j < nterms; ++j) pred += params[j] * t[j];
             if (!found || pred < best) {
                 found = true;
                 best = pred;

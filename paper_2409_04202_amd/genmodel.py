@@ -31,9 +31,20 @@ phase wrote and that phase wrote at most the cache's capacity; otherwise
 it goes to HBM (Dh, Bh).  Fitted by non-negative least squares in relative
 error.
 
-``python -m paper_2409_04202_amd.genmodel`` measures, fits both forms (from
-co-located PS runs as the paper does, and the extended form also from
-co-located PS plus two-level tree runs), predicts Ring, RHD and
+The tiered form splits the cached bytes once more, by the smaller cache an
+access fits (ar_genmodel_terms_tiered with the 256 MiB last-level cache and
+the 32 MiB the eight XCDs' L2 caches hold together):
+
+    T = A * alpha + K * lam + Dh * delta_h + Dc * delta_c + Dl * delta_l
+                            + Bh * beta_h  + Bc * beta_c  + Bl * beta_l
+
+with Dl, Bl the bytes the one-cache rule classes as cached under 32 MiB and
+Dc, Bc the rest of those it classes as cached under 256 MiB.
+
+``python -m paper_2409_04202_amd.genmodel`` measures, fits the forms (the
+paper's and the extended one from co-located PS runs as the paper does; the
+extended and the tiered one also from co-located PS plus two-level tree
+runs), predicts Ring, RHD and
 hierarchical-tree plans, reports the errors and the plan each model picks
 per (n, N), and prints one JSON document.
 """
@@ -63,12 +74,19 @@ def features(plan):
 
 
 LLC_BYTES = 256 << 20   # MI355X last-level (Infinity) cache
+L2_BYTES = 32 << 20     # the L2 caches of its 8 XCDs, 4 MB each
 
 
 def ext_features(plan, cache_bytes=LLC_BYTES):
     """(A, K, Dh, Dc, Bh, Bc) of a plan for the extended form (see the
     module docstring), computed by the library (ar_genmodel_terms)."""
     return tuple(int(x) for x in arplan.ar_genmodel_terms(plan.handle, cache_bytes))
+
+
+def tiered_features(plan, tiers=(LLC_BYTES, L2_BYTES)):
+    """(A, K, Dh, Dc, Dl, Bh, Bc, Bl) of a plan for the tiered form, computed
+    by the library (ar_genmodel_terms_tiered)."""
+    return tuple(int(x) for x in arplan.ar_genmodel_terms_tiered(plan.handle, list(tiers)))
 
 
 def predict(params, feats):
@@ -117,12 +135,17 @@ def candidates(n):
 
 
 def select(params, n, N, dtype="f32", feature_fn=None):
-    """The plan with the smallest predicted time (`feature_fn`: features or
-    ext_features, matching `params`).  The extended form's choice is made by
-    the library (ar_genmodel_select) over the same candidates."""
+    """The plan with the smallest predicted time (`feature_fn`: features,
+    ext_features or tiered_features, matching `params`).  The extended and
+    tiered forms' choice is made by the library (ar_genmodel_select,
+    ar_genmodel_select_tiered) over the same candidates."""
     feature_fn = feature_fn or features
     if feature_fn is ext_features:
         kind, fan, t = arplan.ar_genmodel_select(n, N, dtype, params, LLC_BYTES, 3)
+        return t, kind, fan
+    if feature_fn is tiered_features:
+        kind, fan, t = arplan.ar_genmodel_select_tiered(n, N, dtype, params,
+                                                        [LLC_BYTES, L2_BYTES], 3)
         return t, kind, fan
     best = None
     for kind, fan in candidates(n):
@@ -159,7 +182,7 @@ class Timer:
                 p.execute(ptrs, s)
             e1.record(s)
             e1.synchronize()
-            feats = (features(p), ext_features(p))
+            feats = (features(p), ext_features(p), tiered_features(p))
         del bufs
         return feats, e0.elapsed_time(e1) * 1e-3 / self.reps
 
@@ -205,9 +228,11 @@ def main():
         "paper_cps": (0, False, train),
         "extended_cps": (1, True, train),
         "extended_cps_tree2": (1, True, train + two_level),
+        "tiered_cps_tree2": (2, True, train + two_level),
     }
     out = {"runs": [{"n": n, "N": N, "plan": kind, "fanin": list(fan) if fan else None,
                      "features": list(f[0]), "ext_features": list(f[1]),
+                     "tiered_features": list(f[2]),
                      "measured_ms": t * 1e3}
                     for (n, N, kind, fan), f, t in runs],
            "models": {}}
@@ -233,7 +258,11 @@ def main():
             "params": list(params),
             "param_names": (["alpha_s", "delta_s_per_B", "beta_s_per_B"] if fi == 0 else
                             ["alpha_s", "lambda_s_per_source", "delta_hbm_s_per_B",
-                             "delta_cached_s_per_B", "beta_hbm_s_per_B", "beta_cached_s_per_B"]),
+                             "delta_cached_s_per_B", "beta_hbm_s_per_B", "beta_cached_s_per_B"]
+                            if fi == 1 else
+                            ["alpha_s", "lambda_s_per_source", "delta_hbm_s_per_B",
+                             "delta_cached_s_per_B", "delta_l2_s_per_B", "beta_hbm_s_per_B",
+                             "beta_cached_s_per_B", "beta_l2_s_per_B"]),
             "train_runs": len(tr),
             "fit_max_error": max(fit_err), "fit_mean_error": float(np.mean(fit_err)),
             "test_max_error": max(test_err) if test_err else None,

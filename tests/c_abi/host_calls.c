@@ -54,6 +54,13 @@ int main(void) {
     CHECK(ar_genmodel_terms(plan, (int64_t)256 << 20, terms) == AR_OK && terms[0] == 4.0 &&
               terms[1] == 8 + 8 + 1 + 1 && terms[2] + terms[3] == (double)red,
           "GenModel terms");
+    const int64_t tiers[2] = {(int64_t)256 << 20, (int64_t)32 << 20};
+    double tiered[4 + 2 * 2];
+    CHECK(ar_genmodel_terms_tiered(plan, 2, tiers, tiered) == AR_OK && tiered[0] == 4.0 &&
+              tiered[2] + tiered[3] + tiered[4] == (double)red,
+          "GenModel tiered terms");
+    CHECK(ar_genmodel_terms_tiered(plan, 0, tiers, tiered) == AR_ERR_INVALID_ARG,
+          "no tier refused");
     CHECK(ar_plan_destroy(plan) == AR_OK, "destroy");
     CHECK(ar_plan_destroy(NULL) == AR_OK, "destroy NULL");
 
@@ -85,6 +92,10 @@ int main(void) {
     CHECK(ar_genmodel_select(16, 1 << 20, AR_F32, rounds_only, 0, 3, &kind, &levels, fanin, &sec) ==
                   AR_OK && kind == AR_CPS && levels == 0 && sec == 2.0,
           "GenModel picks co-located PS on rounds alone");
+    const double rounds_only8[4 + 2 * 2] = {1.0, 0, 0, 0, 0, 0, 0, 0};
+    CHECK(ar_genmodel_select_tiered(16, 1 << 20, AR_F32, rounds_only8, 2, tiers, 3, &kind, &levels,
+                                    fanin, &sec) == AR_OK && kind == AR_CPS && sec == 2.0,
+          "tiered GenModel picks co-located PS on rounds alone");
 
     /* errors */
     CHECK(ar_plan_create(0, 10, AR_F32, &topo, &plan) == AR_ERR_INVALID_ARG, "n = 0 refused");

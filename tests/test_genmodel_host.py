@@ -210,3 +210,49 @@ def test_library_select_is_argmin():
         arplan.ar_genmodel_select(0, 10, "f32", params, 0)
     with pytest.raises(arplan.ArError):
         arplan.ar_genmodel_select(8, 10, "f32", params, 0, max_levels=1)
+
+
+@pytest.mark.parametrize("kind,n,fan", [("ring", 5, None), ("rhd", 6, None), ("cps", 9, None),
+                                        ("tree", 24, (2, 3, 4)), ("tree", 64, (8, 8))])
+@pytest.mark.parametrize("N", [1000, 1 << 16, 1 << 20])
+def test_tiered_terms_split_the_cached_bytes(kind, n, fan, N):
+    # two tiers (the last-level cache, then the L2s): HBM bytes as with the
+    # larger cache alone, tier-1 bytes what the smaller cache alone classes as
+    # cached, tier-0 bytes the rest of the larger cache's cached bytes (each
+    # one-cache term from the reference classification above)
+    big, small = 256 << 20, 32 << 20
+    with arplan.Plan(n, N, "f32", kind, fan) as p:
+        t1 = arplan.ar_genmodel_terms_tiered(p.handle, [big])
+        t2 = arplan.ar_genmodel_terms_tiered(p.handle, [big, small])
+        rb, rs = _reference_terms(p, big), _reference_terms(p, small)
+    assert tuple(int(x) for x in t1) == rb
+    A, K, Dh, Dc, Dl, Bh, Bc, Bl = (int(x) for x in t2)
+    assert (A, K, Dh, Bh) == (rb[0], rb[1], rb[2], rb[4])
+    assert Dl == rs[3] and Dc == rb[3] - rs[3] and Bl == rs[5] and Bc == rb[5] - rs[5]
+    assert min(Dc, Dl, Bc, Bl) >= 0
+
+
+def test_tiered_terms_reject_bad_tiers():
+    with arplan.Plan(8, 1000, "f32", "rhd") as p:
+        for tiers in ([], [32 << 20, 256 << 20], [1 << 20, 1 << 20], [-1], [5, 4, 3, 2, 1]):
+            with pytest.raises(arplan.ArError):
+                arplan.ar_genmodel_terms_tiered(p.handle, tiers)
+    with pytest.raises(arplan.ArError):
+        arplan.ar_genmodel_select_tiered(8, 1000, "f32", [1.0] * 8, [1 << 20, 1 << 21])
+
+
+def test_library_select_tiered_is_argmin():
+    params = (2.3e-6, 5.3e-7, 2.41e-13, 1.55e-13, 1.01e-13, 0.0, 1.15e-13, 6.53e-14)
+    tiers = [genmodel.LLC_BYTES, genmodel.L2_BYTES]
+    for n, N in ((8, 1 << 12), (12, 1 << 20), (32, 1 << 22), (16, 1 << 18), (1, 10)):
+        t, kind, fan = genmodel.select(params, n, N, feature_fn=genmodel.tiered_features)
+        preds = []
+        for k, f in genmodel.candidates(n):
+            with arplan.Plan(n, N, "f32", k, f) as p:
+                preds.append((genmodel.predict(params, genmodel.tiered_features(p, tiers)), k, f))
+        best = min(preds, key=lambda x: x[0])
+        assert (kind, fan) == (best[1], best[2]) and t == pytest.approx(best[0], rel=1e-12), (n, N)
+    # one tier: the same choice as ar_genmodel_select
+    p6 = (3.85e-6, 2.92e-7, 2.44e-13, 1.79e-13, 0.0, 7.68e-14)
+    assert arplan.ar_genmodel_select_tiered(12, 1 << 20, "f32", p6, [256 << 20]) == \
+        arplan.ar_genmodel_select(12, 1 << 20, "f32", p6, 256 << 20)
