@@ -704,6 +704,7 @@ AR_EXPORT ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* 
         out[6] = L.rt_group;
         out[7] = L.dsplit;
         out[8] = L.affinity;
+        out[9] = L.wide;
         return AR_OK;
     } catch (const std::exception& e) {
         return fail(AR_ERR_INTERNAL, e.what());

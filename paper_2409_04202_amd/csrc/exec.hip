@@ -243,8 +243,16 @@ template <int DT, int K>
 static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
                       const uint64_t* recs, int64_t stride, const int2* tiles,
                       int64_t nunits, int64_t tps, int64_t te, int rtg,
-                      int dsplit) {
+                      int dsplit, int wide) {
     const dim3 block(64 * kcfg(K).WPB);
+    if constexpr (K == 2) {
+        if (wide && vecok && cm == 3 && dsplit == 1) {  // see kWideBytes
+            hipLaunchKernelGGL((phase_kernel<DT, 2, true, 3, kWideU>),
+                               dim3(static_cast<uint32_t>(blocks)), block, 0, st, recs, stride,
+                               tiles, nunits, tps, te, rtg);
+            return;
+        }
+    }
     if (dsplit > 1 && vecok) {  // a workgroup per table entry
         // the waves of a workgroup all read the tile's sources: cached loads
         // (with nontemporal ones each wave fetched them from memory again)
@@ -278,15 +286,15 @@ template <int DT>
 static void launch_d(int K, bool vecok, int cm, int64_t blocks, hipStream_t st,
                      const uint64_t* recs, int64_t stride, const int2* tiles,
                      int64_t nunits, int64_t tps, int64_t te, int rtg,
-                     int dsplit) {
+                     int dsplit, int wide) {
     switch (K) {
-        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
-        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
-        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
-        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
-        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
-        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
-        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit); break;
+        case 1: launch_dk<DT, 1>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
+        case 2: launch_dk<DT, 2>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
+        case 3: launch_dk<DT, 3>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
+        case 4: launch_dk<DT, 4>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
+        case 8: launch_dk<DT, 8>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
+        case 16: launch_dk<DT, 16>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
+        default: launch_dk<DT, 0>(vecok, cm, blocks, st, recs, stride, tiles, nunits, tps, te, rtg, dsplit, wide); break;
     }
 }
 
@@ -414,17 +422,17 @@ static ar_status launch_all(ar_plan* plan, const ExecState* ex, const DevView& v
                     case AR_F32:
                         launch_d<DT_F32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                         L.tile_elems, L.rt_group, L.dsplit);
+                                         L.tile_elems, L.rt_group, L.dsplit, L.wide);
                         break;
                     case AR_I32:
                         launch_d<DT_I32>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                          L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                         L.tile_elems, L.rt_group, L.dsplit);
+                                         L.tile_elems, L.rt_group, L.dsplit, L.wide);
                         break;
                     default:
                         launch_d<DT_BF16>(L.kern_k, v.aligned, L.cm, blocks, stream, recs,
                                           L.rec_stride, tiles, L.nunits, L.tiles_per_step,
-                                          L.tile_elems, L.rt_group, L.dsplit);
+                                          L.tile_elems, L.rt_group, L.dsplit, L.wide);
                         break;
                 }
             }

@@ -38,6 +38,10 @@ constexpr int64_t kMinUnitsReduce = 16384;
 // 0.60 -> 0.44 ms (bf16), Ring n = 8 and RHD n = 8 at 1 MiB per processor
 // -29 % and -27 %.
 constexpr int64_t kFineTileMinBytes = int64_t(2) << 20;
+// A 2-source launch of at least kWideBytes with nontemporal loads and stores
+// and a full kcfg tile (64 lanes x kWideU vectors) runs the wide instance of
+// the phase kernel (kWideU vectors per lane and source in one pass).
+constexpr int64_t kWideBytes = int64_t(512) << 20;
 // A runtime-source-count launch (a fan-in without an unrolled kernel)
 // moving less than kRtGroupMaxBytes keeps the loads of kRtGroup sources in
 // flight together; larger ones load one source at a time (measured: k = 24
@@ -225,6 +229,7 @@ struct LaunchDesc {
     int32_t rt_group;        // runtime-k kernel: sources with loads in flight together
     int32_t dsplit;          // waves per tile (split_tile), 1: one
     int32_t affinity;        // 1: the tile table places tiles by xcd_of
+    int32_t wide;            // 1: the wide 2-source instance (kWideU per pass)
     int64_t bytes;           // (k + destinations) * len * e over the steps
     int64_t hbm;             // predicted HBM traffic: bytes, less the repeated
                              // reads of a range by the launch's copies

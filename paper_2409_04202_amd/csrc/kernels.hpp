@@ -69,6 +69,7 @@ constexpr int kRecHead = 4;  // header words
 struct KCfg {
     int U, WPB, TE;
 };
+constexpr int kWideU = 16;  // vectors per lane and source of the wide 2-source pass
 __host__ __device__ constexpr KCfg kcfg(int K) {
     return K == 1 ? KCfg{16, 8, 1024}
          : K == 2 ? KCfg{8, 8, 1024}
@@ -587,12 +588,19 @@ __device__ __forceinline__ void split_tile(void* const* __restrict__ sp, int k,
 // `recs`, `stride` words apart.  K = 0 means the source count is read from
 // each step (any k >= 1), folded `rt_group` sources at a time.  VECOK: every
 // buffer is 16-byte aligned.  CM: cache mode of the vector loads and stores.
-template <int DT, int K, bool VECOK, int CM>
+// UW (0: kcfg's U) overrides the vectors per lane and source of a pass: the
+// wide 2-source instance (kWideU) loads a whole 1024-vector tile in one pass,
+// so no load of a tile waits behind one of its stores (the two share the
+// wave's in-order memory counter); it pays on multi-GiB launches with
+// nontemporal loads and stores (RHD's first halving launch, 3 GiB: 531 ->
+// 520 us), while its 148 VGPRs (3 waves per SIMD, against 5) made short
+// launches slower (bf16 Ring as written +10-15 %).
+template <int DT, int K, bool VECOK, int CM, int UW = 0>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
     int64_t nunits, int64_t tiles_per_step, int64_t tile_elems, int rt_group) {
     constexpr int VEC = Elem<DT>::VEC;
-    constexpr int U = kcfg(K).U;
+    constexpr int U = UW ? UW : kcfg(K).U;
     constexpr int WPB = kcfg(K).WPB;
     const int lane = int(threadIdx.x) & 63;
     const int64_t unit = int64_t(blockIdx.x) * WPB +

@@ -539,10 +539,11 @@ def _launch_desc(handle, stage):
     f = arplan._lib.ar_debug_launch_desc
     f.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)]
     f.restype = ctypes.c_int32
-    out = (ctypes.c_int64 * 9)()
+    out = (ctypes.c_int64 * 10)()
     assert f(handle, stage, out) == arplan.AR_OK, arplan.ar_last_error()
     return {"k": out[0], "cm": out[1], "tile": out[2], "tiles": out[3], "wpb": out[4],
-            "table": out[5], "group": out[6], "split": out[7], "affinity": out[8]}
+            "table": out[5], "group": out[6], "split": out[7], "affinity": out[8],
+            "wide": out[9]}
 
 
 def test_full_size_forms_use_the_nontemporal_kernels():
@@ -560,6 +561,8 @@ def test_full_size_forms_use_the_nontemporal_kernels():
         d = [_launch_desc(p.handle, i) for i in range(3)]
         assert [x["k"] for x in d] == [2, 2, 2]
         assert [x["cm"] for x in d] == [3, 1, 1]
+        # the first, nontemporal both ways and 3 GiB, runs the wide instance
+        assert [x["wide"] for x in d] == [1, 0, 0]
         # with the rewrites, the last halving launch stores to all 8 buffers
         # (2 GiB, nontemporal)
         p.set_option(arplan.AR_OPT_FUSE, 1)
@@ -784,3 +787,26 @@ def test_automatic_choice_of_bench_workloads(name):
     c = workloads.CONFIGS[name]
     with arplan.Plan(c["n"], c["N"], c["dtype"], c["kind"], c["fanin"]) as p:
         assert p.launch_kernels() == BENCH_CHOICE[name]
+
+
+@pytest.mark.parametrize("N,dtype", [((1 << 26) + 13, "f32"), (1 << 26, "i32"), (1 << 27, "bf16")])
+def test_wide_two_source_launches(N, dtype):
+    # RHD as written at 2-3 GiB: the first halving launch (nontemporal loads
+    # and stores, over 512 MiB) runs the wide 2-source instance; smaller or
+    # cached launches never do; the tiling check accepts it either way
+    with arplan.Plan(8, N, dtype, "rhd") as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        L = p.launches()
+        d = [_launch_desc(p.handle, i) for i in range(len(L))]
+        assert d[0]["wide"] == 1 and d[0]["cm"] == 3, d[0]
+        for x, y in zip(L, d):
+            if y["wide"]:
+                assert x[1] == 2 and y["cm"] == 3 and x[4] >= 512 << 20, (x, y)
+        for vecok in (1, 0):
+            st, msg = _check_tiling(p.handle, vecok)
+            assert st == arplan.AR_OK, msg
+    with arplan.Plan(8, 1 << 20, dtype, "rhd") as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        assert all(_launch_desc(p.handle, i)["wide"] == 0 for i in range(len(p.launches())))

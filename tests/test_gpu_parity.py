@@ -853,6 +853,17 @@ def test_fine_tile_launches(kind, n, N, fan, dtype, pad):
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
+@pytest.mark.parametrize("N,dtype", [((1 << 26) + 13, "f32"), (1 << 26, "i32"), (1 << 27, "bf16")])
+def test_wide_two_source_launches(N, dtype):
+    # RHD as written at 2-3 GiB: its first halving launch runs the wide
+    # 2-source instance (tests/test_capi_host.py checks which launch); a
+    # ragged size, int32 and bf16; every element against the oracle
+    dist = "int1000" if dtype == "i32" else "uniform"
+    got, xs0 = _full_compare("rhd", 8, N, dtype, None, dist, seed=N % 89, fuse=0, slice_=0)
+    if dtype == "bf16":
+        assert _normwise_bf16(got[0], xs0) <= 1e-2
+
+
 @pytest.mark.parametrize("N,forms", [
     ((1 << 30) + 4099, [(1, 2, 1), (0, 0, 1)]),     # unaligned steps: phase launches
     ((1 << 30) + 8192, [(1, 1, 1), (0, 0, 1)])])    # aligned: one resident launch
