@@ -253,6 +253,19 @@ static void launch_dk(bool vecok, int cm, int64_t blocks, hipStream_t st,
             return;
         }
     }
+    if constexpr (K == 8 && DT != DT_BF16) {
+        if (wide && vecok && (cm & 1) && dsplit == 1) {  // see kWideBytes
+            if (cm & 2)
+                hipLaunchKernelGGL((phase_kernel<DT, 8, true, 3, kWideU8>),
+                                   dim3(static_cast<uint32_t>(blocks)), block, 0, st, recs,
+                                   stride, tiles, nunits, tps, te, rtg);
+            else
+                hipLaunchKernelGGL((phase_kernel<DT, 8, true, 1, kWideU8>),
+                                   dim3(static_cast<uint32_t>(blocks)), block, 0, st, recs,
+                                   stride, tiles, nunits, tps, te, rtg);
+            return;
+        }
+    }
     if (dsplit > 1 && vecok) {  // a workgroup per table entry
         // the waves of a workgroup all read the tile's sources: cached loads
         // (with nontemporal ones each wave fetched them from memory again)

@@ -69,7 +69,8 @@ constexpr int kRecHead = 4;  // header words
 struct KCfg {
     int U, WPB, TE;
 };
-constexpr int kWideU = 16;  // vectors per lane and source of the wide 2-source pass
+constexpr int kWideU = 16;   // vectors per lane and source of the wide 2-source pass
+constexpr int kWideU8 = 4;   // ... and of the wide 8-source pass (4-byte elements)
 __host__ __device__ constexpr KCfg kcfg(int K) {
     return K == 1 ? KCfg{16, 8, 1024}
          : K == 2 ? KCfg{8, 8, 1024}

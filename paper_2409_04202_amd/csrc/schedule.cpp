@@ -224,9 +224,12 @@ static void build_launches(const Plan& p, ExecState& ex) {
                 const int64_t keep = k >= 2 ? kKeepBytesFold : kKeepBytes;
                 if (written > keep || !next_reads_output) L.cm |= 2;
             }
-            L.wide = L.kern_k == 2 && L.cm == 3 && bytes >= kWideBytes &&
-                     maxdst < kSplitMinDst && te == int64_t(64) * kWideU * VEC &&
-                     te == int64_t(cfg.TE) * VEC;
+            L.wide = (L.kern_k == 2 && L.cm == 3 && bytes >= kWideBytes &&
+                      maxdst < kSplitMinDst && te == int64_t(64) * kWideU * VEC &&
+                      te == int64_t(cfg.TE) * VEC) ||
+                     (L.kern_k == 8 && p.esize == 4 && (L.cm & 1) && bytes >= kWideBytes &&
+                      maxdst < kSplitMinDst && te == int64_t(64) * kWideU8 * VEC &&
+                      te == int64_t(cfg.TE) * VEC);
             all_kept = all_kept && !(L.cm & 2);
             phase_written += written;
             L.tile_elems = te;

@@ -789,6 +789,38 @@ def test_automatic_choice_of_bench_workloads(name):
         assert p.launch_kernels() == BENCH_CHOICE[name]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "i32", "bf16"])
+def test_wide_eight_source_launches(dtype):
+    # an 8-source fold of 4-byte elements over 512 MiB or more with
+    # nontemporal loads runs the one-pass wide instance: the first level of
+    # the (8, 8) tree at 2^22 elements per processor, and a lone 8-way reduce
+    # over 128 MiB buffers (nontemporal stores too); bf16 folds never do
+    from paper_2409_04202_amd import workloads
+    c = workloads.CONFIGS["tree8x8_n64_f32"]
+    with arplan.Plan(c["n"], c["N"], dtype, "tree", c["fanin"]) as p:
+        p.set_option(arplan.AR_OPT_FUSE, 0)
+        p.set_option(arplan.AR_OPT_SLICE, 0)
+        L = p.launches()
+        d = [_launch_desc(p.handle, i) for i in range(len(L))]
+        assert [y["wide"] for y in d] == [int(dtype != "bf16"), 0, 0, 0], d
+        assert (L[0][1], d[0]["cm"]) == (8, 1)
+    N = (1 << 25) + 13
+    h = arplan.ar_plan_create_custom(8, N, dtype, [(0, "reduce", 0, list(range(8)), 0, N)])
+    try:
+        d = _launch_desc(h, 0)
+        assert (d["k"], d["cm"], d["wide"]) == (8, 3, int(dtype != "bf16")), d
+        for vecok in (1, 0):
+            st, msg = _check_tiling(h, vecok)
+            assert st == arplan.AR_OK, msg
+    finally:
+        arplan.ar_plan_destroy(h)
+    h = arplan.ar_plan_create_custom(8, 1 << 22, dtype, [(0, "reduce", 0, list(range(8)), 0, 1 << 22)])
+    try:
+        assert _launch_desc(h, 0)["wide"] == 0
+    finally:
+        arplan.ar_plan_destroy(h)
+
+
 @pytest.mark.parametrize("N,dtype", [((1 << 26) + 13, "f32"), (1 << 26, "i32"), (1 << 27, "bf16")])
 def test_wide_two_source_launches(N, dtype):
     # RHD as written at 2-3 GiB: the first halving launch (nontemporal loads

@@ -864,6 +864,34 @@ def test_wide_two_source_launches(N, dtype):
         assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+def test_wide_eight_source_launches(dtype):
+    # a lone 8-way reduce over 128 MiB buffers and a ragged tail runs the
+    # wide 8-source instance with nontemporal loads and stores
+    # (tests/test_capi_host.py checks the choice); the (8, 8) tree's first
+    # level covers the cached-store form; every element against the oracle
+    n, N = 8, (1 << 25) + 13
+    steps = [(0, "reduce", 0, list(range(n)), 0, N)]
+    say("case: custom 8-way reduce N=%d %s" % (N, dtype))
+    dist = "int1000" if dtype == "i32" else "uniform"
+    xs0 = workloads.draw(n, N, dtype, dist, 31)
+    ref = oracle.execute(oracle.Plan("custom", n, N, [[oracle.Step(
+        "reduce", 0, tuple(range(n)), 0, N)]]), [x.copy() for x in xs0], dtype)
+    ts = to_device(xs0, dtype)
+    del xs0
+    h = arplan.ar_plan_create_custom(n, N, dtype, steps)
+    try:
+        arplan.ar_plan_execute(h, ts, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+    finally:
+        arplan.ar_plan_destroy(h)
+    got = to_host(ts, dtype)
+    for q in range(n):
+        assert np.array_equal(got[q], ref[q]), q
+    del ts
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("N,forms", [
     ((1 << 30) + 4099, [(1, 2, 1), (0, 0, 1)]),     # unaligned steps: phase launches
     ((1 << 30) + 8192, [(1, 1, 1), (0, 0, 1)])])    # aligned: one resident launch
