@@ -336,8 +336,10 @@ struct TNode {
 // child order, get quotas of floor(n / s) blocks, one more for the first
 // n mod s, and claim in that order the first unclaimed blocks of what they
 // held below their child; a block left unclaimed goes to its holder in the
-// first child.  Each switch reduces every block over one holder per child;
-// switches of one height share a phase; the AllGather reverses it.
+// first child.  Each switch reduces every block over one holder per child
+// (on children with unequal shares this is Section 4.2's asymmetric CPS:
+// every partial goes straight to the block's new owner); switches of one
+// height share a phase; the AllGather reverses it.
 void expand_gentree(Plan& p, const std::vector<int32_t>& nchild) {
     const int32_t n = p.n;
     const int64_t N = p.N;
