@@ -595,7 +595,9 @@ __device__ __forceinline__ void split_tile(void* const* __restrict__ sp, int k,
 // wave's in-order memory counter); it pays on multi-GiB launches with
 // nontemporal loads and stores (RHD's first halving launch, 3 GiB: 531 ->
 // 520 us), while its 148 VGPRs (3 waves per SIMD, against 5) made short
-// launches slower (bf16 Ring as written +10-15 %).
+// launches slower (bf16 Ring as written +10-15 %).  The wide 8-source
+// instance (kWideU8, 4-byte elements) likewise covers its 256-vector tile in
+// one pass instead of two.
 template <int DT, int K, bool VECOK, int CM, int UW = 0>
 __global__ __launch_bounds__(64 * kcfg(K).WPB) void phase_kernel(
     const uint64_t* __restrict__ recs, int64_t stride, const int2* __restrict__ tiles,
