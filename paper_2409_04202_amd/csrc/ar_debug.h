@@ -47,7 +47,8 @@ ar_status ar_debug_resident(ar_plan* plan, int32_t stage, int64_t* info,
  * runtime-source-count kernel keeps in flight together, out[7] = waves per
  * tile (1, or the wavefronts per block in a split launch), out[8] = 1 when
  * the tile table places tiles on XCDs by position, out[9] = 1 when the launch
- * runs the wide 2-source instance (out has room for 10).
+ * runs a wide instance (2-source, or 8-source of 4-byte elements; out has room
+ * for 10).
  * AR_ERR_INVALID_ARG for a sliced launch.  Host only. */
 ar_status ar_debug_launch_desc(ar_plan* plan, int32_t stage, int64_t* out);
 #ifdef __cplusplus

@@ -171,6 +171,29 @@ constexpr int64_t kResWavesPerCU = 16;
 constexpr int64_t kLdsBytesPerCU = int64_t(160) << 10;
 constexpr int64_t kNumCUs = 256;
 constexpr int64_t kNumXCDs = 8;         // compute dies, each with its own L2
+// A plan of more than kResMaxN buffers may run as one streamed launch
+// (stream_kernel) under AR_OPT_SLICE = 2 as well, when that is predicted
+// below kStreamGain of the runs chosen above.  Its workgroups each run one
+// unit's program, one record after the other, as many at a time as LDS
+// holds (slots, buffer pointers and the longest unit program per
+// workgroup): kLaunchNs + rounds * words * kStreamWordNs, rounds = units
+// over the workgroups that fit.  Measured on MI355X (48 plans, n = 96-512,
+// 4K-1M elements): 120-155 ns per word for Ring and RHD, 77-110 for trees;
+// the streamed form beat the other choice only on Ring (n = 128 and 256 up
+// to 256K fp32 elements, n = 128 up to 1M bf16: 0.45-0.91 of its time).
+// The prediction of those runs was low (88-215 us against 101-408
+// measured), so the streamed form is taken whenever predicted faster
+// (kStreamGain 1): on the 48 plans it was then picked 7 times, each a win.
+constexpr double kStreamWordNs = 145.0;
+constexpr double kStreamGain = 1.0;
+// With more than kResMaxN buffers (beyond the plans the model was fitted
+// on) a plain sliced run leaves out phases whose steps store to at least
+// kSplitMinDst buffers over ranges shorter than kSlicedManyDstMinBytes: a
+// wave of the sliced kernel stores each such step alone, mostly with idle
+// lanes, where their own launch runs split.  Measured: RHD n = 96-256 at
+// 4K-32K fp32 elements took 1.2-1.7 times as long with such a run as with
+// phase launches.
+constexpr int64_t kSlicedManyDstMinBytes = 4096;
 // Copy launches whose steps read a range several times deal their tiles to
 // XCDs by source range (xcd_tiles in schedule.cpp) when a step has at most
 // this many tiles.

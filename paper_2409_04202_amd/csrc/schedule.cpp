@@ -374,6 +374,7 @@ struct PhaseCost {
     bool aligned = true;
     int64_t written = 0, read = 0, bytes = 0, cover = 0;
     int32_t kmax = 0, dmax = 0;
+    bool short_many = false;  // a step to >= kSplitMinDst buffers, short
     uint64_t touched = 0;  // buffers the phase touches (n <= kResMaxN)
     double t_launch = 0.0;
 };
@@ -397,6 +398,9 @@ static std::vector<PhaseCost> phase_costs(const Plan& p, const ExecState& ex) {
             pc[q].read += int64_t(x.srcs.size()) * len * p.esize;
             pc[q].kmax = std::max(pc[q].kmax, int32_t(x.srcs.size()));
             pc[q].dmax = std::max(pc[q].dmax, int32_t(x.dsts.size()));
+            pc[q].short_many = pc[q].short_many ||
+                               (int32_t(x.dsts.size()) >= kSplitMinDst &&
+                                len * p.esize < kSlicedManyDstMinBytes);
             pc[q].bytes += (int64_t(x.srcs.size()) + int64_t(x.dsts.size())) * len * p.esize;
             if (p.n <= kResMaxN) {
                 for (int32_t b : x.srcs) pc[q].touched |= uint64_t(1) << b;
@@ -436,7 +440,7 @@ struct Run {
 };
 
 static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
-                                    const std::vector<PhaseCost>& pc) {
+                                    const std::vector<PhaseCost>& pc, double* t_total) {
     const double per_src = p.dtype == AR_BF16 ? kStepNsPerSrcBF16 : kStepNsPerSrcF32;
     const double bpn = byte_rate(p);
     const double waves = std::max(1.0, double(p.N) * p.esize / (64.0 * kSliceU * 16.0));
@@ -471,7 +475,8 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
         for (int32_t a = b - 1; a >= 0; --a) {
             const PhaseCost& c = pc[size_t(a)];
             if (!c.aligned) break;
-            plain_ok = plain_ok && c.written <= kKeepBytes && c.bytes <= kSliceMaxBytes;
+            plain_ok = plain_ok && c.written <= kKeepBytes && c.bytes <= kSliceMaxBytes &&
+                       !(p.n > kResMaxN && c.short_many);
             if (!plain_ok && !res_ok) break;
             body += std::max({double(c.cover) * (kStepNs + per_src * c.kmax + kStepNsPerDst * c.dmax),
                               stretch * double(c.read) / bpn,
@@ -514,6 +519,7 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
             }
         }
     }
+    *t_total = best[size_t(P)];
     std::vector<Run> runs;
     for (int32_t b = P; b > 0;) {
         if (from[size_t(b)] < 0) {
@@ -527,6 +533,14 @@ static std::vector<Run> choose_runs(const Plan& p, const ExecState& ex,
     return runs;
 }
 
+// Predicted time of a streamed launch (see kStreamWordNs).
+static double stream_time(const Plan& p, const SliceDesc& sd) {
+    const int64_t lds = int64_t(sd.slots) * 1024 + int64_t(p.n) * 8 + int64_t(sd.max_nw) * 4;
+    const int64_t per_cu = std::max<int64_t>(1, kLdsBytesPerCU / lds);
+    const double rounds = std::ceil(double(sd.nunits) / double(kNumCUs * per_cu));
+    return kLaunchNs + rounds * double(sd.max_nw) * kStreamWordNs;
+}
+
 static std::atomic<uint64_t> g_exec_serial{0};
 
 ExecState* exec_state(Plan& p) {
@@ -537,16 +551,31 @@ ExecState* exec_state(Plan& p) {
             ex->phases = exec_phases(p, p.fuse != 0);
             build_launches(p, *ex);
             std::vector<Run> runs;
-            if (p.slice == 1 && !ex->phases.empty()) {
-                runs.push_back({0, int32_t(ex->phases.size()), p.resident != 0});
+            const int32_t P = int32_t(ex->phases.size());
+            SliceDesc streamed;  // the whole plan streamed, when chosen below
+            bool have_streamed = false;
+            if (p.slice == 1 && P > 0) {
+                runs.push_back({0, P, p.resident != 0});
             } else if (p.slice == 2) {
-                runs = choose_runs(p, *ex, phase_costs(p, *ex));
+                double t_runs = 0.0;
+                runs = choose_runs(p, *ex, phase_costs(p, *ex), &t_runs);
+                if (p.resident != 0 && p.n > kResMaxN && P > 0) {
+                    SliceDesc sd = build_slice(p, *ex, 0, P);
+                    if (sd.ok) {
+                        build_resident(p, *ex, sd);
+                        if (sd.streamed && stream_time(p, sd) < kStreamGain * t_runs) {
+                            runs.assign(1, Run{0, P, true});
+                            streamed = std::move(sd);
+                            have_streamed = true;
+                        }
+                    }
+                }
             }
             std::vector<int32_t> slice_of(ex->phases.size(), -1);
             for (const Run& r : runs) {
-                SliceDesc sd = build_slice(p, *ex, r.a, r.b);
+                SliceDesc sd = have_streamed ? std::move(streamed) : build_slice(p, *ex, r.a, r.b);
                 if (!sd.ok) continue;  // phase launches for these phases
-                if (r.resident) build_resident(p, *ex, sd);
+                if (r.resident && !have_streamed) build_resident(p, *ex, sd);
                 sd.cuts_base = ex->slices.empty() ? 0
                                                   : ex->slices.back().cuts_base +
                                                         int64_t(ex->slices.back().cuts.size());

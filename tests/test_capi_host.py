@@ -781,6 +781,28 @@ BENCH_CHOICE = {
 }
 
 
+def test_automatic_choice_beyond_64_buffers():
+    # Ring over 128 and 256 buffers runs as one streamed launch up to the
+    # sizes where it was measured faster; RHD's 128-destination phase of
+    # 128-byte steps runs split, outside the sliced run; trees and large
+    # Rings keep their launches
+    def kernels(kind, n, N, dtype, fan=None):
+        with arplan.Plan(n, N, dtype, kind, fan) as p:
+            return p.launch_kernels()
+    for n, N, dtype in [(128, 1 << 12, "f32"), (256, 1 << 15, "f32"), (128, 1 << 18, "bf16")]:
+        assert kernels("ring", n, N, dtype) == ["stream_kernel"], (n, N, dtype)
+    assert "stream_kernel" not in kernels("ring", 128, 1 << 20, "f32")
+    k = kernels("rhd", 128, 1 << 12, "f32")
+    assert k[-1] == "split_kernel" and "stream_kernel" not in k, k
+    for fan, N in [((8, 8, 8), 1 << 12), ((8, 8, 8), 1 << 18), ((8, 16), 1 << 15)]:
+        assert "stream_kernel" not in kernels("tree", 512 if len(fan) == 3 else 128, N, "f32", fan)
+    # without streamed runs: Ring's last phase, 32-byte steps into 128
+    # buffers, leaves the sliced run too
+    with arplan.Plan(128, 1 << 12, "f32", "ring") as p:
+        p.set_option(arplan.AR_OPT_RESIDENT, 0)
+        assert p.launch_kernels() == ["sliced_kernel", "split_kernel"]
+
+
 @pytest.mark.parametrize("name", sorted(BENCH_CHOICE))
 def test_automatic_choice_of_bench_workloads(name):
     from paper_2409_04202_amd import workloads

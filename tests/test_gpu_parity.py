@@ -137,6 +137,24 @@ def test_sliced_runs_between_phase_launches():
             assert _normwise_bf16(got[0], xs0) <= 1e-2
 
 
+@pytest.mark.parametrize("kind,n,N,dtype,kernel", [
+    ("ring", 128, 1 << 12, "f32", "stream_kernel"), ("ring", 256, 1 << 15, "f32", "stream_kernel"),
+    ("ring", 128, 1 << 18, "bf16", "stream_kernel"), ("rhd", 128, 1 << 12, "f32", "split_kernel")])
+def test_automatic_choice_beyond_64_buffers(kind, n, N, dtype, kernel):
+    # the automatic choice for more than 64 buffers: Ring as one streamed
+    # launch, RHD's short 128-destination phase as a split launch
+    # (tests/test_capi_host.py pins the choices); every element vs the oracle
+    with arplan.Plan(n, N, dtype, kind) as p:
+        assert kernel in p.launch_kernels()
+    got, xs0 = _full_compare(kind, n, N, dtype, None, "uniform", seed=n + 5)
+    if dtype == "bf16":
+        # bit-exact with the oracle above; against the exact sum, Ring's
+        # chain rounds to bf16 (unit roundoff 2^-8) after each of its n - 1
+        # steps: a random walk of about sqrt(n) roundings (0.013 measured
+        # at n = 128, where 1 % holds for the trees and n <= 64)
+        assert _normwise_bf16(got[0], xs0) <= 2.0 ** -8 * np.sqrt(n)
+
+
 # ------------------------------------------- full size, every element
 
 # The executor forms the benchmark times: the default choice, phase launches
