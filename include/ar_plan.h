@@ -288,8 +288,10 @@ ar_status ar_plan_execute_noalloc(ar_plan* plan, void* const* bufs, void* stream
  *  computed depth first and the loads issued ahead.  Every step still folds
  *  the same values with the plan's sources in their listed order, so
  *  results are the same bits.  With AR_OPT_SLICE = 2 the cost model picks
- *  the plain or the resident form per run; with AR_OPT_SLICE = 1 the whole
- *  plan runs resident.  0: sliced launches always run plain. */
+ *  the plain or the resident form per run (n <= 64), or (n > 64) runs the
+ *  whole plan as one streamed launch when it predicts that faster than the
+ *  runs it chose; with AR_OPT_SLICE = 1 the whole plan runs resident.
+ *  0: sliced launches always run plain. */
 typedef enum ar_option { AR_OPT_FUSE = 0, AR_OPT_SLICE = 1, AR_OPT_RESIDENT = 2 } ar_option;
 ar_status ar_plan_set_option(ar_plan* plan, int32_t option, int64_t value);
 
