@@ -744,7 +744,8 @@ def test_runs_on_a_side_stream_in_order():
     ("ring", 8, 8 * 1024, None, 1, 1),           # one resident launch
     ("ring", 8, 8 * 1024, None, 1, 0),           # one plain sliced launch
     ("rhd", 8, 1 << 20, None, 0, 1),             # phase launches
-    ("tree", 64, 64 * 256, (8, 8), 2, 1)])       # the default choice
+    ("tree", 64, 64 * 256, (8, 8), 2, 1),        # the default choice
+    ("ring", 128, 128 * 32, None, 2, 1)])        # the default choice: streamed
 def test_graph_capture_replays(kind, n, N, fan, slice_, resident):
     # an execution captured in a HIP graph after a first eager execution (which
     # uploads the step records, so that capture records kernel launches only)
